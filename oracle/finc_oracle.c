@@ -1,0 +1,422 @@
+/*
+ * finc_oracle.c -- plain, slow CPU reference of the FInC masked k x k
+ * convolution layer, its FInC unit and the multi-scale sampling stack.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test-suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no source,
+ * header, table or helper with the HIP library; the two meet only on the
+ * seeded inputs drawn in Python.
+ *
+ * Everything is float64, nested loops, no blocking, no reordering.
+ *
+ * Layout: activations (B, C, H, W) row-major; weights (C_out, C_in, k, k)
+ * row-major (OIHW).  Corners: 0 = TL, 1 = TR, 2 = BL, 3 = BR.
+ *
+ * Readings of the paper taken here (its text is garbled in places):
+ *  - Convolution (Sec. 3, "Invertible Convolutions", conv equation) is a
+ *    cross-correlation of the padded input with K; with the corner paddings of
+ *    Sec. 4.1 (k-1 zero rows/cols on the two named sides) output pixel (i, j)
+ *    reads input (i + a - oh, j + b - ow) for kernel position (a, b), where
+ *    (oh, ow) = (k-1, k-1) TL, (k-1, 0) TR, (0, k-1) BL, (0, 0) BR.  Reads
+ *    outside the image are zero.
+ *  - The kernel position (oh, ow) multiplies the output pixel itself ("self
+ *    tap").  At that position only c_in <= c_out is used (lower-triangular
+ *    channel block); entries with c_in > c_out are ignored whatever they hold.
+ *    All other positions are used in full.  The paper's own CInC masking fixes
+ *    the self block to the identity (Sec. 1, proof of Theorem 1); that is the
+ *    special case of unit diagonal and zero strictly-lower entries.
+ *  - log|det| of one layer is H*W*sum_c log|K[c,c,oh,ow]|: the convolution
+ *    matrix is triangular in the corner's pixel raster order with those
+ *    diagonal entries (Sec. 3 "Algorithms for Computing Inverse ...", Fig. 1
+ *    caption, Table 1 "Jacobian is 1" for unit diagonal).
+ *  - The inverse here is the naive sequential substitution of Sec. 3
+ *    ("Algorithms for Computing Inverse of Convolutions", the O(n^2 k^2) method
+ *    of CInC / Emerging): pixels in the corner's raster order, channels in
+ *    ascending order inside each pixel.  It deliberately does NOT follow the
+ *    diagonal schedule of Algorithm 1.
+ */
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_OK 0
+#define ORC_EINVAL (-1)
+#define ORC_ESINGULAR (-2)
+#define ORC_ENOMEM (-5)
+
+/* Padding offsets of the four corner variants (Sec. 4.1, corner padding
+ * equations, read as k-1 zero rows/cols on the two named sides). */
+static void corner_offsets(int corner, int k, int *oh, int *ow)
+{
+    *oh = (corner == 0 || corner == 1) ? k - 1 : 0; /* top padded    */
+    *ow = (corner == 0 || corner == 2) ? k - 1 : 0; /* left padded   */
+}
+
+static int bad_shape(long B, int C, int H, int W, int k, int corner)
+{
+    return B < 0 || C < 1 || H < 1 || W < 1 || k < 1 || corner < 0 || corner > 3;
+}
+
+static double kw(const double *K, int C, int k, int co, int ci, int a, int b)
+{
+    return K[(((long)co * C + ci) * k + a) * k + b];
+}
+
+/* Weight as the layer uses it: the channel mask at the self tap. */
+static double kmasked(const double *K, int C, int k, int oh, int ow,
+                      int co, int ci, int a, int b)
+{
+    if (a == oh && b == ow && ci > co)
+        return 0.0;
+    return kw(K, C, k, co, ci, a, b);
+}
+
+/* Forward padded masked convolution, direct loop (Sec. 3 conv equation with
+ * the Sec. 4.1 corner padding). */
+int orc_forward(const double *x, double *y, const double *K, long B, int C,
+                int H, int W, int k, int corner)
+{
+    if (bad_shape(B, C, H, W, k, corner) || !x || !y || !K)
+        return ORC_EINVAL;
+    int oh, ow;
+    corner_offsets(corner, k, &oh, &ow);
+    for (long n = 0; n < B; ++n) {
+        const double *xn = x + n * (long)C * H * W;
+        double *yn = y + n * (long)C * H * W;
+        for (int co = 0; co < C; ++co)
+            for (int i = 0; i < H; ++i)
+                for (int j = 0; j < W; ++j) {
+                    double s = 0.0;
+                    for (int ci = 0; ci < C; ++ci)
+                        for (int a = 0; a < k; ++a)
+                            for (int b = 0; b < k; ++b) {
+                                int ii = i + a - oh, jj = j + b - ow;
+                                if (ii < 0 || ii >= H || jj < 0 || jj >= W)
+                                    continue;
+                                s += kmasked(K, C, k, oh, ow, co, ci, a, b) *
+                                     xn[((long)ci * H + ii) * W + jj];
+                            }
+                    yn[((long)co * H + i) * W + j] = s;
+                }
+    }
+    return ORC_OK;
+}
+
+/* log|det| of one layer's convolution matrix: triangular in the corner's
+ * raster order, diagonal entry K[c,c,self] repeated at every pixel. */
+int orc_logdet(const double *K, int C, int k, int corner, int H, int W,
+               double *out)
+{
+    if (bad_shape(1, C, H, W, k, corner) || !K || !out)
+        return ORC_EINVAL;
+    int oh, ow;
+    corner_offsets(corner, k, &oh, &ow);
+    double s = 0.0;
+    int singular = 0;
+    for (int c = 0; c < C; ++c) {
+        double d = kw(K, C, k, c, c, oh, ow);
+        if (d == 0.0)
+            singular = 1;
+        s += log(fabs(d));
+    }
+    *out = (double)H * (double)W * s;
+    return singular ? ORC_ESINGULAR : ORC_OK;
+}
+
+/* Inverse by sequential substitution in raster order (Sec. 3, "Algorithms
+ * for Computing Inverse of Convolutions"): every pixel is solved after all
+ * pixels it reads, then the channels of the pixel are solved against the
+ * lower-triangular self block, c ascending. */
+int orc_inverse(const double *y, double *x, const double *K, long B, int C,
+                int H, int W, int k, int corner)
+{
+    if (bad_shape(B, C, H, W, k, corner) || !x || !y || !K)
+        return ORC_EINVAL;
+    int oh, ow;
+    corner_offsets(corner, k, &oh, &ow);
+    for (int c = 0; c < C; ++c)
+        if (kw(K, C, k, c, c, oh, ow) == 0.0)
+            return ORC_ESINGULAR;
+    /* Raster order of the corner: rows top-down when the top is padded,
+     * columns left-to-right when the left is padded. */
+    int rows_down = (corner == 0 || corner == 1);
+    int cols_right = (corner == 0 || corner == 2);
+    for (long n = 0; n < B; ++n) {
+        const double *yn = y + n * (long)C * H * W;
+        double *xn = x + n * (long)C * H * W;
+        for (int ri = 0; ri < H; ++ri) {
+            int i = rows_down ? ri : H - 1 - ri;
+            for (int rj = 0; rj < W; ++rj) {
+                int j = cols_right ? rj : W - 1 - rj;
+                for (int c = 0; c < C; ++c) {
+                    double r = yn[((long)c * H + i) * W + j];
+                    for (int a = 0; a < k; ++a)
+                        for (int b = 0; b < k; ++b) {
+                            int ii = i + a - oh, jj = j + b - ow;
+                            if (ii < 0 || ii >= H || jj < 0 || jj >= W)
+                                continue;
+                            int self = (a == oh && b == ow);
+                            int cmax = self ? c : C; /* self tap: ci < c only */
+                            for (int ci = 0; ci < cmax; ++ci)
+                                r -= kw(K, C, k, c, ci, a, b) *
+                                     xn[((long)ci * H + ii) * W + jj];
+                        }
+                    xn[((long)c * H + i) * W + j] = r / kw(K, C, k, c, c, oh, ow);
+                }
+            }
+        }
+    }
+    return ORC_OK;
+}
+
+/* ---- FInC unit: the four padded blocks TL, TR, BL, BR applied one after
+ * the other, each with its own weights (K4 = 4 consecutive OIHW tensors). --- */
+
+static const int UNIT_ORDER[4] = {0, 1, 2, 3};
+
+int orc_unit_forward(const double *x, double *y, const double *K4, long B,
+                     int C, int H, int W, int k)
+{
+    if (bad_shape(B, C, H, W, k, 0) || !x || !y || !K4)
+        return ORC_EINVAL;
+    long n = B * (long)C * H * W;
+    long ksz = (long)C * C * k * k;
+    double *t = (double *)malloc(sizeof(double) * (n > 0 ? n : 1));
+    if (!t)
+        return ORC_ENOMEM;
+    memcpy(t, x, sizeof(double) * n);
+    int rc = ORC_OK;
+    for (int q = 0; q < 4 && rc == ORC_OK; ++q) {
+        rc = orc_forward(t, y, K4 + q * ksz, B, C, H, W, k, UNIT_ORDER[q]);
+        memcpy(t, y, sizeof(double) * n);
+    }
+    free(t);
+    return rc;
+}
+
+int orc_unit_inverse(const double *y, double *x, const double *K4, long B,
+                     int C, int H, int W, int k)
+{
+    if (bad_shape(B, C, H, W, k, 0) || !x || !y || !K4)
+        return ORC_EINVAL;
+    long n = B * (long)C * H * W;
+    long ksz = (long)C * C * k * k;
+    double *t = (double *)malloc(sizeof(double) * (n > 0 ? n : 1));
+    if (!t)
+        return ORC_ENOMEM;
+    memcpy(t, y, sizeof(double) * n);
+    int rc = ORC_OK;
+    for (int q = 3; q >= 0 && rc == ORC_OK; --q) {
+        rc = orc_inverse(t, x, K4 + q * ksz, B, C, H, W, k, UNIT_ORDER[q]);
+        memcpy(t, x, sizeof(double) * n);
+    }
+    free(t);
+    return rc;
+}
+
+int orc_unit_logdet(const double *K4, int C, int k, int H, int W, double *out)
+{
+    if (!out || !K4)
+        return ORC_EINVAL;
+    long ksz = (long)C * C * k * k;
+    double s = 0.0;
+    int rc = ORC_OK;
+    for (int q = 0; q < 4; ++q) {
+        double v;
+        int r = orc_logdet(K4 + q * ksz, C, k, UNIT_ORDER[q], H, W, &v);
+        if (r == ORC_EINVAL)
+            return r;
+        if (r != ORC_OK)
+            rc = r;
+        s += v;
+    }
+    *out = s;
+    return rc;
+}
+
+/* ---- Multi-scale glue (Sec. 4.4). ----------------------------------------
+ * Actnorm: per-channel affine y = s * x + b (Glow's convention).
+ * Squeeze: (C, H, W) -> (4C, H/2, W/2), out[4c + 2dy + dx][i][j] =
+ *          in[c][2i + dy][2j + dx]; unsqueeze is its inverse.
+ * Split:   the first half of the channels goes on, the second half is the
+ *          latent; the inverse concatenates [h, z] on channels. */
+
+void orc_actnorm_forward(const double *x, double *y, const double *s,
+                         const double *b, long B, int C, int H, int W)
+{
+    for (long n = 0; n < B; ++n)
+        for (int c = 0; c < C; ++c)
+            for (long p = 0; p < (long)H * W; ++p) {
+                long o = (n * C + c) * (long)H * W + p;
+                y[o] = s[c] * x[o] + b[c];
+            }
+}
+
+void orc_actnorm_inverse(const double *y, double *x, const double *s,
+                         const double *b, long B, int C, int H, int W)
+{
+    for (long n = 0; n < B; ++n)
+        for (int c = 0; c < C; ++c)
+            for (long p = 0; p < (long)H * W; ++p) {
+                long o = (n * C + c) * (long)H * W + p;
+                x[o] = (y[o] - b[c]) / s[c];
+            }
+}
+
+void orc_squeeze(const double *in, double *out, long B, int C, int H, int W)
+{
+    int H2 = H / 2, W2 = W / 2;
+    for (long n = 0; n < B; ++n)
+        for (int c = 0; c < C; ++c)
+            for (int i = 0; i < H2; ++i)
+                for (int j = 0; j < W2; ++j)
+                    for (int dy = 0; dy < 2; ++dy)
+                        for (int dx = 0; dx < 2; ++dx) {
+                            int co = 4 * c + 2 * dy + dx;
+                            out[((n * 4 * C + co) * H2 + i) * W2 + j] =
+                                in[((n * C + c) * H + 2 * i + dy) * W + 2 * j + dx];
+                        }
+}
+
+void orc_unsqueeze(const double *in, double *out, long B, int C4, int H2, int W2)
+{
+    int C = C4 / 4, H = 2 * H2, W = 2 * W2;
+    for (long n = 0; n < B; ++n)
+        for (int c = 0; c < C; ++c)
+            for (int i = 0; i < H2; ++i)
+                for (int j = 0; j < W2; ++j)
+                    for (int dy = 0; dy < 2; ++dy)
+                        for (int dx = 0; dx < 2; ++dx) {
+                            int ci = 4 * c + 2 * dy + dx;
+                            out[((n * C + c) * H + 2 * i + dy) * W + 2 * j + dx] =
+                                in[((n * C4 + ci) * H2 + i) * W2 + j];
+                        }
+}
+
+/* Stack parameter layout shared with the Python wrapper:
+ *   K:     for level l = 0..L-1, unit u = 0..U-1, block q = 0..3:
+ *          C_l*C_l*k*k doubles, C_l = C1 << l.
+ *   scale, bias: for level l, unit u: C_l doubles.
+ *   z[l]:  l < L-1: (B, C_l/2, H_l, W_l); z[L-1]: (B, C_{L-1}, H, W) top.
+ *   x:     (B, C1, H1, W1). */
+static long stack_koff(int l, int U, int C1, int k)
+{
+    long off = 0;
+    for (int m = 0; m < l; ++m) {
+        long C = (long)C1 << m;
+        off += (long)U * 4 * C * C * k * k;
+    }
+    return off;
+}
+
+static long stack_soff(int l, int U, int C1)
+{
+    long off = 0;
+    for (int m = 0; m < l; ++m)
+        off += (long)U * ((long)C1 << m);
+    return off;
+}
+
+/* Forward direction of the stack: per level U x [unit, actnorm], then (not at
+ * the top) split and squeeze. */
+int orc_stack_forward(const double *x, double *const *z, const double *K,
+                      const double *scale, const double *bias, long B, int L,
+                      int U, int C1, int H1, int W1, int k)
+{
+    if (L < 1 || U < 0 || B < 0 || C1 < 1 || H1 < 1 || W1 < 1 || k < 1 || !x || !z)
+        return ORC_EINVAL;
+    if (((H1 | W1) & ((1 << (L - 1)) - 1)) || (L > 1 && (C1 & 1)))
+        return ORC_EINVAL;
+    long maxn = B * (long)C1 * H1 * W1;
+    double *h = (double *)malloc(sizeof(double) * (maxn > 0 ? maxn : 1));
+    double *t = (double *)malloc(sizeof(double) * (maxn > 0 ? maxn : 1));
+    if (!h || !t) {
+        free(h);
+        free(t);
+        return ORC_ENOMEM;
+    }
+    memcpy(h, x, sizeof(double) * maxn);
+    int rc = ORC_OK;
+    for (int l = 0; l < L && rc == ORC_OK; ++l) {
+        int C = C1 << l, H = H1 >> l, W = W1 >> l;
+        long n = B * (long)C * H * W;
+        long ksz = (long)C * C * k * k;
+        const double *Kl = K + stack_koff(l, U, C1, k);
+        const double *sl = scale + stack_soff(l, U, C1);
+        const double *bl = bias + stack_soff(l, U, C1);
+        for (int u = 0; u < U && rc == ORC_OK; ++u) {
+            rc = orc_unit_forward(h, t, Kl + (long)u * 4 * ksz, B, C, H, W, k);
+            orc_actnorm_forward(t, h, sl + (long)u * C, bl + (long)u * C, B, C, H, W);
+        }
+        if (rc != ORC_OK)
+            break;
+        if (l == L - 1) {
+            memcpy(z[l], h, sizeof(double) * n);
+            break;
+        }
+        int Ch = C / 2;
+        long hw = (long)H * W;
+        for (long b = 0; b < B; ++b) {
+            memcpy(t + b * Ch * hw, h + b * C * hw, sizeof(double) * Ch * hw);
+            memcpy(z[l] + b * Ch * hw, h + (b * C + Ch) * hw, sizeof(double) * Ch * hw);
+        }
+        orc_squeeze(t, h, B, Ch, H, W);
+    }
+    free(h);
+    free(t);
+    return rc;
+}
+
+/* Sampling direction: start from the top latent, per level U x [actnorm^-1,
+ * unit^-1] with the units in reverse, then unsqueeze and concatenate the
+ * level's latent behind it, down to (B, C1, H1, W1). */
+int orc_stack_inverse(const double *const *z, double *x, const double *K,
+                      const double *scale, const double *bias, long B, int L,
+                      int U, int C1, int H1, int W1, int k)
+{
+    if (L < 1 || U < 0 || B < 0 || C1 < 1 || H1 < 1 || W1 < 1 || k < 1 || !x || !z)
+        return ORC_EINVAL;
+    if (((H1 | W1) & ((1 << (L - 1)) - 1)) || (L > 1 && (C1 & 1)))
+        return ORC_EINVAL;
+    long maxn = B * (long)C1 * H1 * W1;
+    double *h = (double *)malloc(sizeof(double) * (maxn > 0 ? maxn : 1));
+    double *t = (double *)malloc(sizeof(double) * (maxn > 0 ? maxn : 1));
+    if (!h || !t) {
+        free(h);
+        free(t);
+        return ORC_ENOMEM;
+    }
+    int rc = ORC_OK;
+    {
+        int C = C1 << (L - 1), H = H1 >> (L - 1), W = W1 >> (L - 1);
+        memcpy(h, z[L - 1], sizeof(double) * B * (long)C * H * W);
+    }
+    for (int l = L - 1; l >= 0 && rc == ORC_OK; --l) {
+        int C = C1 << l, H = H1 >> l, W = W1 >> l;
+        long ksz = (long)C * C * k * k;
+        const double *Kl = K + stack_koff(l, U, C1, k);
+        const double *sl = scale + stack_soff(l, U, C1);
+        const double *bl = bias + stack_soff(l, U, C1);
+        for (int u = U - 1; u >= 0 && rc == ORC_OK; --u) {
+            orc_actnorm_inverse(h, t, sl + (long)u * C, bl + (long)u * C, B, C, H, W);
+            rc = orc_unit_inverse(t, h, Kl + (long)u * 4 * ksz, B, C, H, W, k);
+        }
+        if (rc != ORC_OK || l == 0)
+            break;
+        /* h: (B, C, H, W) at level l -> unsqueeze to (B, C/4, 2H, 2W), then
+         * concatenate the latent of level l-1 (B, C/4, 2H, 2W) behind it. */
+        int Cq = C / 4, H2 = 2 * H, W2 = 2 * W;
+        long hw = (long)H2 * W2;
+        orc_unsqueeze(h, t, B, C, H, W);
+        for (long b = 0; b < B; ++b) {
+            memcpy(h + b * 2 * Cq * hw, t + b * Cq * hw, sizeof(double) * Cq * hw);
+            memcpy(h + (b * 2 * Cq + Cq) * hw, z[l - 1] + b * Cq * hw,
+                   sizeof(double) * Cq * hw);
+        }
+    }
+    if (rc == ORC_OK)
+        memcpy(x, h, sizeof(double) * maxn);
+    free(h);
+    free(t);
+    return rc;
+}

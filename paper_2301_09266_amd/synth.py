@@ -1,0 +1,172 @@
+"""Seeded synthetic inputs for the masked k x k convolution, the FInC unit and
+the multi-scale sampling stack.
+
+This module only draws random numbers and lays them out; it holds none of the
+layer's arithmetic (no convolution, no solve, no determinant).  Both the HIP
+path and the CPU oracle are fed from here, so that every comparison runs on the
+same bits.
+
+Recipe (the paper trains on MNIST / CIFAR-10 / ImageNet / CelebA, Sec. 5 and
+the appendix "Datasets"; those images and any trained weights are replaced by
+tensors of the same shapes drawn here):
+
+* weights of one padded convolution block (Sec. 4.1, Alg. 1 input K of shape
+  (C, C, k, k)): every entry ~ N(0, 0.05^2), drawn for the full OIHW tensor in
+  C order; at the self tap (the kernel position that multiplies the output
+  pixel itself) the entries with c_in > c_out are set to zero (the channel mask)
+  and the diagonal K[c, c, self] is then set to 1 + U(-0.1, 0.1), c ascending.
+  Layer number l of a configuration (forward order) uses default_rng(1000 + l).
+* activations and latents ~ N(0, 1) from default_rng(0), in the order the
+  configuration lists them.
+* actnorm (Sec. 4.4) of level L, unit u: default_rng(2000 + 8 L + u);
+  scale = exp(N(0, 0.1^2)) per channel, then bias ~ N(0, 0.1^2) per channel.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+CORNERS = ("TL", "TR", "BL", "BR")
+CORNER_ID = {name: i for i, name in enumerate(CORNERS)}
+
+# The FInC unit applies its four padded blocks in this corner order
+# (Sec. 4.3; the order of the four corners is listed in Fig. 2a).
+UNIT_CORNERS = (0, 1, 2, 3)
+
+
+def self_tap(corner: int, k: int) -> tuple[int, int]:
+    """Kernel position (a, b) that multiplies the output pixel itself.
+
+    With k-1 zero rows/cols padded on the two named sides (Sec. 4.1,
+    corner paddings), the input pixel aligned with the output sits at the
+    kernel corner opposite to the padding: TL -> (k-1, k-1), TR -> (k-1, 0),
+    BL -> (0, k-1), BR -> (0, 0).
+    """
+    top = corner in (0, 1)
+    left = corner in (0, 2)
+    return (k - 1 if top else 0, k - 1 if left else 0)
+
+
+def masked_kernel(C: int, k: int, corner: int, seed: int) -> np.ndarray:
+    """One block's weights (C_out, C_in, k, k) as float64, recipe above."""
+    rng = np.random.default_rng(seed)
+    K = rng.normal(0.0, 0.05, size=(C, C, k, k))
+    sh, sw = self_tap(corner, k)
+    for co in range(C):
+        K[co, co + 1:, sh, sw] = 0.0
+    diag = 1.0 + rng.uniform(-0.1, 0.1, size=C)
+    for c in range(C):
+        K[c, c, sh, sw] = diag[c]
+    return K
+
+
+def unit_kernels(C: int, k: int, first_layer: int = 0) -> np.ndarray:
+    """Four blocks of one unit, stacked (4, C, C, k, k), corners TL, TR, BL, BR."""
+    return np.stack([masked_kernel(C, k, q, 1000 + first_layer + i)
+                     for i, q in enumerate(UNIT_CORNERS)])
+
+
+def actnorm_params(C: int, level: int, unit: int) -> tuple[np.ndarray, np.ndarray]:
+    rng = np.random.default_rng(2000 + 8 * level + unit)
+    scale = np.exp(rng.normal(0.0, 0.1, size=C))
+    bias = rng.normal(0.0, 0.1, size=C)
+    return scale, bias
+
+
+def gaussian(rng: np.random.Generator, shape) -> np.ndarray:
+    return rng.normal(0.0, 1.0, size=shape)
+
+
+def garbage_in_mask(K: np.ndarray, corner: int, seed: int = 7) -> np.ndarray:
+    """Copy of K whose masked entries (self tap, c_in > c_out) hold large junk.
+
+    The layer is defined for any buffer: those entries must be ignored.
+    """
+    K = np.array(K, copy=True)
+    C, k = K.shape[0], K.shape[-1]
+    sh, sw = self_tap(corner, k)
+    rng = np.random.default_rng(seed)
+    for co in range(C):
+        n = C - co - 1
+        if n:
+            K[co, co + 1:, sh, sw] = rng.uniform(-50.0, 50.0, size=n)
+    return K
+
+
+# ---------------------------------------------------------------------------
+# Workloads.  Shapes follow the paper's datasets after one 2x2 squeeze
+# (CIFAR-10 32x32x3 -> 16x16x12, ImageNet-64 64x64x3 -> 32x32x12, Sec. 4.4),
+# plus the small 8x8 case.  Each builder returns plain float64 arrays.
+# ---------------------------------------------------------------------------
+
+def layer_case(B: int, C: int, H: int, W: int, k: int, corner: int = 0,
+               seed: int = 0, layer: int = 0) -> dict:
+    rng = np.random.default_rng(seed)
+    x = gaussian(rng, (B, C, H, W))
+    z = gaussian(rng, (B, C, H, W))
+    K = masked_kernel(C, k, corner, 1000 + layer)
+    return dict(x=x, z=z, K=K, B=B, C=C, H=H, W=W, k=k, corner=corner)
+
+
+def unit_case(B: int, C: int, H: int, W: int, k: int, seed: int = 0) -> dict:
+    rng = np.random.default_rng(seed)
+    x = gaussian(rng, (B, C, H, W))
+    z = gaussian(rng, (B, C, H, W))
+    K4 = unit_kernels(C, k, 0)
+    return dict(x=x, z=z, K4=K4, B=B, C=C, H=H, W=W, k=k)
+
+
+def stack_case(B: int = 64, C1: int = 12, H1: int = 32, W1: int = 32,
+               levels: int = 3, units: int = 8, k: int = 3, seed: int = 0) -> dict:
+    """Multi-scale sampling stack: `levels` levels of `units` FInC units, each
+    unit followed by an actnorm; between levels the channels are split in
+    half and the rest squeezed (Sec. 4.4, Fig. 2c).
+
+    Latents: z[l] for l < levels-1 is the half split off at level l,
+    shape (B, C_l/2, H_l, W_l); z[levels-1] is the top, (B, C_top, H_top, W_top),
+    with C_l = C1 * 2**l and H_l = H1 / 2**l.  Draw order: top latent first,
+    then downwards (z[levels-1], ..., z[0]).
+    """
+    rng = np.random.default_rng(seed)
+    dims = [(C1 * 2 ** l, H1 >> l, W1 >> l) for l in range(levels)]
+    z = [None] * levels
+    for l in reversed(range(levels)):
+        C, H, W = dims[l]
+        cz = C if l == levels - 1 else C // 2
+        z[l] = gaussian(rng, (B, cz, H, W))
+    K = []      # K[l]: (units, 4, C, C, k, k)
+    scale = []  # scale[l]: (units, C)
+    bias = []
+    for l, (C, H, W) in enumerate(dims):
+        K.append(np.stack([unit_kernels(C, k, 32 * l + 4 * u) for u in range(units)]))
+        sb = [actnorm_params(C, l, u) for u in range(units)]
+        scale.append(np.stack([s for s, _ in sb]))
+        bias.append(np.stack([b for _, b in sb]))
+    x = gaussian(np.random.default_rng(seed + 1), (B, C1, H1, W1))
+    return dict(z=z, K=K, scale=scale, bias=bias, x=x, B=B, C1=C1, H1=H1, W1=W1,
+                levels=levels, units=units, k=k, dims=dims)
+
+
+# The five workloads, by what they are.
+WORKLOADS = {
+    "layer_c3_8x8_b1_k3": dict(kind="layer", B=1, C=3, H=8, W=8, k=3),
+    "layer_c12_16x16_b64_k3": dict(kind="layer", B=64, C=12, H=16, W=16, k=3),
+    "unit_c12_16x16_b256_k3": dict(kind="unit", B=256, C=12, H=16, W=16, k=3),
+    "unit_c48_8x8_b256_k3": dict(kind="unit", B=256, C=48, H=8, W=8, k=3),
+    "layer_c12_32x32_b64_k3": dict(kind="layer", B=64, C=12, H=32, W=32, k=3),
+    "layer_c12_32x32_b64_k5": dict(kind="layer", B=64, C=12, H=32, W=32, k=5),
+    "unit_c12_32x32_b64_k3": dict(kind="unit", B=64, C=12, H=32, W=32, k=3),
+    "unit_c12_32x32_b64_k5": dict(kind="unit", B=64, C=12, H=32, W=32, k=5),
+    "stack_3x8_c12_32x32_b64_k3": dict(kind="stack", B=64, C1=12, H1=32, W1=32,
+                                       levels=3, units=8, k=3),
+}
+
+
+def make(name: str, **override) -> dict:
+    spec = dict(WORKLOADS[name])
+    spec.update(override)
+    kind = spec.pop("kind")
+    if kind == "layer":
+        return layer_case(**spec)
+    if kind == "unit":
+        return unit_case(**spec)
+    return stack_case(**spec)

@@ -1,0 +1,433 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each pin takes an Oracle and raises AssertionError when it does not hold.
+The same functions are run against the real oracle (tests/test_oracle_pins.py,
+all must pass) and against deliberately broken builds of it
+(tests/test_oracle_mutations.py, at least one must fail per mutant), which
+shows that a dropped term, a wrong sign or index, or a transposed operand in
+the oracle cannot slip through.
+
+Nothing here calls the HIP path.
+"""
+from __future__ import annotations
+
+import os
+
+import numpy as np
+import scipy.linalg
+import scipy.signal
+import torch
+import torch.nn.functional as F
+
+from oracle import _p
+from paper_2301_09266_amd import synth
+
+# Written out here independently of the oracle and of synth: which kernel
+# position multiplies the output pixel itself, and which sides are padded,
+# for the four corner paddings of Sec. 4.1 (k-1 rows/cols on two sides).
+SELF = {0: lambda k: (k - 1, k - 1), 1: lambda k: (k - 1, 0),
+        2: lambda k: (0, k - 1), 3: lambda k: (0, 0)}
+# torch F.pad order (left, right, top, bottom)
+PADS = {0: lambda k: (k - 1, 0, k - 1, 0), 1: lambda k: (0, k - 1, k - 1, 0),
+        2: lambda k: (k - 1, 0, 0, k - 1), 3: lambda k: (0, k - 1, 0, k - 1)}
+
+
+def masked(K, corner):
+    """Zero the channel-masked entries (self tap, c_in > c_out)."""
+    K = np.array(K, copy=True)
+    sh, sw = SELF[corner](K.shape[-1])
+    C = K.shape[0]
+    for co in range(C):
+        K[co, co + 1:, sh, sw] = 0.0
+    return K
+
+
+def torch_conv(x, K, corner):
+    """Library route: zero-pad the two corner sides, then conv2d (fp64)."""
+    xt = torch.from_numpy(np.ascontiguousarray(x))
+    Kt = torch.from_numpy(np.ascontiguousarray(masked(K, corner)))
+    return F.conv2d(F.pad(xt, PADS[corner](K.shape[-1])), Kt).numpy()
+
+
+def raster_perm(C, H, W, corner):
+    """NCHW flat indices listed in the corner's pixel-major raster order."""
+    rows = range(H) if corner in (0, 1) else range(H - 1, -1, -1)
+    cols = list(range(W)) if corner in (0, 2) else list(range(W - 1, -1, -1))
+    return np.array([c * H * W + i * W + j for i in rows for j in cols for c in range(C)])
+
+
+def dense_jacobian(fwd, C, H, W):
+    """Columns = fwd applied to every basis vector of one (C, H, W) image."""
+    n = C * H * W
+    basis = np.eye(n).reshape(n, C, H, W)
+    return fwd(basis).reshape(n, n).T
+
+
+def rand_kernel(rng, C, k, corner, diag=(0.6, 1.4)):
+    K = rng.normal(0.0, 0.3, size=(C, C, k, k))
+    sh, sw = SELF[corner](k)
+    for c in range(C):
+        K[c, c, sh, sw] = rng.uniform(*diag) * rng.choice([-1.0, 1.0])
+    return K
+
+
+def close(a, b, tol, what):
+    err = float(np.max(np.abs(np.asarray(a) - np.asarray(b)))) if np.size(a) else 0.0
+    assert err <= tol, f"{what}: max abs err {err:.3e} > {tol:.1e}"
+
+
+# --------------------------------------------------------------------------
+# Forward (Sec. 3 conv equation, Sec. 4.1 corner paddings)
+# --------------------------------------------------------------------------
+
+def pin_forward_conv2d(o):
+    """Forward = torch conv2d of the corner-padded input with the masked
+    kernel, for all corners, k in {1,2,3,5}, H != W; masked entries of the
+    buffer hold junk that must be ignored."""
+    rng = np.random.default_rng(11)
+    for corner in range(4):
+        for (C, H, W, k) in [(3, 5, 7, 3), (2, 6, 4, 2), (4, 3, 3, 1), (2, 7, 6, 5)]:
+            x = rng.normal(size=(2, C, H, W))
+            K = rand_kernel(rng, C, k, corner)
+            Kj = synth.garbage_in_mask(K, corner, seed=corner + 3)
+            close(o.forward(x, Kj, corner), torch_conv(x, K, corner), 1e-12,
+                  f"forward vs conv2d corner={corner} k={k}")
+
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def fig1_matrix(w):
+    """Fig. 1's symbolic convolution matrix from tests/golden, filled with w."""
+    rows = []
+    for line in open(os.path.join(GOLDEN, "fig1_tl_3x3_k2.txt")):
+        line = line.split("#", 1)[0].split()
+        if line:
+            rows.append([0.0 if t == "0" else w[t] for t in line])
+    return np.array(rows)
+
+
+def pin_fig1_matrix(o):
+    """Fig. 1 setting: 3x3 image, 2x2 filter, TL padding, one channel.  The
+    dense Jacobian of the forward equals the matrix written out in the
+    golden fixture, and the inverse solves it."""
+    w = dict(w00=0.3, w01=-0.7, w10=1.9, w11=1.25)
+    K = np.array([[[[w["w00"], w["w01"]], [w["w10"], w["w11"]]]]])
+    M = fig1_matrix(w)
+    J = dense_jacobian(lambda b: o.forward(b, K, 0), 1, 3, 3)
+    close(J, M, 1e-15, "Fig. 1 convolution matrix")
+    y = np.arange(1.0, 10.0).reshape(1, 1, 3, 3)
+    close(o.inverse(y, K, 0).ravel(), np.linalg.solve(M, y.ravel()), 1e-13,
+          "Fig. 1 inverse")
+
+
+def pin_jacobian_triangular(o):
+    """The convolution matrix is lower triangular in the corner's pixel-major
+    raster order with diagonal K[c, c, self] (Fig. 1 caption; Sec. 3)."""
+    rng = np.random.default_rng(12)
+    for corner in range(4):
+        for (C, H, W, k) in [(3, 4, 5, 3), (2, 5, 3, 2)]:
+            K = synth.garbage_in_mask(rand_kernel(rng, C, k, corner), corner)
+            J = dense_jacobian(lambda b: o.forward(b, K, corner), C, H, W)
+            P = raster_perm(C, H, W, corner)
+            Jp = J[np.ix_(P, P)]
+            assert np.count_nonzero(np.triu(Jp, 1)) == 0, f"not triangular, corner {corner}"
+            sh, sw = SELF[corner](k)
+            want = np.tile([K[c, c, sh, sw] for c in range(C)], H * W)
+            close(np.diag(Jp), want, 0.0, f"diagonal corner {corner}")
+
+
+# --------------------------------------------------------------------------
+# log|det| (Table 1: Jacobian 1 for unit diagonal; triangular M)
+# --------------------------------------------------------------------------
+
+def pin_logdet_slogdet(o):
+    """Closed form = numpy slogdet of the dense Jacobian, all corners,
+    including the 8x8x3 workload and negative diagonal entries."""
+    rng = np.random.default_rng(13)
+    cases = [(3, 8, 8, 3, synth.masked_kernel(3, 3, 0, 1000), 0)]
+    for corner in range(4):
+        cases.append((2, 3, 4, 3, rand_kernel(rng, 2, 3, corner), corner))
+    for (C, H, W, k, K, corner) in cases:
+        J = dense_jacobian(lambda b: o.forward(b, K, corner), C, H, W)
+        sign, ld = np.linalg.slogdet(J)
+        close(o.logdet(K, corner, H, W), ld, 1e-9 * max(1.0, abs(ld)),
+              f"logdet corner {corner}")
+    # unit diagonal (the CInC masking of the paper): log|det| = 0
+    K = rand_kernel(rng, 3, 3, 0)
+    for c in range(3):
+        K[c, c, 2, 2] = 1.0
+    close(o.logdet(K, 0, 5, 6), 0.0, 0.0, "unit diagonal logdet")
+
+
+def pin_logdet_singular(o):
+    """A zero diagonal entry is reported (status -2) with -inf."""
+    K = rand_kernel(np.random.default_rng(5), 2, 3, 1)
+    K[1, 1, 2, 0] = 0.0
+    out = np.zeros(1)
+    code = o.lib.orc_logdet(_p(K), 2, 3, 1, 4, 4, _p(out))
+    assert code == -2 and out[0] == -np.inf, (code, out[0])
+
+
+# --------------------------------------------------------------------------
+# Inverse
+# --------------------------------------------------------------------------
+
+def pin_inverse_dense_solve(o):
+    """Inverse = numpy.linalg.solve(J, y) on tiny shapes, all corners, junk in
+    the masked entries."""
+    rng = np.random.default_rng(14)
+    for corner in range(4):
+        for (C, H, W, k) in [(3, 4, 5, 3), (2, 3, 3, 2), (2, 5, 4, 4)]:
+            K = synth.garbage_in_mask(rand_kernel(rng, C, k, corner), corner)
+            J = dense_jacobian(lambda b: o.forward(b, K, corner), C, H, W)
+            y = rng.normal(size=(1, C, H, W))
+            want = np.linalg.solve(J, y.ravel())
+            close(o.inverse(y, K, corner).ravel(), want, 1e-10,
+                  f"inverse vs solve corner {corner}")
+
+
+def pin_inverse_triangular_solve(o, big: bool = False):
+    """Inverse = scipy solve_triangular on the raster-permuted Jacobian of the
+    8x8x3 workload (and, with big=True, one 16x16x12 image)."""
+    shapes = [(3, 8, 8, 3)] + ([(12, 16, 16, 3)] if big else [])
+    for (C, H, W, k) in shapes:
+        for corner in range(4):
+            K = synth.masked_kernel(C, k, corner, 1000)
+            J = dense_jacobian(lambda b: o.forward(b, K, corner), C, H, W)
+            P = raster_perm(C, H, W, corner)
+            y = np.random.default_rng(corner).normal(size=(1, C, H, W))
+            xp = scipy.linalg.solve_triangular(J[np.ix_(P, P)], y.ravel()[P], lower=True)
+            want = np.empty_like(xp)
+            want[P] = xp
+            close(o.inverse(y, K, corner).ravel(), want, 1e-10,
+                  f"inverse vs solve_triangular C={C} corner {corner}")
+
+
+def pin_round_trip(o):
+    rng = np.random.default_rng(15)
+    for corner in range(4):
+        x = rng.normal(size=(3, 5, 9, 7))
+        K = synth.masked_kernel(5, 3, corner, 1000 + corner)
+        close(o.inverse(o.forward(x, K, corner), K, corner), x, 1e-12,
+              f"round trip corner {corner}")
+        close(o.forward(o.inverse(x, K, corner), K, corner), x, 1e-12,
+              f"reverse round trip corner {corner}")
+
+
+def pin_k1_pixelwise(o):
+    """k = 1: the layer is a per-pixel lower-triangular C x C map; the
+    inverse is a per-pixel triangular solve (torch.linalg.solve_triangular)."""
+    rng = np.random.default_rng(16)
+    C = 5
+    for corner in range(4):
+        K = rand_kernel(rng, C, 1, corner)
+        L = np.tril(K[:, :, 0, 0])
+        y = rng.normal(size=(2, C, 3, 4))
+        yt = torch.from_numpy(y.transpose(0, 2, 3, 1).reshape(-1, C, 1).copy())
+        want = torch.linalg.solve_triangular(torch.from_numpy(L), yt, upper=False)
+        want = want.numpy().reshape(2, 3, 4, C).transpose(0, 3, 1, 2)
+        close(o.inverse(y, K, corner), want, 1e-12, "k=1 triangular solve")
+        close(o.forward(want, K, corner), y, 1e-12, "k=1 forward")
+
+
+def pin_impulse_geometric(o):
+    """Self block = identity, one off-self tap of weight w: an impulse at the
+    corner's first pixel inverts to (-w)^m at m times the tap's back-offset
+    and zero elsewhere (closed form of the geometric recursion)."""
+    H, W, k, w = 9, 8, 3, -0.8
+    for corner in range(4):
+        sh, sw = SELF[corner](k)
+        for (a, b) in [(0, 0), (0, 1), (1, 2), (2, 1), (1, 1), (2, 0)]:
+            if (a, b) == (sh, sw):
+                continue
+            K = np.zeros((1, 1, k, k))
+            K[0, 0, sh, sw] = 1.0
+            K[0, 0, a, b] = w
+            i0 = 0 if corner in (0, 1) else H - 1
+            j0 = 0 if corner in (0, 2) else W - 1
+            di, dj = sh - a, sw - b           # output minus source position
+            y = np.zeros((1, 1, H, W))
+            y[0, 0, i0, j0] = 1.0
+            want = np.zeros((H, W))
+            m = 0
+            while 0 <= i0 + m * di < H and 0 <= j0 + m * dj < W:
+                want[i0 + m * di, j0 + m * dj] = (-w) ** m
+                m += 1
+            close(o.inverse(y, K, corner)[0, 0], want, 1e-14,
+                  f"impulse corner {corner} tap {(a, b)}")
+
+
+def pin_row_lfilter(o):
+    """One row, one channel (H = 1): the layer is a causal FIR filter along
+    the row; its inverse is the IIR filter of scipy.signal.lfilter."""
+    rng = np.random.default_rng(17)
+    for corner in range(4):
+        k, W = 4, 23
+        K = rng.normal(0.0, 0.3, size=(1, 1, k, k))
+        sh, sw = SELF[corner](k)
+        K[0, 0, sh, sw] = 1.3
+        y = rng.normal(size=(1, 1, 1, W))
+        row = K[0, 0, sh]                       # only the self row stays in the image
+        if corner in (0, 2):                    # left padded: reads j-(k-1)..j
+            den = row[::-1]
+            want = scipy.signal.lfilter([1.0], den, y[0, 0, 0])
+        else:                                   # right padded: reads j..j+k-1
+            den = row
+            want = scipy.signal.lfilter([1.0], den, y[0, 0, 0][::-1])[::-1]
+        close(o.inverse(y, K, corner)[0, 0, 0], want, 1e-12, f"lfilter corner {corner}")
+
+
+def _flip(a, corner):
+    """Axes flipped to bring a corner to TL (Sec. 4.1, last paragraph)."""
+    axes = {0: (), 1: (-1,), 2: (-2,), 3: (-2, -1)}[corner]
+    return np.flip(a, axis=axes) if axes else a
+
+
+def pin_flip_equivalence(o):
+    """Padded inputs of TR/BL/BR equal TL after flipping (Sec. 4.1):
+    corner(x, K) = flip(TL(flip x, flip K)) for forward and inverse."""
+    rng = np.random.default_rng(18)
+    for corner in (1, 2, 3):
+        x = rng.normal(size=(2, 3, 6, 5))
+        K = rand_kernel(rng, 3, 3, corner)
+        Kf = _flip(K, corner)
+        close(o.forward(x, K, corner), _flip(o.forward(_flip(x, corner), Kf, 0), corner),
+              1e-13, f"flip forward {corner}")
+        close(o.inverse(x, K, corner), _flip(o.inverse(_flip(x, corner), Kf, 0), corner),
+              1e-12, f"flip inverse {corner}")
+
+
+def wavefront_inverse_tl(Y, K):
+    """Algorithm 1 evaluated diagonal by diagonal in numpy (TL block): at
+    diagonal d every pixel with h + w = d is updated at once from the pixels
+    at back-offsets (kh, kw) through K[c, kc, k-1-kh, k-1-kw]; within the
+    pixel itself only the already solved channels kc < c count, then the
+    division by the self weight (channel mask, Sec. 4.1)."""
+    C, H, W = Y.shape
+    k = K.shape[-1]
+    X = np.zeros_like(Y)
+    for d in range(H + W - 1):
+        hs = np.arange(max(0, d - W + 1), min(d, H - 1) + 1)
+        ws = d - hs
+        for c in range(C):
+            r = Y[c, hs, ws].copy()
+            for kh in range(k):
+                for kw_ in range(k):
+                    sh, sw = hs - kh, ws - kw_
+                    ok = (sh >= 0) & (sw >= 0)
+                    kcs = range(c) if (kh, kw_) == (0, 0) else range(C)
+                    for kc in kcs:
+                        r[ok] -= X[kc, sh[ok], sw[ok]] * K[c, kc, k - 1 - kh, k - 1 - kw_]
+            X[c, hs, ws] = r / K[c, c, k - 1, k - 1]
+    return X
+
+
+def pin_wavefront_schedule(o):
+    """Theorem 1: the diagonal schedule gives the same inverse as the raster
+    order; steps = H + W - 1 (Theorem 2)."""
+    rng = np.random.default_rng(19)
+    for (C, H, W, k) in [(3, 8, 8, 3), (4, 5, 9, 3), (2, 7, 4, 5)]:
+        K = rand_kernel(rng, C, k, 0)
+        y = rng.normal(size=(1, C, H, W))
+        close(o.inverse(y, K, 0)[0], wavefront_inverse_tl(y[0], K), 1e-11,
+              f"wavefront schedule {(C, H, W, k)}")
+
+
+# --------------------------------------------------------------------------
+# FInC unit (Sec. 4.3, four blocks in sequence: TL, TR, BL, BR)
+# --------------------------------------------------------------------------
+
+def pin_unit_dense(o):
+    """Unit Jacobian = product of the four layer Jacobians; forward, inverse
+    (dense solve) and logdet (slogdet) of the unit agree with it."""
+    rng = np.random.default_rng(20)
+    C, H, W, k = 2, 4, 3, 3
+    K4 = np.stack([rand_kernel(rng, C, k, q) for q in range(4)])
+    Js = [dense_jacobian(lambda b, q=q: o.forward(b, K4[q], q), C, H, W) for q in range(4)]
+    Ju = Js[3] @ Js[2] @ Js[1] @ Js[0]
+    x = rng.normal(size=(1, C, H, W))
+    close(o.unit_forward(x, K4).ravel(), Ju @ x.ravel(), 1e-12, "unit forward")
+    y = rng.normal(size=(1, C, H, W))
+    close(o.unit_inverse(y, K4).ravel(), np.linalg.solve(Ju, y.ravel()), 1e-10, "unit inverse")
+    close(o.unit_logdet(K4, H, W), np.linalg.slogdet(Ju)[1], 1e-9, "unit logdet")
+
+
+def pin_unit_round_trip(o):
+    rng = np.random.default_rng(21)
+    for k in (3, 5):
+        K4 = synth.unit_kernels(6, k)
+        x = rng.normal(size=(2, 6, 9, 8))
+        close(o.unit_inverse(o.unit_forward(x, K4), K4), x, 1e-12, f"unit round trip k={k}")
+
+
+# --------------------------------------------------------------------------
+# Multi-scale glue (Sec. 4.4)
+# --------------------------------------------------------------------------
+
+def pin_squeeze_reshape(o):
+    """Squeeze = reshape/transpose route: channel 4c + 2dy + dx holds the
+    (dy, dx) sub-grid of channel c; unsqueeze inverts it."""
+    rng = np.random.default_rng(22)
+    x = rng.normal(size=(2, 3, 6, 8))
+    B, C, H, W = x.shape
+    want = x.reshape(B, C, H // 2, 2, W // 2, 2).transpose(0, 1, 3, 5, 2, 4).reshape(
+        B, 4 * C, H // 2, W // 2)
+    close(o.squeeze(x), want, 0.0, "squeeze")
+    close(o.unsqueeze(want), x, 0.0, "unsqueeze")
+
+
+def pin_actnorm(o):
+    rng = np.random.default_rng(23)
+    x = rng.normal(size=(2, 4, 3, 5))
+    s, b = np.exp(rng.normal(size=4)), rng.normal(size=4)
+    y = o.actnorm_forward(x, s, b)
+    close(y, x * s[None, :, None, None] + b[None, :, None, None], 1e-15, "actnorm forward")
+    close(o.actnorm_inverse(y, s, b), x, 1e-14, "actnorm inverse")
+
+
+def _compose_stack_inverse(o, z, K, scale, bias, levels, units):
+    """The sampling direction assembled here from the pinned pieces."""
+    h = z[levels - 1]
+    for l in reversed(range(levels)):
+        for u in reversed(range(units)):
+            s, b = scale[l][u], bias[l][u]
+            h = (h - b[None, :, None, None]) / s[None, :, None, None]
+            h = o.unit_inverse(h, K[l][u])
+        if l:
+            B, C4, H2, W2 = h.shape
+            h = h.reshape(B, C4 // 4, 2, 2, H2, W2).transpose(0, 1, 4, 2, 5, 3).reshape(
+                B, C4 // 4, 2 * H2, 2 * W2)
+            h = np.concatenate([h, z[l - 1]], axis=1)
+    return h
+
+
+def pin_stack(o):
+    """Stack inverse = composition of the pinned pieces, and it inverts the
+    stack forward (split keeps the first half, Sec. 4.4)."""
+    case = synth.stack_case(B=2, C1=4, H1=8, W1=8, levels=3, units=2, k=3)
+    a = dict(levels=3, units=2, k=3)
+    x = o.stack_inverse(case["z"], case["K"], case["scale"], case["bias"], C1=4, H1=8,
+                        W1=8, **a)
+    want = _compose_stack_inverse(o, case["z"], case["K"], case["scale"], case["bias"], 3, 2)
+    close(x, want, 1e-12, "stack inverse vs composition")
+    z2 = o.stack_forward(x, case["K"], case["scale"], case["bias"], **a)
+    for l in range(3):
+        close(z2[l], case["z"][l], 1e-10, f"stack round trip latent {l}")
+    # the first half of the channels goes on: latents of level 0 are channels C/2..C
+    xin = case["x"][:, :4, :8, :8]
+    zf = o.stack_forward(xin, case["K"], case["scale"], case["bias"], **a)
+    h = xin
+    for u in range(2):
+        h = o.unit_forward(h, case["K"][0][u])
+        h = o.actnorm_forward(h, case["scale"][0][u], case["bias"][0][u])
+    close(zf[0], h[:, 2:], 1e-12, "split keeps the first half")
+
+
+ALL_PINS = [
+    pin_forward_conv2d, pin_fig1_matrix, pin_jacobian_triangular, pin_logdet_slogdet,
+    pin_logdet_singular, pin_inverse_dense_solve, pin_inverse_triangular_solve,
+    pin_round_trip, pin_k1_pixelwise, pin_impulse_geometric, pin_row_lfilter,
+    pin_flip_equivalence, pin_wavefront_schedule, pin_unit_dense, pin_unit_round_trip,
+    pin_squeeze_reshape, pin_actnorm, pin_stack,
+]

@@ -1,0 +1,77 @@
+"""Plant plausible mistakes in copies of the oracle (on the CPU) and check
+that the pins catch every one of them."""
+import os
+
+import pytest
+
+import oracle
+import pins
+
+# (label, text in finc_oracle.c, replacement, which occurrence (0-based))
+MUTANTS = [
+    ("forward reads the mirrored tap",
+     "int ii = i + a - oh, jj = j + b - ow;", "int ii = i - a + oh, jj = j + b - ow;", 0),
+    ("forward drops the self diagonal", "if (a == oh && b == ow && ci > co)",
+     "if (a == oh && b == ow && ci >= co)", 0),
+    ("forward keeps the masked entries", "if (a == oh && b == ow && ci > co)",
+     "if (a == oh && b == ow && ci > co + C)", 0),
+    ("forward transposes channels", "s += kmasked(K, C, k, oh, ow, co, ci, a, b)",
+     "s += kmasked(K, C, k, oh, ow, ci, co, a, b)", 0),
+    ("inverse reads the mirrored column",
+     "int ii = i + a - oh, jj = j + b - ow;", "int ii = i + a - oh, jj = j - b + ow;", 1),
+    ("inverse counts the diagonal twice", "int cmax = self ? c : C;",
+     "int cmax = self ? c + 1 : C;", 0),
+    ("inverse drops the self block", "int cmax = self ? c : C;",
+     "int cmax = self ? 0 : C;", 0),
+    ("inverse adds instead of subtracting", "r -= kw(K, C, k, c, ci, a, b)",
+     "r += kw(K, C, k, c, ci, a, b)", 0),
+    ("inverse transposes channels", "r -= kw(K, C, k, c, ci, a, b)",
+     "r -= kw(K, C, k, ci, c, a, b)", 0),
+    ("inverse skips the divide", "= r / kw(K, C, k, c, c, oh, ow);", "= r;", 0),
+    ("inverse walks rows the wrong way", "int rows_down = (corner == 0 || corner == 1);",
+     "int rows_down = (corner == 0 || corner == 2);", 0),
+    ("logdet forgets W", "*out = (double)H * (double)W * s;", "*out = (double)H * s;", 0),
+    ("logdet reads the wrong tap", "double d = kw(K, C, k, c, c, oh, ow);",
+     "double d = kw(K, C, k, c, c, ow, oh);", 0),
+    ("corner offsets swapped", "*ow = (corner == 0 || corner == 2) ? k - 1 : 0;",
+     "*ow = (corner == 0 || corner == 1) ? k - 1 : 0;", 0),
+    ("unit inverse runs the blocks forwards",
+     "for (int q = 3; q >= 0 && rc == ORC_OK; --q)",
+     "for (int q = 0; q < 4 && rc == ORC_OK; ++q)", 0),
+    ("squeeze swaps dy and dx", "int co = 4 * c + 2 * dy + dx;",
+     "int co = 4 * c + dy + 2 * dx;", 0),
+    ("actnorm inverse subtracts after scaling", "x[o] = (y[o] - b[c]) / s[c];",
+     "x[o] = y[o] / s[c] - b[c];", 0),
+    ("stack inverse runs units forwards",
+     "for (int u = U - 1; u >= 0 && rc == ORC_OK; --u)",
+     "for (int u = 0; u < U && rc == ORC_OK; ++u)", 0),
+    ("stack inverse concatenates latent first",
+     "memcpy(h + b * 2 * Cq * hw, t + b * Cq * hw, sizeof(double) * Cq * hw);",
+     "memcpy(h + (b * 2 * Cq + Cq) * hw, t + b * Cq * hw, sizeof(double) * Cq * hw);", 0),
+]
+
+
+def _mutate(src: str, old: str, new: str, nth: int) -> str:
+    pos = -1
+    for _ in range(nth + 1):
+        pos = src.index(old, pos + 1)
+    return src[:pos] + new + src[pos + len(old):]
+
+
+@pytest.mark.parametrize("label,old,new,nth", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_mutant(tmp_path, label, old, new, nth):
+    src = open(oracle.SRC).read()
+    mutated = _mutate(src, old, new, nth)
+    assert mutated != src
+    cpath = os.path.join(tmp_path, "mutant.c")
+    open(cpath, "w").write(mutated)
+    lib = oracle.build(src=cpath, out=os.path.join(tmp_path, "libmutant.so"))
+    o = oracle.Oracle(lib)
+    failed = []
+    for pin in pins.ALL_PINS:
+        try:
+            pin(o)
+        except (AssertionError, oracle.OracleError) as e:
+            failed.append((pin.__name__, str(e)[:80]))
+            break
+    assert failed, f"no pin caught mutant: {label}"

@@ -1,0 +1,258 @@
+"""Throughput of the FInC masked-conv hot path on one MI355X.
+
+A step is one pass of the whole path over one batch: weight preparation
+(L^-1 and L^-1 K_s), the forward masked convolution, log|det| and the
+diagonal-wavefront inverse of the forward's output.  The default workload is
+the single masked 3x3 layer, TL padding, batch 64, 12 channels, 16x16 (a
+CIFAR-10 image after one 2x2 squeeze), fp32.
+
+Prints one JSON line.  `value` is sampled images per second through the
+step; `roofline` is for the inverse kernel (the dominant one): algorithmic
+bytes (read y + write x + the layer's weights) per launch over its mean
+duration, timed with HIP events on the stream it runs on; `cpu_baseline`
+times the CPU oracle on a bounded sample of the same step.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0         # MI355X HBM3E
+FP32_VALU_PEAK_TFLOPS = 157.3
+METRIC = "masked-conv inverse: images/sec & achieved HBM GB/s (fp32, k=3, batch 64)"
+KERNEL_SRC = os.path.join(ROOT, "paper_2301_09266_amd", "csrc", "finc.hip")
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=400)
+    p.add_argument("--warmup", type=int, default=40)
+    p.add_argument("--workload", default="layer_c12_16x16_b64_k3")
+    p.add_argument("--cpu-seconds", type=float, default=10.0,
+                   help="bound on the CPU-oracle sample (0 disables it)")
+    p.add_argument("--no-graph", action="store_true",
+                   help="launch every step eagerly instead of replaying a HIP graph")
+    return p.parse_args()
+
+
+def kernel_hash() -> str:
+    return hashlib.sha256(open(KERNEL_SRC, "rb").read()).hexdigest()[:16]
+
+
+def traffic_for(workload: str):
+    """HBM bytes per inverse launch from committed rocprofv3 counter runs,
+    only if they were taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel_sha") != kernel_hash():
+        return None
+    return rec.get("bytes_per_launch")
+
+
+class LayerStep:
+    """prepare + forward + logdet + inverse of one padded masked conv block."""
+
+    def __init__(self, case, dev):
+        import numpy as np
+        import torch
+
+        from paper_2301_09266_amd import finc
+
+        self.finc = finc
+        self.B, self.C, self.H, self.W, self.k = (case[n] for n in "BCHWk")
+        self.corner = case["corner"]
+        self.x = torch.from_numpy(case["x"].astype(np.float32)).to(dev)
+        self.K = torch.from_numpy(case["K"].astype(np.float32)).to(dev)
+        self.y = torch.empty_like(self.x)
+        self.xr = torch.empty_like(self.x)
+        self.ld = torch.empty(1, dtype=torch.float64, device=dev)
+        self.prep = torch.empty(finc.workspace_bytes(self.C, self.k, 1), dtype=torch.uint8,
+                                device=dev)
+        self.case = case
+
+    def prepare(self):
+        self.finc.prepare(self.K, [self.corner], out=self.prep)
+
+    def forward(self):
+        self.finc.forward(self.x, self.K, self.corner, out=self.y)
+        self.finc.logdet(self.K, self.corner, self.H, self.W, out=self.ld)
+
+    def inverse(self):
+        self.finc.inverse_prepared(self.y, self.prep, self.k, self.corner, out=self.xr)
+
+    def step(self):
+        self.prepare()
+        self.forward()
+        self.inverse()
+
+    def inverse_bytes(self):
+        return 2 * self.B * self.C * self.H * self.W * 4 + self.C * self.C * self.k ** 2 * 4
+
+    def inverse_flops(self):
+        C, k = self.C, self.k
+        return 2 * self.B * self.H * self.W * (C * C * k * k - C * (C - 1) // 2)
+
+    def steps_per_inverse(self):
+        return self.H + self.W - 1
+
+    def pixels(self):
+        return self.B * self.H * self.W
+
+    def cpu_step(self, orc, imgs):
+        import numpy as np
+
+        x = self.case["x"][imgs].astype(np.float32).astype(np.float64)
+        K = self.case["K"].astype(np.float32).astype(np.float64)
+        y = orc.forward(x, K, self.corner)
+        orc.logdet(K, self.corner, self.H, self.W)
+        orc.inverse(y, K, self.corner)
+
+
+def cpu_baseline(step, seconds: float):
+    """The oracle, single-threaded, on whole batches of the same step until
+    `seconds` of CPU time have been spent (at least one image)."""
+    import oracle
+
+    orc = oracle.default()
+    B = step.B
+    done = 0
+    t0 = time.perf_counter()
+    while True:
+        n = min(B, 8)
+        imgs = [(done + i) % B for i in range(n)]
+        step.cpu_step(orc, imgs)
+        done += n
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    return dict(value=done / el, unit="images/s", cores=1, kind="oracle",
+                sample=f"{done} images of the same step (forward, logdet, raster-order "
+                       f"inverse) in fp64, {el:.1f} s, one thread")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the path shards by "
+              "batch with no communication, so one GPU's throughput is the figure.",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2301_09266_amd import finc, synth
+
+    finc.lib()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    case = synth.make(args.workload)
+    if "K" not in case:
+        print("bench.py times single-layer workloads", file=sys.stderr)
+        sys.exit(2)
+    st = LayerStep(case, dev)
+
+    stream = torch.cuda.current_stream()
+    for _ in range(args.warmup):
+        st.step()
+    torch.cuda.synchronize()
+
+    graph = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            st.step()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            st.step()
+        torch.cuda.synchronize()
+        for _ in range(3):
+            graph.replay()
+        torch.cuda.synchronize()
+
+    # timed region: exactly `steps` steps
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for _ in range(args.steps):
+        if graph is not None:
+            graph.replay()
+        else:
+            st.step()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_total = t_start.elapsed_time(t_end)
+    ms_per_step = ms_total / args.steps
+
+    # the dominant kernel alone: HIP events around every launch on its stream
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    for a, b in ev:
+        a.record(stream)
+        st.inverse()
+        b.record(stream)
+    torch.cuda.synchronize()
+    inv_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+
+    # correctness guard on what was timed
+    err = float((st.xr - st.x).abs().max())
+    if not err <= 1e-4:
+        print(f"round-trip error {err:.3e} exceeds 1e-4", file=sys.stderr)
+        sys.exit(1)
+
+    achieved = st.inverse_bytes() / (inv_ms * 1e-3) / 1e9
+    traffic = traffic_for(args.workload)
+    out = {
+        "metric": METRIC,
+        "value": st.B / (ms_per_step * 1e-3),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": args.workload, "B": st.B, "C": st.C, "H": st.H, "W": st.W,
+                   "k": st.k, "corner": "TL", "graph": graph is not None,
+                   "step": "prepare + forward + logdet + inverse"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "inverse_chain_kernel",
+                     "alg_bytes_per_launch": st.inverse_bytes(),
+                     "mean_launch_us": inv_ms * 1e3},
+        "inverse": {
+            "images_per_s": st.B / (inv_ms * 1e-3),
+            "pixels_per_s": st.pixels() / (inv_ms * 1e-3),
+            "us_per_diagonal_step": inv_ms * 1e3 / st.steps_per_inverse(),
+            "fp32_tflops": st.inverse_flops() / (inv_ms * 1e-3) / 1e12,
+            "fp32_frac": st.inverse_flops() / (inv_ms * 1e-3) / 1e12 / FP32_VALU_PEAK_TFLOPS,
+        },
+        "wall_s_timed": wall,
+        "round_trip_max_abs": err,
+    }
+    if args.cpu_seconds > 0:
+        out["cpu_baseline"] = cpu_baseline(st, args.cpu_seconds)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

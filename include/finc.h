@@ -1,0 +1,162 @@
+/*
+ * finc.h -- C ABI of the MI355X (gfx950) FInC Flow masked k x k convolution.
+ *
+ * The layer (Sec. 3 "Invertible Convolutions", Sec. 4.1 "Convolution
+ * Design"): y = K * pad_corner(x), a cross-correlation of the input padded
+ * with k-1 zero rows and columns on two sides (the "corner"), so output pixel
+ * (i, j) reads input (i + a - oh, j + b - ow) for kernel position (a, b):
+ *     TL (oh, ow) = (k-1, k-1)   TR (k-1, 0)   BL (0, k-1)   BR (0, 0).
+ * Kernel position (oh, ow) multiplies the output pixel itself (the "self
+ * tap"); there only channels c_in <= c_out are used (lower-triangular channel
+ * block), every other position is used in full.  Entries with c_in > c_out at
+ * the self tap are ignored whatever the buffer holds.  The convolution matrix
+ * is then triangular in the corner's raster order with diagonal
+ * K[c, c, oh, ow] (Fig. 1), so log|det| = H*W*sum_c log|K[c,c,oh,ow]| and the
+ * inverse can be solved pixel diagonal by pixel diagonal (Algorithm 1,
+ * Theorems 1 and 2).
+ *
+ * Conventions shared by every entry point:
+ *  - Tensors are fp32, C-contiguous.  Activations (B, C, H, W); one layer's
+ *    weights (C_out, C_in, k, k) ("OIHW").  Pointers marked "device" must be
+ *    device memory of the current HIP device; the caller owns every buffer.
+ *  - Calls are asynchronous on `stream` (0 = the null stream) and return after
+ *    enqueueing.  Nothing is allocated, freed or synchronised by the library.
+ *  - Return value: FINC_OK or a negative finc_status.  Arguments are checked
+ *    before any HIP call: a bad argument returns FINC_EINVAL and enqueues
+ *    nothing.  FINC_EUNSUPPORTED: shape valid but outside what the kernels
+ *    handle (per-image working set larger than one workgroup's LDS).
+ *    FINC_EHIP: a HIP runtime call failed (hipGetLastError after the launch).
+ *    Device-side faults surface at the caller's next synchronisation.
+ *  - A zero self-tap diagonal weight makes the layer singular: finc_logdet
+ *    writes -inf and the inverse produces non-finite values (the weights are
+ *    device-resident, so this is not detected on the host).
+ *  - Results are bitwise deterministic and do not depend on B or on an
+ *    image's position in the batch: each image is processed by one workgroup
+ *    in a fixed summation order, without atomics.
+ *  - Supported shapes: 1 <= C <= FINC_MAX_C, 1 <= k <= FINC_MAX_K, H, W >= 1,
+ *    B >= 0 (B == 0 enqueues nothing), B*C*H*W < 2^31.
+ */
+#ifndef FINC_H
+#define FINC_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define FINC_MAX_C 64
+#define FINC_MAX_K 7
+
+/* Corner padding variants (Sec. 4.1, corner padding equations). */
+enum { FINC_TL = 0, FINC_TR = 1, FINC_BL = 2, FINC_BR = 3 };
+
+typedef enum {
+    FINC_OK = 0,
+    FINC_EINVAL = -1,
+    FINC_ESINGULAR = -2,
+    FINC_EUNSUPPORTED = -3,
+    FINC_EHIP = -4
+} finc_status;
+
+/* Library version, major*10000 + minor*100 + patch. */
+int finc_version(void);
+
+/* Static text for a status code (never NULL). */
+const char *finc_strerror(int status);
+
+/* ---- Weight preparation (one-time per weight set) -----------------------
+ * The inverse of one layer solves, per pixel, L x_p = y_p - sum_s K_s x_src
+ * with L the self-tap channel block (lower triangular).  Preparation forms,
+ * in fp64, L^-1 and L^-1 K_s for every other kernel position s, rounded to
+ * fp32, so that every pixel of a diagonal step is a plain accumulation
+ * (see Algorithm 1 and the channel mask of Sec. 4.1).
+ *
+ * finc_workspace_bytes: device bytes of prepared weights for n_layers layers
+ *   of size (C, k); 0 for invalid arguments.
+ * finc_prepare: K = n_layers consecutive OIHW tensors (device); corners =
+ *   host array of n_layers corner ids; prepared = device buffer of at least
+ *   finc_workspace_bytes(C, k, n_layers) bytes, 256-byte aligned, written by
+ *   the call (its layout is private to the library). */
+size_t finc_workspace_bytes(int C, int k, int n_layers);
+int finc_prepare(const float *K, int n_layers, const int *corners, int C, int k,
+                 void *prepared, hipStream_t stream);
+
+/* ---- One padded masked convolution block (PCB) --------------------------
+ * finc_forward: y = layer(x) (Sec. 3 conv equation with Sec. 4.1 padding).
+ *   x, y: device (B, C, H, W); K: device OIHW.  x and y must not overlap.
+ * finc_logdet: out[0] (device double) = log|det| of the layer's H*W*C x
+ *   H*W*C convolution matrix, the same for every image (Table 1 "Jacobian";
+ *   -inf for a zero diagonal).
+ * finc_inverse: x = layer^-1(y) by the diagonal wavefront of Algorithm 1:
+ *   H + W - 1 dependent steps (Theorem 2), every pixel of a diagonal solved
+ *   at once (Theorem 1).  workspace: device, >= finc_workspace_bytes(C, k, 1)
+ *   bytes, 256-byte aligned, overwritten.  x == y (in place) is allowed; any
+ *   other overlap is rejected.
+ * finc_inverse_prepared: the same with weights already prepared by
+ *   finc_prepare (one layer, same corner). */
+int finc_forward(const float *x, float *y, const float *K, int B, int C, int H,
+                 int W, int k, int corner, hipStream_t stream);
+int finc_logdet(const float *K, int C, int k, int corner, int H, int W,
+                double *out, hipStream_t stream);
+int finc_inverse(const float *y, float *x, const float *K, int B, int C, int H,
+                 int W, int k, int corner, void *workspace, hipStream_t stream);
+int finc_inverse_prepared(const float *y, float *x, const void *prepared, int B,
+                          int C, int H, int W, int k, int corner,
+                          hipStream_t stream);
+
+/* ---- FInC unit: four PCBs TL, TR, BL, BR applied in sequence -----------
+ * (Sec. 4.3 and Fig. 2a, read as four full-channel blocks one after the
+ * other; the inverse runs BR^-1, BL^-1, TR^-1, TL^-1 in one launch, as
+ * Algorithm 2 inverts a whole unit at once.)  K4: device, 4 consecutive OIHW
+ * tensors in the order TL, TR, BL, BR.  Activations stay in on-chip memory
+ * between the four blocks.  In-place and overlap rules as for one block.
+ * finc_unit_logdet: sum of the four blocks' log|det|. */
+int finc_unit_forward(const float *x, float *y, const float *K4, int B, int C,
+                      int H, int W, int k, hipStream_t stream);
+int finc_unit_logdet(const float *K4, int C, int k, int H, int W, double *out,
+                     hipStream_t stream);
+int finc_unit_inverse(const float *y, float *x, const float *K4, int B, int C,
+                      int H, int W, int k, void *workspace, hipStream_t stream);
+int finc_unit_inverse_prepared(const float *y, float *x, const void *prepared4,
+                               int B, int C, int H, int W, int k,
+                               hipStream_t stream);
+
+/* ---- Multi-scale sampling stack (Sec. 4.4, Fig. 2c) ---------------------
+ * L levels of U units; level l has C_l = C1 << l channels and spatial size
+ * (H1 >> l, W1 >> l).  Forward direction (for the definition): per level
+ * U x [unit, actnorm y = s*x + b], then, below the top, keep the first half
+ * of the channels and squeeze (C, H, W) -> (4C, H/2, W/2) with channel
+ * 4c + 2dy + dx <- (c, 2i+dy, 2j+dx); the second half is that level's latent.
+ * finc_stack_inverse samples: starting from the top latent, per level
+ * U x [actnorm^-1, unit^-1] with units in reverse, then unsqueeze and append
+ * the level's latent as the second half of the channels.
+ *   z: host array of L device pointers; z[l] for l < L-1 is (B, C_l/2, H_l,
+ *      W_l), z[L-1] is (B, C_{L-1}, H_{L-1}, W_{L-1}).
+ *   x: device (B, C1, H1, W1) output.
+ *   K: device, for l, u, block q (TL, TR, BL, BR): C_l*C_l*k*k floats each.
+ *   scale, bias: device, for l, u: C_l floats each (scale must be nonzero).
+ *   workspace: device, >= finc_stack_workspace_bytes(L, U, C1, k) bytes,
+ *   256-byte aligned, overwritten with prepared weights.
+ * Requirements: C1 even when L > 1, H1 and W1 divisible by 2^(L-1),
+ * C_{L-1} <= FINC_MAX_C, L <= 8, none of z, x overlap. */
+size_t finc_stack_workspace_bytes(int L, int U, int C1, int k);
+int finc_stack_inverse(const float *const *z, float *x, const float *K,
+                       const float *scale, const float *bias, int B, int L,
+                       int U, int C1, int H1, int W1, int k, void *workspace,
+                       hipStream_t stream);
+/* The same with weights already prepared into `prepared` by
+ * finc_stack_prepare (which runs finc_prepare level by level). */
+int finc_stack_prepare(const float *K, int L, int U, int C1, int k,
+                       void *prepared, hipStream_t stream);
+int finc_stack_inverse_prepared(const float *const *z, float *x,
+                                const void *prepared, const float *scale,
+                                const float *bias, int B, int L, int U, int C1,
+                                int H1, int W1, int k, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FINC_H */

@@ -1,0 +1,277 @@
+"""Python binding of libfinc (include/finc.h): argument marshalling only.
+
+Every function takes and returns torch tensors on the current HIP device and
+enqueues on torch's current stream; all arithmetic runs in the HIP kernels of
+csrc/finc.hip.  There is no fallback: if the library is missing or a call
+fails, FincError is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "libfinc.so")
+
+TL, TR, BL, BR = 0, 1, 2, 3
+OK, EINVAL, ESINGULAR, EUNSUPPORTED, EHIP = 0, -1, -2, -3, -4
+
+_vp = ctypes.c_void_p
+_i = ctypes.c_int
+_sz = ctypes.c_size_t
+
+# name -> (restype, argtypes); mirrors include/finc.h
+SIGNATURES = {
+    "finc_version": (_i, []),
+    "finc_strerror": (ctypes.c_char_p, [_i]),
+    "finc_workspace_bytes": (_sz, [_i, _i, _i]),
+    "finc_prepare": (_i, [_vp, _i, ctypes.POINTER(_i), _i, _i, _vp, _vp]),
+    "finc_forward": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "finc_logdet": (_i, [_vp, _i, _i, _i, _i, _i, _vp, _vp]),
+    "finc_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
+    "finc_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "finc_unit_forward": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "finc_unit_logdet": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
+    "finc_unit_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
+    "finc_unit_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "finc_stack_workspace_bytes": (_sz, [_i, _i, _i, _i]),
+    "finc_stack_inverse": (_i, [ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i,
+                                _i, _i, _vp, _vp]),
+    "finc_stack_prepare": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
+    "finc_stack_inverse_prepared": (_i, [ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _i, _i,
+                                         _i, _i, _i, _i, _i, _vp]),
+}
+
+
+class FincError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        msg = _lib.finc_strerror(code).decode() if _lib is not None else str(code)
+        super().__init__(f"{what}: {msg} ({code})")
+        self.code = code
+
+
+_lib = None
+
+
+def lib(path: str = LIB_PATH):
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"libfinc is not built ({path}); run __graft_entry__.build() first")
+    handle = ctypes.CDLL(path)
+    for name, (res, args) in SIGNATURES.items():
+        fn = getattr(handle, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = handle
+    return _lib
+
+
+def _require_lib():
+    return lib()
+
+
+def _check(code: int, what: str):
+    if code != OK:
+        raise FincError(code, what)
+
+
+def _ptr(t: torch.Tensor | None):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t: torch.Tensor, name: str, shape=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if t.dtype != torch.float32:
+        raise ValueError(f"{name} must be float32")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    return t
+
+
+def _workspace(nbytes: int, device, ws):
+    if ws is None:
+        return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+    if ws.numel() * ws.element_size() < nbytes:
+        raise ValueError("workspace too small")
+    return ws
+
+
+# ---------------------------------------------------------------------------
+
+def version() -> int:
+    return _require_lib().finc_version()
+
+
+def workspace_bytes(C: int, k: int, n_layers: int = 1) -> int:
+    return int(_require_lib().finc_workspace_bytes(C, k, n_layers))
+
+
+def stack_workspace_bytes(L: int, U: int, C1: int, k: int) -> int:
+    return int(_require_lib().finc_stack_workspace_bytes(L, U, C1, k))
+
+
+def prepare(K: torch.Tensor, corners, out: torch.Tensor | None = None) -> torch.Tensor:
+    """K: (n, C, C, k, k) or (C, C, k, k); corners: one id per layer."""
+    L = _require_lib()
+    _dev(K, "K")
+    Kn = K.reshape(-1, *K.shape[-3:])
+    n, C, k = Kn.shape[0], Kn.shape[1], Kn.shape[-1]
+    corners = [int(c) for c in (corners if hasattr(corners, "__len__") else [corners])]
+    if len(corners) != n:
+        raise ValueError("one corner per layer")
+    out = _workspace(workspace_bytes(C, k, n), K.device, out)
+    arr = (ctypes.c_int * n)(*corners)
+    _check(L.finc_prepare(_ptr(K), n, arr, C, k, _ptr(out), _stream()), "finc_prepare")
+    return out
+
+
+def forward(x: torch.Tensor, K: torch.Tensor, corner: int, out: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(x, "x")
+    B, C, H, W = x.shape
+    _dev(K, "K", (C, C, K.shape[-1], K.shape[-1]))
+    y = torch.empty_like(x) if out is None else _dev(out, "out", x.shape)
+    _check(L.finc_forward(_ptr(x), _ptr(y), _ptr(K), B, C, H, W, K.shape[-1], corner,
+                          _stream()), "finc_forward")
+    return y
+
+
+def logdet(K: torch.Tensor, corner: int, H: int, W: int, out: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(K, "K")
+    out = torch.empty(1, dtype=torch.float64, device=K.device) if out is None else out
+    _check(L.finc_logdet(_ptr(K), K.shape[0], K.shape[-1], corner, H, W, _ptr(out),
+                         _stream()), "finc_logdet")
+    return out
+
+
+def inverse(y: torch.Tensor, K: torch.Tensor, corner: int, out: torch.Tensor | None = None,
+            workspace: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    k = K.shape[-1]
+    _dev(K, "K", (C, C, k, k))
+    x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
+    ws = _workspace(workspace_bytes(C, k, 1), y.device, workspace)
+    _check(L.finc_inverse(_ptr(y), _ptr(x), _ptr(K), B, C, H, W, k, corner, _ptr(ws),
+                          _stream()), "finc_inverse")
+    return x
+
+
+def inverse_prepared(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: int,
+                     out: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
+    _check(L.finc_inverse_prepared(_ptr(y), _ptr(x), _ptr(prepared), B, C, H, W, k, corner,
+                                   _stream()), "finc_inverse_prepared")
+    return x
+
+
+def unit_forward(x: torch.Tensor, K4: torch.Tensor, out: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(x, "x")
+    B, C, H, W = x.shape
+    k = K4.shape[-1]
+    _dev(K4, "K4", (4, C, C, k, k))
+    y = torch.empty_like(x) if out is None else _dev(out, "out", x.shape)
+    _check(L.finc_unit_forward(_ptr(x), _ptr(y), _ptr(K4), B, C, H, W, k, _stream()),
+           "finc_unit_forward")
+    return y
+
+
+def unit_logdet(K4: torch.Tensor, H: int, W: int, out: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(K4, "K4")
+    out = torch.empty(1, dtype=torch.float64, device=K4.device) if out is None else out
+    _check(L.finc_unit_logdet(_ptr(K4), K4.shape[1], K4.shape[-1], H, W, _ptr(out),
+                              _stream()), "finc_unit_logdet")
+    return out
+
+
+def unit_inverse(y: torch.Tensor, K4: torch.Tensor, out: torch.Tensor | None = None,
+                 workspace: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    k = K4.shape[-1]
+    _dev(K4, "K4", (4, C, C, k, k))
+    x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
+    ws = _workspace(workspace_bytes(C, k, 4), y.device, workspace)
+    _check(L.finc_unit_inverse(_ptr(y), _ptr(x), _ptr(K4), B, C, H, W, k, _ptr(ws),
+                               _stream()), "finc_unit_inverse")
+    return x
+
+
+def unit_inverse_prepared(y: torch.Tensor, prepared4: torch.Tensor, k: int,
+                          out: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
+    _check(L.finc_unit_inverse_prepared(_ptr(y), _ptr(x), _ptr(prepared4), B, C, H, W, k,
+                                        _stream()), "finc_unit_inverse_prepared")
+    return x
+
+
+def _stack_args(z, L_levels):
+    if len(z) != L_levels:
+        raise ValueError("one latent per level")
+    for i, t in enumerate(z):
+        _dev(t, f"z[{i}]")
+    return (ctypes.c_void_p * L_levels)(*[t.data_ptr() for t in z])
+
+
+def stack_prepare(K: torch.Tensor, L: int, U: int, C1: int, k: int,
+                  out: torch.Tensor | None = None):
+    lb = _require_lib()
+    _dev(K, "K")
+    out = _workspace(stack_workspace_bytes(L, U, C1, k), K.device, out)
+    _check(lb.finc_stack_prepare(_ptr(K), L, U, C1, k, _ptr(out), _stream()),
+           "finc_stack_prepare")
+    return out
+
+
+def stack_inverse(z, K: torch.Tensor, scale: torch.Tensor, bias: torch.Tensor, L: int,
+                  U: int, C1: int, H1: int, W1: int, k: int, out: torch.Tensor | None = None,
+                  workspace: torch.Tensor | None = None):
+    """z: list of L latents (see finc.h); K, scale, bias: flat device tensors."""
+    lb = _require_lib()
+    zp = _stack_args(z, L)
+    for name, t in (("K", K), ("scale", scale), ("bias", bias)):
+        _dev(t, name)
+    B = z[0].shape[0]
+    x = (torch.empty((B, C1, H1, W1), dtype=torch.float32, device=z[0].device)
+         if out is None else _dev(out, "out", (B, C1, H1, W1)))
+    ws = _workspace(stack_workspace_bytes(L, U, C1, k), z[0].device, workspace)
+    _check(lb.finc_stack_inverse(zp, _ptr(x), _ptr(K), _ptr(scale), _ptr(bias), B, L, U, C1,
+                                 H1, W1, k, _ptr(ws), _stream()), "finc_stack_inverse")
+    return x
+
+
+def stack_inverse_prepared(z, prepared: torch.Tensor, scale: torch.Tensor,
+                           bias: torch.Tensor, L: int, U: int, C1: int, H1: int, W1: int,
+                           k: int, out: torch.Tensor | None = None):
+    lb = _require_lib()
+    zp = _stack_args(z, L)
+    B = z[0].shape[0]
+    x = (torch.empty((B, C1, H1, W1), dtype=torch.float32, device=z[0].device)
+         if out is None else _dev(out, "out", (B, C1, H1, W1)))
+    _check(lb.finc_stack_inverse_prepared(zp, _ptr(x), _ptr(prepared), _ptr(scale),
+                                          _ptr(bias), B, L, U, C1, H1, W1, k, _stream()),
+           "finc_stack_inverse_prepared")
+    return x

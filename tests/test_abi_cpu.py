@@ -1,0 +1,154 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/finc.h declares, and rejects bad arguments before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2301_09266_amd import finc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "finc.h")
+
+FAKE = ctypes.c_void_p(0x100000)     # never dereferenced on the host
+FAKE2 = ctypes.c_void_p(0x900000)
+NULL = None
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(finc_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ("finc_forward", "finc_logdet", "finc_inverse", "finc_unit_forward",
+                 "finc_unit_inverse", "finc_unit_logdet", "finc_stack_inverse",
+                 "finc_prepare", "finc_strerror"):
+        assert want in names
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(finc.LIB_PATH)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+    # and the binding knows every one of them
+    assert set(declared_functions()) == set(finc.SIGNATURES)
+
+
+def test_version_and_strerror():
+    lib = finc.lib()
+    assert lib.finc_version() >= 100
+    for code in (0, -1, -2, -3, -4, 12345):
+        assert lib.finc_strerror(code)
+
+
+def test_workspace_bytes():
+    lib = finc.lib()
+    for C, k in [(3, 3), (12, 3), (12, 5), (48, 3), (64, 7), (1, 1)]:
+        cp = (C + 3) // 4 * 4
+        floats = -(-(k * k * cp * cp) // 64) * 64
+        assert lib.finc_workspace_bytes(C, k, 1) == floats * 4
+        assert lib.finc_workspace_bytes(C, k, 4) == 4 * floats * 4
+    for bad in [(0, 3, 1), (65, 3, 1), (12, 0, 1), (12, 8, 1), (12, 3, -1)]:
+        assert lib.finc_workspace_bytes(*bad) == 0
+    assert lib.finc_stack_workspace_bytes(3, 8, 12, 3) == sum(
+        8 * 4 * lib.finc_workspace_bytes(12 << l, 3, 1) for l in range(3))
+    assert lib.finc_stack_workspace_bytes(3, 8, 24, 3) == 0   # 96 channels at the top
+
+
+SHAPE = (2, 12, 16, 16, 3)
+
+
+@pytest.mark.parametrize("args", [
+    (NULL, FAKE2, FAKE, *SHAPE, 0),
+    (FAKE, NULL, FAKE2, *SHAPE, 0),
+    (FAKE, FAKE2, NULL, *SHAPE, 0),
+    (FAKE, FAKE2, FAKE, -1, 12, 16, 16, 3, 0),
+    (FAKE, FAKE2, FAKE, 2, 0, 16, 16, 3, 0),
+    (FAKE, FAKE2, FAKE, 2, 65, 16, 16, 3, 0),
+    (FAKE, FAKE2, FAKE, 2, 12, 0, 16, 3, 0),
+    (FAKE, FAKE2, FAKE, 2, 12, 16, 16, 0, 0),
+    (FAKE, FAKE2, FAKE, 2, 12, 16, 16, 8, 0),
+    (FAKE, FAKE2, FAKE, *SHAPE, 4),
+    (FAKE, FAKE2, FAKE, *SHAPE, -1),
+    (FAKE, ctypes.c_void_p(0x100000 + 64), FAKE2, *SHAPE, 0),   # overlapping x / y
+    (FAKE, FAKE2, FAKE, 1 << 20, 64, 64, 64, 3, 0),            # > 2^31 elements
+])
+def test_forward_rejects(args):
+    assert finc.lib().finc_forward(*args, None) == finc.EINVAL
+
+
+def test_inverse_rejects():
+    lib = finc.lib()
+    ws = ctypes.c_void_p(0x4000000)
+    assert lib.finc_inverse(FAKE, FAKE2, FAKE, *SHAPE, 0, NULL, None) == finc.EINVAL
+    assert lib.finc_inverse(FAKE, FAKE2, FAKE, *SHAPE, 0, ctypes.c_void_p(0x4000010),
+                            None) == finc.EINVAL                         # misaligned
+    assert lib.finc_inverse(FAKE, FAKE2, FAKE, *SHAPE, 7, ws, None) == finc.EINVAL
+    # partial overlap of y and x is rejected, identical pointers (in place) are not
+    assert lib.finc_inverse(FAKE, ctypes.c_void_p(0x100000 + 64), FAKE2, *SHAPE, 0, ws,
+                            None) == finc.EINVAL
+    # workspace overlapping the output
+    assert lib.finc_inverse(FAKE2, FAKE, ctypes.c_void_p(0x8000000), *SHAPE, 0,
+                            ctypes.c_void_p(0x100000), None) == finc.EINVAL
+    assert lib.finc_inverse_prepared(FAKE, FAKE2, NULL, *SHAPE, 0, None) == finc.EINVAL
+    assert lib.finc_unit_inverse(FAKE, FAKE2, FAKE, *SHAPE, NULL, None) == finc.EINVAL
+    assert lib.finc_unit_inverse_prepared(FAKE, FAKE2, NULL, *SHAPE, None) == finc.EINVAL
+
+
+def test_logdet_and_prepare_reject():
+    lib = finc.lib()
+    out = ctypes.c_void_p(0x200000)
+    assert lib.finc_logdet(NULL, 12, 3, 0, 16, 16, out, None) == finc.EINVAL
+    assert lib.finc_logdet(FAKE, 12, 3, 5, 16, 16, out, None) == finc.EINVAL
+    assert lib.finc_logdet(FAKE, 12, 3, 0, 16, 16, NULL, None) == finc.EINVAL
+    assert lib.finc_unit_logdet(FAKE, 0, 3, 16, 16, out, None) == finc.EINVAL
+    corners = (ctypes.c_int * 2)(0, 9)
+    ws = ctypes.c_void_p(0x4000000)
+    assert lib.finc_prepare(FAKE, 2, corners, 12, 3, ws, None) == finc.EINVAL
+    corners = (ctypes.c_int * 2)(0, 1)
+    assert lib.finc_prepare(FAKE, 2, corners, 12, 3, ctypes.c_void_p(0x4000004),
+                            None) == finc.EINVAL
+    assert lib.finc_prepare(FAKE, -1, corners, 12, 3, ws, None) == finc.EINVAL
+    assert lib.finc_prepare(FAKE, 0, corners, 12, 3, ws, None) == finc.OK   # nothing to do
+
+
+def test_stack_rejects():
+    lib = finc.lib()
+    z = (ctypes.c_void_p * 3)(0x1000000, 0x2000000, 0x3000000)
+    ws = ctypes.c_void_p(0x40000000)
+    x = ctypes.c_void_p(0x50000000)
+    ok = dict(B=64, L=3, U=8, C1=12, H1=32, W1=32, k=3)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return lib.finc_stack_inverse(z, x, FAKE, FAKE, FAKE, a["B"], a["L"], a["U"], a["C1"],
+                                      a["H1"], a["W1"], a["k"], ws, None)
+
+    assert call(C1=13) == finc.EINVAL          # odd channels cannot be split
+    assert call(H1=30) == finc.EINVAL          # not divisible by 4
+    assert call(L=9) == finc.EINVAL
+    assert call(C1=24) == finc.EINVAL          # 96 channels at the top
+    assert call(k=0) == finc.EINVAL
+    assert call(B=0) == finc.OK                # nothing to enqueue
+    assert lib.finc_stack_inverse(None, x, FAKE, FAKE, FAKE, 64, 3, 8, 12, 32, 32, 3, ws,
+                                  None) == finc.EINVAL
+
+
+def test_empty_batch_enqueues_nothing():
+    lib = finc.lib()
+    ws = ctypes.c_void_p(0x4000000)
+    assert lib.finc_forward(FAKE, FAKE2, FAKE, 0, 12, 16, 16, 3, 0, None) == finc.OK
+    assert lib.finc_unit_forward(FAKE, FAKE2, FAKE, 0, 12, 16, 16, 3, None) == finc.OK
+    assert lib.finc_inverse(FAKE, FAKE2, FAKE, 0, 12, 16, 16, 3, 0, ws, None) == finc.OK
+    assert lib.finc_inverse_prepared(FAKE, FAKE2, ws, 0, 12, 16, 16, 3, 0, None) == finc.OK
+    assert lib.finc_unit_inverse(FAKE, FAKE2, FAKE, 0, 12, 16, 16, 3, ws, None) == finc.OK
+
+
+def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(finc, "_lib", None)
+    with pytest.raises(RuntimeError, match="not built"):
+        finc.lib(str(tmp_path / "missing.so"))

@@ -1,0 +1,218 @@
+"""HIP path vs the CPU oracle, element by element, through the C ABI.
+
+Bar: |gpu - oracle| <= 1e-4 * max(1, |oracle|) elementwise for single
+layers and units; the round trip inverse(forward(x)) within 1e-4 of x.  Both
+sides see the same fp32 inputs (the oracle computes on them in fp64).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2301_09266_amd import finc, synth
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = 1e-4
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(DEV)
+
+
+def f64(a):
+    """fp32-rounded copy in fp64: what the GPU actually sees."""
+    return np.asarray(a, dtype=np.float32).astype(np.float64)
+
+
+def host(t):
+    return t.detach().cpu().numpy().astype(np.float64)
+
+
+def assert_close(g, r, what, tol=TOL):
+    err = np.abs(g - r)
+    bound = tol * np.maximum(1.0, np.abs(r))
+    bad = err > bound
+    assert not np.isnan(g).any(), f"{what}: NaN in GPU output"
+    assert not bad.any(), (f"{what}: {bad.sum()} elements out of tolerance, max abs err "
+                           f"{err.max():.3e}, max rel {np.max(err / np.maximum(1, np.abs(r))):.3e}")
+
+
+def poisoned(shape):
+    return torch.full(shape, float("nan"), dtype=torch.float32, device=DEV)
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle.default()
+
+
+SHAPES = [
+    # (B, C, H, W, k)
+    (2, 1, 1, 1, 3), (2, 3, 1, 7, 3), (2, 3, 7, 1, 3), (3, 5, 5, 9, 2), (2, 12, 13, 17, 3),
+    (2, 4, 6, 6, 1), (1, 7, 9, 6, 5), (2, 12, 24, 24, 3), (1, 16, 11, 8, 4), (1, 33, 7, 9, 3),
+]
+
+
+@pytest.mark.parametrize("corner", [0, 1, 2, 3])
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_layer_forward_inverse(orc, shape, corner):
+    B, C, H, W, k = shape
+    print(f"layer B={B} C={C} H={H} W={W} k={k} corner={corner}", flush=True)
+    rng = np.random.default_rng(hash((shape, corner)) % 2**32)
+    x = rng.normal(size=(B, C, H, W))
+    K = synth.garbage_in_mask(synth.masked_kernel(C, k, corner, 1000 + corner), corner)
+    xd, Kd = dev(x), dev(K)
+    y = finc.forward(xd, Kd, corner, out=poisoned(x.shape))
+    assert_close(host(y), orc.forward(f64(x), f64(K), corner), "forward")
+    # inverse of the GPU forward output, against the oracle on the same input
+    yh = host(y)
+    xr = finc.inverse(y, Kd, corner, out=poisoned(x.shape))
+    assert_close(host(xr), orc.inverse(yh, f64(K), corner), "inverse")
+    assert np.max(np.abs(host(xr) - f64(x))) <= TOL, "round trip"
+    # inverse of an arbitrary input
+    z = rng.normal(size=(B, C, H, W))
+    xz = finc.inverse(dev(z), Kd, corner)
+    assert_close(host(xz), orc.inverse(f64(z), f64(K), corner), "inverse of z")
+    ld = finc.logdet(Kd, corner, H, W)
+    r = orc.logdet(f64(K), corner, H, W)
+    assert abs(float(ld.cpu()[0]) - r) <= TOL * max(1.0, abs(r))
+
+
+def test_inverse_in_place(orc):
+    c = synth.make("layer_c12_16x16_b64_k3", B=5)
+    y = dev(orc.forward(c["x"], c["K"], 0))
+    want = orc.inverse(host(y), f64(c["K"]), 0)
+    finc.inverse(y, dev(c["K"]), 0, out=y)
+    assert_close(host(y), want, "in-place inverse")
+
+
+def test_logdet_singular():
+    K = synth.masked_kernel(4, 3, 2, 5)
+    K[2, 2, 0, 2] = 0.0
+    assert float(finc.logdet(dev(K), 2, 5, 5).cpu()[0]) == -np.inf
+
+
+def test_prepared_matches_unprepared(orc):
+    c = synth.make("layer_c12_16x16_b64_k3", B=4)
+    Kd = dev(c["K"])
+    y = dev(orc.forward(c["x"], c["K"], 0))
+    prep = finc.prepare(Kd, [0])
+    a = finc.inverse_prepared(y, prep, 3, 0)
+    b = finc.inverse(y, Kd, 0)
+    assert torch.equal(a, b)
+
+
+# --- the workloads at full size ------------------------------------------------
+
+def _layer_workload(orc, name):
+    c = synth.make(name)
+    x, K, corner = c["x"], c["K"], c["corner"]
+    xd, Kd = dev(x), dev(K)
+    y = finc.forward(xd, Kd, corner, out=poisoned(x.shape))
+    yh = host(y)
+    assert_close(yh, orc.forward(f64(x), f64(K), corner), f"{name} forward")
+    xr = finc.inverse(y, Kd, corner, out=poisoned(x.shape))
+    assert_close(host(xr), orc.inverse(yh, f64(K), corner), f"{name} inverse")
+    assert np.max(np.abs(host(xr) - f64(x))) <= TOL, f"{name} round trip"
+    xz = finc.inverse(dev(c["z"]), Kd, corner)
+    assert_close(host(xz), orc.inverse(f64(c["z"]), f64(K), corner), f"{name} inverse(z)")
+    ld = float(finc.logdet(Kd, corner, c["H"], c["W"]).cpu()[0])
+    r = orc.logdet(f64(K), corner, c["H"], c["W"])
+    assert abs(ld - r) <= TOL * max(1.0, abs(r))
+    # bitwise determinism and batch invariance
+    xr2 = finc.inverse(y, Kd, corner)
+    assert torch.equal(xr, xr2)
+    one = finc.inverse(y[-1:].contiguous(), Kd, corner)
+    assert torch.equal(one[0], xr[-1])
+    y2 = finc.forward(xd, Kd, corner)
+    assert torch.equal(y, y2)
+    assert torch.equal(finc.forward(xd[-1:].contiguous(), Kd, corner)[0], y[-1])
+
+
+@pytest.mark.parametrize("name", ["layer_c3_8x8_b1_k3", "layer_c12_16x16_b64_k3",
+                                  "layer_c12_32x32_b64_k3", "layer_c12_32x32_b64_k5"])
+def test_layer_workload(orc, name):
+    print(f"workload {name}", flush=True)
+    _layer_workload(orc, name)
+
+
+def test_dense_jacobian_slogdet_8x8():
+    """8x8x3 workload: the GPU forward applied to all 192 basis images gives
+    the dense Jacobian; its slogdet equals the GPU log|det|."""
+    c = synth.make("layer_c3_8x8_b1_k3")
+    n = 3 * 8 * 8
+    basis = torch.eye(n, device=DEV).reshape(n, 3, 8, 8).contiguous()
+    J = host(finc.forward(basis, dev(c["K"]), 0)).reshape(n, n).T
+    sign, ld = np.linalg.slogdet(J)
+    assert sign == 1.0
+    g = float(finc.logdet(dev(c["K"]), 0, 8, 8).cpu()[0])
+    assert abs(g - ld) <= TOL * max(1.0, abs(ld))
+
+
+@pytest.mark.parametrize("name", ["unit_c12_16x16_b256_k3", "unit_c48_8x8_b256_k3",
+                                  "unit_c12_32x32_b64_k3", "unit_c12_32x32_b64_k5"])
+def test_unit_workload(orc, name):
+    print(f"workload {name}", flush=True)
+    c = synth.make(name)
+    x, K4 = c["x"], c["K4"]
+    xd, K4d = dev(x), dev(K4)
+    y = finc.unit_forward(xd, K4d, out=poisoned(x.shape))
+    yh = host(y)
+    assert_close(yh, orc.unit_forward(f64(x), f64(K4)), f"{name} unit forward")
+    xr = finc.unit_inverse(y, K4d, out=poisoned(x.shape))
+    assert_close(host(xr), orc.unit_inverse(yh, f64(K4)), f"{name} unit inverse")
+    assert np.max(np.abs(host(xr) - f64(x))) <= TOL, f"{name} unit round trip"
+    ld = float(finc.unit_logdet(K4d, c["H"], c["W"]).cpu()[0])
+    r = orc.unit_logdet(f64(K4), c["H"], c["W"])
+    assert abs(ld - r) <= TOL * max(1.0, abs(r))
+    xr2 = finc.unit_inverse(y, K4d)
+    assert torch.equal(xr, xr2)
+    assert torch.equal(finc.unit_inverse(y[3:4].contiguous(), K4d)[0], xr[3])
+
+
+def _stack_flat(c):
+    Kf = np.concatenate([a.ravel() for a in c["K"]])
+    sf = np.concatenate([a.ravel() for a in c["scale"]])
+    bf = np.concatenate([a.ravel() for a in c["bias"]])
+    return Kf, sf, bf
+
+
+def test_stack_small(orc):
+    """Small stack (2 images, 3 levels of 2 units): elementwise vs oracle."""
+    c = synth.stack_case(B=2, C1=4, H1=8, W1=8, levels=3, units=2, k=3)
+    Kf, sf, bf = _stack_flat(c)
+    x = finc.stack_inverse([dev(z) for z in c["z"]], dev(Kf), dev(sf), dev(bf), 3, 2, 4, 8,
+                           8, 3)
+    want = orc.stack_inverse([f64(z) for z in c["z"]], [f64(a) for a in c["K"]],
+                             [f64(a) for a in c["scale"]], [f64(a) for a in c["bias"]],
+                             3, 2, 3, 4, 8, 8)
+    assert_close(host(x), want, "small stack")
+
+
+def test_stack_workload(orc):
+    """Three levels of eight units (12x32x32 -> 24x16x16 -> 48x8x8), batch 64:
+    the oracle runs on four sampled images (results do not depend on the
+    batch); criterion is max|gpu - oracle| / max(1, max|oracle|) <= 1e-4,
+    because the random stack's inverse reaches magnitudes where elementwise
+    fp32 error is dominated by cancellation."""
+    print("workload stack_3x8_c12_32x32_b64_k3", flush=True)
+    c = synth.make("stack_3x8_c12_32x32_b64_k3")
+    Kf, sf, bf = _stack_flat(c)
+    zd = [dev(z) for z in c["z"]]
+    args = (dev(Kf), dev(sf), dev(bf), 3, 8, 12, 32, 32, 3)
+    x = finc.stack_inverse(zd, *args, out=poisoned((64, 12, 32, 32)))
+    xh = host(x)
+    assert np.isfinite(xh).all()
+    pick = [0, 17, 42, 63]
+    want = orc.stack_inverse([f64(z[pick]) for z in c["z"]], [f64(a) for a in c["K"]],
+                             [f64(a) for a in c["scale"]], [f64(a) for a in c["bias"]],
+                             3, 8, 3, 12, 32, 32)
+    for n, b in enumerate(pick):
+        err = np.max(np.abs(xh[b] - want[n])) / max(1.0, np.max(np.abs(want[n])))
+        assert err <= TOL, f"image {b}: inf-norm relative error {err:.3e}"
+    x2 = finc.stack_inverse(zd, *args)
+    assert torch.equal(x, x2)
+    one = finc.stack_inverse([z[5:6].contiguous() for z in zd], *args)
+    assert torch.equal(one[0], x[5])

@@ -160,17 +160,21 @@ __device__ inline LaneMap lane_map(int CP) {
     return m;
 }
 
-// Contiguous run of C (padded to CP) inputs times one weight column.
+// Contiguous run of C (padded to CP) inputs times one weight column.  The
+// run is split over four accumulators (c_in mod 4), joined pairwise: four
+// independent FMA chains, and a rounding error that grows with C/4 instead of
+// C (a single chain over a 48-channel unit loses ~1e-4 in a round trip).
 __device__ inline float dot_run(const float *__restrict__ w, const float *__restrict__ v,
-                                int CP, float acc) {
+                                int CP) {
+    float q0 = 0.0f, q1 = 0.0f, q2 = 0.0f, q3 = 0.0f;
     for (int ci = 0; ci < CP; ci += 4) {
         const float4 x = *reinterpret_cast<const float4 *>(v + ci);
-        acc = fmaf(w[(ci + 0) * CP], x.x, acc);
-        acc = fmaf(w[(ci + 1) * CP], x.y, acc);
-        acc = fmaf(w[(ci + 2) * CP], x.z, acc);
-        acc = fmaf(w[(ci + 3) * CP], x.w, acc);
+        q0 = fmaf(w[(ci + 0) * CP], x.x, q0);
+        q1 = fmaf(w[(ci + 1) * CP], x.y, q1);
+        q2 = fmaf(w[(ci + 2) * CP], x.z, q2);
+        q3 = fmaf(w[(ci + 3) * CP], x.w, q3);
     }
-    return acc;
+    return (q0 + q1) + (q2 + q3);
 }
 
 __device__ inline void load_nchw(float *dst, const float *__restrict__ src, const Geo &g) {
@@ -229,7 +233,7 @@ __device__ void solve_layer(const float *Y, float *X, const float *wl, const Geo
                 const int i = flip_h ? H - 1 - ip : ip;
                 const int j = flip_w ? W - 1 - jp : jp;
                 const int p = i * W + j;
-                float acc = dot_run(wl + (size_t)s_self * CP * CP + m.c, Y + p * CP, CP, 0.0f);
+                const float acc = dot_run(wl + (size_t)s_self * CP * CP + m.c, Y + p * CP, CP);
                 float sub = 0.0f;
                 for (int a = 0; a < k; ++a) {
                     const int ii = i + a - oh;
@@ -239,8 +243,8 @@ __device__ void solve_layer(const float *Y, float *X, const float *wl, const Geo
                         const int jj = j + b - ow;
                         if (jj < 0 || jj >= W || (a == oh && b == ow))
                             continue;
-                        sub = dot_run(wl + (size_t)(a * k + b) * CP * CP + m.c,
-                                      X + (ii * W + jj) * CP, CP, sub);
+                        sub += dot_run(wl + (size_t)(a * k + b) * CP * CP + m.c,
+                                       X + (ii * W + jj) * CP, CP);
                     }
                 }
                 X[p * CP + m.c] = m.c < C ? acc - sub : 0.0f;
@@ -386,8 +390,8 @@ __global__ __launch_bounds__(kThreads) void forward_chain_kernel(FwdArgs a) {
                         const int jj = j + kb - ow;
                         if (jj < 0 || jj >= W)
                             continue;
-                        acc = dot_run(wl + (size_t)(ka * k + kb) * CP * CP + m.c,
-                                      Xi + (ii * W + jj) * CP, CP, acc);
+                        acc += dot_run(wl + (size_t)(ka * k + kb) * CP * CP + m.c,
+                                       Xi + (ii * W + jj) * CP, CP);
                     }
                 }
                 Yo[p * CP + m.c] = m.c < C ? acc : 0.0f;

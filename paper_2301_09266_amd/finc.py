@@ -126,8 +126,10 @@ def prepare(K: torch.Tensor, corners, out: torch.Tensor | None = None) -> torch.
     """K: (n, C, C, k, k) or (C, C, k, k); corners: one id per layer."""
     L = _require_lib()
     _dev(K, "K")
-    Kn = K.reshape(-1, *K.shape[-3:])
-    n, C, k = Kn.shape[0], Kn.shape[1], Kn.shape[-1]
+    if K.dim() not in (4, 5) or K.shape[-4] != K.shape[-3] or K.shape[-2] != K.shape[-1]:
+        raise ValueError(f"K has shape {tuple(K.shape)}, expected ([n,] C, C, k, k)")
+    n = 1 if K.dim() == 4 else K.shape[0]
+    C, k = K.shape[-3], K.shape[-1]
     corners = [int(c) for c in (corners if hasattr(corners, "__len__") else [corners])]
     if len(corners) != n:
         raise ValueError("one corner per layer")

@@ -39,6 +39,11 @@ def assert_close(g, r, what, tol=TOL):
                            f"{err.max():.3e}, max rel {np.max(err / np.maximum(1, np.abs(r))):.3e}")
 
 
+def assert_round_trip(xr, x, what, tol=TOL):
+    err = float(np.max(np.abs(xr - x))) if np.size(x) else 0.0
+    assert err <= tol, f"{what}: round trip max abs err {err:.3e} > {tol:.0e}"
+
+
 def poisoned(shape):
     return torch.full(shape, float("nan"), dtype=torch.float32, device=DEV)
 
@@ -70,7 +75,7 @@ def test_layer_forward_inverse(orc, shape, corner):
     yh = host(y)
     xr = finc.inverse(y, Kd, corner, out=poisoned(x.shape))
     assert_close(host(xr), orc.inverse(yh, f64(K), corner), "inverse")
-    assert np.max(np.abs(host(xr) - f64(x))) <= TOL, "round trip"
+    assert_round_trip(host(xr), f64(x), "layer")
     # inverse of an arbitrary input
     z = rng.normal(size=(B, C, H, W))
     xz = finc.inverse(dev(z), Kd, corner)
@@ -115,7 +120,7 @@ def _layer_workload(orc, name):
     assert_close(yh, orc.forward(f64(x), f64(K), corner), f"{name} forward")
     xr = finc.inverse(y, Kd, corner, out=poisoned(x.shape))
     assert_close(host(xr), orc.inverse(yh, f64(K), corner), f"{name} inverse")
-    assert np.max(np.abs(host(xr) - f64(x))) <= TOL, f"{name} round trip"
+    assert_round_trip(host(xr), f64(x), name)
     xz = finc.inverse(dev(c["z"]), Kd, corner)
     assert_close(host(xz), orc.inverse(f64(c["z"]), f64(K), corner), f"{name} inverse(z)")
     ld = float(finc.logdet(Kd, corner, c["H"], c["W"]).cpu()[0])
@@ -163,7 +168,7 @@ def test_unit_workload(orc, name):
     assert_close(yh, orc.unit_forward(f64(x), f64(K4)), f"{name} unit forward")
     xr = finc.unit_inverse(y, K4d, out=poisoned(x.shape))
     assert_close(host(xr), orc.unit_inverse(yh, f64(K4)), f"{name} unit inverse")
-    assert np.max(np.abs(host(xr) - f64(x))) <= TOL, f"{name} unit round trip"
+    assert_round_trip(host(xr), f64(x), f"{name} unit")
     ld = float(finc.unit_logdet(K4d, c["H"], c["W"]).cpu()[0])
     r = orc.unit_logdet(f64(K4), c["H"], c["W"])
     assert abs(ld - r) <= TOL * max(1.0, abs(r))

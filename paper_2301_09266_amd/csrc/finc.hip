@@ -212,46 +212,110 @@ __device__ inline void copy_floats(float *dst, const float *__restrict__ src, si
 }
 
 // ---------------------------------------------------------------------------
-// Inverse of one layer inside LDS: Y (input, pixel-major) -> X.
+// Inverse (Algorithm 1) as an MFMA wavefront.
+//
+// One workgroup per image; the image stays in LDS for the whole chain of
+// layers.  Per layer, with frames flipped so that every corner reads "up and
+// to the left" (the flips of Algorithm 2 become address arithmetic):
+//
+//   x[p] = L^-1 y[p] - sum_{(dp,dq) != 0} (L^-1 K_(dp,dq)) x[p - (dp,dq)]
+//
+// where (dp, dq) in [0, k-1]^2 is the back-offset of a kernel position.  A
+// pixel on anti-diagonal e reads diagonals e - (dp + dq); only the two taps
+// with dp + dq = 1 read the diagonal solved in the previous step.  Every step
+// is a small dense contraction
+//     D[16 frame rows][16 output channels] += A[rows][k] * B[k][channels]
+// over k = (tap, input channel), issued as v_mfma_f32_16x16x4_f32 with the
+// inputs gathered from LDS one 16-byte channel quad per lane and the prepared
+// weights held in registers as the B operand.
+//
+// The k range is cut into "quads" (one tap, four input channels).  Per tile
+// (16 rows x 16 output channels) one critical wave owns the quads of the two
+// dp + dq = 1 taps: it finishes diagonal e.  S further waves own the other
+// quads (the L^-1 y term and dp + dq >= 2): during step e they already
+// compute their share of diagonal e + 1, whose sources are all solved, and
+// leave it as partial tiles in LDS.  So one barrier per diagonal step (Theorems
+// 1 and 2: H + W - 1 steps) and a critical path of only the dp + dq = 1 work.
+//
+// LDS per level: X, the solution, with a zero border of k-1 pixels on every
+// side (the padded image of the paper's padding equation: out-of-image taps
+// read zeros, so gathers never branch); Y, the layer input, unpadded; R, the
+// partial tiles (two parities); Z, a zero block for padding quads.  All
+// pixel-major with the channel axis padded to CP = 4 * ceil(C / 4).
 // ---------------------------------------------------------------------------
-__device__ void solve_layer(const float *Y, float *X, const float *wl, const Geo &g,
-                            int corner) {
-    const int C = g.C, CP = g.CP, H = g.H, W = g.W, k = g.k;
-    int oh, ow;
-    self_tap(corner, k, oh, ow);
-    const bool flip_h = (corner == FINC_BL || corner == FINC_BR);
-    const bool flip_w = (corner == FINC_TR || corner == FINC_BR);
-    const int s_self = oh * k + ow;
-    const LaneMap m = lane_map(CP);
-    for (int d = 0; d < H + W - 1; ++d) {
-        const int i_lo = d - (W - 1) > 0 ? d - (W - 1) : 0;
-        const int i_hi = d < H - 1 ? d : H - 1;
-        const int npix = i_hi - i_lo + 1;
-        if (m.active) {
-            for (int slot = m.group; slot < npix; slot += m.stride) {
-                const int ip = i_lo + slot, jp = d - ip;
-                const int i = flip_h ? H - 1 - ip : ip;
-                const int j = flip_w ? W - 1 - jp : jp;
-                const int p = i * W + j;
-                const float acc = dot_run(wl + (size_t)s_self * CP * CP + m.c, Y + p * CP, CP);
-                float sub = 0.0f;
-                for (int a = 0; a < k; ++a) {
-                    const int ii = i + a - oh;
-                    if (ii < 0 || ii >= H)
-                        continue;
-                    for (int b = 0; b < k; ++b) {
-                        const int jj = j + b - ow;
-                        if (jj < 0 || jj >= W || (a == oh && b == ow))
-                            continue;
-                        sub += dot_run(wl + (size_t)(a * k + b) * CP * CP + m.c,
-                                       X + (ii * W + jj) * CP, CP);
-                    }
-                }
-                X[p * CP + m.c] = m.c < C ? acc - sub : 0.0f;
-            }
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kMaxWaves = 16;
+constexpr int kMaxGroups = 8;                       // quad groups (x4 quads) per wave
+
+// Work split and LDS layout of one level (same for every layer of it).
+struct Plan {
+    int C, CP, H, W, K, P, WP;
+    int MT, NT, T, S, S4, NW;   // row tiles, channel tiles, tiles, helpers per tile (S4 = S
+                                // rounded up to 4: partial-tile slots per tile), waves
+    int ncq, nq, nq_crit, chunk;
+    int offX, offY, offR, offZ;  // LDS offsets, floats
+    int lds_floats;
+};
+
+__host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+__host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
+__host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
+
+// Quad u of a tile: tap number u / ncq, input channels 4 (u % ncq) .. +3.
+// Taps are numbered by diagonal distance dp + dq = 1, 2, ..., 2(k-1) (dp
+// ascending within a distance), the self tap (0, 0) last.
+__host__ __device__ inline void tap_of(int t, int K, int &dp, int &dq) {
+    dp = 0;
+    dq = 0;
+    int n = 0;
+    for (int s = 1; s <= 2 * (K - 1); ++s) {
+        const int lo = s - (K - 1) > 0 ? s - (K - 1) : 0, hi = s < K - 1 ? s : K - 1;
+        const int cnt = hi - lo + 1;
+        if (t < n + cnt) {
+            dp = lo + (t - n);
+            dq = s - dp;
+            return;
         }
-        __syncthreads();
+        n += cnt;
     }
+}
+
+// false if the shape needs more waves or registers than a workgroup has
+inline bool make_plan(int C, int H, int W, int K, Plan &p) {
+    p.C = C;
+    p.CP = round_up4(C);
+    p.H = H;
+    p.W = W;
+    p.K = K;
+    p.P = K - 1;
+    p.WP = W + 2 * p.P;
+    p.MT = ceil_div(H, 16);
+    p.NT = ceil_div(p.CP, 16);
+    p.T = p.MT * p.NT;
+    p.ncq = p.CP / 4;
+    p.nq = K * K * p.ncq;
+    p.nq_crit = K >= 2 ? imin(p.nq, round_up4(2 * p.ncq)) : 0;
+    const int rest = p.nq - p.nq_crit;
+    const int s_max = kMaxWaves / p.T - 1;
+    if (s_max < 1)
+        return false;
+    p.S = imax(1, imin(s_max, ceil_div(rest, imax(4, p.nq_crit))));
+    p.chunk = round_up4(ceil_div(rest, p.S));
+    if (p.nq_crit > 4 * kMaxGroups || p.chunk > 4 * kMaxGroups)
+        return false;
+    p.NW = p.T * (1 + p.S);
+    p.S4 = round_up4(p.S);
+    p.offX = 0;
+    p.offY = (H + 2 * p.P) * p.WP * p.CP;
+    p.offR = p.offY + H * W * p.CP;
+    p.offZ = p.offR + 2 * p.T * p.S4 * 256;
+    p.lds_floats = p.offZ + 256;
+    return true;
+}
+
+__device__ inline f32x4 mfma4(float a, float b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
 // One level of an inverse chain: an input tensor, U units of `lpu` layers,
@@ -261,82 +325,397 @@ struct Level {
     const float *prep;    // n_units * lpu prepared layers
     const float *scale;   // n_units * C, or null
     const float *bias;
-    int C, H, W;
+    Plan pl;
 };
 
 struct InvArgs {
     Level lv[kMaxLevels];
     float *out;           // (B, C_0, H_0, W_0)
-    int L, k, n_units, lpu, corner0;
+    int L, n_units, lpu, corner0;
 };
 
-// Inverse of a whole chain with the image resident in LDS from the first
-// load to the last store.  Level l's two activation buffers sit at
-// [0, A_l) and [A_l, 2 A_l) (A_l = H_l W_l CP_l floats), its weights right
-// after; when going down a level the unsqueezed result is written to
-// [A_l, 2 A_l), which lies beyond everything the level above used
-// (2 A_{l+1} <= A_l), so the transition needs no extra space.
-__global__ __launch_bounds__(kThreads) void inverse_chain_kernel(InvArgs a) {
-    extern __shared__ float sm[];
-    const size_t b = blockIdx.x;
-    const int k = a.k;
-    float *Y = sm, *X = sm;
-    Geo g = {0, 0, 0, 0, 0};
-    for (int l = a.L - 1; l >= 0; --l) {
-        const Level lv = a.lv[l];
-        const Geo gp = g;   // geometry of the level above (valid when l < L-1)
-        g.C = lv.C;
-        g.CP = round_up4(lv.C);
-        g.H = lv.H;
-        g.W = lv.W;
-        g.k = k;
-        const int C = g.C, CP = g.CP, H = g.H, W = g.W, HW = H * W;
-        float *lo = sm, *hi = sm + (size_t)HW * CP;
-        if (l == a.L - 1) {
-            load_nchw(hi, lv.z + b * (size_t)C * HW, g);
-        } else {
-            // concat(unsqueeze(h), z_l): channel c < C/2 of pixel (i, j) is
-            // channel 4c + 2(i&1) + (j&1) of the level above at (i/2, j/2).
-            const int Ch = C / 2;
-            const float *lat = lv.z + b * (size_t)Ch * HW;
-            for (int idx = threadIdx.x; idx < Ch * HW; idx += blockDim.x) {
-                const int c = idx / HW, p = idx - c * HW;
-                const int i = p / W, j = p - i * W;
-                const int ci = 4 * c + 2 * (i & 1) + (j & 1);
-                hi[p * CP + c] = Y[((i >> 1) * gp.W + (j >> 1)) * gp.CP + ci];
-                hi[p * CP + Ch + c] = lat[idx];
+// What one wave does at a level.  role 0: critical wave of `tile`; 1: helper
+// wave `slot` (tile slot / S, chunk slot % S); 2: idle (barriers only).
+struct Role {
+    int role, tile, qbase, qend, slot;
+};
+
+__device__ inline Role role_of(const Plan &pl) {
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    Role r = {2, 0, 0, 0, 0};
+    if (wave < pl.T) {
+        r.role = 0;
+        r.tile = wave;
+        r.qend = pl.nq_crit;
+    } else if (wave < pl.NW) {
+        r.role = 1;
+        r.slot = wave - pl.T;
+        r.tile = r.slot / pl.S;
+        r.qbase = pl.nq_crit + (r.slot % pl.S) * pl.chunk;
+        r.qend = imin(pl.nq, r.qbase + pl.chunk);
+    }
+    return r;
+}
+
+__device__ inline int corner_of(const InvArgs &a, int q) { return a.lpu == 1 ? a.corner0 : q; }
+
+// The B operands (prepared weights, signed) of this lane's quads for one
+// layer: lane (kq, li) holds, for group g and element e, the weight of input
+// channel 4 cq + e of quad qbase + 4 g + kq into output channel 16 nt + li.
+template <int NG>
+__device__ inline void load_weights(float (&w)[NG][4], const Plan &pl, const Role &r,
+                                    const float *__restrict__ prep, int corner) {
+    const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
+    const int co = (r.tile / pl.MT) * 16 + li;
+    int oh, ow;
+    self_tap(corner, pl.K, oh, ow);
+    const bool fh = (corner == FINC_BL || corner == FINC_BR);
+    const bool fw = (corner == FINC_TR || corner == FINC_BR);
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+        const int u = r.qbase + 4 * g + kq;
+        const bool valid = u < r.qend && co < pl.C;
+        const int t = u / pl.ncq, cq = u - t * pl.ncq;
+        int dp, dq;
+        tap_of(t, pl.K, dp, dq);
+        const int ka = fh ? oh + dp : oh - dp, kb = fw ? ow + dq : ow - dq;
+        const float sign = (dp == 0 && dq == 0) ? 1.0f : -1.0f;
+        const float *src = prep + ((size_t)(ka * pl.K + kb) * pl.CP + 4 * cq) * pl.CP + co;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            w[g][e] = valid ? sign * src[(size_t)e * pl.CP] : 0.0f;
+    }
+}
+
+// float4 copies / fills by all threads, four in flight per thread
+__device__ inline void zero_floats(float *dst, int n) {   // n multiple of 4, dst 16B aligned
+    float4 *d4 = reinterpret_cast<float4 *>(dst);
+    const float4 z = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int i = threadIdx.x; i < n / 4; i += blockDim.x)
+        d4[i] = z;
+}
+
+// X interior -> Y (both pixel-major, CP channels)
+__device__ inline void copy_solution(float *sm, const Plan &pl) {
+    const int n4 = pl.H * pl.W * pl.CP / 4, cp4 = pl.CP / 4;
+    float4 *Y = reinterpret_cast<float4 *>(sm + pl.offY);
+    const float4 *X = reinterpret_cast<const float4 *>(sm + pl.offX);
+    for (int idx = threadIdx.x; idx < n4; idx += blockDim.x) {
+        const int p = idx / cp4, c4 = idx - p * cp4;
+        const int i = p / pl.W, j = p - i * pl.W;
+        Y[idx] = X[((i + pl.P) * pl.WP + j + pl.P) * cp4 + c4];
+    }
+}
+
+// Load the top level's input (B, C, H, W) -> Y, pixel-major, padded channels
+// 0.  Vector loads along the pixel axis (four pixels of one channel), all of
+// a thread's loads in flight before the first LDS store.
+__device__ inline void load_input(float *sm, const Plan &pl, const float *__restrict__ src) {
+    const int HW = pl.H * pl.W, CP = pl.CP, C = pl.C;
+    float *Y = sm + pl.offY;
+    constexpr int U = 4;
+    if ((HW & 3) == 0) {
+        const int n4 = C * HW / 4, hw4 = HW / 4;
+        const float4 *s4 = reinterpret_cast<const float4 *>(src);
+        for (int base = threadIdx.x; base < n4; base += U * blockDim.x) {
+            float4 v[U];
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                const int idx = base + k * blockDim.x;
+                if (idx < n4)
+                    v[k] = s4[idx];
             }
-        }
-        Y = hi;
-        X = lo;
-        // Padded channels of the input must read as zero (the prepared weights
-        // are zero there, but 0 * junk may be NaN).  X needs nothing: every
-        // pixel of it, padding included, is written before it is read.
-        zero_pad_channels(Y, g);
-        __syncthreads();
-        float *wl = sm + 2 * (size_t)HW * CP;
-        const size_t lstride = prep_layer_floats(C, k);
-        const size_t wfloats = (size_t)k * k * CP * CP;
-        for (int u = a.n_units - 1; u >= 0; --u) {
-            if (lv.scale) {
-                const float *s = lv.scale + (size_t)u * C;
-                const float *bi = lv.bias + (size_t)u * C;
-                for (int idx = threadIdx.x; idx < HW * C; idx += blockDim.x) {
-                    const int p = idx / C, c = idx - p * C;
-                    Y[p * CP + c] = (Y[p * CP + c] - bi[c]) / s[c];
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                const int idx = base + k * blockDim.x;
+                if (idx < n4) {
+                    const int c = idx / hw4, p = 4 * (idx - c * hw4);
+                    Y[(p + 0) * CP + c] = v[k].x;
+                    Y[(p + 1) * CP + c] = v[k].y;
+                    Y[(p + 2) * CP + c] = v[k].z;
+                    Y[(p + 3) * CP + c] = v[k].w;
                 }
             }
-            for (int q = a.lpu - 1; q >= 0; --q) {
-                copy_floats(wl, lv.prep + (size_t)(u * a.lpu + q) * lstride, wfloats);
-                __syncthreads();
-                solve_layer(Y, X, wl, g, a.lpu == 1 ? a.corner0 : q);
-                float *t = Y;
-                Y = X;
-                X = t;
+        }
+    } else {
+        for (int base = threadIdx.x; base < C * HW; base += U * blockDim.x) {
+            float v[U];
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                const int idx = base + k * blockDim.x;
+                if (idx < C * HW)
+                    v[k] = src[idx];
+            }
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                const int idx = base + k * blockDim.x;
+                if (idx < C * HW) {
+                    const int c = idx / HW, p = idx - c * HW;
+                    Y[p * CP + c] = v[k];
+                }
             }
         }
     }
-    store_nchw(a.out + b * (size_t)g.C * g.H * g.W, Y, g);
+    const int pad = CP - C;
+    for (int idx = threadIdx.x; idx < pad * HW; idx += blockDim.x) {
+        const int p = idx / pad;
+        Y[p * CP + C + (idx - p * pad)] = 0.0f;
+    }
+}
+
+// Input of level l: the chain's input at the top; below, concat(unsqueeze(h),
+// z_l) where h is the level above's solution, still in LDS: channel c < C/2
+// of pixel (i, j) is channel 4c + 2(i&1) + (j&1) of h at (i/2, j/2).  Then
+// the solution buffer (with its zero border) and the zero block are cleared.
+__device__ void level_input(const InvArgs &a, int l, float *sm, size_t b) {
+    const Level &lv = a.lv[l];
+    const Plan &pl = lv.pl;
+    const int C = pl.C, CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
+    float *Y = sm + pl.offY;
+    if (l == a.L - 1) {
+        load_input(sm, pl, lv.z + b * (size_t)C * HW);
+    } else {
+        const Plan &up = a.lv[l + 1].pl;
+        const int Ch = C / 2;
+        const float *lat = lv.z + b * (size_t)Ch * HW;
+        for (int idx = threadIdx.x; idx < CP * HW; idx += blockDim.x) {
+            const int c = idx / HW, p = idx - c * HW;
+            const int i = p / W, j = p - i * W;
+            float v = 0.0f;
+            if (c < Ch) {
+                const int ci = 4 * c + 2 * (i & 1) + (j & 1);
+                v = sm[up.offX + (((i >> 1) + up.P) * up.WP + (j >> 1) + up.P) * up.CP + ci];
+            } else if (c < C) {
+                v = lat[(c - Ch) * HW + p];
+            }
+            Y[p * CP + c] = v;
+        }
+        __syncthreads();
+    }
+    zero_floats(sm + pl.offX, pl.offY - pl.offX);
+    zero_floats(sm + pl.offR, pl.offZ + 256 - pl.offR);   // unused slots and Z stay 0
+    __syncthreads();
+}
+
+// All layers of one level for one wave (NG quad groups).  Weights of the
+// next layer are fetched into registers while the current one runs.
+template <int NG, int MAXT>
+__device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role &r, float *sm,
+                            size_t b) {
+    const Level &lv = a.lv[l];
+    constexpr int G = NG > 0 ? NG : 1;
+    // weights of the next layer prefetched into registers when they fit (with
+    // 16 waves a lane has 128 registers)
+    constexpr bool kPrefetch = NG <= 4 && MAXT <= 512;
+    constexpr int GN = kPrefetch ? G : 1;
+    const int ngw =
+        __builtin_amdgcn_readfirstlane(r.role == 2 ? 0 : imax(0, ceil_div(r.qend - r.qbase, 4)));
+    const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
+    const int C = pl.C, CP = pl.CP, H = pl.H, W = pl.W, P = pl.P, WP = pl.WP;
+    const int HW = H * W;
+    const int mt = r.tile % pl.MT, nt = r.tile / pl.MT;
+    const int E = H + W - 1;
+    const int r0 = mt * 16, r1 = imin(mt * 16 + 15, H - 1);
+    float *R = sm + pl.offR;
+    const size_t lstride = prep_layer_floats(C, pl.K);
+    const int nlayers = a.n_units * a.lpu;
+    float w[G][4], wn[GN][4];
+    // layer index n = 0 .. nlayers-1 runs unit u = U-1-n/lpu, block q = lpu-1-n%lpu
+    auto prep_of = [&](int n) {
+        const int u = a.n_units - 1 - n / a.lpu, q = a.lpu - 1 - n % a.lpu;
+        return lv.prep + (size_t)(u * a.lpu + q) * lstride;
+    };
+    auto corner_at = [&](int n) { return corner_of(a, a.lpu - 1 - n % a.lpu); };
+    // first layer's weights in flight while the level's input is loaded
+    if (kPrefetch && nlayers > 0)
+        load_weights<GN>(wn, pl, r, prep_of(0), corner_at(0));
+    level_input(a, l, sm, b);
+    for (int n = 0; n < nlayers; ++n) {
+        const int u = a.n_units - 1 - n / a.lpu, q = a.lpu - 1 - n % a.lpu;
+        if (n > 0) {   // previous layer's solution is this layer's input
+            copy_solution(sm, pl);
+            __syncthreads();
+        }
+        if (q == a.lpu - 1 && lv.scale) {
+            float *Y = sm + pl.offY;
+            const float *s = lv.scale + (size_t)u * C;
+            const float *bi = lv.bias + (size_t)u * C;
+            for (int idx = threadIdx.x; idx < HW * C; idx += blockDim.x) {
+                const int p = idx / C, c = idx - p * C;
+                Y[p * CP + c] = (Y[p * CP + c] - bi[c]) / s[c];
+            }
+            __syncthreads();
+        }
+        const int corner = corner_at(n);
+        if constexpr (kPrefetch) {
+#pragma unroll
+            for (int g = 0; g < NG; ++g)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    w[g][e] = wn[g][e];
+            if (n + 1 < nlayers)
+                load_weights<GN>(wn, pl, r, prep_of(n + 1), corner_at(n + 1));
+        } else {
+            load_weights<G>(w, pl, r, prep_of(n), corner);
+        }
+
+        // --- addresses: every gather and write address is an affine function
+        // of the frame column of its row, which moves by one per diagonal.
+        const bool fh = (corner == FINC_BL || corner == FINC_BR);
+        const bool fw = (corner == FINC_TR || corner == FINC_BR);
+        const int sh = fh ? -1 : 1, sw = fw ? -1 : 1;
+        int oh, ow;
+        self_tap(corner, pl.K, oh, ow);
+        // gather row (frame) i = r0 + li, clamped into the image
+        const int gi = mt * 16 + li;
+        const int gic = imin(gi, H - 1);
+        const int goi = fh ? H - 1 - gic : gic;
+        const int bx0 = pl.offX + ((goi + P) * WP + P) * CP;
+        const int by0 = pl.offY + goi * W * CP;
+        int gbase[G], guse[G];
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+            const int uq = r.qbase + 4 * g + kq;
+            if (uq >= r.qend) {
+                gbase[g] = pl.offZ + 4 * lane;
+                guse[g] = 0;
+            } else {
+                const int t = uq / pl.ncq, cq = uq - t * pl.ncq;
+                int dp, dq;
+                tap_of(t, pl.K, dp, dq);
+                if (dp == 0 && dq == 0)
+                    gbase[g] = by0 + 4 * cq;
+                else
+                    gbase[g] = bx0 + 4 * cq - (dp * sh * WP + dq * sw) * CP;
+                guse[g] = 1;
+            }
+        }
+        // natural column of frame column j (clamped) times CP
+        auto colx = [&](int j) {
+            const int jc = imin(imax(j, 0), W - 1);
+            return __mul24(fw ? W - 1 - jc : jc, CP);
+        };
+        auto gather = [&](int cx, float4 (&av)[G]) {
+#pragma unroll
+            for (int g = 0; g < NG; ++g)
+                if (g < ngw)
+                    av[g] = *reinterpret_cast<const float4 *>(sm + gbase[g] + guse[g] * cx);
+        };
+        // D[output channel 4 kq + rr][row li] of this wave's quads: weights are
+        // the A operand (rows = output channels), gathered inputs the B
+        // operand (columns = frame rows)
+        auto mma = [&](const float4 (&av)[G]) -> f32x4 {
+            f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+            for (int g = 0; g < NG; ++g) {
+                if (g < ngw) {
+                    acc = mfma4(w[g][0], av[g].x, acc);
+                    acc = mfma4(w[g][1], av[g].y, acc);
+                    acc = mfma4(w[g][2], av[g].z, acc);
+                    acc = mfma4(w[g][3], av[g].w, acc);
+                }
+            }
+            return acc;
+        };
+        auto active = [&](int e) { return r0 <= e && e - W + 1 <= r1; };
+        // the critical wave writes channels 16 nt + 4 kq .. +3 of its row's pixel
+        const int wx0 = bx0 + nt * 16 + 4 * kq;
+        const bool wch = nt * 16 + 4 * kq < CP && gi < H;
+        // partial tiles: R[parity][tile][S4 slots][64 lanes][4]
+        const int rstride = pl.T * pl.S4 * 256;
+        const int rown = (r.tile * pl.S4 + (r.role == 1 ? r.slot % pl.S : 0)) * 256 + 4 * lane;
+
+        if (r.role == 1 && active(0)) {
+            float4 av[G];
+            gather(colx(0 - gi), av);
+            *reinterpret_cast<f32x4 *>(R + rown) = mma(av);
+        }
+        __syncthreads();
+        for (int e = 0; e < E; ++e) {
+            if (r.role == 0 && active(e)) {
+                // operands first, then the helpers' partial tiles, so both LDS
+                // latencies overlap the MFMA chain
+                const int j = e - gi;
+                const int cx = colx(j);
+                float4 av[G];
+                gather(cx, av);
+                const f32x4 *Rp = reinterpret_cast<const f32x4 *>(R + (e & 1) * rstride + rown);
+                f32x4 rs = Rp[0] + Rp[64];
+                rs += Rp[128] + Rp[192];
+                for (int s4 = 4; s4 < pl.S4; s4 += 4) {
+                    rs += Rp[s4 * 64] + Rp[(s4 + 1) * 64];
+                    rs += Rp[(s4 + 2) * 64] + Rp[(s4 + 3) * 64];
+                }
+                f32x4 acc = mma(av);
+                acc += rs;
+                if (wch && j >= 0 && j < W)
+                    *reinterpret_cast<f32x4 *>(sm + wx0 + cx) = acc;
+            } else if (r.role == 1 && e + 1 < E && active(e + 1)) {
+                float4 av[G];
+                gather(colx(e + 1 - gi), av);
+                *reinterpret_cast<f32x4 *>(R + ((e + 1) & 1) * rstride + rown) = mma(av);
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// Inverse of a whole chain with the image in LDS from the first load to the
+// last store.  Levels go from the top (l = L-1) down; between levels the
+// solution of the level above is unsqueezed and the level's latent appended
+// behind it (channel split), straight from LDS into the next level's input.
+template <int NG, int MAXT>
+__global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
+    extern __shared__ float sm[];
+    const size_t b = blockIdx.x;
+    for (int l = a.L - 1; l >= 0; --l) {
+        const Level &lv = a.lv[l];
+        const Plan pl = lv.pl;
+        const int CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
+        float *Y = sm + pl.offY;
+        level_waves<NG, MAXT>(a, l, pl, role_of(pl), sm, b);
+        if (a.n_units * a.lpu == 0) {   // no layers at this level: the input passes through
+            for (int idx = threadIdx.x; idx < HW * CP; idx += blockDim.x) {
+                const int p = idx / CP, c = idx - p * CP;
+                const int i = p / W, j = p - i * W;
+                sm[pl.offX + ((i + pl.P) * pl.WP + j + pl.P) * CP + c] = Y[idx];
+            }
+            __syncthreads();
+        }
+    }
+    const Plan &p0 = a.lv[0].pl;
+    const int HW0 = p0.H * p0.W, n0 = p0.C * HW0;
+    float *dst = a.out + b * (size_t)n0;
+    constexpr int U = 4;
+    if ((p0.W & 3) == 0) {   // four pixels of a row, one channel, per vector store
+        const int n4 = n0 / 4, w4 = p0.W / 4, hw4 = HW0 / 4;
+        float4 *d4 = reinterpret_cast<float4 *>(dst);
+        for (int base = threadIdx.x; base < n4; base += U * blockDim.x) {
+            float4 v[U];
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                const int idx = base + k * blockDim.x;
+                if (idx < n4) {
+                    const int c = idx / hw4, q = idx - c * hw4;
+                    const int i = q / w4, j = 4 * (q - i * w4);
+                    const float *x = sm + p0.offX + ((i + p0.P) * p0.WP + j + p0.P) * p0.CP + c;
+                    v[k] = make_float4(x[0], x[p0.CP], x[2 * p0.CP], x[3 * p0.CP]);
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < U; ++k) {
+                const int idx = base + k * blockDim.x;
+                if (idx < n4)
+                    d4[idx] = v[k];
+            }
+        }
+    } else {
+        for (int idx = threadIdx.x; idx < n0; idx += blockDim.x) {
+            const int c = idx / HW0, p = idx - c * HW0;
+            const int i = p / p0.W, j = p - i * p0.W;
+            dst[idx] = sm[p0.offX + ((i + p0.P) * p0.WP + j + p0.P) * p0.CP + c];
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -424,14 +803,25 @@ bool overlap(const void *a, size_t na, const void *b, size_t nb) {
 
 bool aligned256(const void *p) { return ((uintptr_t)p & 255u) == 0; }
 
-size_t inverse_lds_bytes(const InvArgs &a) {
-    size_t m = 0;
+// Plans of every level, LDS size and waves of an inverse chain launch.
+// Returns FINC_EUNSUPPORTED when a level's work split or the level-to-level
+// hand-over does not fit one workgroup.
+int plan_inverse(InvArgs &a, size_t *lds_bytes, int *threads) {
+    int lds = 0, nw = 1;
     for (int l = 0; l < a.L; ++l) {
-        const size_t cp = (size_t)round_up4(a.lv[l].C);
-        const size_t f = 2 * (size_t)a.lv[l].H * a.lv[l].W * cp + (size_t)a.k * a.k * cp * cp;
-        m = f > m ? f : m;
+        Plan &p = a.lv[l].pl;
+        if (!make_plan(p.C, p.H, p.W, p.K, p))
+            return FINC_EUNSUPPORTED;
+        lds = imax(lds, p.lds_floats);
+        nw = imax(nw, p.NW);
+        // the unsqueeze reads the level above's solution while writing this
+        // level's input: the two regions must not overlap
+        if (l + 1 < a.L && a.lv[l + 1].pl.offY > p.offY)
+            return FINC_EUNSUPPORTED;
     }
-    return m * sizeof(float);
+    *lds_bytes = (size_t)lds * sizeof(float);
+    *threads = nw * kWave;
+    return FINC_OK;
 }
 
 size_t chain_lds_bytes(int C, int H, int W, int k) {
@@ -500,17 +890,45 @@ int launch_prep(const float *K, int n, const int *corners, int C, int k, float *
     return FINC_OK;
 }
 
-int launch_inverse_chain(const InvArgs &a, int B, hipStream_t stream) {
-    if (B == 0)
-        return FINC_OK;
-    const size_t lds = inverse_lds_bytes(a);
-    int rc = check_lds(lds);
+// Kernel instances by quad groups per wave (1..kMaxGroups) and workgroup size.
+typedef void (*InvKernel)(InvArgs);
+template <int MAXT>
+InvKernel inverse_instance(int ng) {
+    switch (ng) {
+    case 1: return inverse_chain_kernel<1, MAXT>;
+    case 2: return inverse_chain_kernel<2, MAXT>;
+    case 3: return inverse_chain_kernel<3, MAXT>;
+    case 4: return inverse_chain_kernel<4, MAXT>;
+    case 5: return inverse_chain_kernel<5, MAXT>;
+    case 6: return inverse_chain_kernel<6, MAXT>;
+    case 7: return inverse_chain_kernel<7, MAXT>;
+    default: return inverse_chain_kernel<8, MAXT>;
+    }
+}
+
+int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
+    size_t lds = 0;
+    int threads = 0;
+    int rc = plan_inverse(a, &lds, &threads);
     if (rc != FINC_OK)
         return rc;
-    if (hipFuncSetAttribute((const void *)inverse_chain_kernel,
-                            hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
+    rc = check_lds(lds);
+    if (rc != FINC_OK)
+        return rc;
+    if (B == 0)
+        return FINC_OK;
+    int ng = 1;
+    for (int l = 0; l < a.L; ++l) {
+        const Plan &p = a.lv[l].pl;
+        ng = imax(ng, imax(ceil_div(p.nq_crit, 4), p.chunk / 4));
+    }
+    const InvKernel k = threads <= 256   ? inverse_instance<256>(ng)
+                        : threads <= 512 ? inverse_instance<512>(ng)
+                                         : inverse_instance<1024>(ng);
+    if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds) != hipSuccess)
         (void)hipGetLastError();   // not needed on every runtime; the launch check decides
-    hipLaunchKernelGGL(inverse_chain_kernel, dim3(B), dim3(kThreads), lds, stream, a);
+    hipLaunchKernelGGL(k, dim3(B), dim3(threads), lds, stream, a);
     return launched();
 }
 
@@ -536,6 +954,21 @@ Geo make_geo(int C, int H, int W, int k) {
     g.W = W;
     g.k = k;
     return g;
+}
+
+Level level(const float *z, const void *prep, const float *scale, const float *bias, int C,
+            int H, int W, int k) {
+    Level v;
+    memset(&v, 0, sizeof(v));
+    v.z = z;
+    v.prep = (const float *)prep;
+    v.scale = scale;
+    v.bias = bias;
+    v.pl.C = C;
+    v.pl.H = H;
+    v.pl.W = W;
+    v.pl.K = k;
+    return v;
 }
 
 // x/y overlap rule of the inverse: identical or disjoint.
@@ -657,10 +1090,10 @@ int finc_inverse_prepared(const float *y, float *x, const void *prepared, int B,
         return FINC_EINVAL;
     InvArgs a;
     memset(&a, 0, sizeof(a));
-    a.lv[0] = Level{y, (const float *)prepared, nullptr, nullptr, C, H, W};
+    a.lv[0] = level(y, prepared, nullptr, nullptr, C, H, W, k);
     a.out = x;
     a.L = 1;
-    a.k = k;
+
     a.n_units = 1;
     a.lpu = 1;
     a.corner0 = corner;
@@ -722,10 +1155,10 @@ int finc_unit_inverse_prepared(const float *y, float *x, const void *prepared4, 
         return FINC_EINVAL;
     InvArgs a;
     memset(&a, 0, sizeof(a));
-    a.lv[0] = Level{y, (const float *)prepared4, nullptr, nullptr, C, H, W};
+    a.lv[0] = level(y, prepared4, nullptr, nullptr, C, H, W, k);
     a.out = x;
     a.L = 1;
-    a.k = k;
+
     a.n_units = 1;
     a.lpu = 4;
     a.corner0 = FINC_TL;
@@ -803,14 +1236,14 @@ int finc_stack_inverse_prepared(const float *const *z, float *x, const void *pre
     size_t poff = 0, soff = 0;
     for (int l = 0; l < L; ++l) {
         const int C = C1 << l;
-        a.lv[l] = Level{z[l], (const float *)((const char *)prepared + poff), scale + soff,
-                        bias + soff, C, H1 >> l, W1 >> l};
+        a.lv[l] = level(z[l], (const char *)prepared + poff, scale + soff, bias + soff, C,
+                        H1 >> l, W1 >> l, k);
         poff += stack_level_bytes(l, U, C1, k);
         soff += (size_t)U * C;
     }
     a.out = x;
     a.L = L;
-    a.k = k;
+
     a.n_units = U;
     a.lpu = 4;
     a.corner0 = FINC_TL;

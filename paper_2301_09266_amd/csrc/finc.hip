@@ -254,7 +254,9 @@ struct Plan {
     int MT, NT, T, S, S4, NW;   // row tiles, channel tiles, tiles, helpers per tile (S4 = S
                                 // rounded up to 4: partial-tile slots per tile), waves
     int ncq, nq, nq_crit, chunk;
-    int offX, offY, offR, offZ;  // LDS offsets, floats
+    int regcrit;                 // 1: the critical taps are fed from registers (one channel tile)
+    int offX, offY, offR, offZ, offT;  // LDS offsets (floats): solution, input, partial
+                                       // tiles, zero block, trash block
     int lds_floats;
 };
 
@@ -295,14 +297,20 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p) {
     p.T = p.MT * p.NT;
     p.ncq = p.CP / 4;
     p.nq = K * K * p.ncq;
-    p.nq_crit = K >= 2 ? imin(p.nq, round_up4(2 * p.ncq)) : 0;
+    // With one channel tile the critical wave holds, in its accumulator, all
+    // channels of its rows' previous pixels: the two dp + dq = 1 taps need no
+    // gather.  Otherwise it gathers them (padded to whole quad groups).
+    p.regcrit = (p.NT == 1 && K >= 2) ? 1 : 0;
+    p.nq_crit = K < 2 ? 0 : (p.regcrit ? 2 * p.ncq : imin(p.nq, round_up4(2 * p.ncq)));
     const int rest = p.nq - p.nq_crit;
     const int s_max = kMaxWaves / p.T - 1;
     if (s_max < 1)
         return false;
-    p.S = imax(1, imin(s_max, ceil_div(rest, imax(4, p.nq_crit))));
+    // helpers own about two quad groups each (one wave per SIMD for a tile of
+    // a 12-channel 3x3 layer); the critical wave runs 8 MFMAs per step
+    p.S = imax(1, imin(s_max, ceil_div(rest, 8)));
     p.chunk = round_up4(ceil_div(rest, p.S));
-    if (p.nq_crit > 4 * kMaxGroups || p.chunk > 4 * kMaxGroups)
+    if ((!p.regcrit && p.nq_crit > 4 * kMaxGroups) || p.chunk > 4 * kMaxGroups)
         return false;
     p.NW = p.T * (1 + p.S);
     p.S4 = round_up4(p.S);
@@ -310,7 +318,8 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p) {
     p.offY = (H + 2 * p.P) * p.WP * p.CP;
     p.offR = p.offY + H * W * p.CP;
     p.offZ = p.offR + 2 * p.T * p.S4 * 256;
-    p.lds_floats = p.offZ + 256;
+    p.offT = p.offZ + 256;
+    p.lds_floats = p.offT + 256;
     return true;
 }
 
@@ -384,6 +393,29 @@ __device__ inline void load_weights(float (&w)[NG][4], const Plan &pl, const Rol
 #pragma unroll
         for (int e = 0; e < 4; ++e)
             w[g][e] = valid ? sign * src[(size_t)e * pl.CP] : 0.0f;
+    }
+}
+
+// Weights of the register-fed critical path (one channel tile): group t is
+// tap t of the quad order ((0,1), then (1,0)); lane (kq, li) holds the
+// weight of input channel 4 kq + e into output channel li (A operand).
+template <int NG>
+__device__ inline void load_crit_weights(float (&w)[NG][4], const Plan &pl,
+                                         const float *__restrict__ prep, int corner) {
+    const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
+    int oh, ow;
+    self_tap(corner, pl.K, oh, ow);
+    const bool fh = (corner == FINC_BL || corner == FINC_BR);
+    const bool fw = (corner == FINC_TR || corner == FINC_BR);
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+        int dp, dq;
+        tap_of(t, pl.K, dp, dq);
+        const int ka = fh ? oh + dp : oh - dp, kb = fw ? ow + dq : ow - dq;
+        const float *src = prep + ((size_t)(ka * pl.K + kb) * pl.CP + 4 * kq) * pl.CP + li;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            w[t][e] = (li < pl.C && 4 * kq + e < pl.C) ? -src[(size_t)e * pl.CP] : 0.0f;
     }
 }
 
@@ -508,8 +540,10 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
     // 16 waves a lane has 128 registers)
     constexpr bool kPrefetch = NG <= 4 && MAXT <= 512;
     constexpr int GN = kPrefetch ? G : 1;
-    const int ngw =
-        __builtin_amdgcn_readfirstlane(r.role == 2 ? 0 : imax(0, ceil_div(r.qend - r.qbase, 4)));
+    // the register-fed critical wave owns the two dp + dq = 1 taps as groups
+    const bool regc = pl.regcrit && r.role == 0;
+    const int ngw = __builtin_amdgcn_readfirstlane(
+        regc ? 2 : (r.role == 2 ? 0 : imax(0, ceil_div(r.qend - r.qbase, 4))));
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int C = pl.C, CP = pl.CP, H = pl.H, W = pl.W, P = pl.P, WP = pl.WP;
     const int HW = H * W;
@@ -526,9 +560,15 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
         return lv.prep + (size_t)(u * a.lpu + q) * lstride;
     };
     auto corner_at = [&](int n) { return corner_of(a, a.lpu - 1 - n % a.lpu); };
+    auto fetch = [&](auto &dst, int n) {
+        if (regc)
+            load_crit_weights(dst, pl, prep_of(n), corner_at(n));
+        else
+            load_weights(dst, pl, r, prep_of(n), corner_at(n));
+    };
     // first layer's weights in flight while the level's input is loaded
     if (kPrefetch && nlayers > 0)
-        load_weights<GN>(wn, pl, r, prep_of(0), corner_at(0));
+        fetch(wn, 0);
     level_input(a, l, sm, b);
     for (int n = 0; n < nlayers; ++n) {
         const int u = a.n_units - 1 - n / a.lpu, q = a.lpu - 1 - n % a.lpu;
@@ -554,9 +594,9 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
                 for (int e = 0; e < 4; ++e)
                     w[g][e] = wn[g][e];
             if (n + 1 < nlayers)
-                load_weights<GN>(wn, pl, r, prep_of(n + 1), corner_at(n + 1));
+                fetch(wn, n + 1);
         } else {
-            load_weights<G>(w, pl, r, prep_of(n), corner);
+            fetch(w, n);
         }
 
         // --- addresses: every gather and write address is an affine function
@@ -590,32 +630,42 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
                 guse[g] = 1;
             }
         }
-        // natural column of frame column j (clamped) times CP
-        auto colx = [&](int j) {
+        // Rows of the frame that have not started (frame column j < 0, or rows
+        // below the image) gather zeros, so their partial tiles and carried
+        // accumulators are exactly 0 and no masking is needed; finished rows
+        // (j >= W) gather clamped garbage that only ever reaches finished rows.
+        // Every gather, load and write is unconditional (no divergent branch on
+        // the critical path); rows that must not be written go to a trash block.
+        // Each role runs its own step loop (same barrier count), so the
+        // critical loop carries nothing but its own work.
+        const int zaddr = pl.offZ + 4 * lane, taddr = pl.offT + 4 * lane;
+        const int dcol = fw ? -CP : CP;   // address step of one frame column
+        auto colx = [&](int j) {   // natural column of frame column j (clamped), times CP
             const int jc = imin(imax(j, 0), W - 1);
             return __mul24(fw ? W - 1 - jc : jc, CP);
         };
-        auto gather = [&](int cx, float4 (&av)[G]) {
+        // D[output channel 4 kq + rr][row li] of this wave's quads: weights are
+        // the A operand (rows = output channels), gathered inputs the B
+        // operand (columns = frame rows); c is the initial accumulator
+        auto gather_mma = [&](int j, f32x4 c) -> f32x4 {
+            const int cx = colx(j);
+            const bool live = j >= 0 && gi < H;
+            float4 av[G];
 #pragma unroll
             for (int g = 0; g < NG; ++g)
                 if (g < ngw)
-                    av[g] = *reinterpret_cast<const float4 *>(sm + gbase[g] + guse[g] * cx);
-        };
-        // D[output channel 4 kq + rr][row li] of this wave's quads: weights are
-        // the A operand (rows = output channels), gathered inputs the B
-        // operand (columns = frame rows)
-        auto mma = [&](const float4 (&av)[G]) -> f32x4 {
-            f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+                    av[g] = *reinterpret_cast<const float4 *>(
+                        sm + (live ? gbase[g] + guse[g] * cx : zaddr));
 #pragma unroll
             for (int g = 0; g < NG; ++g) {
                 if (g < ngw) {
-                    acc = mfma4(w[g][0], av[g].x, acc);
-                    acc = mfma4(w[g][1], av[g].y, acc);
-                    acc = mfma4(w[g][2], av[g].z, acc);
-                    acc = mfma4(w[g][3], av[g].w, acc);
+                    c = mfma4(w[g][0], av[g].x, c);
+                    c = mfma4(w[g][1], av[g].y, c);
+                    c = mfma4(w[g][2], av[g].z, c);
+                    c = mfma4(w[g][3], av[g].w, c);
                 }
             }
-            return acc;
+            return c;
         };
         auto active = [&](int e) { return r0 <= e && e - W + 1 <= r1; };
         // the critical wave writes channels 16 nt + 4 kq .. +3 of its row's pixel
@@ -624,38 +674,107 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
         // partial tiles: R[parity][tile][S4 slots][64 lanes][4]
         const int rstride = pl.T * pl.S4 * 256;
         const int rown = (r.tile * pl.S4 + (r.role == 1 ? r.slot % pl.S : 0)) * 256 + 4 * lane;
-
-        if (r.role == 1 && active(0)) {
-            float4 av[G];
-            gather(colx(0 - gi), av);
-            *reinterpret_cast<f32x4 *>(R + rown) = mma(av);
-        }
-        __syncthreads();
-        for (int e = 0; e < E; ++e) {
-            if (r.role == 0 && active(e)) {
-                // operands first, then the helpers' partial tiles, so both LDS
-                // latencies overlap the MFMA chain
-                const int j = e - gi;
-                const int cx = colx(j);
-                float4 av[G];
-                gather(cx, av);
-                const f32x4 *Rp = reinterpret_cast<const f32x4 *>(R + (e & 1) * rstride + rown);
-                f32x4 rs = Rp[0] + Rp[64];
-                rs += Rp[128] + Rp[192];
-                for (int s4 = 4; s4 < pl.S4; s4 += 4) {
-                    rs += Rp[s4 * 64] + Rp[(s4 + 1) * 64];
-                    rs += Rp[(s4 + 2) * 64] + Rp[(s4 + 3) * 64];
-                }
-                f32x4 acc = mma(av);
-                acc += rs;
-                if (wch && j >= 0 && j < W)
-                    *reinterpret_cast<f32x4 *>(sm + wx0 + cx) = acc;
-            } else if (r.role == 1 && e + 1 < E && active(e + 1)) {
-                float4 av[G];
-                gather(colx(e + 1 - gi), av);
-                *reinterpret_cast<f32x4 *>(R + ((e + 1) & 1) * rstride + rown) = mma(av);
+        // the critical wave's partial-tile sum: the first slot seeds the MFMA
+        // accumulator, the others are added to it
+        auto partial_rest = [&](const f32x4 *Rp) {
+            f32x4 rs = Rp[64] + Rp[128];
+            rs += Rp[192];
+            for (int s4 = 4; s4 < pl.S4; s4 += 4) {
+                rs += Rp[s4 * 64] + Rp[(s4 + 1) * 64];
+                rs += Rp[(s4 + 2) * 64] + Rp[(s4 + 3) * 64];
             }
+            return rs;
+        };
+
+        if (r.role == 1) {
+            // helper: during step e, its share of diagonal e + 1
+            f32x4 *Rw = reinterpret_cast<f32x4 *>(R + rown);
+            const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+            if (active(0))
+                Rw[0] = gather_mma(0 - gi, zero);
             __syncthreads();
+            for (int e = 0; e < E; ++e) {
+                if (e + 1 < E && active(e + 1))
+                    Rw[((e + 1) & 1) * (rstride / 4)] = gather_mma(e + 1 - gi, zero);
+                __syncthreads();
+            }
+        } else if (r.role == 0 && regc) {
+            // register-fed critical wave.  dprev: lane (kq, li) holds channels
+            // 4 kq .. +3 of row li's pixel of the previous diagonal (0 for rows
+            // not started)
+            __syncthreads();
+            f32x4 dprev = {0.0f, 0.0f, 0.0f, 0.0f};
+            int j = -gi;   // frame column of row gi at diagonal 0
+            // write address of frame column j (the affine form; used only while
+            // 0 <= j < W)
+            int wcol = wx0 + (fw ? W - 1 : 0) * CP + j * dcol;
+            // lane li = 0 of a lower tile reads the tile above's last row
+            // (solved in the previous step, in LDS); other lanes read zeros
+            const int ui = mt * 16 - 1;
+            const int uoi = fh ? H - 1 - imax(ui, 0) : imax(ui, 0);
+            int ju = -16 * mt;   // frame column of row 16 mt (and of the row above it) at diagonal 0
+            int ucol = pl.offX + ((uoi + P) * WP + P + (fw ? W - 1 : 0)) * CP + 4 * kq + ju * dcol;
+            const f32x4 *R0 = reinterpret_cast<const f32x4 *>(R + rown);
+            for (int e = 0; e < E; ++e) {
+                if (active(e)) {
+                    const f32x4 *Rp = R0 + (e & 1) * (rstride / 4);
+                    f32x4 up = {0.0f, 0.0f, 0.0f, 0.0f};
+                    if (mt > 0)
+                        up = *reinterpret_cast<const f32x4 *>(
+                            sm + ((li == 0 && (unsigned)ju < (unsigned)W) ? ucol : zaddr));
+                    f32x4 acc = Rp[0];
+                    const f32x4 rs = partial_rest(Rp);
+                    // tap (0,1): own row, previous column; tap (1,0): row above,
+                    // same column -- the neighbouring lane's previous result
+                    if constexpr (G >= 2) {   // (instances with G < 2 never get regc)
+#pragma unroll
+                        for (int e4 = 0; e4 < 4; ++e4)
+                            acc = mfma4(w[0][e4], dprev[e4], acc);
+#pragma unroll
+                        for (int e4 = 0; e4 < 4; ++e4) {
+                            // lane li takes lane li-1's value (row_shr:1 inside each
+                            // row of 16 lanes); lane 0 keeps `up`.  Elements are
+                            // copied to scalars first: this compiler bit-casts a
+                            // vector element lvalue as element 0.
+                            const float de = dprev[e4], ue = up[e4];
+                            const float sh1 = __int_as_float(__builtin_amdgcn_update_dpp(
+                                __float_as_int(ue), __float_as_int(de), 0x111, 0xf, 0xf, false));
+                            acc = mfma4(w[1][e4], sh1, acc);
+                        }
+                    }
+                    acc += rs;
+                    const bool ok = wch && (unsigned)j < (unsigned)W;
+                    *reinterpret_cast<f32x4 *>(sm + (ok ? wcol : taddr)) = acc;
+                    dprev = acc;
+                }
+                j += 1;
+                wcol += dcol;
+                ju += 1;
+                ucol += dcol;
+                __syncthreads();
+            }
+        } else if (r.role == 0) {
+            // critical wave that gathers its dp + dq = 1 taps from LDS (several
+            // channel tiles: the previous diagonal's channels sit in several
+            // waves)
+            __syncthreads();
+            const f32x4 *R0 = reinterpret_cast<const f32x4 *>(R + rown);
+            for (int e = 0; e < E; ++e) {
+                if (active(e)) {
+                    const int j = e - gi;
+                    const f32x4 *Rp = R0 + (e & 1) * (rstride / 4);
+                    const f32x4 rs = partial_rest(Rp);
+                    f32x4 acc = gather_mma(j, Rp[0]);
+                    acc += rs;
+                    const bool ok = wch && (unsigned)j < (unsigned)W;
+                    *reinterpret_cast<f32x4 *>(sm + (ok ? wx0 + colx(j) : taddr)) = acc;
+                }
+                __syncthreads();
+            }
+        } else {
+            __syncthreads();
+            for (int e = 0; e < E; ++e)
+                __syncthreads();
         }
     }
 }
@@ -920,7 +1039,7 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     int ng = 1;
     for (int l = 0; l < a.L; ++l) {
         const Plan &p = a.lv[l].pl;
-        ng = imax(ng, imax(ceil_div(p.nq_crit, 4), p.chunk / 4));
+        ng = imax(ng, imax(p.regcrit ? 2 : ceil_div(p.nq_crit, 4), p.chunk / 4));
     }
     const InvKernel k = threads <= 256   ? inverse_instance<256>(ng)
                         : threads <= 512 ? inverse_instance<512>(ng)

@@ -86,8 +86,8 @@ class LayerStep:
         self.finc.prepare(self.K, [self.corner], out=self.prep)
 
     def forward(self):
-        self.finc.forward(self.x, self.K, self.corner, out=self.y)
-        self.finc.logdet(self.K, self.corner, self.H, self.W, out=self.ld)
+        # y and log|det| from one launch
+        self.finc.forward(self.x, self.K, self.corner, out=self.y, logdet=self.ld)
 
     def inverse(self):
         self.finc.inverse_prepared(self.y, self.prep, self.k, self.corner, out=self.xr)

@@ -32,7 +32,6 @@
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kThreads = 256;   // 4 waves, one per SIMD of a CU
 constexpr int kPrepThreads = 64;
 constexpr int kMaxLayersPerPrep = 64;
 constexpr int kMaxLevels = 8;
@@ -93,9 +92,13 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
     }
     const int ka = s / k, kb = s - ka * k;
     const bool is_self = (ka == sh && kb == sw);
+    // right-hand side first (all loads in flight), then forward substitution
+    // in place
+    for (int co = 0; co < C; ++co)
+        z[co * kPrepThreads + tid] = is_self ? (co == ci ? 1.0 : 0.0)
+                                             : (double)K[((size_t)(co * C + ci) * k + ka) * k + kb];
     for (int co = 0; co < C; ++co) {
-        double t = is_self ? (co == ci ? 1.0 : 0.0)
-                           : (double)K[((size_t)(co * C + ci) * k + ka) * k + kb];
+        double t = z[co * kPrepThreads + tid];
         for (int m = 0; m < co; ++m)
             t -= L[co * C + m] * z[m * kPrepThreads + tid];
         z[co * kPrepThreads + tid] = t / L[co * C + co];
@@ -130,85 +133,6 @@ __global__ __launch_bounds__(kWave) void logdet_kernel(const float *K, int n, in
     }
     if (tid == 0)
         out[0] = (double)H * (double)W * red[0];
-}
-
-// ---------------------------------------------------------------------------
-// Shared pieces of the LDS-resident kernels.
-// ---------------------------------------------------------------------------
-struct Geo {
-    int C, CP, H, W, k;
-};
-
-// Lane mapping: a wave is cut into groups of CP lanes, one group per pixel,
-// lane c of a group computes output channel c.  All lanes of a pixel sit in
-// one wave.
-struct LaneMap {
-    int group, c, per_wave, stride;
-    bool active;
-};
-
-__device__ inline LaneMap lane_map(int CP) {
-    LaneMap m;
-    const int lane = threadIdx.x & (kWave - 1);
-    const int wave = threadIdx.x / kWave;
-    m.per_wave = kWave / CP;
-    m.group = lane / CP;
-    m.c = lane - m.group * CP;
-    m.active = m.group < m.per_wave;
-    m.stride = (blockDim.x / kWave) * m.per_wave;
-    m.group += wave * m.per_wave;
-    return m;
-}
-
-// Contiguous run of C (padded to CP) inputs times one weight column.  The
-// run is split over four accumulators (c_in mod 4), joined pairwise: four
-// independent FMA chains, and a rounding error that grows with C/4 instead of
-// C (a single chain over a 48-channel unit loses ~1e-4 in a round trip).
-__device__ inline float dot_run(const float *__restrict__ w, const float *__restrict__ v,
-                                int CP) {
-    float q0 = 0.0f, q1 = 0.0f, q2 = 0.0f, q3 = 0.0f;
-    for (int ci = 0; ci < CP; ci += 4) {
-        const float4 x = *reinterpret_cast<const float4 *>(v + ci);
-        q0 = fmaf(w[(ci + 0) * CP], x.x, q0);
-        q1 = fmaf(w[(ci + 1) * CP], x.y, q1);
-        q2 = fmaf(w[(ci + 2) * CP], x.z, q2);
-        q3 = fmaf(w[(ci + 3) * CP], x.w, q3);
-    }
-    return (q0 + q1) + (q2 + q3);
-}
-
-__device__ inline void load_nchw(float *dst, const float *__restrict__ src, const Geo &g) {
-    const int HW = g.H * g.W;
-    for (int idx = threadIdx.x; idx < g.C * HW; idx += blockDim.x) {
-        const int c = idx / HW, p = idx - c * HW;
-        dst[p * g.CP + c] = src[idx];
-    }
-}
-
-__device__ inline void zero_pad_channels(float *buf, const Geo &g) {
-    const int pad = g.CP - g.C;
-    if (!pad)
-        return;
-    const int HW = g.H * g.W;
-    for (int idx = threadIdx.x; idx < HW * pad; idx += blockDim.x) {
-        const int p = idx / pad;
-        buf[p * g.CP + g.C + (idx - p * pad)] = 0.0f;
-    }
-}
-
-__device__ inline void store_nchw(float *__restrict__ dst, const float *src, const Geo &g) {
-    const int HW = g.H * g.W;
-    for (int idx = threadIdx.x; idx < g.C * HW; idx += blockDim.x) {
-        const int c = idx / HW, p = idx - c * HW;
-        dst[idx] = src[p * g.CP + c];
-    }
-}
-
-__device__ inline void copy_floats(float *dst, const float *__restrict__ src, size_t n) {
-    const float4 *s4 = reinterpret_cast<const float4 *>(src);
-    float4 *d4 = reinterpret_cast<float4 *>(dst);
-    for (size_t i = threadIdx.x; i < n / 4; i += blockDim.x)
-        d4[i] = s4[i];
 }
 
 // ---------------------------------------------------------------------------
@@ -838,69 +762,169 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Forward of n layers inside LDS (n = 1: one block; n = 4: a unit).
+// Forward (Sec. 3 convolution with the Sec. 4.1 corner padding) as MFMA
+// contractions: for a tile of 16 pixels and 16 output channels
+//     D[c_out][pixel] = sum_{tap, c_in} K[c_out][c_in][tap] x[c_in][pixel + tap]
+// over k = (tap, input-channel quad), the inputs gathered from a zero-bordered
+// LDS copy of the image (out-of-image taps read the border) and the masked
+// weights staged in LDS in the MFMA fragment layout.  A single layer splits
+// each image into blocks of rows (with the k-1 halo rows) so that the grid
+// covers the chip; a unit keeps the image in LDS across its four layers.
 // ---------------------------------------------------------------------------
+struct FwdPlan {
+    int C, CP, H, W, K, P, WP;
+    int NT, ncq, nq, NG;         // channel tiles, quads per tile (all taps), quad groups
+    int RB, nblk;                // rows per block, blocks per image
+    int offI, offO, offW, offD;  // LDS floats: input rows (RB + 2P) x WP x CP, output
+                                 // (chains only), weight fragments, quad offsets (ints)
+    int lds_floats;
+    int n, corner0;              // layers (1, or 4 for a unit: TL, TR, BL, BR)
+};
+
 struct FwdArgs {
     const float *in;
     float *out;
     const float *K;   // n OIHW tensors
-    Geo g;
-    int n, corner0;
+    double *logdet;   // optional: H W sum over layers and channels of log|K[c,c,self]|
+    FwdPlan fp;
 };
 
-__global__ __launch_bounds__(kThreads) void forward_chain_kernel(FwdArgs a) {
+constexpr int kFwdThreads = 256;
+constexpr int kNoQuad = 1 << 30;   // quad offset marker: padding quad (zero weights)
+
+__global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     extern __shared__ float sm[];
-    const Geo g = a.g;
-    const int C = g.C, CP = g.CP, H = g.H, W = g.W, HW = H * W, k = g.k, kk = k * k;
-    float *bufA = sm;
-    float *bufB = sm + HW * CP;
-    float *wl = sm + 2 * HW * CP;
-    const size_t b = blockIdx.x;
-    const size_t img = (size_t)C * HW;
-    load_nchw(bufA, a.in + b * img, g);
-    zero_pad_channels(bufA, g);
-    zero_pad_channels(bufB, g);
-    float *Xi = bufA, *Yo = bufB;
-    const LaneMap m = lane_map(CP);
-    for (int q = 0; q < a.n; ++q) {
-        const int corner = a.n == 1 ? a.corner0 : q;
+    const FwdPlan &fp = a.fp;
+    const int C = fp.C, CP = fp.CP, H = fp.H, W = fp.W, K = fp.K, P = fp.P, WP = fp.WP;
+    const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int nwaves = blockDim.x >> 6;
+    const int b = blockIdx.x / fp.nblk, blk = blockIdx.x - b * fp.nblk;
+    const int i0 = blk * fp.RB, rb = imin(H, i0 + fp.RB) - i0;
+    const int npix = rb * W, ntile = ceil_div(npix, 16), nitem = ntile * fp.NT;
+    float *X = sm + fp.offI;
+    float4 *Wf = reinterpret_cast<float4 *>(sm + fp.offW);
+    int *Dq = reinterpret_cast<int *>(sm + fp.offD);
+    const size_t HW = (size_t)H * W;
+    const float *xb = a.in + (size_t)b * C * HW;
+    float *yb = a.out + (size_t)b * C * HW;
+    // zero-bordered input rows i0 - P .. i0 + rb + P - 1 (the block's rows and
+    // the halo its taps reach; rows outside the image stay zero)
+    zero_floats(X, (rb + 2 * P) * WP * CP);
+    __syncthreads();
+    const int lo = imax(0, i0 - P), hi = imin(H, i0 + rb + P), nr = hi - lo;
+    for (int idx = threadIdx.x; idx < C * nr * W; idx += blockDim.x) {
+        const int c = idx / (nr * W), p = idx - c * (nr * W);
+        const int ir = p / W, j = p - ir * W;
+        const int il = lo + ir - i0;   // row relative to the block, -P .. rb + P - 1
+        X[((il + P) * WP + j + P) * CP + c] = xb[c * HW + (size_t)(lo + ir) * W + j];
+    }
+    double ld_acc = 0.0;
+    for (int q = 0; q < fp.n; ++q) {
+        const int corner = fp.n == 1 ? fp.corner0 : q;
         int oh, ow;
-        self_tap(corner, k, oh, ow);
-        const float *K = a.K + (size_t)q * C * C * kk;
-        // weights transposed to [s][c_in][c_out] with the channel mask applied
-        for (int idx = threadIdx.x; idx < kk * CP * CP; idx += blockDim.x) {
-            const int s = idx / (CP * CP), r = idx - s * CP * CP;
-            const int ci = r / CP, co = r - ci * CP;
-            const int ka = s / k, kb = s - ka * k;
-            const bool keep = ci < C && co < C && !(ka == oh && kb == ow && ci > co);
-            wl[idx] = keep ? K[((size_t)(co * C + ci) * k + ka) * k + kb] : 0.0f;
+        self_tap(corner, K, oh, ow);
+        const float *Kq = a.K + (size_t)q * C * C * K * K;
+        // weight fragments: Wf[(nt NG + g) 64 + lane].e = K[co][ci][tap] for
+        // co = 16 nt + li, quad u = 4 g + kq (tap u / ncq, ci = 4 (u % ncq) + e),
+        // the channel mask applied (self tap: ci <= co only)
+        for (int idx = threadIdx.x; idx < fp.NT * fp.NG * 64; idx += blockDim.x) {
+            const int f = idx >> 6, ln = idx & 63;
+            const int nt = f / fp.NG, g = f - nt * fp.NG;
+            const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
+            const int t = u / fp.ncq, cq = u - t * fp.ncq;
+            const int ka = t / K, kb = t - ka * K;
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int ci = 4 * cq + e;
+                const bool keep = u < fp.nq && co < C && ci < C && !(ka == oh && kb == ow && ci > co);
+                v[e] = keep ? Kq[((size_t)(co * C + ci) * K + ka) * K + kb] : 0.0f;
+            }
+            Wf[idx] = make_float4(v[0], v[1], v[2], v[3]);
+        }
+        // gather offset of quad u relative to the output pixel's address (taps
+        // reach up/left too: offsets are signed); padding quads get kNoQuad
+        for (int u = threadIdx.x; u < fp.NG * 4; u += blockDim.x) {
+            const int t = u / fp.ncq, cq = u - t * fp.ncq;
+            const int ka = t / K, kb = t - ka * K;
+            Dq[u] = u < fp.nq ? ((ka - oh) * WP + (kb - ow)) * CP + 4 * cq : kNoQuad;
         }
         __syncthreads();
-        if (m.active) {
-            for (int p = m.group; p < HW; p += m.stride) {
-                const int i = p / W, j = p - i * W;
-                float acc = 0.0f;
-                for (int ka = 0; ka < k; ++ka) {
-                    const int ii = i + ka - oh;
-                    if (ii < 0 || ii >= H)
-                        continue;
-                    for (int kb = 0; kb < k; ++kb) {
-                        const int jj = j + kb - ow;
-                        if (jj < 0 || jj >= W)
-                            continue;
-                        acc += dot_run(wl + (size_t)(ka * k + kb) * CP * CP + m.c,
-                                       Xi + (ii * W + jj) * CP, CP);
+        // log|det| rides along: block 0's first wave sums log|K[c,c,self]| over
+        // the layers from the staged weights (self tap is quad t = oh K + ow)
+        if (a.logdet && blockIdx.x == 0 && wave == 0) {
+            double v = 0.0;
+            for (int c = lane; c < C; c += 64) {
+                const int u = (oh * K + ow) * fp.ncq + (c >> 2);
+                const int g = u >> 2, l = (u & 3) * 16 + (c & 15);
+                const float4 wv = Wf[((c >> 4) * fp.NG + g) * 64 + l];
+                const float d = (c & 3) == 0 ? wv.x : (c & 3) == 1 ? wv.y : (c & 3) == 2 ? wv.z : wv.w;
+                v += log(fabs((double)d));
+            }
+            for (int off = 32; off > 0; off >>= 1)
+                v += __shfl_xor(v, off);
+            if (lane == 0)
+                ld_acc += v;
+        }
+        const bool last = q == fp.n - 1;
+        float *Yo = sm + fp.offO;
+        for (int item = wave; item < nitem; item += nwaves) {
+            const int tile = item / fp.NT, nt = item - tile * fp.NT;
+            const int p = tile * 16 + li;
+            const bool valid = p < npix;
+            const int pc = valid ? p : 0;
+            const int il = pc / W, j = pc - il * W;
+            const int base = ((il + P) * WP + j + P) * CP;
+            const int zaddr = fp.offW;   // any valid address: its products meet zero weights
+            // four accumulators over the quad groups (group g -> g mod 4), joined
+            // pairwise: the rounding chain is a quarter as long as a single one
+            f32x4 part[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                part[v] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            for (int g0 = 0; g0 < fp.NG; g0 += 4) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int g = g0 + v;
+                    if (g < fp.NG) {
+                        const int d = Dq[4 * g + kq];
+                        const float4 xv = *reinterpret_cast<const float4 *>(
+                            sm + (d != kNoQuad ? fp.offI + base + d : zaddr));
+                        const float4 wv = Wf[(nt * fp.NG + g) * 64 + lane];
+                        part[v] = mfma4(wv.x, xv.x, part[v]);
+                        part[v] = mfma4(wv.y, xv.y, part[v]);
+                        part[v] = mfma4(wv.z, xv.z, part[v]);
+                        part[v] = mfma4(wv.w, xv.w, part[v]);
                     }
                 }
-                Yo[p * CP + m.c] = m.c < C ? acc : 0.0f;
+            }
+            const f32x4 acc = (part[0] + part[1]) + (part[2] + part[3]);
+            const int co0 = nt * 16 + 4 * kq;
+            if (last) {
+                if (valid) {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (co0 + r < C)
+                            yb[(co0 + r) * HW + (size_t)(i0 + il) * W + j] = acc[r];
+                }
+            } else if (valid && co0 < CP) {
+                *reinterpret_cast<f32x4 *>(Yo + (size_t)p * CP + co0) = acc;
             }
         }
-        __syncthreads();
-        float *t = Xi;
-        Xi = Yo;
-        Yo = t;
+        if (!last) {   // this layer's output is the next one's input
+            __syncthreads();
+            for (int idx = threadIdx.x; idx < npix * CP / 4; idx += blockDim.x) {
+                const int p = idx / (CP / 4), c4 = idx - p * (CP / 4);
+                const int il = p / W, j = p - il * W;
+                reinterpret_cast<float4 *>(X)[((il + P) * WP + j + P) * (CP / 4) + c4] =
+                    reinterpret_cast<const float4 *>(Yo)[idx];
+            }
+            __syncthreads();
+        }
     }
-    store_nchw(a.out + b * img, Xi, g);
+    if (a.logdet && blockIdx.x == 0 && threadIdx.x == 0)
+        a.logdet[0] = (double)H * (double)W * ld_acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -943,9 +967,39 @@ int plan_inverse(InvArgs &a, size_t *lds_bytes, int *threads) {
     return FINC_OK;
 }
 
-size_t chain_lds_bytes(int C, int H, int W, int k) {
-    const size_t cp = (size_t)round_up4(C);
-    return (2 * (size_t)H * W * cp + (size_t)k * k * cp * cp) * sizeof(float);
+// Work split and LDS layout of a forward launch: n = 1 splits each image into
+// blocks of rows (about 4 pixel tiles a block, and at least ~512 blocks when
+// the batch allows); a unit (n = 4) keeps whole images.
+FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B) {
+    FwdPlan p;
+    memset(&p, 0, sizeof(p));
+    p.C = C;
+    p.CP = round_up4(C);
+    p.H = H;
+    p.W = W;
+    p.K = K;
+    p.P = K - 1;
+    p.WP = W + 2 * p.P;
+    p.NT = ceil_div(p.CP, 16);
+    p.ncq = p.CP / 4;
+    p.nq = K * K * p.ncq;
+    p.NG = ceil_div(p.nq, 4);
+    p.n = n;
+    p.corner0 = corner0;
+    if (n == 1) {
+        p.RB = imax(1, imin(H, ceil_div(64, W)));
+        while (p.RB > 1 && (long long)B * ceil_div(H, p.RB) < 512)
+            p.RB /= 2;
+    } else {
+        p.RB = H;
+    }
+    p.nblk = ceil_div(H, p.RB);
+    p.offI = 0;
+    p.offO = (p.RB + 2 * p.P) * p.WP * p.CP;
+    p.offW = p.offO + (n > 1 ? H * W * p.CP : 0);
+    p.offD = p.offW + p.NT * p.NG * 256;
+    p.lds_floats = p.offD + round_up4(4 * p.NG);
+    return p;
 }
 
 size_t prep_lds_bytes(int C) {
@@ -1031,11 +1085,11 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     int rc = plan_inverse(a, &lds, &threads);
     if (rc != FINC_OK)
         return rc;
+    if (B == 0)
+        return FINC_OK;
     rc = check_lds(lds);
     if (rc != FINC_OK)
         return rc;
-    if (B == 0)
-        return FINC_OK;
     int ng = 1;
     for (int l = 0; l < a.L; ++l) {
         const Plan &p = a.lv[l].pl;
@@ -1051,28 +1105,26 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     return launched();
 }
 
-int launch_forward_chain(const FwdArgs &a, int B, hipStream_t stream) {
+int launch_forward(const float *x, float *y, const float *K, double *logdet, int B, int C,
+                   int H, int W, int k, int n, int corner0, hipStream_t stream) {
+    FwdArgs a;
+    a.in = x;
+    a.out = y;
+    a.K = K;
+    a.logdet = logdet;
+    a.fp = make_fwd_plan(C, H, W, k, n, corner0, B);
     if (B == 0)
         return FINC_OK;
-    const size_t lds = chain_lds_bytes(a.g.C, a.g.H, a.g.W, a.g.k);
+    const size_t lds = (size_t)a.fp.lds_floats * sizeof(float);
     int rc = check_lds(lds);
     if (rc != FINC_OK)
         return rc;
-    if (hipFuncSetAttribute((const void *)forward_chain_kernel,
+    if (hipFuncSetAttribute((const void *)forward_kernel,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
         (void)hipGetLastError();   // not needed on every runtime; the launch check decides
-    hipLaunchKernelGGL(forward_chain_kernel, dim3(B), dim3(kThreads), lds, stream, a);
+    hipLaunchKernelGGL(forward_kernel, dim3((unsigned)B * a.fp.nblk), dim3(kFwdThreads), lds,
+                       stream, a);
     return launched();
-}
-
-Geo make_geo(int C, int H, int W, int k) {
-    Geo g;
-    g.C = C;
-    g.CP = round_up4(C);
-    g.H = H;
-    g.W = W;
-    g.k = k;
-    return g;
 }
 
 Level level(const float *z, const void *prep, const float *scale, const float *bias, int C,
@@ -1172,21 +1224,16 @@ int finc_prepare(const float *K, int n_layers, const int *corners, int C, int k,
     return launch_prep(K, n_layers, corners, C, k, (float *)prepared, stream);
 }
 
-int finc_forward(const float *x, float *y, const float *K, int B, int C, int H, int W,
-                 int k, int corner, hipStream_t stream) {
+int finc_forward(const float *x, float *y, const float *K, double *logdet, int B, int C, int H,
+                 int W, int k, int corner, hipStream_t stream) {
     if (!valid_shape(B, C, H, W, k) || !valid_corner(corner) || !x || !y || !K)
         return FINC_EINVAL;
     const size_t bytes = (size_t)B * C * H * W * sizeof(float);
     if (overlap(x, bytes, y, bytes))
         return FINC_EINVAL;
-    FwdArgs a;
-    a.in = x;
-    a.out = y;
-    a.K = K;
-    a.g = make_geo(C, H, W, k);
-    a.n = 1;
-    a.corner0 = corner;
-    return launch_forward_chain(a, B, stream);
+    if (logdet && B == 0)   // nothing to run the forward on: log|det| on its own
+        return finc_logdet(K, C, k, corner, H, W, logdet, stream);
+    return launch_forward(x, y, K, logdet, B, C, H, W, k, 1, corner, stream);
 }
 
 int finc_logdet(const float *K, int C, int k, int corner, int H, int W, double *out,
@@ -1238,21 +1285,16 @@ int finc_inverse(const float *y, float *x, const float *K, int B, int C, int H, 
     return finc_inverse_prepared(y, x, workspace, B, C, H, W, k, corner, stream);
 }
 
-int finc_unit_forward(const float *x, float *y, const float *K4, int B, int C, int H,
-                      int W, int k, hipStream_t stream) {
+int finc_unit_forward(const float *x, float *y, const float *K4, double *logdet, int B, int C,
+                      int H, int W, int k, hipStream_t stream) {
     if (!valid_shape(B, C, H, W, k) || !x || !y || !K4)
         return FINC_EINVAL;
     const size_t bytes = (size_t)B * C * H * W * sizeof(float);
     if (overlap(x, bytes, y, bytes) && x != y)
         return FINC_EINVAL;
-    FwdArgs a;
-    a.in = x;
-    a.out = y;
-    a.K = K4;
-    a.g = make_geo(C, H, W, k);
-    a.n = 4;
-    a.corner0 = FINC_TL;
-    return launch_forward_chain(a, B, stream);
+    if (logdet && B == 0)
+        return finc_unit_logdet(K4, C, k, H, W, logdet, stream);
+    return launch_forward(x, y, K4, logdet, B, C, H, W, k, 4, FINC_TL, stream);
 }
 
 int finc_unit_logdet(const float *K4, int C, int k, int H, int W, double *out,

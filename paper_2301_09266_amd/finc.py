@@ -27,11 +27,11 @@ SIGNATURES = {
     "finc_strerror": (ctypes.c_char_p, [_i]),
     "finc_workspace_bytes": (_sz, [_i, _i, _i]),
     "finc_prepare": (_i, [_vp, _i, ctypes.POINTER(_i), _i, _i, _vp, _vp]),
-    "finc_forward": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "finc_forward": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "finc_logdet": (_i, [_vp, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
-    "finc_unit_forward": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "finc_unit_forward": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "finc_unit_logdet": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
@@ -100,6 +100,14 @@ def _dev(t: torch.Tensor, name: str, shape=None):
     return t
 
 
+def _logdet_out(t: torch.Tensor | None):
+    if t is None:
+        return None
+    if not t.is_cuda or t.dtype != torch.float64 or t.numel() < 1:
+        raise ValueError("logdet must be a device float64 tensor with at least one element")
+    return t
+
+
 def _workspace(nbytes: int, device, ws):
     if ws is None:
         return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
@@ -139,14 +147,17 @@ def prepare(K: torch.Tensor, corners, out: torch.Tensor | None = None) -> torch.
     return out
 
 
-def forward(x: torch.Tensor, K: torch.Tensor, corner: int, out: torch.Tensor | None = None):
+def forward(x: torch.Tensor, K: torch.Tensor, corner: int, out: torch.Tensor | None = None,
+            logdet: torch.Tensor | None = None):
+    """y = layer(x); with `logdet` (a device float64 tensor of one element) the
+    same launch also writes the layer's log|det|."""
     L = _require_lib()
     _dev(x, "x")
     B, C, H, W = x.shape
     _dev(K, "K", (C, C, K.shape[-1], K.shape[-1]))
     y = torch.empty_like(x) if out is None else _dev(out, "out", x.shape)
-    _check(L.finc_forward(_ptr(x), _ptr(y), _ptr(K), B, C, H, W, K.shape[-1], corner,
-                          _stream()), "finc_forward")
+    _check(L.finc_forward(_ptr(x), _ptr(y), _ptr(K), _ptr(_logdet_out(logdet)), B, C, H, W,
+                          K.shape[-1], corner, _stream()), "finc_forward")
     return y
 
 
@@ -184,15 +195,16 @@ def inverse_prepared(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: in
     return x
 
 
-def unit_forward(x: torch.Tensor, K4: torch.Tensor, out: torch.Tensor | None = None):
+def unit_forward(x: torch.Tensor, K4: torch.Tensor, out: torch.Tensor | None = None,
+                 logdet: torch.Tensor | None = None):
     L = _require_lib()
     _dev(x, "x")
     B, C, H, W = x.shape
     k = K4.shape[-1]
     _dev(K4, "K4", (4, C, C, k, k))
     y = torch.empty_like(x) if out is None else _dev(out, "out", x.shape)
-    _check(L.finc_unit_forward(_ptr(x), _ptr(y), _ptr(K4), B, C, H, W, k, _stream()),
-           "finc_unit_forward")
+    _check(L.finc_unit_forward(_ptr(x), _ptr(y), _ptr(K4), _ptr(_logdet_out(logdet)), B, C, H,
+                               W, k, _stream()), "finc_unit_forward")
     return y
 
 

@@ -83,6 +83,11 @@ def test_layer_forward_inverse(orc, shape, corner):
     ld = finc.logdet(Kd, corner, H, W)
     r = orc.logdet(f64(K), corner, H, W)
     assert abs(float(ld.cpu()[0]) - r) <= TOL * max(1.0, abs(r))
+    # the forward's own log|det| output, and its y unchanged by asking for it
+    ldf = torch.full((1,), float("nan"), dtype=torch.float64, device=DEV)
+    y2 = finc.forward(xd, Kd, corner, logdet=ldf)
+    assert abs(float(ldf.cpu()[0]) - r) <= TOL * max(1.0, abs(r))
+    assert torch.equal(y2, y)
 
 
 def test_inverse_in_place(orc):
@@ -172,8 +177,14 @@ def test_unit_workload(orc, name):
     ld = float(finc.unit_logdet(K4d, c["H"], c["W"]).cpu()[0])
     r = orc.unit_logdet(f64(K4), c["H"], c["W"])
     assert abs(ld - r) <= TOL * max(1.0, abs(r))
+    ldf = torch.full((1,), float("nan"), dtype=torch.float64, device=DEV)
+    assert torch.equal(finc.unit_forward(xd, K4d, logdet=ldf), y)
+    assert abs(float(ldf.cpu()[0]) - r) <= TOL * max(1.0, abs(r))
     xr2 = finc.unit_inverse(y, K4d)
     assert torch.equal(xr, xr2)
+    inplace = xd.clone()
+    finc.unit_forward(inplace, K4d, out=inplace)
+    assert torch.equal(inplace, y)
     assert torch.equal(finc.unit_inverse(y[3:4].contiguous(), K4d)[0], xr[3])
 
 

@@ -42,7 +42,24 @@ def parse():
                    help="bound on the CPU-oracle sample (0 disables it)")
     p.add_argument("--no-graph", action="store_true",
                    help="launch every step eagerly instead of replaying a HIP graph")
+    p.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                   help="only run a plain device copy of MIB MiB ten times (the known-size "
+                        "reference for rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
     return p.parse_args()
+
+
+def calibrate_copy(mib: int):
+    """Ten plain device-to-device copies of `mib` MiB: each dispatch reads and
+    writes exactly mib MiB, the scale for the HBM byte counters."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(10):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_dispatch": n * 4, "dispatches": 10}))
 
 
 def kernel_hash() -> str:
@@ -120,6 +137,41 @@ class LayerStep:
         orc.inverse(y, K, self.corner)
 
 
+def time_back_to_back(fn, stream, n: int, use_graph: bool) -> float:
+    """Mean milliseconds per call of `fn` over about `n` back-to-back calls on
+    `stream`, bracketed by HIP events."""
+    import torch
+
+    per = 20
+    reps = max(1, n // per)
+    g = None
+    if use_graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(per):
+                fn()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for _ in range(reps):
+        if g is not None:
+            g.replay()
+        else:
+            for _ in range(per):
+                fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (reps * per)
+
+
 def cpu_baseline(step, seconds: float):
     """The oracle, single-threaded, on whole batches of the same step until
     `seconds` of CPU time have been spent (at least one image)."""
@@ -149,6 +201,9 @@ def main():
               "batch with no communication, so one GPU's throughput is the figure.",
               file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     import numpy as np
     import torch
 
@@ -200,7 +255,10 @@ def main():
     ms_total = t_start.elapsed_time(t_end)
     ms_per_step = ms_total / args.steps
 
-    # the dominant kernel alone: HIP events around every launch on its stream
+    # the dominant kernel alone, on the stream it is launched on: HIP events
+    # around `steps` back-to-back launches (replays of a graph of 20 launches
+    # when graphs are on), and around every single launch for comparison
+    inv_ms = time_back_to_back(st.inverse, stream, args.steps, graph is not None)
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     for a, b in ev:
@@ -208,7 +266,7 @@ def main():
         st.inverse()
         b.record(stream)
     torch.cuda.synchronize()
-    inv_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    inv_single_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
 
     # correctness guard on what was timed
     err = float((st.xr - st.x).abs().max())
@@ -238,7 +296,9 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "inverse_chain_kernel",
                      "alg_bytes_per_launch": st.inverse_bytes(),
-                     "mean_launch_us": inv_ms * 1e3},
+                     "mean_launch_us": inv_ms * 1e3,
+                     "timing": "HIP events around back-to-back launches on the kernel's stream",
+                     "single_launch_event_us": inv_single_ms * 1e3},
         "inverse": {
             "images_per_s": st.B / (inv_ms * 1e-3),
             "pixels_per_s": st.pixels() / (inv_ms * 1e-3),

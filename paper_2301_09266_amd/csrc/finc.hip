@@ -37,6 +37,48 @@ constexpr int kMaxLayersPerPrep = 64;
 constexpr int kMaxLevels = 8;
 
 __host__ __device__ inline int round_up4(int c) { return (c + 3) & ~3; }
+__host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
+__host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
+__host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
+
+// Pins a loaded value in a register at this point, so that the compiler
+// cannot move the load into the branch that uses it: a group of loads whose
+// results are pinned right after they are issued costs one memory latency,
+// not one per load.
+template <typename T>
+__device__ inline void pin(T &x) {
+    asm volatile("" : "+v"(x));
+}
+
+// Taps in the frame of a corner: back-offset (dp, dq) in [0, k-1]^2 of the
+// source pixel.  They are numbered by diagonal distance dp + dq = 1, 2, ...,
+// 2(k-1) (dp ascending within a distance), the self tap (0, 0) last.
+__host__ __device__ inline void tap_of(int t, int K, int &dp, int &dq) {
+    dp = 0;
+    dq = 0;
+    int n = 0;
+    for (int s = 1; s <= 2 * (K - 1); ++s) {
+        const int lo = s - (K - 1) > 0 ? s - (K - 1) : 0, hi = s < K - 1 ? s : K - 1;
+        const int cnt = hi - lo + 1;
+        if (t < n + cnt) {
+            dp = lo + (t - n);
+            dq = s - dp;
+            return;
+        }
+        n += cnt;
+    }
+}
+
+// Number of the tap with back-offset (dp, dq) (the inverse of tap_of).
+__host__ __device__ inline int tap_index(int dp, int dq, int K) {
+    const int d = dp + dq;
+    if (d == 0)
+        return K * K - 1;
+    int n = 0;
+    for (int s = 1; s < d; ++s)
+        n += imin(s, K - 1) - imax(0, s - (K - 1)) + 1;
+    return n + dp - imax(0, d - (K - 1));
+}
 
 // Self tap (= padding offsets) of a corner.
 __host__ __device__ inline void self_tap(int corner, int k, int &oh, int &ow) {
@@ -44,67 +86,176 @@ __host__ __device__ inline void self_tap(int corner, int k, int &oh, int &ow) {
     ow = (corner == FINC_TL || corner == FINC_BL) ? k - 1 : 0;
 }
 
-// Prepared weights of one layer: k*k blocks of CP x CP floats, block s =
-// a*k + b, entry [c_in][c_out]; block s_self holds L^-1 (transposed), the
-// others L^-1 K_s.  Padded rows/columns are zero.
-__host__ __device__ inline size_t prep_layer_floats(int C, int k) {
+// Prepared weights of one layer, in the order the inverse's MFMA operands
+// take them: quad u = t ncq + cq (tap t in the corner's frame, numbered by
+// tap_of; input channels 4 cq .. 4 cq + 3), then output channel co, then the
+// four input channels: W[u][co][e].  The self tap holds L^-1, the others
+// -(L^-1 K_s) (negated: the inverse subtracts them).  Padded channels are
+// zero, and a block of 64 zero floats follows (the load address of weight
+// slots that do not exist).  ncq = CP / 4.
+__host__ __device__ inline size_t prep_zero_offset(int C, int k) {
     const size_t cp = (size_t)round_up4(C);
     const size_t f = (size_t)k * k * cp * cp;
     return (f + 63) & ~(size_t)63;   // 256-byte multiple
 }
+__host__ __device__ inline size_t prep_layer_floats(int C, int k) {
+    return prep_zero_offset(C, k) + 64;
+}
 
 // ---------------------------------------------------------------------------
-// Weight preparation: every column of L^-1 and of L^-1 K_s is one triangular
-// solve L z = rhs (forward substitution in fp64), one solve per thread.
+// Weight preparation: every column of L^-1 and of L^-1 K_s is one
+// lower-triangular solve L z = rhs in fp64, one solve per thread.
+// Column-oriented, in blocks of 16 channels: the block's 16 unknowns are
+// solved in registers (as soon as z_c is final it is eliminated from the rows
+// below, so the dependent chain is one multiply and one FMA per channel),
+// written out, and eliminated from the rows of later blocks, which wait in
+// LDS.  L (strictly lower part, column-major, zero-padded) and the reciprocals
+// of its diagonal are staged in LDS; all threads of a block read the same
+// entries (broadcast).
 // ---------------------------------------------------------------------------
 struct PrepArgs {
     const float *K;      // n layers, OIHW each
     float *out;          // n layers, prep_layer_floats each
     int C, k, n;
-    unsigned char corner[kMaxLayersPerPrep];
+    unsigned int corner_bits[kMaxLayersPerPrep / 16];   // 2 bits per layer
 };
 
+constexpr int kPrepBlk = 16;             // unknowns solved in registers at a time
+constexpr int kPrepMax = 64;             // FINC_MAX_C rounded up to kPrepBlk
+
 __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
-    extern __shared__ double psm[];
+    __shared__ double Lt[kPrepMax * kPrepMax];     // Lt[c 64 + m] = L[m][c] for m > c, else 0
+    __shared__ double zs[kPrepMax * kPrepThreads]; // zs[m 64 + thread]: rows not yet solved
+    __shared__ double rinv[kPrepMax];              // 1 / L[c][c]; 1 beyond C
     const int C = a.C, k = a.k, kk = k * k, CP = round_up4(C);
-    const int layer = blockIdx.y;
-    const int tid = threadIdx.x;
+    const int CB = (C + kPrepBlk - 1) / kPrepBlk * kPrepBlk;
+    const int layer = blockIdx.y, tid = threadIdx.x;
+    const unsigned int cw = layer < 16   ? a.corner_bits[0]
+                            : layer < 32 ? a.corner_bits[1]
+                            : layer < 48 ? a.corner_bits[2]
+                                         : a.corner_bits[3];
     int sh, sw;
-    self_tap(a.corner[layer], k, sh, sw);
-    const float *K = a.K + (size_t)layer * C * C * kk;
+    self_tap((cw >> (2 * (layer & 15))) & 3, k, sh, sw);
+    const float *__restrict__ K = a.K + (size_t)layer * C * C * kk;
     float *out = a.out + (size_t)layer * prep_layer_floats(C, k);
-    double *L = psm;                 // C x C, row-major, upper part zero
-    double *z = psm + C * C;         // column of this thread: z[m * 64 + tid]
-    for (int idx = tid; idx < C * C; idx += kPrepThreads) {
-        const int co = idx / C, m = idx - co * C;
-        L[idx] = (m <= co) ? (double)K[((size_t)(co * C + m) * k + sh) * k + sw] : 0.0;
-    }
-    __syncthreads();
     const int r = blockIdx.x * kPrepThreads + tid;   // row (s, ci) of the output
-    if (r >= kk * CP)
-        return;
+    const bool row_ok = r < kk * CP;
     const int s = r / CP, ci = r - s * CP;
-    float *row = out + (size_t)r * CP;
-    if (ci >= C) {
-        for (int co = 0; co < CP; ++co)
-            row[co] = 0.0f;
-        return;
-    }
     const int ka = s / k, kb = s - ka * k;
     const bool is_self = (ka == sh && kb == sw);
-    // right-hand side first (all loads in flight), then forward substitution
-    // in place
-    for (int co = 0; co < C; ++co)
-        z[co * kPrepThreads + tid] = is_self ? (co == ci ? 1.0 : 0.0)
-                                             : (double)K[((size_t)(co * C + ci) * k + ka) * k + kb];
-    for (int co = 0; co < C; ++co) {
-        double t = z[co * kPrepThreads + tid];
-        for (int m = 0; m < co; ++m)
-            t -= L[co * C + m] * z[m * kPrepThreads + tid];
-        z[co * kPrepThreads + tid] = t / L[co * C + co];
+    const bool real = row_ok && ci < C;   // padding rows stay zero
+    const int ci_c = real ? ci : 0, ka_c = row_ok ? ka : 0, kb_c = row_ok ? kb : 0;
+    auto Kself = [&](int m, int c) {   // clamped into K
+        return K[((size_t)((m < C ? m : 0) * C + (c < C ? c : 0)) * k + sh) * k + sw];
+    };
+    // Staging: every load of a round is unconditional (clamped index) and
+    // pinned right after issue, so a round costs one memory latency; the
+    // first round holds the first 16 right-hand-side rows, 8 entries of L per
+    // thread and the diagonal (all of it for C <= 16).
+    constexpr int U = 8;
+    const int nl = CB * CB;
+    auto rhs = [&](int m) {
+        return K[((size_t)((m < C ? m : 0) * C + ci_c) * k + ka_c) * k + kb_c];
+    };
+    auto put_rhs = [&](int m, float v) {
+        if (m < CB)
+            zs[m * kPrepThreads + tid] =
+                (m < C && real) ? (is_self ? (m == ci ? 1.0 : 0.0) : (double)v) : 0.0;
+    };
+    auto put_l = [&](int idx, float v) {
+        const int c = idx / CB, m = idx - c * CB;
+        if (idx < nl)
+            Lt[c * kPrepMax + m] = (m > c && m < C) ? (double)v : 0.0;
+    };
+    auto l_at = [&](int idx) {
+        const int c = idx / CB, m = idx - c * CB;
+        return Kself(m, c);
+    };
+    {
+        float rv[kPrepBlk], lv[U];
+#pragma unroll
+        for (int u = 0; u < kPrepBlk; ++u)
+            rv[u] = rhs(u);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            lv[u] = l_at(tid + u * kPrepThreads);
+        float dv = Kself(tid, tid);
+#pragma unroll
+        for (int u = 0; u < kPrepBlk; ++u)
+            pin(rv[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            pin(lv[u]);
+        pin(dv);
+#pragma unroll
+        for (int u = 0; u < kPrepBlk; ++u)
+            put_rhs(u, rv[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            put_l(tid + u * kPrepThreads, lv[u]);
+        if (tid < kPrepMax)
+            rinv[tid] = tid < C ? 1.0 / (double)dv : 1.0;
     }
-    for (int co = 0; co < CP; ++co)
-        row[co] = co < C ? (float)z[co * kPrepThreads + tid] : 0.0f;
+    for (int base = tid + U * kPrepThreads; base < nl; base += U * kPrepThreads) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            v[u] = l_at(base + u * kPrepThreads);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            pin(v[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            put_l(base + u * kPrepThreads, v[u]);
+    }
+    for (int base = kPrepBlk; base < CB; base += kPrepBlk) {
+        float v[kPrepBlk];
+#pragma unroll
+        for (int u = 0; u < kPrepBlk; ++u)
+            v[u] = rhs(base + u);
+#pragma unroll
+        for (int u = 0; u < kPrepBlk; ++u)
+            pin(v[u]);
+#pragma unroll
+        for (int u = 0; u < kPrepBlk; ++u)
+            put_rhs(base + u, v[u]);
+    }
+    __syncthreads();
+    // kernel position (ka, kb) is back-offset (|ka - sh|, |kb - sw|) in the
+    // corner's frame; this thread's column is element ci % 4 of quad
+    // u = t ncq + ci / 4, for every output channel
+    const double sg = is_self ? 1.0 : -1.0;
+    const int t = tap_index(ka > sh ? ka - sh : sh - ka, kb > sw ? kb - sw : sw - kb, k);
+    float *dst = out + ((size_t)(t * (CP / 4) + (ci >> 2)) * CP) * 4 + (ci & 3);
+    for (int b0 = 0; b0 < CB; b0 += kPrepBlk) {
+        double z[kPrepBlk];
+#pragma unroll
+        for (int i = 0; i < kPrepBlk; ++i)
+            z[i] = zs[(b0 + i) * kPrepThreads + tid];
+#pragma unroll
+        for (int c = 0; c < kPrepBlk; ++c) {
+            z[c] *= rinv[b0 + c];
+#pragma unroll
+            for (int m = c + 1; m < kPrepBlk; ++m)
+                z[m] -= Lt[(b0 + c) * kPrepMax + b0 + m] * z[c];
+        }
+        if (row_ok) {
+#pragma unroll
+            for (int i = 0; i < kPrepBlk; ++i)
+                if (b0 + i < CP)
+                    dst[4 * (b0 + i)] = (float)(sg * z[i]);
+        }
+        for (int m = b0 + kPrepBlk; m < CB; ++m) {
+            double acc = zs[m * kPrepThreads + tid];
+#pragma unroll
+            for (int c = 0; c < kPrepBlk; ++c)
+                acc -= Lt[(b0 + c) * kPrepMax + m] * z[c];
+            zs[m * kPrepThreads + tid] = acc;
+        }
+    }
+    if (blockIdx.x == 0 && tid < 16)
+        reinterpret_cast<float4 *>(out + prep_zero_offset(C, k))[tid] =
+            make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 }
 
 // ---------------------------------------------------------------------------
@@ -147,25 +298,34 @@ __global__ __launch_bounds__(kWave) void logdet_kernel(const float *K, int n, in
 // where (dp, dq) in [0, k-1]^2 is the back-offset of a kernel position.  A
 // pixel on anti-diagonal e reads diagonals e - (dp + dq); only the two taps
 // with dp + dq = 1 read the diagonal solved in the previous step.  Every step
-// is a small dense contraction
-//     D[16 frame rows][16 output channels] += A[rows][k] * B[k][channels]
-// over k = (tap, input channel), issued as v_mfma_f32_16x16x4_f32 with the
-// inputs gathered from LDS one 16-byte channel quad per lane and the prepared
-// weights held in registers as the B operand.
+// is a small dense contraction per tile of 16 output channels x 16 frame rows
+//     D[c_out][row] += A[c_out][k] * B[k][row]
+// over k = (tap, input channel), issued as v_mfma_f32_16x16x4_f32: the
+// prepared weights are the A operand, held in registers; the inputs are the B
+// operand, gathered from LDS one 16-byte channel quad per lane.
 //
-// The k range is cut into "quads" (one tap, four input channels).  Per tile
-// (16 rows x 16 output channels) one critical wave owns the quads of the two
-// dp + dq = 1 taps: it finishes diagonal e.  S further waves own the other
-// quads (the L^-1 y term and dp + dq >= 2): during step e they already
-// compute their share of diagonal e + 1, whose sources are all solved, and
-// leave it as partial tiles in LDS.  So one barrier per diagonal step (Theorems
-// 1 and 2: H + W - 1 steps) and a critical path of only the dp + dq = 1 work.
+// The k range is cut into "quads" (one tap, four input channels), four quads
+// to a group (one group = four MFMAs).  Per tile one critical wave owns the
+// two dp + dq = 1 taps and finishes diagonal e.  S helper waves own the rest,
+// round-robin by group: "fresh" groups (dp + dq = 2, which read diagonal
+// e - 1) and "stale" groups (dp + dq >= 3, and the L^-1 y term).  During step
+// e a helper computes its share of diagonal e + 1 and leaves it as a partial
+// tile in LDS.  Its stale sources were all solved a step earlier, so it
+// gathers them at the end of step e - 1 and starts their MFMAs right after
+// the barrier, while the fresh gathers are in flight.  One barrier per
+// diagonal step (Theorems 1 and 2: H + W - 1 steps).
+//
+// With a single channel tile the critical wave keeps its rows' previous
+// pixels in its accumulator: its MFMA chain for diagonal e starts right after
+// the barrier from registers (own row, and the row above by a DPP lane shift)
+// while the partial tiles are read, which are added last.
 //
 // LDS per level: X, the solution, with a zero border of k-1 pixels on every
 // side (the padded image of the paper's padding equation: out-of-image taps
 // read zeros, so gathers never branch); Y, the layer input, unpadded; R, the
-// partial tiles (two parities); Z, a zero block for padding quads.  All
-// pixel-major with the channel axis padded to CP = 4 * ceil(C / 4).
+// partial tiles (two parities); Z, a zero block; T, a trash block for writes
+// of rows that must not land.  All pixel-major with the channel axis padded
+// to CP = 4 * ceil(C / 4).
 // ---------------------------------------------------------------------------
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
@@ -175,36 +335,21 @@ constexpr int kMaxGroups = 8;                       // quad groups (x4 quads) pe
 // Work split and LDS layout of one level (same for every layer of it).
 struct Plan {
     int C, CP, H, W, K, P, WP;
-    int MT, NT, T, S, S4, NW;   // row tiles, channel tiles, tiles, helpers per tile (S4 = S
-                                // rounded up to 4: partial-tile slots per tile), waves
-    int ncq, nq, nq_crit, chunk;
-    int regcrit;                 // 1: the critical taps are fed from registers (one channel tile)
+    int MT, NT, T, S, S4, NW;   // row tiles, channel tiles, tiles, helpers per tile,
+                                // partial-tile slots per tile, waves
+    int ncq, nq, nq_crit;       // quads per tap, quads of a tile, quads of the critical wave
+    int fq0, fq1;               // fresh quads [fq0, fq1); stale quads [fq1, nq)
+    int FG, SG;                 // fresh and stale groups of a tile's helpers
+    int regcrit;                // 1: the critical taps are fed from registers (one channel tile)
     int offX, offY, offR, offZ, offT;  // LDS offsets (floats): solution, input, partial
                                        // tiles, zero block, trash block
     int lds_floats;
 };
 
-__host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; }
-__host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
-__host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
-
-// Quad u of a tile: tap number u / ncq, input channels 4 (u % ncq) .. +3.
-// Taps are numbered by diagonal distance dp + dq = 1, 2, ..., 2(k-1) (dp
-// ascending within a distance), the self tap (0, 0) last.
-__host__ __device__ inline void tap_of(int t, int K, int &dp, int &dq) {
-    dp = 0;
-    dq = 0;
-    int n = 0;
-    for (int s = 1; s <= 2 * (K - 1); ++s) {
-        const int lo = s - (K - 1) > 0 ? s - (K - 1) : 0, hi = s < K - 1 ? s : K - 1;
-        const int cnt = hi - lo + 1;
-        if (t < n + cnt) {
-            dp = lo + (t - n);
-            dq = s - dp;
-            return;
-        }
-        n += cnt;
-    }
+// Quad groups of the busiest wave of a plan.
+inline int plan_groups(const Plan &p) {
+    const int crit = p.regcrit ? 2 : ceil_div(p.nq_crit, 4);
+    return imax(crit, ceil_div(p.FG + p.SG, p.S));
 }
 
 // false if the shape needs more waves or registers than a workgroup has
@@ -226,15 +371,20 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p) {
     // gather.  Otherwise it gathers them (padded to whole quad groups).
     p.regcrit = (p.NT == 1 && K >= 2) ? 1 : 0;
     p.nq_crit = K < 2 ? 0 : (p.regcrit ? 2 * p.ncq : imin(p.nq, round_up4(2 * p.ncq)));
-    const int rest = p.nq - p.nq_crit;
+    // taps up to distance 2: the two of distance 1 and (k = 2) one or three
+    // of distance 2
+    const int taps2 = K < 2 ? 0 : (K == 2 ? 3 : 5);
+    p.fq0 = p.nq_crit;
+    p.fq1 = imax(p.nq_crit, imin(p.nq, taps2 * p.ncq));
+    p.FG = ceil_div(p.fq1 - p.fq0, 4);
+    p.SG = ceil_div(p.nq - p.fq1, 4);
     const int s_max = kMaxWaves / p.T - 1;
     if (s_max < 1)
         return false;
-    // helpers own about two quad groups each (one wave per SIMD for a tile of
-    // a 12-channel 3x3 layer); the critical wave runs 8 MFMAs per step
-    p.S = imax(1, imin(s_max, ceil_div(rest, 8)));
-    p.chunk = round_up4(ceil_div(rest, p.S));
-    if ((!p.regcrit && p.nq_crit > 4 * kMaxGroups) || p.chunk > 4 * kMaxGroups)
+    // every fresh group on its own helper when possible, and about two
+    // groups a helper
+    p.S = imax(1, imin(s_max, imax(p.FG, ceil_div(p.FG + p.SG, 2))));
+    if (plan_groups(p) > kMaxGroups)
         return false;
     p.NW = p.T * (1 + p.S);
     p.S4 = round_up4(p.S);
@@ -268,55 +418,81 @@ struct InvArgs {
 };
 
 // What one wave does at a level.  role 0: critical wave of `tile`; 1: helper
-// wave `slot` (tile slot / S, chunk slot % S); 2: idle (barriers only).
+// h of `tile`; 2: idle (barriers only).
 struct Role {
-    int role, tile, qbase, qend, slot;
+    int role, tile, h;
 };
 
 __device__ inline Role role_of(const Plan &pl) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    Role r = {2, 0, 0, 0, 0};
+    Role r = {2, 0, 0};
     if (wave < pl.T) {
         r.role = 0;
         r.tile = wave;
-        r.qend = pl.nq_crit;
     } else if (wave < pl.NW) {
         r.role = 1;
-        r.slot = wave - pl.T;
-        r.tile = r.slot / pl.S;
-        r.qbase = pl.nq_crit + (r.slot % pl.S) * pl.chunk;
-        r.qend = imin(pl.nq, r.qbase + pl.chunk);
+        r.tile = (wave - pl.T) / pl.S;
+        r.h = (wave - pl.T) - r.tile * pl.S;
     }
     return r;
 }
 
+// Quad that lane group kq of group g of a wave covers, or -1.  Critical wave
+// (gathering form): quads 4 g + kq of [0, nq_crit).  Helper h: groups
+// h, h + S, h + 2S, ... of the tile's fresh groups followed by its stale
+// groups, so a helper's fresh groups come first.
+__device__ inline int quad_of(const Plan &pl, const Role &r, int g, int kq) {
+    if (r.role == 0) {
+        const int u = 4 * g + kq;
+        return u < pl.nq_crit ? u : -1;
+    }
+    if (r.role != 1)
+        return -1;
+    const int G = r.h + g * pl.S;
+    if (G < pl.FG) {
+        const int u = pl.fq0 + 4 * G + kq;
+        return u < pl.fq1 ? u : -1;
+    }
+    const int u = pl.fq1 + 4 * (G - pl.FG) + kq;
+    return G < pl.FG + pl.SG && u < pl.nq ? u : -1;
+}
+
+// Groups of a wave, and how many of them (first) are fresh.
+__device__ inline int groups_of(const Plan &pl, const Role &r) {
+    if (r.role == 0)
+        return pl.regcrit ? 2 : ceil_div(pl.nq_crit, 4);
+    if (r.role != 1 || r.h >= pl.FG + pl.SG)
+        return 0;
+    return ceil_div(pl.FG + pl.SG - r.h, pl.S);
+}
+__device__ inline int fresh_of(const Plan &pl, const Role &r) {
+    return (r.role == 1 && r.h < pl.FG) ? ceil_div(pl.FG - r.h, pl.S) : 0;
+}
+
 __device__ inline int corner_of(const InvArgs &a, int q) { return a.lpu == 1 ? a.corner0 : q; }
 
-// The B operands (prepared weights, signed) of this lane's quads for one
-// layer: lane (kq, li) holds, for group g and element e, the weight of input
-// channel 4 cq + e of quad qbase + 4 g + kq into output channel 16 nt + li.
+// The A operands (prepared weights) of this lane's quads for one layer: lane
+// (kq, li) holds, for group g and element e, the weight of input channel
+// 4 (u % ncq) + e of quad u = quad_of(g, kq) into output channel 16 nt + li --
+// one 16-byte load per group.  Nothing is computed on the loaded values, so
+// the wait for them sinks to their first use (slots that do not exist read
+// the zero block of the prepared layer).
 template <int NG>
 __device__ inline void load_weights(float (&w)[NG][4], const Plan &pl, const Role &r,
-                                    const float *__restrict__ prep, int corner) {
+                                    const float *__restrict__ prep) {
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int co = (r.tile / pl.MT) * 16 + li;
-    int oh, ow;
-    self_tap(corner, pl.K, oh, ow);
-    const bool fh = (corner == FINC_BL || corner == FINC_BR);
-    const bool fw = (corner == FINC_TR || corner == FINC_BR);
+    const float4 *W4 = reinterpret_cast<const float4 *>(prep);
+    const float4 *zero = reinterpret_cast<const float4 *>(prep + prep_zero_offset(pl.C, pl.K)) + li;
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-        const int u = r.qbase + 4 * g + kq;
-        const bool valid = u < r.qend && co < pl.C;
-        const int t = u / pl.ncq, cq = u - t * pl.ncq;
-        int dp, dq;
-        tap_of(t, pl.K, dp, dq);
-        const int ka = fh ? oh + dp : oh - dp, kb = fw ? ow + dq : ow - dq;
-        const float sign = (dp == 0 && dq == 0) ? 1.0f : -1.0f;
-        const float *src = prep + ((size_t)(ka * pl.K + kb) * pl.CP + 4 * cq) * pl.CP + co;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            w[g][e] = valid ? sign * src[(size_t)e * pl.CP] : 0.0f;
+        const int u = quad_of(pl, r, g, kq);
+        const bool valid = u >= 0 && co < pl.C;
+        const float4 v = *(valid ? W4 + (size_t)u * pl.CP + co : zero);
+        w[g][0] = v.x;
+        w[g][1] = v.y;
+        w[g][2] = v.z;
+        w[g][3] = v.w;
     }
 }
 
@@ -325,21 +501,18 @@ __device__ inline void load_weights(float (&w)[NG][4], const Plan &pl, const Rol
 // weight of input channel 4 kq + e into output channel li (A operand).
 template <int NG>
 __device__ inline void load_crit_weights(float (&w)[NG][4], const Plan &pl,
-                                         const float *__restrict__ prep, int corner) {
+                                         const float *__restrict__ prep) {
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
-    int oh, ow;
-    self_tap(corner, pl.K, oh, ow);
-    const bool fh = (corner == FINC_BL || corner == FINC_BR);
-    const bool fw = (corner == FINC_TR || corner == FINC_BR);
+    const float4 *W4 = reinterpret_cast<const float4 *>(prep);
+    const float4 *zero = reinterpret_cast<const float4 *>(prep + prep_zero_offset(pl.C, pl.K)) + li;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-        int dp, dq;
-        tap_of(t, pl.K, dp, dq);
-        const int ka = fh ? oh + dp : oh - dp, kb = fw ? ow + dq : ow - dq;
-        const float *src = prep + ((size_t)(ka * pl.K + kb) * pl.CP + 4 * kq) * pl.CP + li;
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            w[t][e] = (li < pl.C && 4 * kq + e < pl.C) ? -src[(size_t)e * pl.CP] : 0.0f;
+    for (int t = 0; t < (NG < 2 ? NG : 2); ++t) {
+        const bool valid = kq < pl.ncq && li < pl.C;
+        const float4 v = *(valid ? W4 + (size_t)(t * pl.ncq + kq) * pl.CP + li : zero);
+        w[t][0] = v.x;
+        w[t][1] = v.y;
+        w[t][2] = v.z;
+        w[t][3] = v.w;
     }
 }
 
@@ -365,11 +538,15 @@ __device__ inline void copy_solution(float *sm, const Plan &pl) {
 
 // Load the top level's input (B, C, H, W) -> Y, pixel-major, padded channels
 // 0.  Vector loads along the pixel axis (four pixels of one channel), all of
-// a thread's loads in flight before the first LDS store.
-__device__ inline void load_input(float *sm, const Plan &pl, const float *__restrict__ src) {
+// a thread's loads in flight before the first LDS store; `during` (LDS work
+// that does not touch Y) runs while the first round of loads is in flight.
+template <typename F>
+__device__ inline void load_input(float *sm, const Plan &pl, const float *__restrict__ src,
+                                  F during) {
     const int HW = pl.H * pl.W, CP = pl.CP, C = pl.C;
     float *Y = sm + pl.offY;
     constexpr int U = 4;
+    bool first = true;
     if ((HW & 3) == 0) {
         const int n4 = C * HW / 4, hw4 = HW / 4;
         const float4 *s4 = reinterpret_cast<const float4 *>(src);
@@ -381,6 +558,9 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
                 if (idx < n4)
                     v[k] = s4[idx];
             }
+            if (first)
+                during();
+            first = false;
 #pragma unroll
             for (int k = 0; k < U; ++k) {
                 const int idx = base + k * blockDim.x;
@@ -402,6 +582,9 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
                 if (idx < C * HW)
                     v[k] = src[idx];
             }
+            if (first)
+                during();
+            first = false;
 #pragma unroll
             for (int k = 0; k < U; ++k) {
                 const int idx = base + k * blockDim.x;
@@ -412,6 +595,8 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
             }
         }
     }
+    if (first)   // this thread had nothing to load
+        during();
     const int pad = CP - C;
     for (int idx = threadIdx.x; idx < pad * HW; idx += blockDim.x) {
         const int p = idx / pad;
@@ -428,8 +613,14 @@ __device__ void level_input(const InvArgs &a, int l, float *sm, size_t b) {
     const Plan &pl = lv.pl;
     const int C = pl.C, CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
     float *Y = sm + pl.offY;
+    auto clear = [&] {
+        zero_floats(sm + pl.offX, pl.offY - pl.offX);
+        zero_floats(sm + pl.offR, pl.offZ + 256 - pl.offR);   // unused slots and Z stay 0
+    };
     if (l == a.L - 1) {
-        load_input(sm, pl, lv.z + b * (size_t)C * HW);
+        // the solution buffer and the partial tiles are cleared while the
+        // image is on its way
+        load_input(sm, pl, lv.z + b * (size_t)C * HW, clear);
     } else {
         const Plan &up = a.lv[l + 1].pl;
         const int Ch = C / 2;
@@ -446,10 +637,9 @@ __device__ void level_input(const InvArgs &a, int l, float *sm, size_t b) {
             }
             Y[p * CP + c] = v;
         }
-        __syncthreads();
+        __syncthreads();   // the level above's solution has been read
+        clear();
     }
-    zero_floats(sm + pl.offX, pl.offY - pl.offX);
-    zero_floats(sm + pl.offR, pl.offZ + 256 - pl.offR);   // unused slots and Z stay 0
     __syncthreads();
 }
 
@@ -466,8 +656,8 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
     constexpr int GN = kPrefetch ? G : 1;
     // the register-fed critical wave owns the two dp + dq = 1 taps as groups
     const bool regc = pl.regcrit && r.role == 0;
-    const int ngw = __builtin_amdgcn_readfirstlane(
-        regc ? 2 : (r.role == 2 ? 0 : imax(0, ceil_div(r.qend - r.qbase, 4))));
+    const int ngw = __builtin_amdgcn_readfirstlane(groups_of(pl, r));
+    const int nfw = __builtin_amdgcn_readfirstlane(fresh_of(pl, r));
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int C = pl.C, CP = pl.CP, H = pl.H, W = pl.W, P = pl.P, WP = pl.WP;
     const int HW = H * W;
@@ -486,13 +676,17 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
     auto corner_at = [&](int n) { return corner_of(a, a.lpu - 1 - n % a.lpu); };
     auto fetch = [&](auto &dst, int n) {
         if (regc)
-            load_crit_weights(dst, pl, prep_of(n), corner_at(n));
+            load_crit_weights(dst, pl, prep_of(n));
         else
-            load_weights(dst, pl, r, prep_of(n), corner_at(n));
+            load_weights(dst, pl, r, prep_of(n));
     };
     // first layer's weights in flight while the level's input is loaded
-    if (kPrefetch && nlayers > 0)
-        fetch(wn, 0);
+    if (nlayers > 0) {
+        if constexpr (kPrefetch)
+            fetch(wn, 0);
+        else
+            fetch(w, 0);
+    }
     level_input(a, l, sm, b);
     for (int n = 0; n < nlayers; ++n) {
         const int u = a.n_units - 1 - n / a.lpu, q = a.lpu - 1 - n % a.lpu;
@@ -519,7 +713,7 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
                     w[g][e] = wn[g][e];
             if (n + 1 < nlayers)
                 fetch(wn, n + 1);
-        } else {
+        } else if (n > 0) {
             fetch(w, n);
         }
 
@@ -528,21 +722,21 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
         const bool fh = (corner == FINC_BL || corner == FINC_BR);
         const bool fw = (corner == FINC_TR || corner == FINC_BR);
         const int sh = fh ? -1 : 1, sw = fw ? -1 : 1;
-        int oh, ow;
-        self_tap(corner, pl.K, oh, ow);
         // gather row (frame) i = r0 + li, clamped into the image
         const int gi = mt * 16 + li;
         const int gic = imin(gi, H - 1);
         const int goi = fh ? H - 1 - gic : gic;
         const int bx0 = pl.offX + ((goi + P) * WP + P) * CP;
         const int by0 = pl.offY + goi * W * CP;
-        int gbase[G], guse[G];
+        // gather base of each group's quad (plus the column offset of the
+        // step).  Quads that do not exist meet zero weights: they read the
+        // layer input at the lane's own pixel (in bounds, finite).
+        int gbase[G];
 #pragma unroll
         for (int g = 0; g < NG; ++g) {
-            const int uq = r.qbase + 4 * g + kq;
-            if (uq >= r.qend) {
-                gbase[g] = pl.offZ + 4 * lane;
-                guse[g] = 0;
+            const int uq = quad_of(pl, r, g, kq);
+            if (uq < 0) {
+                gbase[g] = by0;
             } else {
                 const int t = uq / pl.ncq, cq = uq - t * pl.ncq;
                 int dp, dq;
@@ -551,7 +745,6 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
                     gbase[g] = by0 + 4 * cq;
                 else
                     gbase[g] = bx0 + 4 * cq - (dp * sh * WP + dq * sw) * CP;
-                guse[g] = 1;
             }
         }
         // Rows of the frame that have not started (frame column j < 0, or rows
@@ -568,21 +761,23 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
             const int jc = imin(imax(j, 0), W - 1);
             return __mul24(fw ? W - 1 - jc : jc, CP);
         };
-        // D[output channel 4 kq + rr][row li] of this wave's quads: weights are
-        // the A operand (rows = output channels), gathered inputs the B
-        // operand (columns = frame rows); c is the initial accumulator
-        auto gather_mma = [&](int j, f32x4 c) -> f32x4 {
+        // gathered B operands of groups [g0, g1) at frame column j (one load
+        // per group, all in flight together)
+        auto gather = [&](float4 (&av)[G], int g0, int g1, int j) {
             const int cx = colx(j);
             const bool live = j >= 0 && gi < H;
-            float4 av[G];
 #pragma unroll
             for (int g = 0; g < NG; ++g)
-                if (g < ngw)
-                    av[g] = *reinterpret_cast<const float4 *>(
-                        sm + (live ? gbase[g] + guse[g] * cx : zaddr));
+                if (g >= g0 && g < g1)
+                    av[g] = *reinterpret_cast<const float4 *>(sm + (live ? gbase[g] + cx : zaddr));
+        };
+        // D[output channel 4 kq + rr][row li] += groups [g0, g1): weights are
+        // the A operand (rows = output channels), gathered inputs the B
+        // operand (columns = frame rows)
+        auto mma = [&](const float4 (&av)[G], f32x4 c, int g0, int g1) -> f32x4 {
 #pragma unroll
             for (int g = 0; g < NG; ++g) {
-                if (g < ngw) {
+                if (g >= g0 && g < g1) {
                     c = mfma4(w[g][0], av[g].x, c);
                     c = mfma4(w[g][1], av[g].y, c);
                     c = mfma4(w[g][2], av[g].z, c);
@@ -591,49 +786,65 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
             }
             return c;
         };
-        auto active = [&](int e) { return r0 <= e && e - W + 1 <= r1; };
+        auto active = [&](int e) { return e >= 0 && e < E && r0 <= e && e - W + 1 <= r1; };
         // the critical wave writes channels 16 nt + 4 kq .. +3 of its row's pixel
         const int wx0 = bx0 + nt * 16 + 4 * kq;
         const bool wch = nt * 16 + 4 * kq < CP && gi < H;
         // partial tiles: R[parity][tile][S4 slots][64 lanes][4]
         const int rstride = pl.T * pl.S4 * 256;
-        const int rown = (r.tile * pl.S4 + (r.role == 1 ? r.slot % pl.S : 0)) * 256 + 4 * lane;
-        // the critical wave's partial-tile sum: the first slot seeds the MFMA
-        // accumulator, the others are added to it
-        auto partial_rest = [&](const f32x4 *Rp) {
-            f32x4 rs = Rp[64] + Rp[128];
-            rs += Rp[192];
+        const int rown = (r.tile * pl.S4 + (r.role == 1 ? r.h : 0)) * 256 + 4 * lane;
+        // the sum of a tile's partial tiles (slots without a writer are zero)
+        auto partial_sum = [&](const f32x4 *Rp) {
+            f32x4 s0 = Rp[0] + Rp[64];
+            const f32x4 s1 = Rp[128] + Rp[192];
+            s0 += s1;
             for (int s4 = 4; s4 < pl.S4; s4 += 4) {
-                rs += Rp[s4 * 64] + Rp[(s4 + 1) * 64];
-                rs += Rp[(s4 + 2) * 64] + Rp[(s4 + 3) * 64];
+                f32x4 t0 = Rp[s4 * 64] + Rp[(s4 + 1) * 64];
+                const f32x4 t1 = Rp[(s4 + 2) * 64] + Rp[(s4 + 3) * 64];
+                t0 += t1;
+                s0 += t0;
             }
-            return rs;
+            return s0;
         };
+        const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
 
         if (r.role == 1) {
-            // helper: during step e, its share of diagonal e + 1
+            // helper: during step e, diagonal e + 1 (fresh groups on top of
+            // the stale part computed in step e - 1) and the stale part of
+            // diagonal e + 2
+            // helper: during step e, diagonal e + 1.  Its stale operands
+            // (sources on diagonals <= e - 1, and y) were gathered at the end
+            // of step e - 1, so their MFMAs start right after the barrier while
+            // the fresh gathers (diagonal e - 1, just solved) are in flight.
             f32x4 *Rw = reinterpret_cast<f32x4 *>(R + rown);
-            const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-            if (active(0))
-                Rw[0] = gather_mma(0 - gi, zero);
+            float4 av[G];
+            if (active(0)) {   // diagonal 0: every group (all sources are zero but y)
+                gather(av, 0, ngw, -gi);
+                Rw[0] = mma(av, zero, 0, ngw);
+            }
             __syncthreads();
             for (int e = 0; e < E; ++e) {
-                if (e + 1 < E && active(e + 1))
-                    Rw[((e + 1) & 1) * (rstride / 4)] = gather_mma(e + 1 - gi, zero);
+                if (active(e + 1)) {
+                    gather(av, 0, ngw, e + 1 - gi);
+                    Rw[((e + 1) & 1) * (rstride / 4)] = mma(av, zero, 0, ngw);
+                }
                 __syncthreads();
             }
         } else if (r.role == 0 && regc) {
             // register-fed critical wave.  dprev: lane (kq, li) holds channels
             // 4 kq .. +3 of row li's pixel of the previous diagonal (0 for rows
-            // not started)
+            // not started).  Its MFMA chain needs nothing from LDS but, in a
+            // lower tile, lane li = 0's row above (the last row of the tile
+            // above); the partial tiles are read meanwhile and added last.
             __syncthreads();
-            f32x4 dprev = {0.0f, 0.0f, 0.0f, 0.0f};
+            f32x4 dprev = zero;
             int j = -gi;   // frame column of row gi at diagonal 0
             // write address of frame column j (the affine form; used only while
             // 0 <= j < W)
             int wcol = wx0 + (fw ? W - 1 : 0) * CP + j * dcol;
             // lane li = 0 of a lower tile reads the tile above's last row
-            // (solved in the previous step, in LDS); other lanes read zeros
+            // (solved in the previous step; channel quads that exist); other
+            // lanes read zeros
             const int ui = mt * 16 - 1;
             const int uoi = fh ? H - 1 - imax(ui, 0) : imax(ui, 0);
             int ju = -16 * mt;   // frame column of row 16 mt (and of the row above it) at diagonal 0
@@ -642,34 +853,46 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
             for (int e = 0; e < E; ++e) {
                 if (active(e)) {
                     const f32x4 *Rp = R0 + (e & 1) * (rstride / 4);
-                    f32x4 up = {0.0f, 0.0f, 0.0f, 0.0f};
+                    f32x4 up = zero;
                     if (mt > 0)
                         up = *reinterpret_cast<const f32x4 *>(
-                            sm + ((li == 0 && (unsigned)ju < (unsigned)W) ? ucol : zaddr));
-                    f32x4 acc = Rp[0];
-                    const f32x4 rs = partial_rest(Rp);
+                            sm + ((li == 0 && 4 * kq < CP && (unsigned)ju < (unsigned)W) ? ucol
+                                                                                    : zaddr));
+                    // the first four partial tiles in flight during the MFMAs
+                    const f32x4 q0 = Rp[0], q1 = Rp[64], q2 = Rp[128], q3 = Rp[192];
+                    __builtin_amdgcn_sched_barrier(0);
+                    f32x4 p = zero;
                     // tap (0,1): own row, previous column; tap (1,0): row above,
                     // same column -- the neighbouring lane's previous result
+                    // (row_shr:1 inside each row of 16 lanes; lane 0 takes `up`).
+                    // Elements are copied to scalars first: this compiler
+                    // bit-casts a vector element lvalue as element 0.
                     if constexpr (G >= 2) {   // (instances with G < 2 never get regc)
 #pragma unroll
                         for (int e4 = 0; e4 < 4; ++e4)
-                            acc = mfma4(w[0][e4], dprev[e4], acc);
+                            p = mfma4(w[0][e4], dprev[e4], p);
 #pragma unroll
                         for (int e4 = 0; e4 < 4; ++e4) {
-                            // lane li takes lane li-1's value (row_shr:1 inside each
-                            // row of 16 lanes); lane 0 keeps `up`.  Elements are
-                            // copied to scalars first: this compiler bit-casts a
-                            // vector element lvalue as element 0.
                             const float de = dprev[e4], ue = up[e4];
-                            const float sh1 = __int_as_float(__builtin_amdgcn_update_dpp(
+                            const float s1 = __int_as_float(__builtin_amdgcn_update_dpp(
                                 __float_as_int(ue), __float_as_int(de), 0x111, 0xf, 0xf, false));
-                            acc = mfma4(w[1][e4], sh1, acc);
+                            p = mfma4(w[1][e4], s1, p);
                         }
                     }
-                    acc += rs;
+                    __builtin_amdgcn_sched_barrier(0);
+                    f32x4 rs = q0 + q1;
+                    const f32x4 rt = q2 + q3;
+                    rs += rt;
+                    for (int s4 = 4; s4 < pl.S4; s4 += 4) {
+                        f32x4 t0 = Rp[s4 * 64] + Rp[(s4 + 1) * 64];
+                        const f32x4 t1 = Rp[(s4 + 2) * 64] + Rp[(s4 + 3) * 64];
+                        t0 += t1;
+                        rs += t0;
+                    }
+                    const f32x4 x = rs + p;
                     const bool ok = wch && (unsigned)j < (unsigned)W;
-                    *reinterpret_cast<f32x4 *>(sm + (ok ? wcol : taddr)) = acc;
-                    dprev = acc;
+                    *reinterpret_cast<f32x4 *>(sm + (ok ? wcol : taddr)) = x;
+                    dprev = x;
                 }
                 j += 1;
                 wcol += dcol;
@@ -683,15 +906,17 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
             // waves)
             __syncthreads();
             const f32x4 *R0 = reinterpret_cast<const f32x4 *>(R + rown);
+            float4 av[G];
             for (int e = 0; e < E; ++e) {
                 if (active(e)) {
                     const int j = e - gi;
                     const f32x4 *Rp = R0 + (e & 1) * (rstride / 4);
-                    const f32x4 rs = partial_rest(Rp);
-                    f32x4 acc = gather_mma(j, Rp[0]);
-                    acc += rs;
+                    gather(av, 0, ngw, j);
+                    const f32x4 rs = partial_sum(Rp);
+                    f32x4 x = mma(av, zero, 0, ngw);
+                    x += rs;
                     const bool ok = wch && (unsigned)j < (unsigned)W;
-                    *reinterpret_cast<f32x4 *>(sm + (ok ? wx0 + colx(j) : taddr)) = acc;
+                    *reinterpret_cast<f32x4 *>(sm + (ok ? wx0 + colx(j) : taddr)) = x;
                 }
                 __syncthreads();
             }
@@ -808,16 +1033,41 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     const size_t HW = (size_t)H * W;
     const float *xb = a.in + (size_t)b * C * HW;
     float *yb = a.out + (size_t)b * C * HW;
-    // zero-bordered input rows i0 - P .. i0 + rb + P - 1 (the block's rows and
-    // the halo its taps reach; rows outside the image stay zero)
-    zero_floats(X, (rb + 2 * P) * WP * CP);
-    __syncthreads();
-    const int lo = imax(0, i0 - P), hi = imin(H, i0 + rb + P), nr = hi - lo;
-    for (int idx = threadIdx.x; idx < C * nr * W; idx += blockDim.x) {
-        const int c = idx / (nr * W), p = idx - c * (nr * W);
-        const int ir = p / W, j = p - ir * W;
-        const int il = lo + ir - i0;   // row relative to the block, -P .. rb + P - 1
-        X[((il + P) * WP + j + P) * CP + c] = xb[c * HW + (size_t)(lo + ir) * W + j];
+    // zero-bordered input rows i0 - P .. i0 + rb + P - 1: every element of
+    // the block is written once, with x where the taps of this launch read
+    // the image and zero elsewhere (outside the image, padding channels, and
+    // for a single layer the halo side its corner never reads).  Loads are
+    // unconditional from clamped indices, eight in flight per thread.
+    {
+        int oh0, ow0;
+        self_tap(fp.corner0, K, oh0, ow0);
+        const int up = fp.n == 1 ? oh0 : P, down = fp.n == 1 ? P - oh0 : P;
+        const int lo = imax(0, i0 - up), hi = imin(H, i0 + rb + down);   // rows read
+        const int nrow = rb + 2 * P, plane = nrow * WP, total = CP * plane;
+        constexpr int U = 8;
+        for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
+            float v[U];
+            bool inb[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int idx = base + u * blockDim.x;
+                const int c = idx / plane, rem = idx - c * plane;
+                const int pr = rem / WP, pc = rem - pr * WP;
+                const int i = i0 - P + pr, j = pc - P;
+                inb[u] = idx < total && c < C && i >= lo && i < hi && j >= 0 && j < W;
+                v[u] = xb[inb[u] ? c * HW + (size_t)i * W + j : 0];
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                pin(v[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int idx = base + u * blockDim.x;
+                const int c = idx / plane, rem = idx - c * plane;
+                if (idx < total)
+                    X[rem * CP + c] = inb[u] ? v[u] : 0.0f;
+            }
+        }
     }
     double ld_acc = 0.0;
     for (int q = 0; q < fp.n; ++q) {
@@ -828,20 +1078,51 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         // weight fragments: Wf[(nt NG + g) 64 + lane].e = K[co][ci][tap] for
         // co = 16 nt + li, quad u = 4 g + kq (tap u / ncq, ci = 4 (u % ncq) + e),
         // the channel mask applied (self tap: ci <= co only)
-        for (int idx = threadIdx.x; idx < fp.NT * fp.NG * 64; idx += blockDim.x) {
-            const int f = idx >> 6, ln = idx & 63;
-            const int nt = f / fp.NG, g = f - nt * fp.NG;
-            const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
-            const int t = u / fp.ncq, cq = u - t * fp.ncq;
-            const int ka = t / K, kb = t - ka * K;
-            float v[4];
+        // (unconditional loads from clamped indices, two fragments = eight
+        // loads in flight per thread, masked afterwards)
+        const int nfrag = fp.NT * fp.NG * 64;
+        for (int base = threadIdx.x; base < nfrag; base += 2 * blockDim.x) {
+            float v[2][4];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int ci = 4 * cq + e;
-                const bool keep = u < fp.nq && co < C && ci < C && !(ka == oh && kb == ow && ci > co);
-                v[e] = keep ? Kq[((size_t)(co * C + ci) * K + ka) * K + kb] : 0.0f;
+            for (int h = 0; h < 2; ++h) {
+                const int idx = base + h * blockDim.x;
+                const int f = idx >> 6, ln = idx & 63;
+                const int nt = f / fp.NG, g = f - nt * fp.NG;
+                const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
+                const int t = u / fp.ncq, cq = u - t * fp.ncq;
+                const bool ok = idx < nfrag && u < fp.nq;
+                const int ka = ok ? t / K : 0, kb = ok ? t - (t / K) * K : 0;
+                const int co_c = co < C ? co : 0;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int ci = 4 * cq + e;
+                    v[h][e] = Kq[((size_t)(co_c * C + (ci < C ? ci : 0)) * K + ka) * K + kb];
+                }
             }
-            Wf[idx] = make_float4(v[0], v[1], v[2], v[3]);
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    pin(v[h][e]);
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int idx = base + h * blockDim.x;
+                const int f = idx >> 6, ln = idx & 63;
+                const int nt = f / fp.NG, g = f - nt * fp.NG;
+                const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
+                const int t = u / fp.ncq, cq = u - t * fp.ncq;
+                const int ka = t / K, kb = t - ka * K;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int ci = 4 * cq + e;
+                    const bool keep =
+                        u < fp.nq && co < C && ci < C && !(ka == oh && kb == ow && ci > co);
+                    if (!keep)
+                        v[h][e] = 0.0f;
+                }
+                if (idx < nfrag)
+                    Wf[idx] = make_float4(v[h][0], v[h][1], v[h][2], v[h][3]);
+            }
         }
         // gather offset of quad u relative to the output pixel's address (taps
         // reach up/left too: offsets are signed); padding quads get kNoQuad
@@ -1002,10 +1283,6 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B) {
     return p;
 }
 
-size_t prep_lds_bytes(int C) {
-    return ((size_t)C * C + (size_t)kPrepThreads * C) * sizeof(double);
-}
-
 // Per-workgroup LDS limit of the current device (queried once per device).
 int lds_limit(size_t *out) {
     static size_t cache[64] = {0};
@@ -1040,10 +1317,6 @@ int launched() {
 int launch_prep(const float *K, int n, const int *corners, int C, int k, float *out,
                 hipStream_t stream) {
     const int CP = round_up4(C);
-    const size_t lds = prep_lds_bytes(C);
-    int rc = check_lds(lds);
-    if (rc != FINC_OK)
-        return rc;
     for (int first = 0; first < n; first += kMaxLayersPerPrep) {
         PrepArgs a;
         memset(&a, 0, sizeof(a));
@@ -1053,10 +1326,10 @@ int launch_prep(const float *K, int n, const int *corners, int C, int k, float *
         a.K = K + (size_t)first * C * C * k * k;
         a.out = out + (size_t)first * prep_layer_floats(C, k);
         for (int q = 0; q < a.n; ++q)
-            a.corner[q] = (unsigned char)corners[first + q];
+            a.corner_bits[q >> 4] |= (unsigned)(corners[first + q] & 3) << (2 * (q & 15));
         dim3 grid((k * k * CP + kPrepThreads - 1) / kPrepThreads, a.n);
-        hipLaunchKernelGGL(prep_kernel, grid, dim3(kPrepThreads), lds, stream, a);
-        rc = launched();
+        hipLaunchKernelGGL(prep_kernel, grid, dim3(kPrepThreads), 0, stream, a);
+        const int rc = launched();
         if (rc != FINC_OK)
             return rc;
     }
@@ -1093,7 +1366,7 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     int ng = 1;
     for (int l = 0; l < a.L; ++l) {
         const Plan &p = a.lv[l].pl;
-        ng = imax(ng, imax(p.regcrit ? 2 : ceil_div(p.nq_crit, 4), p.chunk / 4));
+        ng = imax(ng, plan_groups(p));
     }
     const InvKernel k = threads <= 256   ? inverse_instance<256>(ng)
                         : threads <= 512 ? inverse_instance<512>(ng)

@@ -49,7 +49,7 @@ def test_workspace_bytes():
     lib = finc.lib()
     for C, k in [(3, 3), (12, 3), (12, 5), (48, 3), (64, 7), (1, 1)]:
         cp = (C + 3) // 4 * 4
-        floats = -(-(k * k * cp * cp) // 64) * 64
+        floats = -(-(k * k * cp * cp) // 64) * 64 + 64
         assert lib.finc_workspace_bytes(C, k, 1) == floats * 4
         assert lib.finc_workspace_bytes(C, k, 4) == 4 * floats * 4
     for bad in [(0, 3, 1), (65, 3, 1), (12, 0, 1), (12, 8, 1), (12, 3, -1)]:

@@ -42,6 +42,8 @@ def parse():
                    help="bound on the CPU-oracle sample (0 disables it)")
     p.add_argument("--no-graph", action="store_true",
                    help="launch every step eagerly instead of replaying a HIP graph")
+    p.add_argument("--no-configs", action="store_true",
+                   help="skip the per-configuration table (forward / inverse of every workload)")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                    help="only run a plain device copy of MIB MiB ten times (the known-size "
                         "reference for rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -170,6 +172,72 @@ def time_back_to_back(fn, stream, n: int, use_graph: bool) -> float:
     b.record(stream)
     torch.cuda.synchronize()
     return a.elapsed_time(b) / (reps * per)
+
+
+def graph_time_us(fn, reps: int, per: int) -> float:
+    """Mean microseconds per call of `fn`: a HIP graph of `per` back-to-back
+    calls replayed `reps` times between two events on the current stream."""
+    import torch
+
+    return time_back_to_back(fn, torch.cuda.current_stream(), reps * per, True) * 1e3
+
+
+def per_config(dev) -> list:
+    """Forward and inverse of every workload (inputs resident, weights
+    prepared once outside the timed region), with the inverse's algorithmic
+    HBM bytes over its time against the HBM peak."""
+    import numpy as np
+    import torch
+
+    from paper_2301_09266_amd import finc, synth
+
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    rows = []
+    for name, spec in synth.WORKLOADS.items():
+        c = synth.make(name)
+        kind = spec["kind"]
+        if kind == "layer":
+            B, C, H, W, k = (c[n] for n in "BCHWk")
+            x, K = d(c["x"]), d(c["K"])
+            y = finc.forward(x, K, c["corner"])
+            prep = finc.prepare(K, [c["corner"]])
+            out = torch.empty_like(x)
+            fwd = graph_time_us(lambda: finc.forward(x, K, c["corner"], out=out), 5, 20)
+            inv = graph_time_us(lambda: finc.inverse_prepared(y, prep, k, c["corner"], out=out), 5, 20)
+            act, wts, layers = 2 * C * H * W * 4, C * C * k * k * 4, 1
+        elif kind == "unit":
+            B, C, H, W, k = (c[n] for n in "BCHWk")
+            x, K4 = d(c["x"]), d(c["K4"])
+            y = finc.unit_forward(x, K4)
+            prep = finc.prepare(K4, [0, 1, 2, 3])
+            out = torch.empty_like(x)
+            fwd = graph_time_us(lambda: finc.unit_forward(x, K4, out=out), 5, 10)
+            inv = graph_time_us(lambda: finc.unit_inverse_prepared(y, prep, k, out=out), 5, 10)
+            act, wts, layers = 2 * C * H * W * 4, 4 * C * C * k * k * 4, 4
+        else:
+            B, C1, H1, W1, k, L, U = (c[n] for n in ("B", "C1", "H1", "W1", "k", "levels", "units"))
+            Kf = d(np.concatenate([a.ravel() for a in c["K"]]))
+            sf = d(np.concatenate([a.ravel() for a in c["scale"]]))
+            bf = d(np.concatenate([a.ravel() for a in c["bias"]]))
+            zd = [d(z) for z in c["z"]]
+            prep = finc.stack_prepare(Kf, L, U, C1, k)
+            out = torch.empty((B, C1, H1, W1), device=dev)
+            fwd = None
+            inv = graph_time_us(lambda: finc.stack_inverse_prepared(zd, prep, sf, bf, L, U, C1, H1,
+                                                                    W1, k, out=out), 2, 3)
+            C, H, W = C1, H1, W1
+            act = (sum(z[0].size for z in c["z"]) + C1 * H1 * W1) * 4
+            wts = sum(a.size for a in c["K"]) * 4
+            layers = 4 * U * L
+        alg = B * act + wts
+        gbs = alg / (inv * 1e-6) / 1e9
+        rows.append({"workload": name, "B": B, "C": C, "H": H, "W": W, "k": k, "layers": layers,
+                     "forward_us": fwd, "inverse_us": inv,
+                     "inverse_images_per_s": B / (inv * 1e-6),
+                     "inverse_pixels_per_s": B * H * W / (inv * 1e-6),
+                     "inverse_alg_bytes": alg, "inverse_hbm_gbs": gbs,
+                     "inverse_hbm_frac": gbs / HBM_PEAK_GBS})
+    return rows
 
 
 def cpu_baseline(step, seconds: float):
@@ -309,6 +377,8 @@ def main():
         "wall_s_timed": wall,
         "round_trip_max_abs": err,
     }
+    if not args.no_configs:
+        out["per_config"] = per_config(dev)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(st, args.cpu_seconds)
     print(json.dumps(out))

@@ -1,8 +1,9 @@
 """Throughput of the FInC masked-conv hot path on one MI355X.
 
-A step is one pass of the whole path over one batch: weight preparation
-(L^-1 and L^-1 K_s), the forward masked convolution, log|det| and the
-diagonal-wavefront inverse of the forward's output.  The default workload is
+A step is one pass of the whole path over one batch: the forward masked
+convolution, with log|det| and the weight preparation for the inverse (L^-1
+and L^-1 K_s) as side outputs of the same launch, then the diagonal-wavefront
+inverse of the forward's output.  The default workload is
 the single masked 3x3 layer, TL padding, batch 64, 12 channels, 16x16 (a
 CIFAR-10 image after one 2x2 squeeze), fp32.
 
@@ -81,7 +82,8 @@ def traffic_for(workload: str):
 
 
 class LayerStep:
-    """prepare + forward + logdet + inverse of one padded masked conv block."""
+    """forward (with log|det| and the prepared weights) + inverse of one padded
+    masked conv block."""
 
     def __init__(self, case, dev):
         import numpy as np
@@ -101,18 +103,15 @@ class LayerStep:
                                 device=dev)
         self.case = case
 
-    def prepare(self):
-        self.finc.prepare(self.K, [self.corner], out=self.prep)
-
     def forward(self):
-        # y and log|det| from one launch
-        self.finc.forward(self.x, self.K, self.corner, out=self.y, logdet=self.ld)
+        # y, log|det| and the weights prepared for the inverse, from one launch
+        self.finc.forward(self.x, self.K, self.corner, out=self.y, logdet=self.ld,
+                          prepared=self.prep)
 
     def inverse(self):
         self.finc.inverse_prepared(self.y, self.prep, self.k, self.corner, out=self.xr)
 
     def step(self):
-        self.prepare()
         self.forward()
         self.inverse()
 
@@ -359,7 +358,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": args.workload, "B": st.B, "C": st.C, "H": st.H, "W": st.W,
                    "k": st.k, "corner": "TL", "graph": graph is not None,
-                   "step": "prepare + forward + logdet + inverse"},
+                   "step": "forward + logdet + weight preparation (one launch), inverse"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "inverse_chain_kernel",

@@ -88,6 +88,11 @@ int finc_prepare(const float *K, int n_layers, const int *corners, int C, int k,
  *   x, y: device (B, C, H, W); K: device OIHW.  x and y must not overlap.
  *   logdet: NULL, or device double that receives the layer's log|det| (as
  *   finc_logdet) from the same launch, as a flow layer's forward pass does.
+ *   prepared: NULL, or device buffer of finc_workspace_bytes(C, k, 1) bytes,
+ *   256-byte aligned, clear of x, y and K, that receives the weights as
+ *   finc_prepare would write them (for finc_inverse_prepared) -- computed
+ *   by extra workgroups of the same launch for C <= 16, by a second launch
+ *   on the same stream otherwise.  B == 0 still fills both side outputs.
  * finc_logdet: out[0] (device double) = log|det| of the layer's H*W*C x
  *   H*W*C convolution matrix, the same for every image (Table 1 "Jacobian";
  *   -inf for a zero diagonal).
@@ -98,8 +103,9 @@ int finc_prepare(const float *K, int n_layers, const int *corners, int C, int k,
  *   other overlap is rejected.
  * finc_inverse_prepared: the same with weights already prepared by
  *   finc_prepare (one layer, same corner). */
-int finc_forward(const float *x, float *y, const float *K, double *logdet, int B,
-                 int C, int H, int W, int k, int corner, hipStream_t stream);
+int finc_forward(const float *x, float *y, const float *K, double *logdet,
+                 void *prepared, int B, int C, int H, int W, int k, int corner,
+                 hipStream_t stream);
 int finc_logdet(const float *K, int C, int k, int corner, int H, int W,
                 double *out, hipStream_t stream);
 int finc_inverse(const float *y, float *x, const float *K, int B, int C, int H,
@@ -115,10 +121,13 @@ int finc_inverse_prepared(const float *y, float *x, const void *prepared, int B,
  * tensors in the order TL, TR, BL, BR.  Activations stay in on-chip memory
  * between the four blocks.  finc_unit_forward allows x == y (each image is
  * read whole before it is written); the inverse's rules are as for one block.
- * logdet (finc_unit_forward): NULL, or device double for the unit's log|det|.
+ * logdet (finc_unit_forward): NULL, or device double for the unit's log|det|;
+ * prepared4: NULL, or device buffer of finc_workspace_bytes(C, k, 4) bytes
+ * (rules as for finc_forward) for finc_unit_inverse_prepared.
  * finc_unit_logdet: sum of the four blocks' log|det|. */
-int finc_unit_forward(const float *x, float *y, const float *K4, double *logdet, int B,
-                      int C, int H, int W, int k, hipStream_t stream);
+int finc_unit_forward(const float *x, float *y, const float *K4, double *logdet,
+                      void *prepared4, int B, int C, int H, int W, int k,
+                      hipStream_t stream);
 int finc_unit_logdet(const float *K4, int C, int k, int H, int W, double *out,
                      hipStream_t stream);
 int finc_unit_inverse(const float *y, float *x, const float *K4, int B, int C,

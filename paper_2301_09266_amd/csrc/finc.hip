@@ -123,22 +123,29 @@ struct PrepArgs {
 constexpr int kPrepBlk = 16;             // unknowns solved in registers at a time
 constexpr int kPrepMax = 64;             // FINC_MAX_C rounded up to kPrepBlk
 
-__global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
-    __shared__ double Lt[kPrepMax * kPrepMax];     // Lt[c 64 + m] = L[m][c] for m > c, else 0
-    __shared__ double zs[kPrepMax * kPrepThreads]; // zs[m 64 + thread]: rows not yet solved
-    __shared__ double rinv[kPrepMax];              // 1 / L[c][c]; 1 beyond C
-    const int C = a.C, k = a.k, kk = k * k, CP = round_up4(C);
-    const int CB = (C + kPrepBlk - 1) / kPrepBlk * kPrepBlk;
-    const int layer = blockIdx.y, tid = threadIdx.x;
-    const unsigned int cw = layer < 16   ? a.corner_bits[0]
-                            : layer < 32 ? a.corner_bits[1]
-                            : layer < 48 ? a.corner_bits[2]
-                                         : a.corner_bits[3];
+__host__ __device__ inline int prep_cb(int C) { return (C + kPrepBlk - 1) / kPrepBlk * kPrepBlk; }
+
+// LDS (doubles) of prep_columns: L's strictly lower part (CB x CB), the
+// reciprocals of its diagonal (CB), and the rows beyond the first register
+// block of every thread's right-hand side.
+__host__ __device__ inline int prep_lds_doubles(int C, int nth) {
+    const int cb = prep_cb(C);
+    return cb * cb + cb + (cb - kPrepBlk) * nth;
+}
+
+// One block's share of one layer's preparation: output rows (columns of the
+// solves) col0 .. col0 + NTH - 1, row = (kernel position s, input channel
+// ci).  zero_tail: this block also writes the layer's zero block.
+template <int NTH>
+__device__ void prep_columns(const float *__restrict__ K, float *out, int C, int k, int corner,
+                             int col0, bool zero_tail, double *lds) {
+    const int kk = k * k, CP = round_up4(C), CB = prep_cb(C), tid = threadIdx.x;
+    double *Lt = lds;                  // Lt[c CB + m] = L[m][c] for m > c, else 0
+    double *rinv = lds + CB * CB;      // 1 / L[c][c]; 1 beyond C
+    double *zs = rinv + CB;            // zs[(m - 16) NTH + thread]: rows of later blocks
     int sh, sw;
-    self_tap((cw >> (2 * (layer & 15))) & 3, k, sh, sw);
-    const float *__restrict__ K = a.K + (size_t)layer * C * C * kk;
-    float *out = a.out + (size_t)layer * prep_layer_floats(C, k);
-    const int r = blockIdx.x * kPrepThreads + tid;   // row (s, ci) of the output
+    self_tap(corner, k, sh, sw);
+    const int r = col0 + tid;
     const bool row_ok = r < kk * CP;
     const int s = r / CP, ci = r - s * CP;
     const int ka = s / k, kb = s - ka * k;
@@ -150,27 +157,27 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
     };
     // Staging: every load of a round is unconditional (clamped index) and
     // pinned right after issue, so a round costs one memory latency; the
-    // first round holds the first 16 right-hand-side rows, 8 entries of L per
-    // thread and the diagonal (all of it for C <= 16).
+    // first round holds the first 16 right-hand-side rows (kept in
+    // registers), 8 entries of L per thread and the diagonal (all of it for
+    // C <= 16).
     constexpr int U = 8;
     const int nl = CB * CB;
     auto rhs = [&](int m) {
         return K[((size_t)((m < C ? m : 0) * C + ci_c) * k + ka_c) * k + kb_c];
     };
-    auto put_rhs = [&](int m, float v) {
-        if (m < CB)
-            zs[m * kPrepThreads + tid] =
-                (m < C && real) ? (is_self ? (m == ci ? 1.0 : 0.0) : (double)v) : 0.0;
+    auto rhs_val = [&](int m, float v) {
+        return (m < C && real) ? (is_self ? (m == ci ? 1.0 : 0.0) : (double)v) : 0.0;
     };
     auto put_l = [&](int idx, float v) {
         const int c = idx / CB, m = idx - c * CB;
         if (idx < nl)
-            Lt[c * kPrepMax + m] = (m > c && m < C) ? (double)v : 0.0;
+            Lt[c * CB + m] = (m > c && m < C) ? (double)v : 0.0;
     };
     auto l_at = [&](int idx) {
         const int c = idx / CB, m = idx - c * CB;
         return Kself(m, c);
     };
+    double z[kPrepBlk];
     {
         float rv[kPrepBlk], lv[U];
 #pragma unroll
@@ -178,7 +185,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
             rv[u] = rhs(u);
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            lv[u] = l_at(tid + u * kPrepThreads);
+            lv[u] = l_at(tid + u * NTH);
         float dv = Kself(tid, tid);
 #pragma unroll
         for (int u = 0; u < kPrepBlk; ++u)
@@ -189,24 +196,24 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
         pin(dv);
 #pragma unroll
         for (int u = 0; u < kPrepBlk; ++u)
-            put_rhs(u, rv[u]);
+            z[u] = rhs_val(u, rv[u]);
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            put_l(tid + u * kPrepThreads, lv[u]);
-        if (tid < kPrepMax)
+            put_l(tid + u * NTH, lv[u]);
+        if (tid < CB)
             rinv[tid] = tid < C ? 1.0 / (double)dv : 1.0;
     }
-    for (int base = tid + U * kPrepThreads; base < nl; base += U * kPrepThreads) {
+    for (int base = tid + U * NTH; base < nl; base += U * NTH) {
         float v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            v[u] = l_at(base + u * kPrepThreads);
+            v[u] = l_at(base + u * NTH);
 #pragma unroll
         for (int u = 0; u < U; ++u)
             pin(v[u]);
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            put_l(base + u * kPrepThreads, v[u]);
+            put_l(base + u * NTH, v[u]);
     }
     for (int base = kPrepBlk; base < CB; base += kPrepBlk) {
         float v[kPrepBlk];
@@ -218,7 +225,7 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
             pin(v[u]);
 #pragma unroll
         for (int u = 0; u < kPrepBlk; ++u)
-            put_rhs(base + u, v[u]);
+            zs[(base + u - kPrepBlk) * NTH + tid] = rhs_val(base + u, v[u]);
     }
     __syncthreads();
     // kernel position (ka, kb) is back-offset (|ka - sh|, |kb - sw|) in the
@@ -228,16 +235,17 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
     const int t = tap_index(ka > sh ? ka - sh : sh - ka, kb > sw ? kb - sw : sw - kb, k);
     float *dst = out + ((size_t)(t * (CP / 4) + (ci >> 2)) * CP) * 4 + (ci & 3);
     for (int b0 = 0; b0 < CB; b0 += kPrepBlk) {
-        double z[kPrepBlk];
+        if (b0 > 0) {
 #pragma unroll
-        for (int i = 0; i < kPrepBlk; ++i)
-            z[i] = zs[(b0 + i) * kPrepThreads + tid];
+            for (int i = 0; i < kPrepBlk; ++i)
+                z[i] = zs[(b0 + i - kPrepBlk) * NTH + tid];
+        }
 #pragma unroll
         for (int c = 0; c < kPrepBlk; ++c) {
             z[c] *= rinv[b0 + c];
 #pragma unroll
             for (int m = c + 1; m < kPrepBlk; ++m)
-                z[m] -= Lt[(b0 + c) * kPrepMax + b0 + m] * z[c];
+                z[m] -= Lt[(b0 + c) * CB + b0 + m] * z[c];
         }
         if (row_ok) {
 #pragma unroll
@@ -246,16 +254,29 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
                     dst[4 * (b0 + i)] = (float)(sg * z[i]);
         }
         for (int m = b0 + kPrepBlk; m < CB; ++m) {
-            double acc = zs[m * kPrepThreads + tid];
+            double acc = zs[(m - kPrepBlk) * NTH + tid];
 #pragma unroll
             for (int c = 0; c < kPrepBlk; ++c)
-                acc -= Lt[(b0 + c) * kPrepMax + m] * z[c];
-            zs[m * kPrepThreads + tid] = acc;
+                acc -= Lt[(b0 + c) * CB + m] * z[c];
+            zs[(m - kPrepBlk) * NTH + tid] = acc;
         }
     }
-    if (blockIdx.x == 0 && tid < 16)
+    if (zero_tail && tid < 16)
         reinterpret_cast<float4 *>(out + prep_zero_offset(C, k))[tid] =
             make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+}
+
+__global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
+    __shared__ double lds[kPrepMax * kPrepMax + kPrepMax + (kPrepMax - kPrepBlk) * kPrepThreads];
+    const int layer = blockIdx.y;
+    const unsigned int cw = layer < 16   ? a.corner_bits[0]
+                            : layer < 32 ? a.corner_bits[1]
+                            : layer < 48 ? a.corner_bits[2]
+                                         : a.corner_bits[3];
+    prep_columns<kPrepThreads>(a.K + (size_t)layer * a.C * a.C * a.k * a.k,
+                               a.out + (size_t)layer * prep_layer_floats(a.C, a.k), a.C, a.k,
+                               (cw >> (2 * (layer & 15))) & 3, blockIdx.x * kPrepThreads,
+                               blockIdx.x == 0, lds);
 }
 
 // ---------------------------------------------------------------------------
@@ -457,16 +478,13 @@ __device__ inline int quad_of(const Plan &pl, const Role &r, int g, int kq) {
     return G < pl.FG + pl.SG && u < pl.nq ? u : -1;
 }
 
-// Groups of a wave, and how many of them (first) are fresh.
+// Groups of a wave.
 __device__ inline int groups_of(const Plan &pl, const Role &r) {
     if (r.role == 0)
         return pl.regcrit ? 2 : ceil_div(pl.nq_crit, 4);
     if (r.role != 1 || r.h >= pl.FG + pl.SG)
         return 0;
     return ceil_div(pl.FG + pl.SG - r.h, pl.S);
-}
-__device__ inline int fresh_of(const Plan &pl, const Role &r) {
-    return (r.role == 1 && r.h < pl.FG) ? ceil_div(pl.FG - r.h, pl.S) : 0;
 }
 
 __device__ inline int corner_of(const InvArgs &a, int q) { return a.lpu == 1 ? a.corner0 : q; }
@@ -657,7 +675,6 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
     // the register-fed critical wave owns the two dp + dq = 1 taps as groups
     const bool regc = pl.regcrit && r.role == 0;
     const int ngw = __builtin_amdgcn_readfirstlane(groups_of(pl, r));
-    const int nfw = __builtin_amdgcn_readfirstlane(fresh_of(pl, r));
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int C = pl.C, CP = pl.CP, H = pl.H, W = pl.W, P = pl.P, WP = pl.WP;
     const int HW = H * W;
@@ -1011,6 +1028,8 @@ struct FwdArgs {
     float *out;
     const float *K;   // n OIHW tensors
     double *logdet;   // optional: H W sum over layers and channels of log|K[c,c,self]|
+    float *prepared;  // optional: the n layers' prepared weights, by blocks nfwd ..
+    int nfwd, ppl;    // forward blocks; preparation blocks per layer
     FwdPlan fp;
 };
 
@@ -1020,6 +1039,16 @@ constexpr int kNoQuad = 1 << 30;   // quad offset marker: padding quad (zero wei
 __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     extern __shared__ float sm[];
     const FwdPlan &fp = a.fp;
+    if (a.prepared && (int)blockIdx.x >= a.nfwd) {
+        // the weights for the inverse, prepared by the launch's last blocks
+        // (the forward blocks do not wait for them)
+        const int pb = blockIdx.x - a.nfwd, layer = pb / a.ppl, part = pb - layer * a.ppl;
+        prep_columns<kFwdThreads>(a.K + (size_t)layer * fp.C * fp.C * fp.K * fp.K,
+                                  a.prepared + (size_t)layer * prep_layer_floats(fp.C, fp.K),
+                                  fp.C, fp.K, fp.n == 1 ? fp.corner0 : layer, part * kFwdThreads,
+                                  part == 0, reinterpret_cast<double *>(sm));
+        return;
+    }
     const int C = fp.C, CP = fp.CP, H = fp.H, W = fp.W, K = fp.K, P = fp.P, WP = fp.WP;
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -1378,9 +1407,15 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     return launched();
 }
 
-int launch_forward(const float *x, float *y, const float *K, double *logdet, int B, int C,
-                   int H, int W, int k, int n, int corner0, hipStream_t stream) {
+// Channels up to which the forward launch also prepares the inverse's
+// weights in its own blocks (their LDS is small); wider layers get a
+// separate preparation launch.
+constexpr int kFusedPrepMaxC = 16;
+
+int launch_forward(const float *x, float *y, const float *K, double *logdet, float *prepared,
+                   int B, int C, int H, int W, int k, int n, int corner0, hipStream_t stream) {
     FwdArgs a;
+    memset(&a, 0, sizeof(a));
     a.in = x;
     a.out = y;
     a.K = K;
@@ -1388,16 +1423,30 @@ int launch_forward(const float *x, float *y, const float *K, double *logdet, int
     a.fp = make_fwd_plan(C, H, W, k, n, corner0, B);
     if (B == 0)
         return FINC_OK;
-    const size_t lds = (size_t)a.fp.lds_floats * sizeof(float);
+    const bool fuse = prepared && C <= kFusedPrepMaxC;
+    a.nfwd = B * a.fp.nblk;
+    a.ppl = ceil_div(k * k * round_up4(C), kFwdThreads);
+    a.prepared = fuse ? prepared : nullptr;
+    size_t lds = (size_t)a.fp.lds_floats * sizeof(float);
+    if (fuse)
+        lds = lds > prep_lds_doubles(C, kFwdThreads) * sizeof(double)
+                  ? lds
+                  : prep_lds_doubles(C, kFwdThreads) * sizeof(double);
     int rc = check_lds(lds);
     if (rc != FINC_OK)
         return rc;
     if (hipFuncSetAttribute((const void *)forward_kernel,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
         (void)hipGetLastError();   // not needed on every runtime; the launch check decides
-    hipLaunchKernelGGL(forward_kernel, dim3((unsigned)B * a.fp.nblk), dim3(kFwdThreads), lds,
-                       stream, a);
-    return launched();
+    const unsigned blocks = (unsigned)(a.nfwd + (fuse ? n * a.ppl : 0));
+    hipLaunchKernelGGL(forward_kernel, dim3(blocks), dim3(kFwdThreads), lds, stream, a);
+    rc = launched();
+    if (rc != FINC_OK || !prepared || fuse)
+        return rc;
+    int corners[4] = {corner0, FINC_TR, FINC_BL, FINC_BR};
+    if (n > 1)
+        corners[0] = FINC_TL;
+    return launch_prep(K, n, corners, C, k, prepared, stream);
 }
 
 Level level(const float *z, const void *prep, const float *scale, const float *bias, int C,
@@ -1497,16 +1546,33 @@ int finc_prepare(const float *K, int n_layers, const int *corners, int C, int k,
     return launch_prep(K, n_layers, corners, C, k, (float *)prepared, stream);
 }
 
-int finc_forward(const float *x, float *y, const float *K, double *logdet, int B, int C, int H,
-                 int W, int k, int corner, hipStream_t stream) {
+// The prepared-weights side output of a forward call: aligned, and clear of
+// the activations and weights.
+bool prepared_out_ok(const void *prepared, size_t pbytes, const void *x, const void *y,
+                     size_t bytes, const void *K, size_t kbytes) {
+    return aligned256(prepared) && !overlap(prepared, pbytes, x, bytes) &&
+           !overlap(prepared, pbytes, y, bytes) && !overlap(prepared, pbytes, K, kbytes);
+}
+
+int finc_forward(const float *x, float *y, const float *K, double *logdet, void *prepared,
+                 int B, int C, int H, int W, int k, int corner, hipStream_t stream) {
     if (!valid_shape(B, C, H, W, k) || !valid_corner(corner) || !x || !y || !K)
         return FINC_EINVAL;
     const size_t bytes = (size_t)B * C * H * W * sizeof(float);
     if (overlap(x, bytes, y, bytes))
         return FINC_EINVAL;
-    if (logdet && B == 0)   // nothing to run the forward on: log|det| on its own
-        return finc_logdet(K, C, k, corner, H, W, logdet, stream);
-    return launch_forward(x, y, K, logdet, B, C, H, W, k, 1, corner, stream);
+    if (prepared && !prepared_out_ok(prepared, finc_workspace_bytes(C, k, 1), x, y, bytes, K,
+                                     (size_t)C * C * k * k * sizeof(float)))
+        return FINC_EINVAL;
+    if (B == 0) {   // nothing to run the forward on: the side outputs on their own
+        int rc = FINC_OK;
+        if (logdet)
+            rc = finc_logdet(K, C, k, corner, H, W, logdet, stream);
+        if (rc == FINC_OK && prepared)
+            rc = finc_prepare(K, 1, &corner, C, k, prepared, stream);
+        return rc;
+    }
+    return launch_forward(x, y, K, logdet, (float *)prepared, B, C, H, W, k, 1, corner, stream);
 }
 
 int finc_logdet(const float *K, int C, int k, int corner, int H, int W, double *out,
@@ -1558,16 +1624,28 @@ int finc_inverse(const float *y, float *x, const float *K, int B, int C, int H, 
     return finc_inverse_prepared(y, x, workspace, B, C, H, W, k, corner, stream);
 }
 
-int finc_unit_forward(const float *x, float *y, const float *K4, double *logdet, int B, int C,
-                      int H, int W, int k, hipStream_t stream) {
+int finc_unit_forward(const float *x, float *y, const float *K4, double *logdet,
+                      void *prepared4, int B, int C, int H, int W, int k, hipStream_t stream) {
     if (!valid_shape(B, C, H, W, k) || !x || !y || !K4)
         return FINC_EINVAL;
     const size_t bytes = (size_t)B * C * H * W * sizeof(float);
     if (overlap(x, bytes, y, bytes) && x != y)
         return FINC_EINVAL;
-    if (logdet && B == 0)
-        return finc_unit_logdet(K4, C, k, H, W, logdet, stream);
-    return launch_forward(x, y, K4, logdet, B, C, H, W, k, 4, FINC_TL, stream);
+    if (prepared4 && !prepared_out_ok(prepared4, finc_workspace_bytes(C, k, 4), x, y, bytes, K4,
+                                      (size_t)4 * C * C * k * k * sizeof(float)))
+        return FINC_EINVAL;
+    if (B == 0) {
+        int rc = FINC_OK;
+        if (logdet)
+            rc = finc_unit_logdet(K4, C, k, H, W, logdet, stream);
+        if (rc == FINC_OK && prepared4) {
+            const int corners[4] = {FINC_TL, FINC_TR, FINC_BL, FINC_BR};
+            rc = finc_prepare(K4, 4, corners, C, k, prepared4, stream);
+        }
+        return rc;
+    }
+    return launch_forward(x, y, K4, logdet, (float *)prepared4, B, C, H, W, k, 4, FINC_TL,
+                          stream);
 }
 
 int finc_unit_logdet(const float *K4, int C, int k, int H, int W, double *out,

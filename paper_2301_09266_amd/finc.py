@@ -27,11 +27,11 @@ SIGNATURES = {
     "finc_strerror": (ctypes.c_char_p, [_i]),
     "finc_workspace_bytes": (_sz, [_i, _i, _i]),
     "finc_prepare": (_i, [_vp, _i, ctypes.POINTER(_i), _i, _i, _vp, _vp]),
-    "finc_forward": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "finc_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "finc_logdet": (_i, [_vp, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
-    "finc_unit_forward": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "finc_unit_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "finc_unit_logdet": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
@@ -148,16 +148,20 @@ def prepare(K: torch.Tensor, corners, out: torch.Tensor | None = None) -> torch.
 
 
 def forward(x: torch.Tensor, K: torch.Tensor, corner: int, out: torch.Tensor | None = None,
-            logdet: torch.Tensor | None = None):
+            logdet: torch.Tensor | None = None, prepared: torch.Tensor | None = None):
     """y = layer(x); with `logdet` (a device float64 tensor of one element) the
-    same launch also writes the layer's log|det|."""
+    same launch also writes the layer's log|det|; with `prepared` (a uint8
+    device tensor of workspace_bytes(C, k, 1)) it also writes the weights
+    prepared for inverse_prepared."""
     L = _require_lib()
     _dev(x, "x")
     B, C, H, W = x.shape
-    _dev(K, "K", (C, C, K.shape[-1], K.shape[-1]))
+    k = K.shape[-1]
+    _dev(K, "K", (C, C, k, k))
     y = torch.empty_like(x) if out is None else _dev(out, "out", x.shape)
-    _check(L.finc_forward(_ptr(x), _ptr(y), _ptr(K), _ptr(_logdet_out(logdet)), B, C, H, W,
-                          K.shape[-1], corner, _stream()), "finc_forward")
+    pp = None if prepared is None else _workspace(workspace_bytes(C, k, 1), x.device, prepared)
+    _check(L.finc_forward(_ptr(x), _ptr(y), _ptr(K), _ptr(_logdet_out(logdet)), _ptr(pp), B, C,
+                          H, W, k, corner, _stream()), "finc_forward")
     return y
 
 
@@ -196,15 +200,18 @@ def inverse_prepared(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: in
 
 
 def unit_forward(x: torch.Tensor, K4: torch.Tensor, out: torch.Tensor | None = None,
-                 logdet: torch.Tensor | None = None):
+                 logdet: torch.Tensor | None = None, prepared: torch.Tensor | None = None):
+    """The unit (TL, TR, BL, BR); optional side outputs as for forward, with
+    `prepared` of workspace_bytes(C, k, 4) for unit_inverse_prepared."""
     L = _require_lib()
     _dev(x, "x")
     B, C, H, W = x.shape
     k = K4.shape[-1]
     _dev(K4, "K4", (4, C, C, k, k))
     y = torch.empty_like(x) if out is None else _dev(out, "out", x.shape)
-    _check(L.finc_unit_forward(_ptr(x), _ptr(y), _ptr(K4), _ptr(_logdet_out(logdet)), B, C, H,
-                               W, k, _stream()), "finc_unit_forward")
+    pp = None if prepared is None else _workspace(workspace_bytes(C, k, 4), x.device, prepared)
+    _check(L.finc_unit_forward(_ptr(x), _ptr(y), _ptr(K4), _ptr(_logdet_out(logdet)), _ptr(pp),
+                               B, C, H, W, k, _stream()), "finc_unit_forward")
     return y
 
 

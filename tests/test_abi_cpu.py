@@ -63,19 +63,21 @@ SHAPE = (2, 12, 16, 16, 3)
 
 
 @pytest.mark.parametrize("args", [
-    (NULL, FAKE2, FAKE, NULL, *SHAPE, 0),
-    (FAKE, NULL, FAKE2, NULL, *SHAPE, 0),
-    (FAKE, FAKE2, NULL, NULL, *SHAPE, 0),
-    (FAKE, FAKE2, FAKE, NULL, -1, 12, 16, 16, 3, 0),
-    (FAKE, FAKE2, FAKE, NULL, 2, 0, 16, 16, 3, 0),
-    (FAKE, FAKE2, FAKE, NULL, 2, 65, 16, 16, 3, 0),
-    (FAKE, FAKE2, FAKE, NULL, 2, 12, 0, 16, 3, 0),
-    (FAKE, FAKE2, FAKE, NULL, 2, 12, 16, 16, 0, 0),
-    (FAKE, FAKE2, FAKE, NULL, 2, 12, 16, 16, 8, 0),
-    (FAKE, FAKE2, FAKE, NULL, *SHAPE, 4),
-    (FAKE, FAKE2, FAKE, NULL, *SHAPE, -1),
-    (FAKE, ctypes.c_void_p(0x100000 + 64), FAKE2, NULL, *SHAPE, 0),   # overlapping x / y
-    (FAKE, FAKE2, FAKE, NULL, 1 << 20, 64, 64, 64, 3, 0),            # > 2^31 elements
+    (NULL, FAKE2, FAKE, NULL, NULL, *SHAPE, 0),
+    (FAKE, NULL, FAKE2, NULL, NULL, *SHAPE, 0),
+    (FAKE, FAKE2, NULL, NULL, NULL, *SHAPE, 0),
+    (FAKE, FAKE2, FAKE, NULL, NULL, -1, 12, 16, 16, 3, 0),
+    (FAKE, FAKE2, FAKE, NULL, NULL, 2, 0, 16, 16, 3, 0),
+    (FAKE, FAKE2, FAKE, NULL, NULL, 2, 65, 16, 16, 3, 0),
+    (FAKE, FAKE2, FAKE, NULL, NULL, 2, 12, 0, 16, 3, 0),
+    (FAKE, FAKE2, FAKE, NULL, NULL, 2, 12, 16, 16, 0, 0),
+    (FAKE, FAKE2, FAKE, NULL, NULL, 2, 12, 16, 16, 8, 0),
+    (FAKE, FAKE2, FAKE, NULL, NULL, *SHAPE, 4),
+    (FAKE, FAKE2, FAKE, NULL, NULL, *SHAPE, -1),
+    (FAKE, ctypes.c_void_p(0x100000 + 64), FAKE2, NULL, NULL, *SHAPE, 0),   # overlapping x / y
+    (FAKE, FAKE2, FAKE, NULL, NULL, 1 << 20, 64, 64, 64, 3, 0),            # > 2^31 elements
+    (FAKE, FAKE2, FAKE, NULL, ctypes.c_void_p(0x4000000 + 16), *SHAPE, 0),  # unaligned prepared
+    (FAKE, FAKE2, FAKE, NULL, ctypes.c_void_p(0x100000), *SHAPE, 0),        # prepared over x
 ])
 def test_forward_rejects(args):
     assert finc.lib().finc_forward(*args, None) == finc.EINVAL
@@ -141,8 +143,8 @@ def test_stack_rejects():
 def test_empty_batch_enqueues_nothing():
     lib = finc.lib()
     ws = ctypes.c_void_p(0x4000000)
-    assert lib.finc_forward(FAKE, FAKE2, FAKE, NULL, 0, 12, 16, 16, 3, 0, None) == finc.OK
-    assert lib.finc_unit_forward(FAKE, FAKE2, FAKE, NULL, 0, 12, 16, 16, 3, None) == finc.OK
+    assert lib.finc_forward(FAKE, FAKE2, FAKE, NULL, NULL, 0, 12, 16, 16, 3, 0, None) == finc.OK
+    assert lib.finc_unit_forward(FAKE, FAKE2, FAKE, NULL, NULL, 0, 12, 16, 16, 3, None) == finc.OK
     assert lib.finc_inverse(FAKE, FAKE2, FAKE, 0, 12, 16, 16, 3, 0, ws, None) == finc.OK
     assert lib.finc_inverse_prepared(FAKE, FAKE2, ws, 0, 12, 16, 16, 3, 0, None) == finc.OK
     assert lib.finc_unit_inverse(FAKE, FAKE2, FAKE, 0, 12, 16, 16, 3, ws, None) == finc.OK

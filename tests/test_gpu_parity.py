@@ -114,6 +114,32 @@ def test_prepared_matches_unprepared(orc):
     assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("C,k,unit", [(12, 3, False), (3, 2, False), (33, 3, False),
+                                      (12, 3, True), (20, 5, True)])
+def test_forward_prepares_weights(C, k, unit):
+    """The forward's prepared-weights side output equals finc_prepare's, bit for
+    bit (its own workgroups for C <= 16, a second launch above), and the
+    forward's y is unchanged by asking for it."""
+    print(f"forward+prepare C={C} k={k} unit={unit}", flush=True)
+    rng = np.random.default_rng(C * 10 + k)
+    x = dev(rng.normal(size=(3, C, 9, 7)))
+    if unit:
+        Kd = dev(synth.unit_kernels(C, k, 0))
+        ref = torch.full((finc.workspace_bytes(C, k, 4),), 0xAB, dtype=torch.uint8, device=DEV)
+        finc.prepare(Kd, [0, 1, 2, 3], out=ref)   # (the same filler in unwritten gaps)
+        pp = torch.full_like(ref, 0xAB)
+        y = finc.unit_forward(x, Kd, prepared=pp)
+        assert torch.equal(y, finc.unit_forward(x, Kd))
+    else:
+        Kd = dev(synth.masked_kernel(C, k, 1, 77))
+        ref = torch.full((finc.workspace_bytes(C, k, 1),), 0xAB, dtype=torch.uint8, device=DEV)
+        finc.prepare(Kd, [1], out=ref)
+        pp = torch.full_like(ref, 0xAB)
+        y = finc.forward(x, Kd, 1, prepared=pp)
+        assert torch.equal(y, finc.forward(x, Kd, 1))
+    assert torch.equal(pp, ref)
+
+
 # --- the workloads at full size ------------------------------------------------
 
 def _layer_workload(orc, name):

@@ -23,6 +23,7 @@
 //    deterministic and independent of the batch size.
 
 #include <hip/hip_runtime.h>
+#include <type_traits>
 
 #include <stdint.h>
 #include <string.h>
@@ -331,10 +332,8 @@ __global__ __launch_bounds__(kWave) void logdet_kernel(const float *K, int n, in
 // round-robin by group: "fresh" groups (dp + dq = 2, which read diagonal
 // e - 1) and "stale" groups (dp + dq >= 3, and the L^-1 y term).  During step
 // e a helper computes its share of diagonal e + 1 and leaves it as a partial
-// tile in LDS.  Its stale sources were all solved a step earlier, so it
-// gathers them at the end of step e - 1 and starts their MFMAs right after
-// the barrier, while the fresh gathers are in flight.  One barrier per
-// diagonal step (Theorems 1 and 2: H + W - 1 steps).
+// tile in LDS.  One barrier per diagonal step (Theorems 1 and 2: H + W - 1
+// steps).
 //
 // With a single channel tile the critical wave keeps its rows' previous
 // pixels in its accumulator: its MFMA chain for diagonal e starts right after
@@ -352,6 +351,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxWaves = 16;
 constexpr int kMaxGroups = 8;                       // quad groups (x4 quads) per wave
+// critical-wave forms an inverse instance is built with
+constexpr int kCritGather = 0, kCritRegs = 1, kCritBoth = 2;
 
 // Work split and LDS layout of one level (same for every layer of it).
 struct Plan {
@@ -663,7 +664,7 @@ __device__ void level_input(const InvArgs &a, int l, float *sm, size_t b) {
 
 // All layers of one level for one wave (NG quad groups).  Weights of the
 // next layer are fetched into registers while the current one runs.
-template <int NG, int MAXT>
+template <int NG, int MAXT, int MODE>
 __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role &r, float *sm,
                             size_t b) {
     const Level &lv = a.lv[l];
@@ -673,7 +674,11 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
     constexpr bool kPrefetch = NG <= 4 && MAXT <= 512;
     constexpr int GN = kPrefetch ? G : 1;
     // the register-fed critical wave owns the two dp + dq = 1 taps as groups
-    const bool regc = pl.regcrit && r.role == 0;
+    // (MODE: kCritGather / kCritRegs / kCritBoth -- the instance carries only
+    // the critical loop(s) its levels use)
+    const bool regc = MODE == kCritRegs    ? r.role == 0
+                      : MODE == kCritGather ? false
+                                            : pl.regcrit && r.role == 0;
     const int ngw = __builtin_amdgcn_readfirstlane(groups_of(pl, r));
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int C = pl.C, CP = pl.CP, H = pl.H, W = pl.W, P = pl.P, WP = pl.WP;
@@ -774,27 +779,35 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
         // critical loop carries nothing but its own work.
         const int zaddr = pl.offZ + 4 * lane, taddr = pl.offT + 4 * lane;
         const int dcol = fw ? -CP : CP;   // address step of one frame column
+        const int fwo = fw ? (W - 1) * CP : 0;
         auto colx = [&](int j) {   // natural column of frame column j (clamped), times CP
-            const int jc = imin(imax(j, 0), W - 1);
-            return __mul24(fw ? W - 1 - jc : jc, CP);
+            return fwo + __mul24(imin(imax(j, 0), W - 1), dcol);
         };
-        // gathered B operands of groups [g0, g1) at frame column j (one load
-        // per group, all in flight together)
-        auto gather = [&](float4 (&av)[G], int g0, int g1, int j) {
+        // Gather addresses of every group at frame column j.
+        auto addrs = [&](int (&ad)[G], int j) {
             const int cx = colx(j);
             const bool live = j >= 0 && gi < H;
 #pragma unroll
             for (int g = 0; g < NG; ++g)
-                if (g >= g0 && g < g1)
-                    av[g] = *reinterpret_cast<const float4 *>(sm + (live ? gbase[g] + cx : zaddr));
+                ad[g] = live ? gbase[g] + cx : zaddr;
         };
-        // D[output channel 4 kq + rr][row li] += groups [g0, g1): weights are
-        // the A operand (rows = output channels), gathered inputs the B
-        // operand (columns = frame rows)
-        auto mma = [&](const float4 (&av)[G], f32x4 c, int g0, int g1) -> f32x4 {
+        // The wave's B operands, one 16-byte load per group, all in flight
+        // together.  `full`: the wave owns every group of the instance (no
+        // per-group test); otherwise groups [0, ngw).
+        auto load = [&](float4 (&av)[G], const int (&ad)[G], auto full) {
+#pragma unroll
+            for (int g = 0; g < NG; ++g)
+                if (decltype(full)::value || g < ngw)
+                    av[g] = *reinterpret_cast<const float4 *>(sm + ad[g]);
+        };
+        // D[output channel 4 kq + rr][row li] = sum over the wave's groups:
+        // weights are the A operand (rows = output channels), gathered inputs
+        // the B operand (columns = frame rows)
+        auto mma = [&](const float4 (&av)[G], auto full) -> f32x4 {
+            f32x4 c = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
             for (int g = 0; g < NG; ++g) {
-                if (g >= g0 && g < g1) {
+                if (decltype(full)::value || g < ngw) {
                     c = mfma4(w[g][0], av[g].x, c);
                     c = mfma4(w[g][1], av[g].y, c);
                     c = mfma4(w[g][2], av[g].z, c);
@@ -803,7 +816,9 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
             }
             return c;
         };
-        auto active = [&](int e) { return e >= 0 && e < E && r0 <= e && e - W + 1 <= r1; };
+        // Diagonals that meet the tile's rows; a role's other steps only keep
+        // the barrier count (every role passes 1 + E barriers per layer).
+        const int e_lo = r0, e_hi = imin(r1 + W - 1, E - 1);
         // the critical wave writes channels 16 nt + 4 kq .. +3 of its row's pixel
         const int wx0 = bx0 + nt * 16 + 4 * kq;
         const bool wch = nt * 16 + 4 * kq < CP && gi < H;
@@ -826,49 +841,67 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
         const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
 
         if (r.role == 1) {
-            // helper: during step e, diagonal e + 1 (fresh groups on top of
-            // the stale part computed in step e - 1) and the stale part of
-            // diagonal e + 2
-            // helper: during step e, diagonal e + 1.  Its stale operands
-            // (sources on diagonals <= e - 1, and y) were gathered at the end
-            // of step e - 1, so their MFMAs start right after the barrier while
-            // the fresh gathers (diagonal e - 1, just solved) are in flight.
+            // helper: during step e, the partial tile of diagonal e + 1 (every
+            // source is on diagonal e - 1 or earlier, or is y).  The next
+            // step's gather addresses are formed while the tile's write lands.
             f32x4 *Rw = reinterpret_cast<f32x4 *>(R + rown);
-            float4 av[G];
-            if (active(0)) {   // diagonal 0: every group (all sources are zero but y)
-                gather(av, 0, ngw, -gi);
-                Rw[0] = mma(av, zero, 0, ngw);
-            }
-            __syncthreads();
-            for (int e = 0; e < E; ++e) {
-                if (active(e + 1)) {
-                    gather(av, 0, ngw, e + 1 - gi);
-                    Rw[((e + 1) & 1) * (rstride / 4)] = mma(av, zero, 0, ngw);
+            auto run = [&](auto full) {
+                float4 av[G];
+                int ad[G];
+                if (e_lo == 0) {   // diagonal 0: all sources are zero but y
+                    addrs(ad, -gi);
+                    load(av, ad, full);
+                    Rw[0] = mma(av, full);
                 }
+                // steps e whose diagonal e + 1 meets the tile
+                const int lo = imax(e_lo - 1, 0), hi = e_hi - 1;
+                addrs(ad, lo + 1 - gi);
                 __syncthreads();
-            }
-        } else if (r.role == 0 && regc) {
+                int e = 0;
+                for (; e < lo; ++e)
+                    __syncthreads();
+                for (; e <= hi; ++e) {
+                    load(av, ad, full);
+                    Rw[((e + 1) & 1) * (rstride / 4)] = mma(av, full);
+                    addrs(ad, e + 2 - gi);
+                    __syncthreads();
+                }
+                for (; e < E; ++e)
+                    __syncthreads();
+            };
+            if (ngw == NG)
+                run(std::true_type{});
+            else
+                run(std::false_type{});
+        } else if (MODE != kCritGather && r.role == 0 && regc) {
             // register-fed critical wave.  dprev: lane (kq, li) holds channels
             // 4 kq .. +3 of row li's pixel of the previous diagonal (0 for rows
             // not started).  Its MFMA chain needs nothing from LDS but, in a
             // lower tile, lane li = 0's row above (the last row of the tile
             // above); the partial tiles are read meanwhile and added last.
-            __syncthreads();
-            f32x4 dprev = zero;
-            int j = -gi;   // frame column of row gi at diagonal 0
+            // The chain's first kPre MFMAs (own row) depend on nothing but
+            // dprev: they are issued before the barrier, while the write of
+            // the diagonal becomes visible.
+            constexpr int kPre = 3;
+            f32x4 dprev = zero, pre = zero;
+            int j = e_lo - gi;   // frame column of row gi at the tile's first diagonal
             // write address of frame column j (the affine form; used only while
             // 0 <= j < W)
-            int wcol = wx0 + (fw ? W - 1 : 0) * CP + j * dcol;
+            int wcol = wx0 + fwo + j * dcol;
             // lane li = 0 of a lower tile reads the tile above's last row
             // (solved in the previous step; channel quads that exist); other
             // lanes read zeros
             const int ui = mt * 16 - 1;
             const int uoi = fh ? H - 1 - imax(ui, 0) : imax(ui, 0);
-            int ju = -16 * mt;   // frame column of row 16 mt (and of the row above it) at diagonal 0
-            int ucol = pl.offX + ((uoi + P) * WP + P + (fw ? W - 1 : 0)) * CP + 4 * kq + ju * dcol;
+            int ju = e_lo - 16 * mt;   // frame column of row 16 mt (and of the row above it)
+            int ucol = pl.offX + ((uoi + P) * WP + P) * CP + fwo + 4 * kq + ju * dcol;
             const f32x4 *R0 = reinterpret_cast<const f32x4 *>(R + rown);
-            for (int e = 0; e < E; ++e) {
-                if (active(e)) {
+            __syncthreads();
+            int e = 0;
+            for (; e < e_lo; ++e)
+                __syncthreads();
+            for (; e <= e_hi; ++e) {
+                {
                     const f32x4 *Rp = R0 + (e & 1) * (rstride / 4);
                     f32x4 up = zero;
                     if (mt > 0)
@@ -877,8 +910,10 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
                                                                                     : zaddr));
                     // the first four partial tiles in flight during the MFMAs
                     const f32x4 q0 = Rp[0], q1 = Rp[64], q2 = Rp[128], q3 = Rp[192];
+                    const bool ok = wch && (unsigned)j < (unsigned)W;
+                    const int waddr = ok ? wcol : taddr;
                     __builtin_amdgcn_sched_barrier(0);
-                    f32x4 p = zero;
+                    f32x4 p = pre;
                     // tap (0,1): own row, previous column; tap (1,0): row above,
                     // same column -- the neighbouring lane's previous result
                     // (row_shr:1 inside each row of 16 lanes; lane 0 takes `up`).
@@ -886,7 +921,7 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
                     // bit-casts a vector element lvalue as element 0.
                     if constexpr (G >= 2) {   // (instances with G < 2 never get regc)
 #pragma unroll
-                        for (int e4 = 0; e4 < 4; ++e4)
+                        for (int e4 = kPre; e4 < 4; ++e4)
                             p = mfma4(w[0][e4], dprev[e4], p);
 #pragma unroll
                         for (int e4 = 0; e4 < 4; ++e4) {
@@ -907,9 +942,16 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
                         rs += t0;
                     }
                     const f32x4 x = rs + p;
-                    const bool ok = wch && (unsigned)j < (unsigned)W;
-                    *reinterpret_cast<f32x4 *>(sm + (ok ? wcol : taddr)) = x;
+                    *reinterpret_cast<f32x4 *>(sm + waddr) = x;
                     dprev = x;
+                    __builtin_amdgcn_sched_barrier(0);
+                    // next diagonal's own-row MFMAs, overlapping the write
+                    pre = zero;
+                    if constexpr (G >= 2) {
+#pragma unroll
+                        for (int e4 = 0; e4 < kPre; ++e4)
+                            pre = mfma4(w[0][e4], dprev[e4], pre);
+                    }
                 }
                 j += 1;
                 wcol += dcol;
@@ -917,26 +959,39 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
                 ucol += dcol;
                 __syncthreads();
             }
-        } else if (r.role == 0) {
+            for (; e < E; ++e)
+                __syncthreads();
+        } else if (MODE != kCritRegs && r.role == 0) {
             // critical wave that gathers its dp + dq = 1 taps from LDS (several
             // channel tiles: the previous diagonal's channels sit in several
             // waves)
-            __syncthreads();
             const f32x4 *R0 = reinterpret_cast<const f32x4 *>(R + rown);
-            float4 av[G];
-            for (int e = 0; e < E; ++e) {
-                if (active(e)) {
+            auto run = [&](auto full) {
+                float4 av[G];
+                int ad[G];
+                addrs(ad, e_lo - gi);
+                __syncthreads();
+                int e = 0;
+                for (; e < e_lo; ++e)
+                    __syncthreads();
+                for (; e <= e_hi; ++e) {
                     const int j = e - gi;
-                    const f32x4 *Rp = R0 + (e & 1) * (rstride / 4);
-                    gather(av, 0, ngw, j);
-                    const f32x4 rs = partial_sum(Rp);
-                    f32x4 x = mma(av, zero, 0, ngw);
+                    load(av, ad, full);
+                    const f32x4 rs = partial_sum(R0 + (e & 1) * (rstride / 4));
+                    f32x4 x = mma(av, full);
                     x += rs;
                     const bool ok = wch && (unsigned)j < (unsigned)W;
                     *reinterpret_cast<f32x4 *>(sm + (ok ? wx0 + colx(j) : taddr)) = x;
+                    addrs(ad, e + 1 - gi);
+                    __syncthreads();
                 }
-                __syncthreads();
-            }
+                for (; e < E; ++e)
+                    __syncthreads();
+            };
+            if (ngw == NG)
+                run(std::true_type{});
+            else
+                run(std::false_type{});
         } else {
             __syncthreads();
             for (int e = 0; e < E; ++e)
@@ -949,7 +1004,7 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
 // last store.  Levels go from the top (l = L-1) down; between levels the
 // solution of the level above is unsqueezed and the level's latent appended
 // behind it (channel split), straight from LDS into the next level's input.
-template <int NG, int MAXT>
+template <int NG, int MAXT, int MODE>
 __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
     extern __shared__ float sm[];
     const size_t b = blockIdx.x;
@@ -958,7 +1013,7 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
         const Plan pl = lv.pl;
         const int CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
         float *Y = sm + pl.offY;
-        level_waves<NG, MAXT>(a, l, pl, role_of(pl), sm, b);
+        level_waves<NG, MAXT, MODE>(a, l, pl, role_of(pl), sm, b);
         if (a.n_units * a.lpu == 0) {   // no layers at this level: the input passes through
             for (int idx = threadIdx.x; idx < HW * CP; idx += blockDim.x) {
                 const int p = idx / CP, c = idx - p * CP;
@@ -1367,18 +1422,24 @@ int launch_prep(const float *K, int n, const int *corners, int C, int k, float *
 
 // Kernel instances by quad groups per wave (1..kMaxGroups) and workgroup size.
 typedef void (*InvKernel)(InvArgs);
-template <int MAXT>
-InvKernel inverse_instance(int ng) {
+template <int MAXT, int MODE>
+InvKernel inverse_instance_mode(int ng) {
     switch (ng) {
-    case 1: return inverse_chain_kernel<1, MAXT>;
-    case 2: return inverse_chain_kernel<2, MAXT>;
-    case 3: return inverse_chain_kernel<3, MAXT>;
-    case 4: return inverse_chain_kernel<4, MAXT>;
-    case 5: return inverse_chain_kernel<5, MAXT>;
-    case 6: return inverse_chain_kernel<6, MAXT>;
-    case 7: return inverse_chain_kernel<7, MAXT>;
-    default: return inverse_chain_kernel<8, MAXT>;
+    case 1: return inverse_chain_kernel<1, MAXT, MODE>;
+    case 2: return inverse_chain_kernel<2, MAXT, MODE>;
+    case 3: return inverse_chain_kernel<3, MAXT, MODE>;
+    case 4: return inverse_chain_kernel<4, MAXT, MODE>;
+    case 5: return inverse_chain_kernel<5, MAXT, MODE>;
+    case 6: return inverse_chain_kernel<6, MAXT, MODE>;
+    case 7: return inverse_chain_kernel<7, MAXT, MODE>;
+    default: return inverse_chain_kernel<8, MAXT, MODE>;
     }
+}
+template <int MAXT>
+InvKernel inverse_instance(int ng, int mode) {
+    return mode == kCritGather ? inverse_instance_mode<MAXT, kCritGather>(ng)
+           : mode == kCritRegs ? inverse_instance_mode<MAXT, kCritRegs>(ng)
+                               : inverse_instance_mode<MAXT, kCritBoth>(ng);
 }
 
 int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
@@ -1392,14 +1453,16 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     rc = check_lds(lds);
     if (rc != FINC_OK)
         return rc;
-    int ng = 1;
+    int ng = 1, nreg = 0;
     for (int l = 0; l < a.L; ++l) {
         const Plan &p = a.lv[l].pl;
         ng = imax(ng, plan_groups(p));
+        nreg += p.regcrit;
     }
-    const InvKernel k = threads <= 256   ? inverse_instance<256>(ng)
-                        : threads <= 512 ? inverse_instance<512>(ng)
-                                         : inverse_instance<1024>(ng);
+    const int mode = nreg == a.L ? kCritRegs : nreg == 0 ? kCritGather : kCritBoth;
+    const InvKernel k = threads <= 256   ? inverse_instance<256>(ng, mode)
+                        : threads <= 512 ? inverse_instance<512>(ng, mode)
+                                         : inverse_instance<1024>(ng, mode);
     if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)lds) != hipSuccess)
         (void)hipGetLastError();   // not needed on every runtime; the launch check decides

@@ -41,6 +41,8 @@ def parse():
     p.add_argument("--workload", default="layer_c12_16x16_b64_k3")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="bound on the CPU-oracle sample (0 disables it)")
+    p.add_argument("--graph-steps", type=int, default=20,
+                   help="steps captured in one HIP graph (the timed region replays it)")
     p.add_argument("--no-graph", action="store_true",
                    help="launch every step eagerly instead of replaying a HIP graph")
     p.add_argument("--no-configs", action="store_true",
@@ -290,20 +292,32 @@ def main():
         st.step()
     torch.cuda.synchronize()
 
-    graph = None
+    # HIP graphs of P steps each (and one of the remainder), so that exactly
+    # `steps` steps run in the timed region with one submission per P steps
+    graphs = []
     if not args.no_graph:
         side = torch.cuda.Stream()
         side.wait_stream(stream)
         with torch.cuda.stream(side):
             st.step()
         torch.cuda.synchronize()
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            st.step()
-        torch.cuda.synchronize()
-        for _ in range(3):
-            graph.replay()
-        torch.cuda.synchronize()
+        per = max(1, min(args.graph_steps, args.steps))
+
+        def capture(n):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                for _ in range(n):
+                    st.step()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            return g
+
+        full = capture(per) if args.steps >= per else None
+        graphs = [full] * (args.steps // per) if full is not None else []
+        if args.steps % per:
+            graphs.append(capture(args.steps % per))
+    graph = graphs[0] if graphs else None
 
     # timed region: exactly `steps` steps
     t_start = torch.cuda.Event(enable_timing=True)
@@ -311,10 +325,11 @@ def main():
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record(stream)
-    for _ in range(args.steps):
-        if graph is not None:
-            graph.replay()
-        else:
+    if graphs:
+        for g in graphs:
+            g.replay()
+    else:
+        for _ in range(args.steps):
             st.step()
     t_end.record(stream)
     torch.cuda.synchronize()
@@ -357,7 +372,8 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": args.workload, "B": st.B, "C": st.C, "H": st.H, "W": st.W,
-                   "k": st.k, "corner": "TL", "graph": graph is not None,
+                   "k": st.k, "corner": "TL",
+                   "graph_steps": (min(args.graph_steps, args.steps) if graphs else 0),
                    "step": "forward + logdet + weight preparation (one launch), inverse"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,

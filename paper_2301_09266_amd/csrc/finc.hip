@@ -366,6 +366,8 @@ struct Plan {
     int offX, offY, offR, offZ, offT;  // LDS offsets (floats): solution, input, partial
                                        // tiles, zero block, trash block
     int lds_floats;
+    int lstride;                // floats of one prepared layer
+    int wave[kMaxWaves];        // per wave: role | mt << 2 | nt << 6 | h << 10 | groups << 14
 };
 
 // Quad groups of the busiest wave of a plan.
@@ -416,6 +418,23 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p) {
     p.offZ = p.offR + 2 * p.T * p.S4 * 256;
     p.offT = p.offZ + 256;
     p.lds_floats = p.offT + 256;
+    p.lstride = (int)prep_layer_floats(C, K);
+    // wave roles: critical waves of the tiles first, then S helpers per tile,
+    // then idle waves; with the number of quad groups each one owns
+    for (int w = 0; w < kMaxWaves; ++w) {
+        int role = 2, tile = 0, h = 0, ng = 0;
+        if (w < p.T) {
+            role = 0;
+            tile = w;
+            ng = p.regcrit ? 2 : ceil_div(p.nq_crit, 4);
+        } else if (w < p.NW) {
+            role = 1;
+            tile = (w - p.T) / p.S;
+            h = (w - p.T) - tile * p.S;
+            ng = h < p.FG + p.SG ? ceil_div(p.FG + p.SG - h, p.S) : 0;
+        }
+        p.wave[w] = role | (tile % p.MT) << 2 | (tile / p.MT) << 6 | h << 10 | ng << 14;
+    }
     return true;
 }
 
@@ -434,29 +453,23 @@ struct Level {
 };
 
 struct InvArgs {
-    Level lv[kMaxLevels];
-    float *out;           // (B, C_0, H_0, W_0)
     int L, n_units, lpu, corner0;
+    float *out;           // output of the last level: (B, C, H, W)
+    Level lv[kMaxLevels]; // in the order they run
 };
 
 // What one wave does at a level.  role 0: critical wave of `tile`; 1: helper
 // h of `tile`; 2: idle (barriers only).
 struct Role {
-    int role, tile, h;
+    int role, tile, mt, nt, h, ng;   // tile = nt * MT + mt; ng: quad groups the wave owns
 };
 
-__device__ inline Role role_of(const Plan &pl) {
+// This wave's role at level i (from the table the host filled in).
+__device__ inline Role role_of(const InvArgs &a, int i) {
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    Role r = {2, 0, 0};
-    if (wave < pl.T) {
-        r.role = 0;
-        r.tile = wave;
-    } else if (wave < pl.NW) {
-        r.role = 1;
-        r.tile = (wave - pl.T) / pl.S;
-        r.h = (wave - pl.T) - r.tile * pl.S;
-    }
-    return r;
+    const int c = a.lv[i].pl.wave[wave];
+    const int mt = (c >> 2) & 15, nt = (c >> 6) & 15;
+    return Role{c & 3, nt * a.lv[i].pl.MT + mt, mt, nt, (c >> 10) & 15, (c >> 14) & 15};
 }
 
 // Quad that lane group kq of group g of a wave covers, or -1.  Critical wave
@@ -479,15 +492,6 @@ __device__ inline int quad_of(const Plan &pl, const Role &r, int g, int kq) {
     return G < pl.FG + pl.SG && u < pl.nq ? u : -1;
 }
 
-// Groups of a wave.
-__device__ inline int groups_of(const Plan &pl, const Role &r) {
-    if (r.role == 0)
-        return pl.regcrit ? 2 : ceil_div(pl.nq_crit, 4);
-    if (r.role != 1 || r.h >= pl.FG + pl.SG)
-        return 0;
-    return ceil_div(pl.FG + pl.SG - r.h, pl.S);
-}
-
 __device__ inline int corner_of(const InvArgs &a, int q) { return a.lpu == 1 ? a.corner0 : q; }
 
 // The A operands (prepared weights) of this lane's quads for one layer: lane
@@ -500,7 +504,7 @@ template <int NG>
 __device__ inline void load_weights(float (&w)[NG][4], const Plan &pl, const Role &r,
                                     const float *__restrict__ prep) {
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
-    const int co = (r.tile / pl.MT) * 16 + li;
+    const int co = r.nt * 16 + li;
     const float4 *W4 = reinterpret_cast<const float4 *>(prep);
     const float4 *zero = reinterpret_cast<const float4 *>(prep + prep_zero_offset(pl.C, pl.K)) + li;
 #pragma unroll
@@ -564,7 +568,7 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
                                   F during) {
     const int HW = pl.H * pl.W, CP = pl.CP, C = pl.C;
     float *Y = sm + pl.offY;
-    constexpr int U = 4;
+    constexpr int U = 8;
     bool first = true;
     if ((HW & 3) == 0) {
         const int n4 = C * HW / 4, hw4 = HW / 4;
@@ -627,8 +631,11 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
 // z_l) where h is the level above's solution, still in LDS: channel c < C/2
 // of pixel (i, j) is channel 4c + 2(i&1) + (j&1) of h at (i/2, j/2).  Then
 // the solution buffer (with its zero border) and the zero block are cleared.
-__device__ void level_input(const InvArgs &a, int l, float *sm, size_t b) {
-    const Level &lv = a.lv[l];
+// `work` (register-only set-up) runs while the top level's input is on its
+// way.
+template <typename F>
+__device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm, size_t b,
+                            F work) {
     const Plan &pl = lv.pl;
     const int C = pl.C, CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
     float *Y = sm + pl.offY;
@@ -636,12 +643,15 @@ __device__ void level_input(const InvArgs &a, int l, float *sm, size_t b) {
         zero_floats(sm + pl.offX, pl.offY - pl.offX);
         zero_floats(sm + pl.offR, pl.offZ + 256 - pl.offR);   // unused slots and Z stay 0
     };
-    if (l == a.L - 1) {
+    if (top) {
         // the solution buffer and the partial tiles are cleared while the
         // image is on its way
-        load_input(sm, pl, lv.z + b * (size_t)C * HW, clear);
+        load_input(sm, pl, lv.z + b * (size_t)C * HW, [&] {
+            work();
+            clear();
+        });
     } else {
-        const Plan &up = a.lv[l + 1].pl;
+        work();
         const int Ch = C / 2;
         const float *lat = lv.z + b * (size_t)Ch * HW;
         for (int idx = threadIdx.x; idx < CP * HW; idx += blockDim.x) {
@@ -665,9 +675,8 @@ __device__ void level_input(const InvArgs &a, int l, float *sm, size_t b) {
 // All layers of one level for one wave (NG quad groups).  Weights of the
 // next layer are fetched into registers while the current one runs.
 template <int NG, int MAXT, int MODE>
-__device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role &r, float *sm,
-                            size_t b) {
-    const Level &lv = a.lv[l];
+__device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const Plan &up,
+                            const Plan &pl, const Role &r, float *sm, size_t b) {
     constexpr int G = NG > 0 ? NG : 1;
     // weights of the next layer prefetched into registers when they fit (with
     // 16 waves a lane has 128 registers)
@@ -679,15 +688,15 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
     const bool regc = MODE == kCritRegs    ? r.role == 0
                       : MODE == kCritGather ? false
                                             : pl.regcrit && r.role == 0;
-    const int ngw = __builtin_amdgcn_readfirstlane(groups_of(pl, r));
+    const int ngw = r.ng;
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int C = pl.C, CP = pl.CP, H = pl.H, W = pl.W, P = pl.P, WP = pl.WP;
     const int HW = H * W;
-    const int mt = r.tile % pl.MT, nt = r.tile / pl.MT;
+    const int mt = r.mt, nt = r.nt;
     const int E = H + W - 1;
     const int r0 = mt * 16, r1 = imin(mt * 16 + 15, H - 1);
     float *R = sm + pl.offR;
-    const size_t lstride = prep_layer_floats(C, pl.K);
+    const size_t lstride = pl.lstride;
     const int nlayers = a.n_units * a.lpu;
     float w[G][4], wn[GN][4];
     // layer index n = 0 .. nlayers-1 runs unit u = U-1-n/lpu, block q = lpu-1-n%lpu
@@ -709,7 +718,23 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
         else
             fetch(w, 0);
     }
-    level_input(a, l, sm, b);
+    // corner-free geometry of each group's quad: dp | dq << 4 | cq << 8, or
+    // -1 where the quad does not exist (decoded while the input loads)
+    int geo[G];
+    level_input(lv, top, up, sm, b, [&] {
+#pragma unroll
+        for (int g = 0; g < NG; ++g) {
+            const int uq = quad_of(pl, r, g, kq);
+            if (uq < 0) {
+                geo[g] = -1;
+            } else {
+                const int t = uq / pl.ncq, cq = uq - t * pl.ncq;
+                int dp, dq;
+                tap_of(t, pl.K, dp, dq);
+                geo[g] = dp | dq << 4 | cq << 8;
+            }
+        }
+    });
     for (int n = 0; n < nlayers; ++n) {
         const int u = a.n_units - 1 - n / a.lpu, q = a.lpu - 1 - n % a.lpu;
         if (n > 0) {   // previous layer's solution is this layer's input
@@ -756,18 +781,13 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
         int gbase[G];
 #pragma unroll
         for (int g = 0; g < NG; ++g) {
-            const int uq = quad_of(pl, r, g, kq);
-            if (uq < 0) {
+            const int dp = geo[g] & 15, dq = (geo[g] >> 4) & 15, cq4 = (geo[g] >> 8) << 2;
+            if (geo[g] < 0)
                 gbase[g] = by0;
-            } else {
-                const int t = uq / pl.ncq, cq = uq - t * pl.ncq;
-                int dp, dq;
-                tap_of(t, pl.K, dp, dq);
-                if (dp == 0 && dq == 0)
-                    gbase[g] = by0 + 4 * cq;
-                else
-                    gbase[g] = bx0 + 4 * cq - (dp * sh * WP + dq * sw) * CP;
-            }
+            else if (dp == 0 && dq == 0)
+                gbase[g] = by0 + cq4;
+            else
+                gbase[g] = bx0 + cq4 - (dp * sh * WP + dq * sw) * CP;
         }
         // Rows of the frame that have not started (frame column j < 0, or rows
         // below the image) gather zeros, so their partial tiles and carried
@@ -1001,19 +1021,31 @@ __device__ void level_waves(const InvArgs &a, int l, const Plan &pl, const Role 
 }
 
 // Inverse of a whole chain with the image in LDS from the first load to the
-// last store.  Levels go from the top (l = L-1) down; between levels the
-// solution of the level above is unsqueezed and the level's latent appended
-// behind it (channel split), straight from LDS into the next level's input.
+// last store.  Levels run in argument order (the top of a stack first);
+// between levels the solution of the level above is unsqueezed and the
+// level's latent appended behind it (channel split), straight from LDS into
+// the next level's input.  The first level sits at a fixed argument offset,
+// so its arguments arrive in the kernel's first round of scalar loads.
 template <int NG, int MAXT, int MODE>
 __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
     extern __shared__ float sm[];
     const size_t b = blockIdx.x;
-    for (int l = a.L - 1; l >= 0; --l) {
-        const Level &lv = a.lv[l];
-        const Plan pl = lv.pl;
+    Level lv = a.lv[0];
+    Plan above = lv.pl;   // plan of the level run before (unused at the first)
+    {   // one round of scalar loads for everything the first level starts with
+        const int L = a.L, nu = a.n_units, lpu = a.lpu, c0 = a.corner0;
+        asm volatile("" ::"s"(L), "s"(nu), "s"(lpu), "s"(c0), "s"(lv.z), "s"(lv.prep),
+                     "s"(lv.scale));
+    }
+    for (int i = 0; i < a.L; ++i) {
+        if (i > 0) {
+            above = lv.pl;
+            lv = a.lv[i];
+        }
+        const Plan &pl = lv.pl;
         const int CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
         float *Y = sm + pl.offY;
-        level_waves<NG, MAXT, MODE>(a, l, pl, role_of(pl), sm, b);
+        level_waves<NG, MAXT, MODE>(a, lv, i == 0, above, pl, role_of(a, i), sm, b);
         if (a.n_units * a.lpu == 0) {   // no layers at this level: the input passes through
             for (int idx = threadIdx.x; idx < HW * CP; idx += blockDim.x) {
                 const int p = idx / CP, c = idx - p * CP;
@@ -1023,7 +1055,7 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
             __syncthreads();
         }
     }
-    const Plan &p0 = a.lv[0].pl;
+    const Plan &p0 = lv.pl;   // the last level run
     const int HW0 = p0.H * p0.W, n0 = p0.C * HW0;
     float *dst = a.out + b * (size_t)n0;
     constexpr int U = 4;
@@ -1322,10 +1354,15 @@ int plan_inverse(InvArgs &a, size_t *lds_bytes, int *threads) {
             return FINC_EUNSUPPORTED;
         lds = imax(lds, p.lds_floats);
         nw = imax(nw, p.NW);
-        // the unsqueeze reads the level above's solution while writing this
-        // level's input: the two regions must not overlap
-        if (l + 1 < a.L && a.lv[l + 1].pl.offY > p.offY)
-            return FINC_EUNSUPPORTED;
+        // the unsqueeze reads the level above's solution (its image, not the
+        // zero border) while writing this level's input: the two must not
+        // overlap
+        if (l > 0) {
+            const Plan &u = a.lv[l - 1].pl;
+            const int last = u.offX + ((u.H - 1 + u.P) * u.WP + u.W - 1 + u.P) * u.CP + u.CP - 1;
+            if (last >= p.offY)
+                return FINC_EUNSUPPORTED;
+        }
     }
     *lds_bytes = (size_t)lds * sizeof(float);
     *threads = nw * kWave;
@@ -1809,10 +1846,10 @@ int finc_stack_inverse_prepared(const float *const *z, float *x, const void *pre
     InvArgs a;
     memset(&a, 0, sizeof(a));
     size_t poff = 0, soff = 0;
-    for (int l = 0; l < L; ++l) {
+    for (int l = 0; l < L; ++l) {   // levels run top first
         const int C = C1 << l;
-        a.lv[l] = level(z[l], (const char *)prepared + poff, scale + soff, bias + soff, C,
-                        H1 >> l, W1 >> l, k);
+        a.lv[L - 1 - l] = level(z[l], (const char *)prepared + poff, scale + soff, bias + soff, C,
+                                H1 >> l, W1 >> l, k);
         poff += stack_level_bytes(l, U, C1, k);
         soff += (size_t)U * C;
     }

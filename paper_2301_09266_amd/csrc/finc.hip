@@ -42,6 +42,29 @@ __host__ __device__ inline int ceil_div(int a, int b) { return (a + b - 1) / b; 
 __host__ __device__ inline int imin(int a, int b) { return a < b ? a : b; }
 __host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
 
+// Division of a non-negative int by a divisor fixed on the host, as a
+// multiply-high and two shifts (Granlund and Montgomery's round-up method:
+// l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1; exact for every
+// 32-bit dividend).
+struct FastDiv {
+    unsigned m;
+    int s1, s2;
+};
+inline FastDiv make_fastdiv(int d) {
+    int l = 0;
+    while ((1ull << l) < (unsigned long long)d)
+        ++l;
+    FastDiv f;
+    f.m = (unsigned)((((1ull << l) - (unsigned long long)d) << 32) / (unsigned long long)d + 1);
+    f.s1 = l < 1 ? l : 1;
+    f.s2 = l > 1 ? l - 1 : 0;
+    return f;
+}
+__device__ inline int fdiv(int x, const FastDiv &f) {
+    const unsigned t = __umulhi(f.m, (unsigned)x);
+    return (int)((t + (((unsigned)x - t) >> f.s1)) >> f.s2);
+}
+
 // Pins a loaded value in a register at this point, so that the compiler
 // cannot move the load into the branch that uses it: a group of loads whose
 // results are pinned right after they are issued costs one memory latency,
@@ -1108,6 +1131,9 @@ struct FwdPlan {
                                  // (chains only), weight fragments, quad offsets (ints)
     int lds_floats;
     int n, corner0;              // layers (1, or 4 for a unit: TL, TR, BL, BR)
+    // divisions of the index arithmetic: staged plane of a full and of the
+    // last row block, WP, NG, ncq, K, NT, W, CP / 4
+    FastDiv d_plane, d_plane_last, d_WP, d_NG, d_ncq, d_K, d_NT, d_W, d_cp4;
 };
 
 struct FwdArgs {
@@ -1160,29 +1186,29 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         const int up = fp.n == 1 ? oh0 : P, down = fp.n == 1 ? P - oh0 : P;
         const int lo = imax(0, i0 - up), hi = imin(H, i0 + rb + down);   // rows read
         const int nrow = rb + 2 * P, plane = nrow * WP, total = CP * plane;
+        const FastDiv dpl = blk == fp.nblk - 1 ? fp.d_plane_last : fp.d_plane;
         constexpr int U = 8;
         for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
             float v[U];
             bool inb[U];
+            int dst[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int idx = base + u * blockDim.x;
-                const int c = idx / plane, rem = idx - c * plane;
-                const int pr = rem / WP, pc = rem - pr * WP;
+                const int c = fdiv(idx, dpl), rem = idx - c * plane;
+                const int pr = fdiv(rem, fp.d_WP), pc = rem - pr * WP;
                 const int i = i0 - P + pr, j = pc - P;
                 inb[u] = idx < total && c < C && i >= lo && i < hi && j >= 0 && j < W;
                 v[u] = xb[inb[u] ? c * HW + (size_t)i * W + j : 0];
+                dst[u] = idx < total ? rem * CP + c : -1;
             }
 #pragma unroll
             for (int u = 0; u < U; ++u)
                 pin(v[u]);
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int idx = base + u * blockDim.x;
-                const int c = idx / plane, rem = idx - c * plane;
-                if (idx < total)
-                    X[rem * CP + c] = inb[u] ? v[u] : 0.0f;
-            }
+            for (int u = 0; u < U; ++u)
+                if (dst[u] >= 0)
+                    X[dst[u]] = inb[u] ? v[u] : 0.0f;
         }
     }
     double ld_acc = 0.0;
@@ -1203,11 +1229,11 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
             for (int h = 0; h < 2; ++h) {
                 const int idx = base + h * blockDim.x;
                 const int f = idx >> 6, ln = idx & 63;
-                const int nt = f / fp.NG, g = f - nt * fp.NG;
+                const int nt = fdiv(f, fp.d_NG), g = f - nt * fp.NG;
                 const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
-                const int t = u / fp.ncq, cq = u - t * fp.ncq;
+                const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
                 const bool ok = idx < nfrag && u < fp.nq;
-                const int ka = ok ? t / K : 0, kb = ok ? t - (t / K) * K : 0;
+                const int ka = ok ? fdiv(t, fp.d_K) : 0, kb = ok ? t - ka * K : 0;
                 const int co_c = co < C ? co : 0;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -1224,10 +1250,10 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
             for (int h = 0; h < 2; ++h) {
                 const int idx = base + h * blockDim.x;
                 const int f = idx >> 6, ln = idx & 63;
-                const int nt = f / fp.NG, g = f - nt * fp.NG;
+                const int nt = fdiv(f, fp.d_NG), g = f - nt * fp.NG;
                 const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
-                const int t = u / fp.ncq, cq = u - t * fp.ncq;
-                const int ka = t / K, kb = t - ka * K;
+                const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
+                const int ka = fdiv(t, fp.d_K), kb = t - ka * K;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int ci = 4 * cq + e;
@@ -1243,8 +1269,8 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         // gather offset of quad u relative to the output pixel's address (taps
         // reach up/left too: offsets are signed); padding quads get kNoQuad
         for (int u = threadIdx.x; u < fp.NG * 4; u += blockDim.x) {
-            const int t = u / fp.ncq, cq = u - t * fp.ncq;
-            const int ka = t / K, kb = t - ka * K;
+            const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
+            const int ka = fdiv(t, fp.d_K), kb = t - ka * K;
             Dq[u] = u < fp.nq ? ((ka - oh) * WP + (kb - ow)) * CP + 4 * cq : kNoQuad;
         }
         __syncthreads();
@@ -1267,11 +1293,11 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         const bool last = q == fp.n - 1;
         float *Yo = sm + fp.offO;
         for (int item = wave; item < nitem; item += nwaves) {
-            const int tile = item / fp.NT, nt = item - tile * fp.NT;
+            const int tile = fdiv(item, fp.d_NT), nt = item - tile * fp.NT;
             const int p = tile * 16 + li;
             const bool valid = p < npix;
             const int pc = valid ? p : 0;
-            const int il = pc / W, j = pc - il * W;
+            const int il = fdiv(pc, fp.d_W), j = pc - il * W;
             const int base = ((il + P) * WP + j + P) * CP;
             const int zaddr = fp.offW;   // any valid address: its products meet zero weights
             // four accumulators over the quad groups (group g -> g mod 4), joined
@@ -1312,8 +1338,8 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         if (!last) {   // this layer's output is the next one's input
             __syncthreads();
             for (int idx = threadIdx.x; idx < npix * CP / 4; idx += blockDim.x) {
-                const int p = idx / (CP / 4), c4 = idx - p * (CP / 4);
-                const int il = p / W, j = p - il * W;
+                const int p = fdiv(idx, fp.d_cp4), c4 = idx - p * (CP / 4);
+                const int il = fdiv(p, fp.d_W), j = p - il * W;
                 reinterpret_cast<float4 *>(X)[((il + P) * WP + j + P) * (CP / 4) + c4] =
                     reinterpret_cast<const float4 *>(Yo)[idx];
             }
@@ -1401,6 +1427,16 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B) {
     p.offW = p.offO + (n > 1 ? H * W * p.CP : 0);
     p.offD = p.offW + p.NT * p.NG * 256;
     p.lds_floats = p.offD + round_up4(4 * p.NG);
+    const int rb_last = H - (p.nblk - 1) * p.RB;
+    p.d_plane = make_fastdiv((p.RB + 2 * p.P) * p.WP);
+    p.d_plane_last = make_fastdiv((rb_last + 2 * p.P) * p.WP);
+    p.d_WP = make_fastdiv(p.WP);
+    p.d_NG = make_fastdiv(p.NG);
+    p.d_ncq = make_fastdiv(p.ncq);
+    p.d_K = make_fastdiv(K);
+    p.d_NT = make_fastdiv(p.NT);
+    p.d_W = make_fastdiv(W);
+    p.d_cp4 = make_fastdiv(p.ncq);
     return p;
 }
 

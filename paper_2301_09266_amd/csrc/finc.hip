@@ -391,6 +391,9 @@ struct Plan {
     int lds_floats;
     int lstride;                // floats of one prepared layer
     int wave[kMaxWaves];        // per wave: role | mt << 2 | nt << 6 | h << 10 | groups << 14
+    // divisions of the index arithmetic: CP / 4, W, H W / 4, H W, CP - C,
+    // C, CP, W / 4, ncq (divisors below 1 are replaced by 1)
+    FastDiv d_cp4, d_W, d_hw4, d_HW, d_pad, d_C, d_CP, d_w4, d_ncq;
 };
 
 // Quad groups of the busiest wave of a plan.
@@ -442,6 +445,15 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p) {
     p.offT = p.offZ + 256;
     p.lds_floats = p.offT + 256;
     p.lstride = (int)prep_layer_floats(C, K);
+    p.d_cp4 = make_fastdiv(p.CP / 4);
+    p.d_W = make_fastdiv(W);
+    p.d_hw4 = make_fastdiv(imax(H * W / 4, 1));
+    p.d_HW = make_fastdiv(H * W);
+    p.d_pad = make_fastdiv(imax(p.CP - C, 1));
+    p.d_C = make_fastdiv(C);
+    p.d_CP = make_fastdiv(p.CP);
+    p.d_w4 = make_fastdiv(imax(W / 4, 1));
+    p.d_ncq = make_fastdiv(p.ncq);
     // wave roles: critical waves of the tiles first, then S helpers per tile,
     // then idle waves; with the number of quad groups each one owns
     for (int w = 0; w < kMaxWaves; ++w) {
@@ -480,6 +492,7 @@ struct InvArgs {
     float *out;           // output of the last level: (B, C, H, W)
     Level lv[kMaxLevels]; // in the order they run
 };
+static_assert(sizeof(InvArgs) <= 4096, "kernel arguments are limited to 4 KB");
 
 // What one wave does at a level.  role 0: critical wave of `tile`; 1: helper
 // h of `tile`; 2: idle (barriers only).
@@ -576,8 +589,8 @@ __device__ inline void copy_solution(float *sm, const Plan &pl) {
     float4 *Y = reinterpret_cast<float4 *>(sm + pl.offY);
     const float4 *X = reinterpret_cast<const float4 *>(sm + pl.offX);
     for (int idx = threadIdx.x; idx < n4; idx += blockDim.x) {
-        const int p = idx / cp4, c4 = idx - p * cp4;
-        const int i = p / pl.W, j = p - i * pl.W;
+        const int p = fdiv(idx, pl.d_cp4), c4 = idx - p * cp4;
+        const int i = fdiv(p, pl.d_W), j = p - i * pl.W;
         Y[idx] = X[((i + pl.P) * pl.WP + j + pl.P) * cp4 + c4];
     }
 }
@@ -611,7 +624,7 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
             for (int k = 0; k < U; ++k) {
                 const int idx = base + k * blockDim.x;
                 if (idx < n4) {
-                    const int c = idx / hw4, p = 4 * (idx - c * hw4);
+                    const int c = fdiv(idx, pl.d_hw4), p = 4 * (idx - c * hw4);
                     Y[(p + 0) * CP + c] = v[k].x;
                     Y[(p + 1) * CP + c] = v[k].y;
                     Y[(p + 2) * CP + c] = v[k].z;
@@ -635,7 +648,7 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
             for (int k = 0; k < U; ++k) {
                 const int idx = base + k * blockDim.x;
                 if (idx < C * HW) {
-                    const int c = idx / HW, p = idx - c * HW;
+                    const int c = fdiv(idx, pl.d_HW), p = idx - c * HW;
                     Y[p * CP + c] = v[k];
                 }
             }
@@ -645,7 +658,7 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
         during();
     const int pad = CP - C;
     for (int idx = threadIdx.x; idx < pad * HW; idx += blockDim.x) {
-        const int p = idx / pad;
+        const int p = fdiv(idx, pl.d_pad);
         Y[p * CP + C + (idx - p * pad)] = 0.0f;
     }
 }
@@ -678,8 +691,8 @@ __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm
         const int Ch = C / 2;
         const float *lat = lv.z + b * (size_t)Ch * HW;
         for (int idx = threadIdx.x; idx < CP * HW; idx += blockDim.x) {
-            const int c = idx / HW, p = idx - c * HW;
-            const int i = p / W, j = p - i * W;
+            const int c = fdiv(idx, pl.d_HW), p = idx - c * HW;
+            const int i = fdiv(p, pl.d_W), j = p - i * W;
             float v = 0.0f;
             if (c < Ch) {
                 const int ci = 4 * c + 2 * (i & 1) + (j & 1);
@@ -751,7 +764,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
             if (uq < 0) {
                 geo[g] = -1;
             } else {
-                const int t = uq / pl.ncq, cq = uq - t * pl.ncq;
+                const int t = fdiv(uq, pl.d_ncq), cq = uq - t * pl.ncq;
                 int dp, dq;
                 tap_of(t, pl.K, dp, dq);
                 geo[g] = dp | dq << 4 | cq << 8;
@@ -769,7 +782,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
             const float *s = lv.scale + (size_t)u * C;
             const float *bi = lv.bias + (size_t)u * C;
             for (int idx = threadIdx.x; idx < HW * C; idx += blockDim.x) {
-                const int p = idx / C, c = idx - p * C;
+                const int p = fdiv(idx, pl.d_C), c = idx - p * C;
                 Y[p * CP + c] = (Y[p * CP + c] - bi[c]) / s[c];
             }
             __syncthreads();
@@ -1071,8 +1084,8 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
         level_waves<NG, MAXT, MODE>(a, lv, i == 0, above, pl, role_of(a, i), sm, b);
         if (a.n_units * a.lpu == 0) {   // no layers at this level: the input passes through
             for (int idx = threadIdx.x; idx < HW * CP; idx += blockDim.x) {
-                const int p = idx / CP, c = idx - p * CP;
-                const int i = p / W, j = p - i * W;
+                const int p = fdiv(idx, pl.d_CP), c = idx - p * CP;
+                const int i = fdiv(p, pl.d_W), j = p - i * W;
                 sm[pl.offX + ((i + pl.P) * pl.WP + j + pl.P) * CP + c] = Y[idx];
             }
             __syncthreads();
@@ -1091,8 +1104,8 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
             for (int k = 0; k < U; ++k) {
                 const int idx = base + k * blockDim.x;
                 if (idx < n4) {
-                    const int c = idx / hw4, q = idx - c * hw4;
-                    const int i = q / w4, j = 4 * (q - i * w4);
+                    const int c = fdiv(idx, p0.d_hw4), q = idx - c * hw4;
+                    const int i = fdiv(q, p0.d_w4), j = 4 * (q - i * w4);
                     const float *x = sm + p0.offX + ((i + p0.P) * p0.WP + j + p0.P) * p0.CP + c;
                     v[k] = make_float4(x[0], x[p0.CP], x[2 * p0.CP], x[3 * p0.CP]);
                 }
@@ -1106,8 +1119,8 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
         }
     } else {
         for (int idx = threadIdx.x; idx < n0; idx += blockDim.x) {
-            const int c = idx / HW0, p = idx - c * HW0;
-            const int i = p / p0.W, j = p - i * p0.W;
+            const int c = fdiv(idx, p0.d_HW), p = idx - c * HW0;
+            const int i = fdiv(p, p0.d_W), j = p - i * p0.W;
             dst[idx] = sm[p0.offX + ((i + p0.P) * p0.WP + j + p0.P) * p0.CP + c];
         }
     }

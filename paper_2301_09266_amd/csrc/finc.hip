@@ -1154,7 +1154,7 @@ struct FwdArgs {
     float *out;
     const float *K;   // n OIHW tensors
     double *logdet;   // optional: H W sum over layers and channels of log|K[c,c,self]|
-    float *prepared;  // optional: the n layers' prepared weights, by blocks nfwd ..
+    float *prepared;  // optional: the n layers' prepared weights, by the first n ppl blocks
     int nfwd, ppl;    // forward blocks; preparation blocks per layer
     FwdPlan fp;
 };
@@ -1165,10 +1165,12 @@ constexpr int kNoQuad = 1 << 30;   // quad offset marker: padding quad (zero wei
 __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     extern __shared__ float sm[];
     const FwdPlan &fp = a.fp;
-    if (a.prepared && (int)blockIdx.x >= a.nfwd) {
-        // the weights for the inverse, prepared by the launch's last blocks
-        // (the forward blocks do not wait for them)
-        const int pb = blockIdx.x - a.nfwd, layer = pb / a.ppl, part = pb - layer * a.ppl;
+    const int npre = a.prepared ? fp.n * a.ppl : 0;
+    if ((int)blockIdx.x < npre) {
+        // the weights for the inverse, prepared by the launch's first blocks
+        // (dispatched first: their latency chain is the longest; the forward
+        // blocks do not wait for them)
+        const int pb = blockIdx.x, layer = pb / a.ppl, part = pb - layer * a.ppl;
         prep_columns<kFwdThreads>(a.K + (size_t)layer * fp.C * fp.C * fp.K * fp.K,
                                   a.prepared + (size_t)layer * prep_layer_floats(fp.C, fp.K),
                                   fp.C, fp.K, fp.n == 1 ? fp.corner0 : layer, part * kFwdThreads,
@@ -1179,7 +1181,8 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int nwaves = blockDim.x >> 6;
-    const int b = blockIdx.x / fp.nblk, blk = blockIdx.x - b * fp.nblk;
+    const int bid = blockIdx.x - npre;
+    const int b = bid / fp.nblk, blk = bid - b * fp.nblk;
     const int i0 = blk * fp.RB, rb = imin(H, i0 + fp.RB) - i0;
     const int npix = rb * W, ntile = ceil_div(npix, 16), nitem = ntile * fp.NT;
     float *X = sm + fp.offI;
@@ -1289,7 +1292,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         __syncthreads();
         // log|det| rides along: block 0's first wave sums log|K[c,c,self]| over
         // the layers from the staged weights (self tap is quad t = oh K + ow)
-        if (a.logdet && blockIdx.x == 0 && wave == 0) {
+        if (a.logdet && bid == 0 && wave == 0) {
             double v = 0.0;
             for (int c = lane; c < C; c += 64) {
                 const int u = (oh * K + ow) * fp.ncq + (c >> 2);
@@ -1359,7 +1362,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
             __syncthreads();
         }
     }
-    if (a.logdet && blockIdx.x == 0 && threadIdx.x == 0)
+    if (a.logdet && bid == 0 && threadIdx.x == 0)
         a.logdet[0] = (double)H * (double)W * ld_acc;
 }
 

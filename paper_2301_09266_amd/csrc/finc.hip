@@ -374,8 +374,10 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxWaves = 16;
 constexpr int kMaxGroups = 8;                       // quad groups (x4 quads) per wave
-// critical-wave forms an inverse instance is built with
-constexpr int kCritGather = 0, kCritRegs = 1, kCritBoth = 2;
+// critical-wave forms an inverse instance is built with (low two bits of
+// its MODE), and kOneLayer: a single level of a single layer without actnorm
+// (the chain's loops and hand-overs compiled out)
+constexpr int kCritGather = 0, kCritRegs = 1, kCritBoth = 2, kOneLayer = 4;
 
 // Work split and LDS layout of one level (same for every layer of it).
 struct Plan {
@@ -721,8 +723,10 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
     // the register-fed critical wave owns the two dp + dq = 1 taps as groups
     // (MODE: kCritGather / kCritRegs / kCritBoth -- the instance carries only
     // the critical loop(s) its levels use)
-    const bool regc = MODE == kCritRegs    ? r.role == 0
-                      : MODE == kCritGather ? false
+    constexpr int CRIT = MODE & 3;
+    constexpr bool kOne = (MODE & kOneLayer) != 0;
+    const bool regc = CRIT == kCritRegs    ? r.role == 0
+                      : CRIT == kCritGather ? false
                                             : pl.regcrit && r.role == 0;
     const int ngw = r.ng;
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
@@ -733,14 +737,16 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
     const int r0 = mt * 16, r1 = imin(mt * 16 + 15, H - 1);
     float *R = sm + pl.offR;
     const size_t lstride = pl.lstride;
-    const int nlayers = a.n_units * a.lpu;
+    const int nlayers = kOne ? 1 : a.n_units * a.lpu;
     float w[G][4], wn[GN][4];
     // layer index n = 0 .. nlayers-1 runs unit u = U-1-n/lpu, block q = lpu-1-n%lpu
     auto prep_of = [&](int n) {
+        if (kOne)
+            return lv.prep;
         const int u = a.n_units - 1 - n / a.lpu, q = a.lpu - 1 - n % a.lpu;
         return lv.prep + (size_t)(u * a.lpu + q) * lstride;
     };
-    auto corner_at = [&](int n) { return corner_of(a, a.lpu - 1 - n % a.lpu); };
+    auto corner_at = [&](int n) { return kOne ? a.corner0 : corner_of(a, a.lpu - 1 - n % a.lpu); };
     auto fetch = [&](auto &dst, int n) {
         if (regc)
             load_crit_weights(dst, pl, prep_of(n));
@@ -772,12 +778,12 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
         }
     });
     for (int n = 0; n < nlayers; ++n) {
-        const int u = a.n_units - 1 - n / a.lpu, q = a.lpu - 1 - n % a.lpu;
-        if (n > 0) {   // previous layer's solution is this layer's input
+        const int u = kOne ? 0 : a.n_units - 1 - n / a.lpu, q = kOne ? 0 : a.lpu - 1 - n % a.lpu;
+        if (!kOne && n > 0) {   // previous layer's solution is this layer's input
             copy_solution(sm, pl);
             __syncthreads();
         }
-        if (q == a.lpu - 1 && lv.scale) {
+        if (!kOne && q == a.lpu - 1 && lv.scale) {
             float *Y = sm + pl.offY;
             const float *s = lv.scale + (size_t)u * C;
             const float *bi = lv.bias + (size_t)u * C;
@@ -929,7 +935,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                 run(std::true_type{});
             else
                 run(std::false_type{});
-        } else if (MODE != kCritGather && r.role == 0 && regc) {
+        } else if (CRIT != kCritGather && r.role == 0 && regc) {
             // register-fed critical wave.  dprev: lane (kq, li) holds channels
             // 4 kq .. +3 of row li's pixel of the previous diagonal (0 for rows
             // not started).  Its MFMA chain needs nothing from LDS but, in a
@@ -1017,7 +1023,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
             }
             for (; e < E; ++e)
                 __syncthreads();
-        } else if (MODE != kCritRegs && r.role == 0) {
+        } else if (CRIT != kCritRegs && r.role == 0) {
             // critical wave that gathers its dp + dq = 1 taps from LDS (several
             // channel tiles: the previous diagonal's channels sit in several
             // waves)
@@ -1073,7 +1079,8 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
         asm volatile("" ::"s"(L), "s"(nu), "s"(lpu), "s"(c0), "s"(lv.z), "s"(lv.prep),
                      "s"(lv.scale));
     }
-    for (int i = 0; i < a.L; ++i) {
+    constexpr bool kOne = (MODE & kOneLayer) != 0;
+    for (int i = 0; i < (kOne ? 1 : a.L); ++i) {
         if (i > 0) {
             above = lv.pl;
             lv = a.lv[i];
@@ -1082,7 +1089,7 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
         const int CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
         float *Y = sm + pl.offY;
         level_waves<NG, MAXT, MODE>(a, lv, i == 0, above, pl, role_of(a, i), sm, b);
-        if (a.n_units * a.lpu == 0) {   // no layers at this level: the input passes through
+        if (!kOne && a.n_units * a.lpu == 0) {   // no layers at this level: the input passes through
             for (int idx = threadIdx.x; idx < HW * CP; idx += blockDim.x) {
                 const int p = fdiv(idx, pl.d_CP), c = idx - p * CP;
                 const int i = fdiv(p, pl.d_W), j = p - i * W;
@@ -1526,9 +1533,13 @@ InvKernel inverse_instance_mode(int ng) {
 }
 template <int MAXT>
 InvKernel inverse_instance(int ng, int mode) {
-    return mode == kCritGather ? inverse_instance_mode<MAXT, kCritGather>(ng)
-           : mode == kCritRegs ? inverse_instance_mode<MAXT, kCritRegs>(ng)
-                               : inverse_instance_mode<MAXT, kCritBoth>(ng);
+    switch (mode) {
+    case kCritGather: return inverse_instance_mode<MAXT, kCritGather>(ng);
+    case kCritRegs: return inverse_instance_mode<MAXT, kCritRegs>(ng);
+    case kCritGather | kOneLayer: return inverse_instance_mode<MAXT, kCritGather | kOneLayer>(ng);
+    case kCritRegs | kOneLayer: return inverse_instance_mode<MAXT, kCritRegs | kOneLayer>(ng);
+    default: return inverse_instance_mode<MAXT, kCritBoth>(ng);
+    }
 }
 
 int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
@@ -1548,7 +1559,9 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
         ng = imax(ng, plan_groups(p));
         nreg += p.regcrit;
     }
-    const int mode = nreg == a.L ? kCritRegs : nreg == 0 ? kCritGather : kCritBoth;
+    int mode = nreg == a.L ? kCritRegs : nreg == 0 ? kCritGather : kCritBoth;
+    if (a.L == 1 && a.n_units * a.lpu == 1 && !a.lv[0].scale)
+        mode |= kOneLayer;   // (a single level has one critical form)
     const InvKernel k = threads <= 256   ? inverse_instance<256>(ng, mode)
                         : threads <= 512 ? inverse_instance<512>(ng, mode)
                                          : inverse_instance<1024>(ng, mode);

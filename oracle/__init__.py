@@ -49,6 +49,9 @@ def load(path: str = LIB):
         "orc_unit_forward": [_dp, _dp, _dp, L, I, I, I, I],
         "orc_unit_inverse": [_dp, _dp, _dp, L, I, I, I, I],
         "orc_unit_logdet": [_dp, I, I, I, I, _dp],
+        "orc_split_forward": [_dp, _dp, _dp, L, I, I, I, I],
+        "orc_split_inverse": [_dp, _dp, _dp, L, I, I, I, I],
+        "orc_split_logdet": [_dp, I, I, I, I, _dp],
         "orc_actnorm_forward": [_dp, _dp, _dp, _dp, L, I, I, I],
         "orc_actnorm_inverse": [_dp, _dp, _dp, _dp, L, I, I, I],
         "orc_squeeze": [_dp, _dp, L, I, I, I],
@@ -129,6 +132,28 @@ class Oracle:
         K4 = _c(K4)
         out = np.zeros(1)
         _check(self.lib.orc_unit_logdet(_p(K4), K4.shape[1], K4.shape[-1], H, W, _p(out)))
+        return float(out[0])
+
+    # channel-split unit: Kq4 = (4, C/4, C/4, k, k); quarter g has corner g
+    def split_forward(self, x, Kq4) -> np.ndarray:
+        x, Kq4 = _c(x), _c(Kq4)
+        B, C, H, W = x.shape
+        y = np.empty_like(x)
+        _check(self.lib.orc_split_forward(_p(x), _p(y), _p(Kq4), B, C, H, W, Kq4.shape[-1]))
+        return y
+
+    def split_inverse(self, y, Kq4) -> np.ndarray:
+        y, Kq4 = _c(y), _c(Kq4)
+        B, C, H, W = y.shape
+        x = np.empty_like(y)
+        _check(self.lib.orc_split_inverse(_p(y), _p(x), _p(Kq4), B, C, H, W, Kq4.shape[-1]))
+        return x
+
+    def split_logdet(self, Kq4, H: int, W: int) -> float:
+        Kq4 = _c(Kq4)
+        out = np.zeros(1)
+        _check(self.lib.orc_split_logdet(_p(Kq4), 4 * Kq4.shape[1], Kq4.shape[-1], H, W,
+                                         _p(out)))
         return float(out[0])
 
     def actnorm_forward(self, x, s, b) -> np.ndarray:

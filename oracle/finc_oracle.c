@@ -234,6 +234,79 @@ int orc_unit_logdet(const double *K4, int C, int k, int H, int W, double *out)
     return rc;
 }
 
+/* ---- Channel-split FInC unit (Sec. 4.3, Fig. 2a, Alg. 2): the channels are
+ * cut into four equal quarters; quarter g is one padded convolution block of
+ * its own (C/4 channels, its own weights K_g, corner g: TL, TR, BL, BR), the
+ * four side by side on the same pixels; the outputs are concatenated.  Each
+ * quarter is inverted independently.  (Reading: the text names the fourth
+ * quarter's padding TR again; the fourth corner, BR, is taken.)
+ * Kq4 = 4 consecutive OIHW tensors of shape (C/4, C/4, k, k). ------------- */
+
+typedef int (*orc_layer_fn)(const double *, double *, const double *, long, int, int,
+                            int, int, int);
+
+static int split_apply(const double *in, double *out, const double *Kq4, long B, int C,
+                       int H, int W, int k, orc_layer_fn fn)
+{
+    if (bad_shape(B, C, H, W, k, 0) || C % 4 != 0 || !in || !out || !Kq4)
+        return ORC_EINVAL;
+    const int Cq = C / 4;
+    const long part = (long)Cq * H * W;
+    const long ksz = (long)Cq * Cq * k * k;
+    double *a = (double *)malloc(sizeof(double) * (part > 0 ? part : 1));
+    double *r = (double *)malloc(sizeof(double) * (part > 0 ? part : 1));
+    if (!a || !r) {
+        free(a);
+        free(r);
+        return ORC_ENOMEM;
+    }
+    int rc = ORC_OK;
+    for (long b = 0; b < B && rc == ORC_OK; ++b) {
+        for (int g = 0; g < 4 && rc == ORC_OK; ++g) {
+            const long off = (b * C + (long)g * Cq) * H * W;
+            memcpy(a, in + off, sizeof(double) * part);
+            rc = fn(a, r, Kq4 + g * ksz, 1, Cq, H, W, k, g);
+            memcpy(out + off, r, sizeof(double) * part);
+        }
+    }
+    free(a);
+    free(r);
+    return rc;
+}
+
+int orc_split_forward(const double *x, double *y, const double *Kq4, long B, int C,
+                      int H, int W, int k)
+{
+    return split_apply(x, y, Kq4, B, C, H, W, k, orc_forward);
+}
+
+int orc_split_inverse(const double *y, double *x, const double *Kq4, long B, int C,
+                      int H, int W, int k)
+{
+    return split_apply(y, x, Kq4, B, C, H, W, k, orc_inverse);
+}
+
+int orc_split_logdet(const double *Kq4, int C, int k, int H, int W, double *out)
+{
+    if (!out || !Kq4 || C < 4 || C % 4 != 0)
+        return ORC_EINVAL;
+    const int Cq = C / 4;
+    const long ksz = (long)Cq * Cq * k * k;
+    double s = 0.0;
+    int rc = ORC_OK;
+    for (int g = 0; g < 4; ++g) {
+        double v;
+        int r = orc_logdet(Kq4 + g * ksz, Cq, k, g, H, W, &v);
+        if (r == ORC_EINVAL)
+            return r;
+        if (r != ORC_OK)
+            rc = r;
+        s += v;
+    }
+    *out = s;
+    return rc;
+}
+
 /* ---- Multi-scale glue (Sec. 4.4). ----------------------------------------
  * Actnorm: per-channel affine y = s * x + b (Glow's convention).
  * Squeeze: (C, H, W) -> (4C, H/2, W/2), out[4c + 2dy + dx][i][j] =

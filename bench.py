@@ -215,6 +215,15 @@ def per_config(dev) -> list:
             fwd = graph_time_us(lambda: finc.unit_forward(x, K4, out=out), 5, 10)
             inv = graph_time_us(lambda: finc.unit_inverse_prepared(y, prep, k, out=out), 5, 10)
             act, wts, layers = 2 * C * H * W * 4, 4 * C * C * k * k * 4, 4
+        elif kind == "split":
+            B, C, H, W, k = (c[n] for n in "BCHWk")
+            x, Kq4 = d(c["x"]), d(c["Kq4"])
+            y = finc.split_forward(x, Kq4)
+            prep = finc.prepare(Kq4, [0, 1, 2, 3])
+            out = torch.empty_like(x)
+            fwd = graph_time_us(lambda: finc.split_forward(x, Kq4, out=out), 5, 20)
+            inv = graph_time_us(lambda: finc.split_inverse_prepared(y, prep, k, out=out), 5, 20)
+            act, wts, layers = 2 * C * H * W * 4, 4 * (C // 4) ** 2 * k * k * 4, 1
         else:
             B, C1, H1, W1, k, L, U = (c[n] for n in ("B", "C1", "H1", "W1", "k", "levels", "units"))
             Kf = d(np.concatenate([a.ravel() for a in c["K"]]))

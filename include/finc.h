@@ -136,6 +136,35 @@ int finc_unit_inverse_prepared(const float *y, float *x, const void *prepared4,
                                int B, int C, int H, int W, int k,
                                hipStream_t stream);
 
+/* ---- Channel-split FInC unit: four PCBs side by side --------------------
+ * (Sec. 4.3, Fig. 2a, Algorithm 2: the channels are cut into four equal
+ * quarters; quarter g is a PCB of its own with C/4 channels, its own masked
+ * weights and corner g in the order TL, TR, BL, BR; the four act on the same
+ * pixels in parallel and their outputs are concatenated.  The text names the
+ * fourth quarter's padding TR a second time; BR is taken.)  Each quarter is
+ * inverted independently, all four in one launch (a workgroup per image and
+ * quarter, as Algorithm 2's grid of batch x 4).
+ *   C: the unit's channels, a multiple of 4, C/4 <= FINC_MAX_C.
+ *   Kq4: device, 4 consecutive OIHW tensors (C/4, C/4, k, k), quarter order.
+ *   logdet (finc_split_forward): NULL, or device double for the unit's
+ *     log|det| (the sum over the quarters); finc_split_logdet writes it alone.
+ *   prepared4 / workspace: device buffer of finc_workspace_bytes(C/4, k, 4)
+ *     bytes, 256-byte aligned: the quarters' prepared weights in quarter
+ *     order (what finc_prepare(Kq4, 4, {TL, TR, BL, BR}, C/4, k, .) writes).
+ * Aliasing and errors as for finc_forward / finc_inverse: the forward needs
+ * x and y disjoint; the inverse allows x == y; FINC_EINVAL for C not a
+ * multiple of 4 or any other bad argument. */
+int finc_split_forward(const float *x, float *y, const float *Kq4, double *logdet,
+                       void *prepared4, int B, int C, int H, int W, int k,
+                       hipStream_t stream);
+int finc_split_logdet(const float *Kq4, int C, int k, int H, int W, double *out,
+                      hipStream_t stream);
+int finc_split_inverse(const float *y, float *x, const float *Kq4, int B, int C,
+                       int H, int W, int k, void *workspace, hipStream_t stream);
+int finc_split_inverse_prepared(const float *y, float *x, const void *prepared4,
+                                int B, int C, int H, int W, int k,
+                                hipStream_t stream);
+
 /* ---- Multi-scale sampling stack (Sec. 4.4, Fig. 2c) ---------------------
  * L levels of U units; level l has C_l = C1 << l channels and spatial size
  * (H1 >> l, W1 >> l).  Forward direction (for the definition): per level

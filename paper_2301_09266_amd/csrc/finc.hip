@@ -491,6 +491,10 @@ struct Level {
 
 struct InvArgs {
     int L, n_units, lpu, corner0;
+    // split: the channel-split unit, its batch seen as (4B, C/4, H, W): the
+    // workgroup of image b' = 4 b + g inverts quarter g with corner g and the
+    // g-th prepared layer (one level of one layer)
+    int split;
     float *out;           // output of the last level: (B, C, H, W)
     Level lv[kMaxLevels]; // in the order they run
 };
@@ -740,13 +744,18 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
     const int nlayers = kOne ? 1 : a.n_units * a.lpu;
     float w[G][4], wn[GN][4];
     // layer index n = 0 .. nlayers-1 runs unit u = U-1-n/lpu, block q = lpu-1-n%lpu
+    const int quarter = blockIdx.x & 3;   // (split unit only)
     auto prep_of = [&](int n) {
+        if (a.split)
+            return lv.prep + (size_t)quarter * lstride;
         if (kOne)
             return lv.prep;
         const int u = a.n_units - 1 - n / a.lpu, q = a.lpu - 1 - n % a.lpu;
         return lv.prep + (size_t)(u * a.lpu + q) * lstride;
     };
-    auto corner_at = [&](int n) { return kOne ? a.corner0 : corner_of(a, a.lpu - 1 - n % a.lpu); };
+    auto corner_at = [&](int n) {
+        return a.split ? quarter : kOne ? a.corner0 : corner_of(a, a.lpu - 1 - n % a.lpu);
+    };
     auto fetch = [&](auto &dst, int n) {
         if (regc)
             load_crit_weights(dst, pl, prep_of(n));
@@ -1075,8 +1084,8 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
     Level lv = a.lv[0];
     Plan above = lv.pl;   // plan of the level run before (unused at the first)
     {   // one round of scalar loads for everything the first level starts with
-        const int L = a.L, nu = a.n_units, lpu = a.lpu, c0 = a.corner0;
-        asm volatile("" ::"s"(L), "s"(nu), "s"(lpu), "s"(c0), "s"(lv.z), "s"(lv.prep),
+        const int L = a.L, nu = a.n_units, lpu = a.lpu, c0 = a.corner0, sp = a.split;
+        asm volatile("" ::"s"(L), "s"(nu), "s"(lpu), "s"(c0), "s"(sp), "s"(lv.z), "s"(lv.prep),
                      "s"(lv.scale));
     }
     constexpr bool kOne = (MODE & kOneLayer) != 0;
@@ -1161,8 +1170,12 @@ struct FwdArgs {
     float *out;
     const float *K;   // n OIHW tensors
     double *logdet;   // optional: H W sum over layers and channels of log|K[c,c,self]|
-    float *prepared;  // optional: the n layers' prepared weights, by the first n ppl blocks
+    float *prepared;  // optional: the layers' prepared weights, by the first blocks (ppl each)
     int nfwd, ppl;    // forward blocks; preparation blocks per layer
+    // split: the channel-split unit, its batch seen as (4B, C/4, H, W): image
+    // b' = 4 b + g is quarter g, with corner g and weights K + g C^2 k^2 (one
+    // layer per block; four layers prepared)
+    int split;
     FwdPlan fp;
 };
 
@@ -1172,7 +1185,8 @@ constexpr int kNoQuad = 1 << 30;   // quad offset marker: padding quad (zero wei
 __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     extern __shared__ float sm[];
     const FwdPlan &fp = a.fp;
-    const int npre = a.prepared ? fp.n * a.ppl : 0;
+    const int nprep = a.split ? 4 : fp.n;   // layers prepared
+    const int npre = a.prepared ? nprep * a.ppl : 0;
     if ((int)blockIdx.x < npre) {
         // the weights for the inverse, prepared by the launch's first blocks
         // (dispatched first: their latency chain is the longest; the forward
@@ -1180,7 +1194,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         const int pb = blockIdx.x, layer = pb / a.ppl, part = pb - layer * a.ppl;
         prep_columns<kFwdThreads>(a.K + (size_t)layer * fp.C * fp.C * fp.K * fp.K,
                                   a.prepared + (size_t)layer * prep_layer_floats(fp.C, fp.K),
-                                  fp.C, fp.K, fp.n == 1 ? fp.corner0 : layer, part * kFwdThreads,
+                                  fp.C, fp.K, nprep == 1 ? fp.corner0 : layer, part * kFwdThreads,
                                   part == 0, reinterpret_cast<double *>(sm));
         return;
     }
@@ -1190,6 +1204,8 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     const int nwaves = blockDim.x >> 6;
     const int bid = blockIdx.x - npre;
     const int b = bid / fp.nblk, blk = bid - b * fp.nblk;
+    const int corner0 = a.split ? (b & 3) : fp.corner0;   // this block's (first) corner
+    const float *Kb = a.K + (a.split ? (size_t)(b & 3) * fp.C * fp.C * fp.K * fp.K : 0);
     const int i0 = blk * fp.RB, rb = imin(H, i0 + fp.RB) - i0;
     const int npix = rb * W, ntile = ceil_div(npix, 16), nitem = ntile * fp.NT;
     float *X = sm + fp.offI;
@@ -1205,7 +1221,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     // unconditional from clamped indices, eight in flight per thread.
     {
         int oh0, ow0;
-        self_tap(fp.corner0, K, oh0, ow0);
+        self_tap(corner0, K, oh0, ow0);
         const int up = fp.n == 1 ? oh0 : P, down = fp.n == 1 ? P - oh0 : P;
         const int lo = imax(0, i0 - up), hi = imin(H, i0 + rb + down);   // rows read
         const int nrow = rb + 2 * P, plane = nrow * WP, total = CP * plane;
@@ -1236,10 +1252,10 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     }
     double ld_acc = 0.0;
     for (int q = 0; q < fp.n; ++q) {
-        const int corner = fp.n == 1 ? fp.corner0 : q;
+        const int corner = fp.n == 1 ? corner0 : q;
         int oh, ow;
         self_tap(corner, K, oh, ow);
-        const float *Kq = a.K + (size_t)q * C * C * K * K;
+        const float *Kq = Kb + (size_t)q * C * C * K * K;
         // weight fragments: Wf[(nt NG + g) 64 + lane].e = K[co][ci][tap] for
         // co = 16 nt + li, quad u = 4 g + kq (tap u / ncq, ci = 4 (u % ncq) + e),
         // the channel mask applied (self tap: ci <= co only)
@@ -1299,7 +1315,21 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         __syncthreads();
         // log|det| rides along: block 0's first wave sums log|K[c,c,self]| over
         // the layers from the staged weights (self tap is quad t = oh K + ow)
-        if (a.logdet && bid == 0 && wave == 0) {
+        if (a.logdet && bid == 0 && wave == 0 && a.split) {
+            // the four quarters' diagonals straight from K, in a fixed order
+            double v = 0.0;
+            for (int m = lane; m < 4 * C; m += 64) {
+                const int g = m / C, c = m - g * C;
+                int gh, gw;
+                self_tap(g, K, gh, gw);
+                const float d = a.K[(((size_t)g * C + c) * C + c) * K * K + gh * K + gw];
+                v += log(fabs((double)d));
+            }
+            for (int off = 32; off > 0; off >>= 1)
+                v += __shfl_xor(v, off);
+            if (lane == 0)
+                ld_acc += v;
+        } else if (a.logdet && bid == 0 && wave == 0) {
             double v = 0.0;
             for (int c = lane; c < C; c += 64) {
                 const int u = (oh * K + ow) * fp.ncq + (c >> 2);
@@ -1577,17 +1607,22 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
 // separate preparation launch.
 constexpr int kFusedPrepMaxC = 16;
 
+// split: the channel-split unit on (B, 4 C, H, W) seen as (4B, C, H, W), C
+// here being the quarter's channels (n = 1).
 int launch_forward(const float *x, float *y, const float *K, double *logdet, float *prepared,
-                   int B, int C, int H, int W, int k, int n, int corner0, hipStream_t stream) {
+                   int B, int C, int H, int W, int k, int n, int corner0, int split,
+                   hipStream_t stream) {
     FwdArgs a;
     memset(&a, 0, sizeof(a));
     a.in = x;
     a.out = y;
     a.K = K;
     a.logdet = logdet;
+    a.split = split;
     a.fp = make_fwd_plan(C, H, W, k, n, corner0, B);
     if (B == 0)
         return FINC_OK;
+    const int nprep = split ? 4 : n;
     const bool fuse = prepared && C <= kFusedPrepMaxC;
     a.nfwd = B * a.fp.nblk;
     a.ppl = ceil_div(k * k * round_up4(C), kFwdThreads);
@@ -1603,15 +1638,15 @@ int launch_forward(const float *x, float *y, const float *K, double *logdet, flo
     if (hipFuncSetAttribute((const void *)forward_kernel,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
         (void)hipGetLastError();   // not needed on every runtime; the launch check decides
-    const unsigned blocks = (unsigned)(a.nfwd + (fuse ? n * a.ppl : 0));
+    const unsigned blocks = (unsigned)(a.nfwd + (fuse ? nprep * a.ppl : 0));
     hipLaunchKernelGGL(forward_kernel, dim3(blocks), dim3(kFwdThreads), lds, stream, a);
     rc = launched();
     if (rc != FINC_OK || !prepared || fuse)
         return rc;
     int corners[4] = {corner0, FINC_TR, FINC_BL, FINC_BR};
-    if (n > 1)
+    if (nprep > 1)
         corners[0] = FINC_TL;
-    return launch_prep(K, n, corners, C, k, prepared, stream);
+    return launch_prep(K, nprep, corners, C, k, prepared, stream);
 }
 
 Level level(const float *z, const void *prep, const float *scale, const float *bias, int C,
@@ -1737,7 +1772,8 @@ int finc_forward(const float *x, float *y, const float *K, double *logdet, void 
             rc = finc_prepare(K, 1, &corner, C, k, prepared, stream);
         return rc;
     }
-    return launch_forward(x, y, K, logdet, (float *)prepared, B, C, H, W, k, 1, corner, stream);
+    return launch_forward(x, y, K, logdet, (float *)prepared, B, C, H, W, k, 1, corner, 0,
+                          stream);
 }
 
 int finc_logdet(const float *K, int C, int k, int corner, int H, int W, double *out,
@@ -1809,7 +1845,7 @@ int finc_unit_forward(const float *x, float *y, const float *K4, double *logdet,
         }
         return rc;
     }
-    return launch_forward(x, y, K4, logdet, (float *)prepared4, B, C, H, W, k, 4, FINC_TL,
+    return launch_forward(x, y, K4, logdet, (float *)prepared4, B, C, H, W, k, 4, FINC_TL, 0,
                           stream);
 }
 
@@ -1820,6 +1856,86 @@ int finc_unit_logdet(const float *K4, int C, int k, int H, int W, double *out,
     hipLaunchKernelGGL(logdet_kernel, dim3(1), dim3(kWave), 0, stream, K4, 4, FINC_TL, C, k,
                        H, W, out);
     return launched();
+}
+
+// Channel-split unit: C a multiple of 4; seen as (4B, C/4, H, W).
+static bool valid_split(int B, int C, int H, int W, int k) {
+    return C >= 4 && C % 4 == 0 && B >= 0 && B <= (1 << 28) &&
+           valid_shape(4 * B, C / 4, H, W, k);
+}
+
+int finc_split_logdet(const float *Kq4, int C, int k, int H, int W, double *out,
+                      hipStream_t stream) {
+    if (!valid_split(1, C, H, W, k))
+        return FINC_EINVAL;
+    return finc_unit_logdet(Kq4, C / 4, k, H, W, out, stream);   // same four corners
+}
+
+int finc_split_forward(const float *x, float *y, const float *Kq4, double *logdet,
+                       void *prepared4, int B, int C, int H, int W, int k, hipStream_t stream) {
+    if (!valid_split(B, C, H, W, k) || !x || !y || !Kq4)
+        return FINC_EINVAL;
+    const int Cq = C / 4;
+    const size_t bytes = (size_t)B * C * H * W * sizeof(float);
+    if (overlap(x, bytes, y, bytes))
+        return FINC_EINVAL;
+    if (prepared4 &&
+        !prepared_out_ok(prepared4, finc_workspace_bytes(Cq, k, 4), x, y, bytes, Kq4,
+                         (size_t)4 * Cq * Cq * k * k * sizeof(float)))
+        return FINC_EINVAL;
+    if (B == 0) {
+        int rc = FINC_OK;
+        if (logdet)
+            rc = finc_split_logdet(Kq4, C, k, H, W, logdet, stream);
+        if (rc == FINC_OK && prepared4) {
+            const int corners[4] = {FINC_TL, FINC_TR, FINC_BL, FINC_BR};
+            rc = finc_prepare(Kq4, 4, corners, Cq, k, prepared4, stream);
+        }
+        return rc;
+    }
+    return launch_forward(x, y, Kq4, logdet, (float *)prepared4, 4 * B, Cq, H, W, k, 1, FINC_TL,
+                          1, stream);
+}
+
+int finc_split_inverse_prepared(const float *y, float *x, const void *prepared4, int B, int C,
+                                int H, int W, int k, hipStream_t stream) {
+    if (!valid_split(B, C, H, W, k) || !x || !y || !prepared4 || !aligned256(prepared4))
+        return FINC_EINVAL;
+    const int Cq = C / 4;
+    const size_t bytes = (size_t)B * C * H * W * sizeof(float);
+    if (!inverse_alias_ok(y, x, bytes) ||
+        overlap(x, bytes, prepared4, finc_workspace_bytes(Cq, k, 4)))
+        return FINC_EINVAL;
+    InvArgs a;
+    memset(&a, 0, sizeof(a));
+    a.lv[0] = level(y, prepared4, nullptr, nullptr, Cq, H, W, k);
+    a.out = x;
+    a.L = 1;
+    a.n_units = 1;
+    a.lpu = 1;
+    a.corner0 = FINC_TL;
+    a.split = 1;
+    return launch_inverse_chain(a, 4 * B, stream);
+}
+
+int finc_split_inverse(const float *y, float *x, const float *Kq4, int B, int C, int H, int W,
+                       int k, void *workspace, hipStream_t stream) {
+    if (!valid_split(B, C, H, W, k) || !x || !y || !Kq4 || !workspace || !aligned256(workspace))
+        return FINC_EINVAL;
+    const int Cq = C / 4;
+    const size_t bytes = (size_t)B * C * H * W * sizeof(float);
+    const size_t wsb = finc_workspace_bytes(Cq, k, 4);
+    if (!inverse_alias_ok(y, x, bytes) || overlap(workspace, wsb, x, bytes) ||
+        overlap(workspace, wsb, y, bytes) ||
+        overlap(workspace, wsb, Kq4, (size_t)4 * Cq * Cq * k * k * sizeof(float)))
+        return FINC_EINVAL;
+    if (B == 0)
+        return FINC_OK;
+    const int corners[4] = {FINC_TL, FINC_TR, FINC_BL, FINC_BR};
+    const int rc = finc_prepare(Kq4, 4, corners, Cq, k, workspace, stream);
+    if (rc != FINC_OK)
+        return rc;
+    return finc_split_inverse_prepared(y, x, workspace, B, C, H, W, k, stream);
 }
 
 int finc_unit_inverse_prepared(const float *y, float *x, const void *prepared4, int B,

@@ -35,6 +35,10 @@ SIGNATURES = {
     "finc_unit_logdet": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "finc_split_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "finc_split_logdet": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
+    "finc_split_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
+    "finc_split_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "finc_stack_workspace_bytes": (_sz, [_i, _i, _i, _i]),
     "finc_stack_inverse": (_i, [ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i,
                                 _i, _i, _vp, _vp]),
@@ -246,6 +250,60 @@ def unit_inverse_prepared(y: torch.Tensor, prepared4: torch.Tensor, k: int,
     x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
     _check(L.finc_unit_inverse_prepared(_ptr(y), _ptr(x), _ptr(prepared4), B, C, H, W, k,
                                         _stream()), "finc_unit_inverse_prepared")
+    return x
+
+
+# channel-split unit (four quarter-channel PCBs side by side; quarter g has
+# corner g): Kq4 of shape (4, C/4, C/4, k, k)
+
+def split_forward(x: torch.Tensor, Kq4: torch.Tensor, out: torch.Tensor | None = None,
+                  logdet: torch.Tensor | None = None, prepared: torch.Tensor | None = None):
+    """Optional side outputs as for forward, with `prepared` of
+    workspace_bytes(C/4, k, 4) for split_inverse_prepared."""
+    L = _require_lib()
+    _dev(x, "x")
+    B, C, H, W = x.shape
+    k = Kq4.shape[-1]
+    _dev(Kq4, "Kq4", (4, C // 4, C // 4, k, k))
+    y = torch.empty_like(x) if out is None else _dev(out, "out", x.shape)
+    pp = None if prepared is None else _workspace(workspace_bytes(C // 4, k, 4), x.device,
+                                                  prepared)
+    _check(L.finc_split_forward(_ptr(x), _ptr(y), _ptr(Kq4), _ptr(_logdet_out(logdet)), _ptr(pp),
+                                B, C, H, W, k, _stream()), "finc_split_forward")
+    return y
+
+
+def split_logdet(Kq4: torch.Tensor, H: int, W: int, out: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(Kq4, "Kq4")
+    out = torch.empty(1, dtype=torch.float64, device=Kq4.device) if out is None else out
+    _check(L.finc_split_logdet(_ptr(Kq4), 4 * Kq4.shape[1], Kq4.shape[-1], H, W, _ptr(out),
+                               _stream()), "finc_split_logdet")
+    return out
+
+
+def split_inverse(y: torch.Tensor, Kq4: torch.Tensor, out: torch.Tensor | None = None,
+                  workspace: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    k = Kq4.shape[-1]
+    _dev(Kq4, "Kq4", (4, C // 4, C // 4, k, k))
+    x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
+    ws = _workspace(workspace_bytes(C // 4, k, 4), y.device, workspace)
+    _check(L.finc_split_inverse(_ptr(y), _ptr(x), _ptr(Kq4), B, C, H, W, k, _ptr(ws),
+                                _stream()), "finc_split_inverse")
+    return x
+
+
+def split_inverse_prepared(y: torch.Tensor, prepared4: torch.Tensor, k: int,
+                           out: torch.Tensor | None = None):
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
+    _check(L.finc_split_inverse_prepared(_ptr(y), _ptr(x), _ptr(prepared4), B, C, H, W, k,
+                                         _stream()), "finc_split_inverse_prepared")
     return x
 
 

@@ -115,6 +115,20 @@ def unit_case(B: int, C: int, H: int, W: int, k: int, seed: int = 0) -> dict:
     return dict(x=x, z=z, K4=K4, B=B, C=C, H=H, W=W, k=k)
 
 
+def split_kernels(C: int, k: int, first_layer: int = 0) -> np.ndarray:
+    """The four quarter-channel blocks of one channel-split unit, stacked
+    (4, C/4, C/4, k, k); quarter g has corner g (TL, TR, BL, BR)."""
+    return np.stack([masked_kernel(C // 4, k, g, 1000 + first_layer + g) for g in range(4)])
+
+
+def split_case(B: int, C: int, H: int, W: int, k: int, seed: int = 0) -> dict:
+    rng = np.random.default_rng(seed)
+    x = gaussian(rng, (B, C, H, W))
+    z = gaussian(rng, (B, C, H, W))
+    Kq4 = split_kernels(C, k, 0)
+    return dict(x=x, z=z, Kq4=Kq4, B=B, C=C, H=H, W=W, k=k)
+
+
 def stack_case(B: int = 64, C1: int = 12, H1: int = 32, W1: int = 32,
                levels: int = 3, units: int = 8, k: int = 3, seed: int = 0) -> dict:
     """Multi-scale sampling stack: `levels` levels of `units` FInC units, each
@@ -146,7 +160,7 @@ def stack_case(B: int = 64, C1: int = 12, H1: int = 32, W1: int = 32,
                 levels=levels, units=units, k=k, dims=dims)
 
 
-# The five workloads, by what they are.
+# The workloads, by what they are.
 WORKLOADS = {
     "layer_c3_8x8_b1_k3": dict(kind="layer", B=1, C=3, H=8, W=8, k=3),
     "layer_c12_16x16_b64_k3": dict(kind="layer", B=64, C=12, H=16, W=16, k=3),
@@ -158,6 +172,10 @@ WORKLOADS = {
     "unit_c12_32x32_b64_k5": dict(kind="unit", B=64, C=12, H=32, W=32, k=5),
     "stack_3x8_c12_32x32_b64_k3": dict(kind="stack", B=64, C1=12, H1=32, W1=32,
                                        levels=3, units=8, k=3),
+    # the paper's channel-split unit (Sec. 4.3, Alg. 2): quarters of 3 and 12
+    # channels
+    "split_c12_16x16_b64_k3": dict(kind="split", B=64, C=12, H=16, W=16, k=3),
+    "split_c48_16x16_b64_k3": dict(kind="split", B=64, C=48, H=16, W=16, k=3),
 }
 
 
@@ -169,4 +187,6 @@ def make(name: str, **override) -> dict:
         return layer_case(**spec)
     if kind == "unit":
         return unit_case(**spec)
+    if kind == "split":
+        return split_case(**spec)
     return stack_case(**spec)

@@ -26,6 +26,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("finc_forward", "finc_logdet", "finc_inverse", "finc_unit_forward",
                  "finc_unit_inverse", "finc_unit_logdet", "finc_stack_inverse",
+                 "finc_split_forward", "finc_split_inverse", "finc_split_logdet",
                  "finc_prepare", "finc_strerror"):
         assert want in names
 
@@ -116,6 +117,25 @@ def test_logdet_and_prepare_reject():
                             None) == finc.EINVAL
     assert lib.finc_prepare(FAKE, -1, corners, 12, 3, ws, None) == finc.EINVAL
     assert lib.finc_prepare(FAKE, 0, corners, 12, 3, ws, None) == finc.OK   # nothing to do
+
+
+def test_split_rejects():
+    lib = finc.lib()
+    ws = ctypes.c_void_p(0x4000000)
+    for C in (0, 2, 13, 260):   # not a multiple of 4, or quarters above FINC_MAX_C
+        assert lib.finc_split_forward(FAKE, FAKE2, FAKE, NULL, NULL, 2, C, 8, 8, 3,
+                                      None) == finc.EINVAL
+        assert lib.finc_split_inverse(FAKE, FAKE2, FAKE, 2, C, 8, 8, 3, ws, None) == finc.EINVAL
+        assert lib.finc_split_logdet(FAKE, C, 3, 8, 8, ctypes.c_void_p(0x200000),
+                                     None) == finc.EINVAL
+    assert lib.finc_split_forward(NULL, FAKE2, FAKE, NULL, NULL, 2, 12, 8, 8, 3, None) == finc.EINVAL
+    assert lib.finc_split_forward(FAKE, ctypes.c_void_p(0x100000 + 64), FAKE2, NULL, NULL, 2,
+                                  12, 8, 8, 3, None) == finc.EINVAL   # x / y overlap
+    assert lib.finc_split_inverse(FAKE, FAKE2, FAKE, 2, 12, 8, 8, 3, NULL, None) == finc.EINVAL
+    assert lib.finc_split_inverse_prepared(FAKE, FAKE2, ctypes.c_void_p(0x4000010), 2, 12, 8,
+                                           8, 3, None) == finc.EINVAL   # misaligned
+    assert lib.finc_split_inverse_prepared(FAKE, FAKE2, ws, 0, 12, 8, 8, 3, None) == finc.OK
+    assert lib.finc_split_inverse(FAKE, FAKE2, FAKE, 0, 12, 8, 8, 3, ws, None) == finc.OK
 
 
 def test_stack_rejects():

@@ -214,6 +214,72 @@ def test_unit_workload(orc, name):
     assert torch.equal(finc.unit_inverse(y[3:4].contiguous(), K4d)[0], xr[3])
 
 
+SPLIT_SHAPES = [
+    # (B, C, H, W, k): quarters of 1 .. 16 channels, ragged sizes, k = 1 .. 5
+    (2, 4, 5, 7, 3), (3, 8, 6, 4, 2), (2, 12, 13, 17, 3), (1, 16, 9, 6, 5), (2, 4, 3, 3, 1),
+    (1, 64, 8, 8, 3), (2, 20, 1, 9, 3),
+]
+
+
+@pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_split_unit(orc, shape):
+    """Channel-split unit (Sec. 4.3, Alg. 2): forward, log|det|, inverse and the
+    prepared side output, elementwise against the oracle; junk in the masked
+    slots is ignored."""
+    B, C, H, W, k = shape
+    print(f"split B={B} C={C} H={H} W={W} k={k}", flush=True)
+    rng = np.random.default_rng(hash(shape) % 2**32)
+    x = rng.normal(size=(B, C, H, W))
+    Kq4 = np.stack([synth.garbage_in_mask(synth.masked_kernel(C // 4, k, g, 1200 + g), g)
+                    for g in range(4)])
+    xd, Kd = dev(x), dev(Kq4)
+    ldf = torch.full((1,), float("nan"), dtype=torch.float64, device=DEV)
+    y = finc.split_forward(xd, Kd, out=poisoned(x.shape), logdet=ldf)
+    yh = host(y)
+    assert_close(yh, orc.split_forward(f64(x), f64(Kq4)), "split forward")
+    r = orc.split_logdet(f64(Kq4), H, W)
+    assert abs(float(ldf.cpu()[0]) - r) <= TOL * max(1.0, abs(r))
+    ld = float(finc.split_logdet(Kd, H, W).cpu()[0])
+    assert abs(ld - r) <= TOL * max(1.0, abs(r))
+    xr = finc.split_inverse(y, Kd, out=poisoned(x.shape))
+    assert_close(host(xr), orc.split_inverse(yh, f64(Kq4)), "split inverse")
+    assert_round_trip(host(xr), f64(x), "split")
+    z = rng.normal(size=(B, C, H, W))
+    assert_close(host(finc.split_inverse(dev(z), Kd)), orc.split_inverse(f64(z), f64(Kq4)),
+                 "split inverse of arbitrary input")
+    # the forward's prepared side output is what prepare writes, and drives
+    # the prepared inverse to the same bits
+    nb = finc.workspace_bytes(C // 4, k, 4)
+    pp = torch.full((nb,), 0xAB, dtype=torch.uint8, device=DEV)
+    ref = torch.full((nb,), 0xAB, dtype=torch.uint8, device=DEV)
+    assert torch.equal(finc.split_forward(xd, Kd, prepared=pp), y)
+    finc.prepare(Kd, [0, 1, 2, 3], out=ref)
+    assert torch.equal(pp, ref)
+    assert torch.equal(finc.split_inverse_prepared(y, pp, k, out=poisoned(x.shape)), xr)
+    # in place, and batch-invariant bits
+    inplace = y.clone()
+    finc.split_inverse(inplace, Kd, out=inplace)
+    assert torch.equal(inplace, xr)
+    assert torch.equal(finc.split_inverse(y[B - 1:B].contiguous(), Kd)[0], xr[B - 1])
+
+
+@pytest.mark.parametrize("name", [n for n, s in synth.WORKLOADS.items() if s["kind"] == "split"])
+def test_split_workload(orc, name):
+    """Full-size channel-split workloads; the oracle runs on four sampled images
+    (results do not depend on the batch)."""
+    print(f"workload {name}", flush=True)
+    c = synth.make(name)
+    x, Kq4 = c["x"], c["Kq4"]
+    xd, Kd = dev(x), dev(Kq4)
+    y = finc.split_forward(xd, Kd, out=poisoned(x.shape))
+    xr = finc.split_inverse(y, Kd, out=poisoned(x.shape))
+    idx = [0, 1, c["B"] // 2, c["B"] - 1]
+    yh, xh = host(y)[idx], host(xr)[idx]
+    assert_close(yh, orc.split_forward(f64(x[idx]), f64(Kq4)), f"{name} forward")
+    assert_close(xh, orc.split_inverse(yh, f64(Kq4)), f"{name} inverse")
+    assert_round_trip(host(xr), f64(x), f"{name} round trip")
+
+
 def _stack_flat(c):
     Kf = np.concatenate([a.ravel() for a in c["K"]])
     sf = np.concatenate([a.ravel() for a in c["scale"]])

@@ -1,8 +1,16 @@
-"""Build the HIP library in-tree for gfx950: paper_2301_09266_amd/csrc/libfinc.so."""
+"""Build the HIP library in-tree for gfx950: paper_2301_09266_amd/csrc/libfinc.so.
+
+finc.hip compiles as several translation units in parallel (FINC_PART: one
+per group of inverse kernel instances, and one with everything else), which
+are then linked into the one shared library.
+"""
 from __future__ import annotations
 
+import concurrent.futures
 import os
+import shutil
 import subprocess
+import tempfile
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
@@ -10,19 +18,43 @@ SRC = os.path.join(PKG, "csrc", "finc.hip")
 LIB = os.path.join(PKG, "csrc", "libfinc.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
+ARCH = "--offload-arch=gfx950"
 FLAGS = [
-    "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    ARCH, "-O3", "-std=c++17", "-fPIC",
     # packed fp32 VALU ops stay off: plain fp32 FMAs only
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    "-Wall", "-Wno-unused-function",
+    "-Wall", "-Wno-unused-function", "-Wno-unused-const-variable",
 ]
+INVERSE_GROUPS = 15   # kInverseGroups in finc.hip
+
+
+def _jobs() -> int:
+    for var in ("MAX_JOBS", "CMAKE_BUILD_PARALLEL_LEVEL"):
+        if os.environ.get(var, "").isdigit() and int(os.environ[var]) > 0:
+            return min(int(os.environ[var]), 16)
+    return max(1, min(os.cpu_count() or 1, 16))
 
 
 def build(out: str = LIB, extra: list[str] | None = None) -> str:
-    tmp = out + ".tmp"
-    cmd = [HIPCC, *FLAGS, *(extra or []), "-I", os.path.join(ROOT, "include"), "-o", tmp, SRC]
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, out)
+    """Compile every part of finc.hip and link them into `out`."""
+    tmpdir = tempfile.mkdtemp(prefix="finc_build_")
+    try:
+        parts = [-2] + list(range(INVERSE_GROUPS))
+        objs = [os.path.join(tmpdir, f"part{p + 2}.o") for p in parts]
+
+        def compile_part(i: int) -> None:
+            cmd = [HIPCC, *FLAGS, *(extra or []), f"-DFINC_PART={parts[i]}",
+                   "-I", os.path.join(ROOT, "include"), "-c", "-o", objs[i], SRC]
+            subprocess.run(cmd, check=True)
+
+        with concurrent.futures.ThreadPoolExecutor(_jobs()) as pool:
+            for f in [pool.submit(compile_part, i) for i in range(len(parts))]:
+                f.result()
+        tmp = out + ".tmp"
+        subprocess.run([HIPCC, ARCH, "-shared", "-fPIC", "-o", tmp, *objs], check=True)
+        os.replace(tmp, out)
+    finally:
+        shutil.rmtree(tmpdir, ignore_errors=True)
     return out
 
 

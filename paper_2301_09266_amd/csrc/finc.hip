@@ -30,6 +30,14 @@
 
 #include "finc.h"
 
+// The library is one translation unit, or several compiled in parallel:
+// FINC_PART = g (0 <= g < kInverseGroups) holds only the inverse kernel
+// instances of group g, FINC_PART = -2 everything else.  -1, the default,
+// is the single unit with everything.
+#ifndef FINC_PART
+#define FINC_PART -1
+#endif
+
 namespace {
 
 constexpr int kWave = 64;
@@ -290,6 +298,7 @@ __device__ void prep_columns(const float *__restrict__ K, float *out, int C, int
             make_float4(0.0f, 0.0f, 0.0f, 0.0f);
 }
 
+#if FINC_PART < 0
 __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
     __shared__ double lds[kPrepMax * kPrepMax + kPrepMax + (kPrepMax - kPrepBlk) * kPrepThreads];
     const int layer = blockIdx.y;
@@ -302,11 +311,13 @@ __global__ __launch_bounds__(kPrepThreads) void prep_kernel(PrepArgs a) {
                                (cw >> (2 * (layer & 15))) & 3, blockIdx.x * kPrepThreads,
                                blockIdx.x == 0, lds);
 }
+#endif
 
 // ---------------------------------------------------------------------------
 // log|det|: H*W*sum over layers and channels of log|K[c,c,self]| (fp64,
 // fixed-order tree sum).
 // ---------------------------------------------------------------------------
+#if FINC_PART < 0
 __global__ __launch_bounds__(kWave) void logdet_kernel(const float *K, int n, int corner0,
                                                        int C, int k, int H, int W,
                                                        double *out) {
@@ -330,6 +341,7 @@ __global__ __launch_bounds__(kWave) void logdet_kernel(const float *K, int n, in
     if (tid == 0)
         out[0] = (double)H * (double)W * red[0];
 }
+#endif
 
 // ---------------------------------------------------------------------------
 // Inverse (Algorithm 1) as an MFMA wavefront.
@@ -495,6 +507,10 @@ struct InvArgs {
     // workgroup of image b' = 4 b + g inverts quarter g with corner g and the
     // g-th prepared layer (one level of one layer)
     int split;
+    // vec bit 0: the top level's input may be read 16 bytes at a time (H W a
+    // multiple of 4, z 16-byte aligned); bit 1: the output may be written so
+    // (the last level's W a multiple of 4, out 16-byte aligned)
+    int vec;
     float *out;           // output of the last level: (B, C, H, W)
     Level lv[kMaxLevels]; // in the order they run
 };
@@ -602,71 +618,98 @@ __device__ inline void copy_solution(float *sm, const Plan &pl) {
 }
 
 // Load the top level's input (B, C, H, W) -> Y, pixel-major, padded channels
-// 0.  Vector loads along the pixel axis (four pixels of one channel), all of
-// a thread's loads in flight before the first LDS store; `during` (LDS work
-// that does not touch Y) runs while the first round of loads is in flight.
+// 0.  With vec4 (H W a multiple of 4 and src 16-byte aligned), a thread
+// takes a block of four pixels by
+// four channels (one channel quad): four 16-byte loads, one per channel,
+// coalesced across the lanes, transposed in registers into four 16-byte LDS
+// stores, one per pixel.  Otherwise it takes one pixel's channel quad (four
+// scalar loads, one LDS store).  All of a thread's loads are in flight before
+// the first store; `during` (work that does not touch Y) runs while the
+// first round of loads is in flight.
 template <typename F>
 __device__ inline void load_input(float *sm, const Plan &pl, const float *__restrict__ src,
-                                  F during) {
-    const int HW = pl.H * pl.W, CP = pl.CP, C = pl.C;
+                                  bool vec4, F during) {
+    const int HW = pl.H * pl.W, CP = pl.CP, C = pl.C, nq = CP / 4;
     float *Y = sm + pl.offY;
-    constexpr int U = 8;
     bool first = true;
-    if ((HW & 3) == 0) {
-        const int n4 = C * HW / 4, hw4 = HW / 4;
+    auto pad0 = [&](float4 w, int cq) {   // padding channels are zero
+        if (4 * cq + 3 >= C) {
+            w.x = 4 * cq < C ? w.x : 0.0f;
+            w.y = 4 * cq + 1 < C ? w.y : 0.0f;
+            w.z = 4 * cq + 2 < C ? w.z : 0.0f;
+            w.w = 0.0f;
+        }
+        return w;
+    };
+    if (vec4) {
+        const int total = nq * (HW / 4);   // (pixel group, quad), quad fastest
         const float4 *s4 = reinterpret_cast<const float4 *>(src);
-        for (int base = threadIdx.x; base < n4; base += U * blockDim.x) {
-            float4 v[U];
+        constexpr int U = 2;
+        for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
+            float e4[U][4][4];
 #pragma unroll
-            for (int k = 0; k < U; ++k) {
-                const int idx = base + k * blockDim.x;
-                if (idx < n4)
-                    v[k] = s4[idx];
+            for (int u = 0; u < U; ++u) {
+                const int idx = base + u * blockDim.x;
+                const int pg = fdiv(idx, pl.d_cp4), cq = idx - pg * nq;
+                const bool in = idx < total;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int c = 4 * cq + e;
+                    const float4 v = s4[in && c < C ? (size_t)c * (HW / 4) + pg : 0];
+                    e4[u][e][0] = v.x;
+                    e4[u][e][1] = v.y;
+                    e4[u][e][2] = v.z;
+                    e4[u][e][3] = v.w;
+                }
             }
             if (first)
                 during();
             first = false;
 #pragma unroll
-            for (int k = 0; k < U; ++k) {
-                const int idx = base + k * blockDim.x;
-                if (idx < n4) {
-                    const int c = fdiv(idx, pl.d_hw4), p = 4 * (idx - c * hw4);
-                    Y[(p + 0) * CP + c] = v[k].x;
-                    Y[(p + 1) * CP + c] = v[k].y;
-                    Y[(p + 2) * CP + c] = v[k].z;
-                    Y[(p + 3) * CP + c] = v[k].w;
+            for (int u = 0; u < U; ++u) {
+                const int idx = base + u * blockDim.x;
+                if (idx < total) {
+                    const int pg = fdiv(idx, pl.d_cp4), cq = idx - pg * nq;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        *reinterpret_cast<float4 *>(Y + (size_t)(4 * pg + i) * CP + 4 * cq) =
+                            pad0(make_float4(e4[u][0][i], e4[u][1][i], e4[u][2][i], e4[u][3][i]),
+                                 cq);
                 }
             }
         }
     } else {
-        for (int base = threadIdx.x; base < C * HW; base += U * blockDim.x) {
-            float v[U];
+        const int total = nq * HW;   // (quad, pixel), pixel fastest
+        constexpr int U = 4;
+        for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
+            float e4[U][4];
 #pragma unroll
-            for (int k = 0; k < U; ++k) {
-                const int idx = base + k * blockDim.x;
-                if (idx < C * HW)
-                    v[k] = src[idx];
+            for (int u = 0; u < U; ++u) {
+                const int idx = base + u * blockDim.x;
+                const int cq = fdiv(idx, pl.d_HW), p = idx - cq * HW;
+                const bool in = idx < total;
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int c = 4 * cq + e;
+                    e4[u][e] = src[in && c < C ? (size_t)c * HW + p : 0];
+                }
             }
             if (first)
                 during();
             first = false;
 #pragma unroll
-            for (int k = 0; k < U; ++k) {
-                const int idx = base + k * blockDim.x;
-                if (idx < C * HW) {
-                    const int c = fdiv(idx, pl.d_HW), p = idx - c * HW;
-                    Y[p * CP + c] = v[k];
+            for (int u = 0; u < U; ++u) {
+                const int idx = base + u * blockDim.x;
+                if (idx < total) {
+                    const int cq = fdiv(idx, pl.d_HW), p = idx - cq * HW;
+                    *reinterpret_cast<float4 *>(Y + (size_t)p * CP + 4 * cq) =
+                        pad0(make_float4(e4[u][0], e4[u][1], e4[u][2], e4[u][3]), cq);
                 }
             }
         }
     }
     if (first)   // this thread had nothing to load
         during();
-    const int pad = CP - C;
-    for (int idx = threadIdx.x; idx < pad * HW; idx += blockDim.x) {
-        const int p = fdiv(idx, pl.d_pad);
-        Y[p * CP + C + (idx - p * pad)] = 0.0f;
-    }
 }
 
 // Input of level l: the chain's input at the top; below, concat(unsqueeze(h),
@@ -677,7 +720,7 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
 // way.
 template <typename F>
 __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm, size_t b,
-                            F work) {
+                            bool vec4, F work) {
     const Plan &pl = lv.pl;
     const int C = pl.C, CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
     float *Y = sm + pl.offY;
@@ -688,7 +731,7 @@ __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm
     if (top) {
         // the solution buffer and the partial tiles are cleared while the
         // image is on its way
-        load_input(sm, pl, lv.z + b * (size_t)C * HW, [&] {
+        load_input(sm, pl, lv.z + b * (size_t)C * HW, vec4, [&] {
             work();
             clear();
         });
@@ -772,7 +815,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
     // corner-free geometry of each group's quad: dp | dq << 4 | cq << 8, or
     // -1 where the quad does not exist (decoded while the input loads)
     int geo[G];
-    level_input(lv, top, up, sm, b, [&] {
+    level_input(lv, top, up, sm, b, (a.vec & 1) != 0, [&] {
 #pragma unroll
         for (int g = 0; g < NG; ++g) {
             const int uq = quad_of(pl, r, g, kq);
@@ -1084,9 +1127,10 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
     Level lv = a.lv[0];
     Plan above = lv.pl;   // plan of the level run before (unused at the first)
     {   // one round of scalar loads for everything the first level starts with
-        const int L = a.L, nu = a.n_units, lpu = a.lpu, c0 = a.corner0, sp = a.split;
-        asm volatile("" ::"s"(L), "s"(nu), "s"(lpu), "s"(c0), "s"(sp), "s"(lv.z), "s"(lv.prep),
-                     "s"(lv.scale));
+        const int L = a.L, nu = a.n_units, lpu = a.lpu, c0 = a.corner0, sp = a.split,
+                  vc = a.vec;
+        asm volatile("" ::"s"(L), "s"(nu), "s"(lpu), "s"(c0), "s"(sp), "s"(vc), "s"(lv.z),
+                     "s"(lv.prep), "s"(lv.scale));
     }
     constexpr bool kOne = (MODE & kOneLayer) != 0;
     for (int i = 0; i < (kOne ? 1 : a.L); ++i) {
@@ -1110,37 +1154,122 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
     const Plan &p0 = lv.pl;   // the last level run
     const int HW0 = p0.H * p0.W, n0 = p0.C * HW0;
     float *dst = a.out + b * (size_t)n0;
-    constexpr int U = 4;
-    if ((p0.W & 3) == 0) {   // four pixels of a row, one channel, per vector store
-        const int n4 = n0 / 4, w4 = p0.W / 4, hw4 = HW0 / 4;
+    // With vec bit 1, a thread takes four pixels of a row by one
+    // channel quad: four 16-byte LDS reads, one per pixel, transposed in
+    // registers into four 16-byte stores, one per channel, coalesced across
+    // the lanes.  Otherwise one pixel's quad: one LDS read, four scalar stores.
+    const int nq0 = p0.CP / 4;
+    auto xat = [&](int p, int cq) {
+        const int i = fdiv(p, p0.d_W), j = p - i * p0.W;
+        return *reinterpret_cast<const float4 *>(
+            sm + p0.offX + ((i + p0.P) * p0.WP + j + p0.P) * p0.CP + 4 * cq);
+    };
+    if (a.vec & 2) {
+        const int tot = nq0 * (HW0 / 4);   // (pixel group, quad), quad fastest
         float4 *d4 = reinterpret_cast<float4 *>(dst);
-        for (int base = threadIdx.x; base < n4; base += U * blockDim.x) {
-            float4 v[U];
+        constexpr int U = 2;
+        for (int base = threadIdx.x; base < tot; base += U * blockDim.x) {
+            float4 v[U][4];
 #pragma unroll
-            for (int k = 0; k < U; ++k) {
-                const int idx = base + k * blockDim.x;
-                if (idx < n4) {
-                    const int c = fdiv(idx, p0.d_hw4), q = idx - c * hw4;
-                    const int i = fdiv(q, p0.d_w4), j = 4 * (q - i * w4);
-                    const float *x = sm + p0.offX + ((i + p0.P) * p0.WP + j + p0.P) * p0.CP + c;
-                    v[k] = make_float4(x[0], x[p0.CP], x[2 * p0.CP], x[3 * p0.CP]);
-                }
+            for (int u = 0; u < U; ++u) {
+                const int idx = imin(base + u * blockDim.x, tot - 1);
+                const int pg = fdiv(idx, p0.d_cp4), cq = idx - pg * nq0;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    v[u][i] = xat(4 * pg + i, cq);
             }
 #pragma unroll
-            for (int k = 0; k < U; ++k) {
-                const int idx = base + k * blockDim.x;
-                if (idx < n4)
-                    d4[idx] = v[k];
+            for (int u = 0; u < U; ++u) {
+                const int idx = base + u * blockDim.x;
+                if (idx < tot) {
+                    const int pg = fdiv(idx, p0.d_cp4), cq = idx - pg * nq0, c = 4 * cq;
+                    float4 *d = d4 + (size_t)c * (HW0 / 4) + pg;
+                    d[0] = make_float4(v[u][0].x, v[u][1].x, v[u][2].x, v[u][3].x);
+                    if (c + 1 < p0.C)
+                        d[HW0 / 4] = make_float4(v[u][0].y, v[u][1].y, v[u][2].y, v[u][3].y);
+                    if (c + 2 < p0.C)
+                        d[HW0 / 2] = make_float4(v[u][0].z, v[u][1].z, v[u][2].z, v[u][3].z);
+                    if (c + 3 < p0.C)
+                        d[3 * (HW0 / 4)] =
+                            make_float4(v[u][0].w, v[u][1].w, v[u][2].w, v[u][3].w);
+                }
             }
         }
     } else {
-        for (int idx = threadIdx.x; idx < n0; idx += blockDim.x) {
-            const int c = fdiv(idx, p0.d_HW), p = idx - c * HW0;
-            const int i = fdiv(p, p0.d_W), j = p - i * p0.W;
-            dst[idx] = sm[p0.offX + ((i + p0.P) * p0.WP + j + p0.P) * p0.CP + c];
+        constexpr int U = 4;
+        const int tot = nq0 * HW0;   // (quad, pixel), pixel fastest
+        for (int base = threadIdx.x; base < tot; base += U * blockDim.x) {
+            float4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int idx = imin(base + u * blockDim.x, tot - 1);
+                const int cq = fdiv(idx, p0.d_HW), p = idx - cq * HW0;
+                v[u] = xat(p, cq);
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int idx = base + u * blockDim.x;
+                if (idx < tot) {
+                    const int cq = fdiv(idx, p0.d_HW), p = idx - cq * HW0, c = 4 * cq;
+                    float *d = dst + (size_t)c * HW0 + p;
+                    d[0] = v[u].x;
+                    if (c + 1 < p0.C)
+                        d[HW0] = v[u].y;
+                    if (c + 2 < p0.C)
+                        d[2 * HW0] = v[u].z;
+                    if (c + 3 < p0.C)
+                        d[3 * HW0] = v[u].w;
+                }
+            }
         }
     }
 }
+
+// Inverse kernel instances, in groups of one workgroup size and one mode, by
+// quad groups per wave (1..kMaxGroups).  The host picks one by address.
+constexpr int kInverseGroups = 15;
+constexpr int kGroupThreads[kInverseGroups] = {256, 256, 256, 256, 256, 512, 512, 512,
+                                               512, 512, 1024, 1024, 1024, 1024, 1024};
+constexpr int kGroupModes[5] = {kCritGather, kCritRegs, kCritBoth, kCritGather | kOneLayer,
+                                kCritRegs | kOneLayer};
+constexpr int kGroupMode[kInverseGroups] = {
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4],
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4],
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4]};
+
+template <int MAXT, int MODE>
+const void *inverse_instance_of(int ng) {
+    switch (ng) {
+    case 1: return reinterpret_cast<const void *>(inverse_chain_kernel<1, MAXT, MODE>);
+    case 2: return reinterpret_cast<const void *>(inverse_chain_kernel<2, MAXT, MODE>);
+    case 3: return reinterpret_cast<const void *>(inverse_chain_kernel<3, MAXT, MODE>);
+    case 4: return reinterpret_cast<const void *>(inverse_chain_kernel<4, MAXT, MODE>);
+    case 5: return reinterpret_cast<const void *>(inverse_chain_kernel<5, MAXT, MODE>);
+    case 6: return reinterpret_cast<const void *>(inverse_chain_kernel<6, MAXT, MODE>);
+    case 7: return reinterpret_cast<const void *>(inverse_chain_kernel<7, MAXT, MODE>);
+    default: return reinterpret_cast<const void *>(inverse_chain_kernel<8, MAXT, MODE>);
+    }
+}
+
+}  // namespace
+
+#define FINC_GROUPS(X) \
+    X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14)
+#define FINC_CAT2(a, b) a##b
+#define FINC_CAT(a, b) FINC_CAT2(a, b)
+
+namespace finc_parts {
+#define FINC_DECLARE(g) const void *inverse_group_##g(int ng);
+FINC_GROUPS(FINC_DECLARE)
+#if FINC_PART >= 0
+const void *FINC_CAT(inverse_group_, FINC_PART)(int ng) {
+    return inverse_instance_of<kGroupThreads[FINC_PART], kGroupMode[FINC_PART]>(ng);
+}
+#endif
+}  // namespace finc_parts
+
+#if FINC_PART < 0
+namespace {
 
 // ---------------------------------------------------------------------------
 // Forward (Sec. 3 convolution with the Sec. 4.1 corner padding) as MFMA
@@ -1546,30 +1675,22 @@ int launch_prep(const float *K, int n, const int *corners, int C, int k, float *
     return FINC_OK;
 }
 
-// Kernel instances by quad groups per wave (1..kMaxGroups) and workgroup size.
-typedef void (*InvKernel)(InvArgs);
-template <int MAXT, int MODE>
-InvKernel inverse_instance_mode(int ng) {
-    switch (ng) {
-    case 1: return inverse_chain_kernel<1, MAXT, MODE>;
-    case 2: return inverse_chain_kernel<2, MAXT, MODE>;
-    case 3: return inverse_chain_kernel<3, MAXT, MODE>;
-    case 4: return inverse_chain_kernel<4, MAXT, MODE>;
-    case 5: return inverse_chain_kernel<5, MAXT, MODE>;
-    case 6: return inverse_chain_kernel<6, MAXT, MODE>;
-    case 7: return inverse_chain_kernel<7, MAXT, MODE>;
-    default: return inverse_chain_kernel<8, MAXT, MODE>;
-    }
-}
-template <int MAXT>
-InvKernel inverse_instance(int ng, int mode) {
-    switch (mode) {
-    case kCritGather: return inverse_instance_mode<MAXT, kCritGather>(ng);
-    case kCritRegs: return inverse_instance_mode<MAXT, kCritRegs>(ng);
-    case kCritGather | kOneLayer: return inverse_instance_mode<MAXT, kCritGather | kOneLayer>(ng);
-    case kCritRegs | kOneLayer: return inverse_instance_mode<MAXT, kCritRegs | kOneLayer>(ng);
-    default: return inverse_instance_mode<MAXT, kCritBoth>(ng);
-    }
+// The inverse kernel for a workgroup size (threads), a mode and quad groups
+// per wave.
+const void *inverse_instance(int threads, int mode, int ng) {
+#if FINC_PART == -1
+#define FINC_ENTRY(g) &inverse_instance_of<kGroupThreads[g], kGroupMode[g]>,
+#else
+#define FINC_ENTRY(g) &finc_parts::inverse_group_##g,
+#endif
+    static const void *(*const groups[kInverseGroups])(int) = {FINC_GROUPS(FINC_ENTRY)};
+#undef FINC_ENTRY
+    int m = 2;   // kCritBoth stands for any other mode
+    for (int i = 0; i < 5; ++i)
+        if (kGroupModes[i] == mode)
+            m = i;
+    const int t = threads <= 256 ? 0 : threads <= 512 ? 1 : 2;
+    return groups[5 * t + m](ng);
 }
 
 int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
@@ -1590,15 +1711,20 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
         nreg += p.regcrit;
     }
     int mode = nreg == a.L ? kCritRegs : nreg == 0 ? kCritGather : kCritBoth;
+    {
+        const Plan &top = a.lv[0].pl, &last = a.lv[a.L - 1].pl;
+        const bool in4 = (top.H * top.W) % 4 == 0 && ((uintptr_t)a.lv[0].z & 15u) == 0;
+        const bool out4 = last.W % 4 == 0 && ((uintptr_t)a.out & 15u) == 0;
+        a.vec = (in4 ? 1 : 0) | (out4 ? 2 : 0);
+    }
     if (a.L == 1 && a.n_units * a.lpu == 1 && !a.lv[0].scale)
         mode |= kOneLayer;   // (a single level has one critical form)
-    const InvKernel k = threads <= 256   ? inverse_instance<256>(ng, mode)
-                        : threads <= 512 ? inverse_instance<512>(ng, mode)
-                                         : inverse_instance<1024>(ng, mode);
-    if (hipFuncSetAttribute((const void *)k, hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds) != hipSuccess)
+    const void *k = inverse_instance(threads, mode, ng);
+    if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+        hipSuccess)
         (void)hipGetLastError();   // not needed on every runtime; the launch check decides
-    hipLaunchKernelGGL(k, dim3(B), dim3(threads), lds, stream, a);
+    void *args[] = {&a};
+    (void)hipLaunchKernel(k, dim3(B), dim3(threads), args, lds, stream);
     return launched();
 }
 
@@ -2062,3 +2188,4 @@ int finc_stack_inverse(const float *const *z, float *x, const float *K, const fl
 }
 
 }  // extern "C"
+#endif  // FINC_PART < 0

@@ -98,6 +98,40 @@ def test_inverse_in_place(orc):
     assert_close(host(y), want, "in-place inverse")
 
 
+def offset_copy(t, floats=1):
+    """A copy of t whose data starts `floats` floats past a 256-byte boundary."""
+    buf = torch.empty(t.numel() + floats, dtype=t.dtype, device=t.device)
+    u = buf[floats:].view(t.shape)
+    u.copy_(t)
+    return u
+
+
+@pytest.mark.parametrize("shape", [(3, 12, 16, 16, 3), (2, 5, 8, 12, 3), (2, 3, 6, 10, 2)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_unaligned_buffers(orc, shape):
+    """Input and output 4 bytes off 16-byte alignment: the inverse's staging
+    takes its scalar route and gives the aligned call's result bit for bit."""
+    B, C, H, W, k = shape
+    print(f"unaligned B={B} C={C} H={H} W={W} k={k}", flush=True)
+    rng = np.random.default_rng(7 + C)
+    K = dev(synth.masked_kernel(C, k, 1, 21))
+    y = dev(rng.normal(size=(B, C, H, W)))
+    want = finc.inverse(y, K, 1)
+    assert_close(host(want), orc.inverse(host(y), host(K), 1), "aligned inverse")
+    for fi, fo in [(1, 0), (0, 1), (1, 3), (2, 2)]:
+        yu = offset_copy(y, fi) if fi else y
+        out = offset_copy(poisoned(y.shape), fo) if fo else poisoned(y.shape)
+        got = finc.inverse(yu, K, 1, out=out)
+        assert torch.equal(got, want), (fi, fo)
+    # the forward and the unit (four layers in one launch) likewise
+    assert torch.equal(finc.forward(offset_copy(y, 3), K, 1, out=offset_copy(y, 1)),
+                       finc.forward(y, K, 1))
+    K4 = dev(synth.unit_kernels(C, k))
+    wantu = finc.unit_inverse(y, K4)
+    gotu = finc.unit_inverse(offset_copy(y, 1), K4, out=offset_copy(poisoned(y.shape), 3))
+    assert torch.equal(gotu, wantu)
+
+
 def test_logdet_singular():
     K = synth.masked_kernel(4, 3, 2, 5)
     K[2, 2, 0, 2] = 0.0

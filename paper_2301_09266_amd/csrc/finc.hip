@@ -385,6 +385,7 @@ __global__ __launch_bounds__(kWave) void logdet_kernel(const float *K, int n, in
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxWaves = 16;
+constexpr size_t kLdsBytes = 160 * 1024;   // LDS of a gfx950 workgroup
 constexpr int kMaxGroups = 8;                       // quad groups (x4 quads) per wave
 // critical-wave forms an inverse instance is built with (low two bits of
 // its MODE), and kOneLayer: a single level of a single layer without actnorm
@@ -395,7 +396,12 @@ constexpr int kCritGather = 0, kCritRegs = 1, kCritBoth = 2, kOneLayer = 4;
 struct Plan {
     int C, CP, H, W, K, P, WP;
     int MT, NT, T, S, S4, NW;   // row tiles, channel tiles, tiles, helpers per tile,
-                                // partial-tile slots per tile, waves
+                                // partial-tile slots read per tile (S rounded up
+                                // to 4), waves
+    // partial tiles stored per tile: S4 (padded; slots from S on stay zero),
+    // or S with one shared zero slot per parity (compact, when the padded
+    // layout would not fit in LDS)
+    int RS, compact;
     int ncq, nq, nq_crit;       // quads per tap, quads of a tile, quads of the critical wave
     int fq0, fq1;               // fresh quads [fq0, fq1); stale quads [fq1, nq)
     int FG, SG;                 // fresh and stale groups of a tile's helpers
@@ -455,9 +461,14 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p) {
     p.offX = 0;
     p.offY = (H + 2 * p.P) * p.WP * p.CP;
     p.offR = p.offY + H * W * p.CP;
-    p.offZ = p.offR + 2 * p.T * p.S4 * 256;
-    p.offT = p.offZ + 256;
-    p.lds_floats = p.offT + 256;
+    for (p.compact = 0; p.compact < 2; ++p.compact) {
+        p.RS = p.compact ? p.S : p.S4;
+        p.offZ = p.offR + 2 * (p.T * p.RS + p.compact) * 256;
+        p.offT = p.offZ + 256;
+        p.lds_floats = p.offT + 256;
+        if ((size_t)p.lds_floats * sizeof(float) <= kLdsBytes || p.RS == p.S)
+            break;
+    }
     p.lstride = (int)prep_layer_floats(C, K);
     p.d_cp4 = make_fastdiv(p.CP / 4);
     p.d_W = make_fastdiv(W);
@@ -726,7 +737,7 @@ __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm
     float *Y = sm + pl.offY;
     auto clear = [&] {
         zero_floats(sm + pl.offX, pl.offY - pl.offX);
-        zero_floats(sm + pl.offR, pl.offZ + 256 - pl.offR);   // unused slots and Z stay 0
+        zero_floats(sm + pl.offR, pl.offZ + 256 - pl.offR);   // (Z stays 0)
     };
     if (top) {
         // the solution buffer and the partial tiles are cleared while the
@@ -936,17 +947,26 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
         // the critical wave writes channels 16 nt + 4 kq .. +3 of its row's pixel
         const int wx0 = bx0 + nt * 16 + 4 * kq;
         const bool wch = nt * 16 + 4 * kq < CP && gi < H;
-        // partial tiles: R[parity][tile][S4 slots][64 lanes][4]
-        const int rstride = pl.T * pl.S4 * 256;
-        const int rown = (r.tile * pl.S4 + (r.role == 1 ? r.h : 0)) * 256 + 4 * lane;
-        // the sum of a tile's partial tiles (slots without a writer are zero)
-        auto partial_sum = [&](const f32x4 *Rp) {
-            f32x4 s0 = Rp[0] + Rp[64];
-            const f32x4 s1 = Rp[128] + Rp[192];
+        // partial tiles: R[parity][T RS slots (+ one zero slot)][64 lanes][4].
+        // The critical wave reads S4 slots, four at a time: padded, slot s of
+        // its tile; compact, slots from S on are the zero slot of the parity.
+        const int rstride = (pl.T * pl.RS + pl.compact) * 256;
+        const int rown = (r.tile * pl.RS + (r.role == 1 ? r.h : 0)) * 256 + 4 * lane;
+        const f32x4 *R0 = reinterpret_cast<const f32x4 *>(R + rown);
+        const f32x4 *Rz = reinterpret_cast<const f32x4 *>(R + pl.T * pl.RS * 256 + 4 * lane);
+        auto sbase = [&](int s, auto pad) {
+            return decltype(pad)::value || s < pl.S ? R0 + s * 64 : Rz;
+        };
+        // slot s at parity offset po (in f32x4)
+        auto slot = [&](int s, int po, auto pad) { return sbase(s, pad)[po]; };
+        // the sum of a tile's partial tiles, in a fixed order
+        auto partial_sum = [&](int po, auto pad) {
+            f32x4 s0 = slot(0, po, pad) + slot(1, po, pad);
+            const f32x4 s1 = slot(2, po, pad) + slot(3, po, pad);
             s0 += s1;
             for (int s4 = 4; s4 < pl.S4; s4 += 4) {
-                f32x4 t0 = Rp[s4 * 64] + Rp[(s4 + 1) * 64];
-                const f32x4 t1 = Rp[(s4 + 2) * 64] + Rp[(s4 + 3) * 64];
+                f32x4 t0 = slot(s4, po, pad) + slot(s4 + 1, po, pad);
+                const f32x4 t1 = slot(s4 + 2, po, pad) + slot(s4 + 3, po, pad);
                 t0 += t1;
                 s0 += t0;
             }
@@ -996,91 +1016,96 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
             // The chain's first kPre MFMAs (own row) depend on nothing but
             // dprev: they are issued before the barrier, while the write of
             // the diagonal becomes visible.
-            constexpr int kPre = 3;
-            f32x4 dprev = zero, pre = zero;
-            int j = e_lo - gi;   // frame column of row gi at the tile's first diagonal
-            // write address of frame column j (the affine form; used only while
-            // 0 <= j < W)
-            int wcol = wx0 + fwo + j * dcol;
-            // lane li = 0 of a lower tile reads the tile above's last row
-            // (solved in the previous step; channel quads that exist); other
-            // lanes read zeros
-            const int ui = mt * 16 - 1;
-            const int uoi = fh ? H - 1 - imax(ui, 0) : imax(ui, 0);
-            int ju = e_lo - 16 * mt;   // frame column of row 16 mt (and of the row above it)
-            int ucol = pl.offX + ((uoi + P) * WP + P) * CP + fwo + 4 * kq + ju * dcol;
-            const f32x4 *R0 = reinterpret_cast<const f32x4 *>(R + rown);
-            __syncthreads();
-            int e = 0;
-            for (; e < e_lo; ++e)
+            auto crit = [&](auto pad) {
+                constexpr int kPre = 3;
+                f32x4 dprev = zero, pre = zero;
+                int j = e_lo - gi;   // frame column of row gi at the tile's first diagonal
+                // write address of frame column j (the affine form; used only while
+                // 0 <= j < W)
+                int wcol = wx0 + fwo + j * dcol;
+                // lane li = 0 of a lower tile reads the tile above's last row
+                // (solved in the previous step; channel quads that exist); other
+                // lanes read zeros
+                const int ui = mt * 16 - 1;
+                const int uoi = fh ? H - 1 - imax(ui, 0) : imax(ui, 0);
+                int ju = e_lo - 16 * mt;   // frame column of row 16 mt (and of the row above it)
+                int ucol = pl.offX + ((uoi + P) * WP + P) * CP + fwo + 4 * kq + ju * dcol;
+                const f32x4 *b1 = sbase(1, pad), *b2 = sbase(2, pad), *b3 = sbase(3, pad);
                 __syncthreads();
-            for (; e <= e_hi; ++e) {
-                {
-                    const f32x4 *Rp = R0 + (e & 1) * (rstride / 4);
-                    f32x4 up = zero;
-                    if (mt > 0)
-                        up = *reinterpret_cast<const f32x4 *>(
-                            sm + ((li == 0 && 4 * kq < CP && (unsigned)ju < (unsigned)W) ? ucol
-                                                                                    : zaddr));
-                    // the first four partial tiles in flight during the MFMAs
-                    const f32x4 q0 = Rp[0], q1 = Rp[64], q2 = Rp[128], q3 = Rp[192];
-                    const bool ok = wch && (unsigned)j < (unsigned)W;
-                    const int waddr = ok ? wcol : taddr;
-                    __builtin_amdgcn_sched_barrier(0);
-                    f32x4 p = pre;
-                    // tap (0,1): own row, previous column; tap (1,0): row above,
-                    // same column -- the neighbouring lane's previous result
-                    // (row_shr:1 inside each row of 16 lanes; lane 0 takes `up`).
-                    // Elements are copied to scalars first: this compiler
-                    // bit-casts a vector element lvalue as element 0.
-                    if constexpr (G >= 2) {   // (instances with G < 2 never get regc)
-#pragma unroll
-                        for (int e4 = kPre; e4 < 4; ++e4)
-                            p = mfma4(w[0][e4], dprev[e4], p);
-#pragma unroll
-                        for (int e4 = 0; e4 < 4; ++e4) {
-                            const float de = dprev[e4], ue = up[e4];
-                            const float s1 = __int_as_float(__builtin_amdgcn_update_dpp(
-                                __float_as_int(ue), __float_as_int(de), 0x111, 0xf, 0xf, false));
-                            p = mfma4(w[1][e4], s1, p);
+                int e = 0;
+                for (; e < e_lo; ++e)
+                    __syncthreads();
+                for (; e <= e_hi; ++e) {
+                    {
+                        const int po = (e & 1) * (rstride / 4);
+                        f32x4 up = zero;
+                        if (mt > 0)
+                            up = *reinterpret_cast<const f32x4 *>(
+                                sm + ((li == 0 && 4 * kq < CP && (unsigned)ju < (unsigned)W) ? ucol
+                                                                                        : zaddr));
+                        // the first four partial tiles in flight during the MFMAs
+                        const f32x4 q0 = R0[po], q1 = b1[po], q2 = b2[po], q3 = b3[po];
+                        const bool ok = wch && (unsigned)j < (unsigned)W;
+                        const int waddr = ok ? wcol : taddr;
+                        __builtin_amdgcn_sched_barrier(0);
+                        f32x4 p = pre;
+                        // tap (0,1): own row, previous column; tap (1,0): row above,
+                        // same column -- the neighbouring lane's previous result
+                        // (row_shr:1 inside each row of 16 lanes; lane 0 takes `up`).
+                        // Elements are copied to scalars first: this compiler
+                        // bit-casts a vector element lvalue as element 0.
+                        if constexpr (G >= 2) {   // (instances with G < 2 never get regc)
+    #pragma unroll
+                            for (int e4 = kPre; e4 < 4; ++e4)
+                                p = mfma4(w[0][e4], dprev[e4], p);
+    #pragma unroll
+                            for (int e4 = 0; e4 < 4; ++e4) {
+                                const float de = dprev[e4], ue = up[e4];
+                                const float s1 = __int_as_float(__builtin_amdgcn_update_dpp(
+                                    __float_as_int(ue), __float_as_int(de), 0x111, 0xf, 0xf, false));
+                                p = mfma4(w[1][e4], s1, p);
+                            }
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                        f32x4 rs = q0 + q1;
+                        const f32x4 rt = q2 + q3;
+                        rs += rt;
+                        for (int s4 = 4; s4 < pl.S4; s4 += 4) {
+                            f32x4 t0 = slot(s4, po, pad) + slot(s4 + 1, po, pad);
+                            const f32x4 t1 = slot(s4 + 2, po, pad) + slot(s4 + 3, po, pad);
+                            t0 += t1;
+                            rs += t0;
+                        }
+                        const f32x4 x = rs + p;
+                        *reinterpret_cast<f32x4 *>(sm + waddr) = x;
+                        dprev = x;
+                        __builtin_amdgcn_sched_barrier(0);
+                        // next diagonal's own-row MFMAs, overlapping the write
+                        pre = zero;
+                        if constexpr (G >= 2) {
+    #pragma unroll
+                            for (int e4 = 0; e4 < kPre; ++e4)
+                                pre = mfma4(w[0][e4], dprev[e4], pre);
                         }
                     }
-                    __builtin_amdgcn_sched_barrier(0);
-                    f32x4 rs = q0 + q1;
-                    const f32x4 rt = q2 + q3;
-                    rs += rt;
-                    for (int s4 = 4; s4 < pl.S4; s4 += 4) {
-                        f32x4 t0 = Rp[s4 * 64] + Rp[(s4 + 1) * 64];
-                        const f32x4 t1 = Rp[(s4 + 2) * 64] + Rp[(s4 + 3) * 64];
-                        t0 += t1;
-                        rs += t0;
-                    }
-                    const f32x4 x = rs + p;
-                    *reinterpret_cast<f32x4 *>(sm + waddr) = x;
-                    dprev = x;
-                    __builtin_amdgcn_sched_barrier(0);
-                    // next diagonal's own-row MFMAs, overlapping the write
-                    pre = zero;
-                    if constexpr (G >= 2) {
-#pragma unroll
-                        for (int e4 = 0; e4 < kPre; ++e4)
-                            pre = mfma4(w[0][e4], dprev[e4], pre);
-                    }
+                    j += 1;
+                    wcol += dcol;
+                    ju += 1;
+                    ucol += dcol;
+                    __syncthreads();
                 }
-                j += 1;
-                wcol += dcol;
-                ju += 1;
-                ucol += dcol;
-                __syncthreads();
-            }
-            for (; e < E; ++e)
-                __syncthreads();
+                for (; e < E; ++e)
+                    __syncthreads();
+            };
+            if (pl.compact)
+                crit(std::false_type{});
+            else
+                crit(std::true_type{});
         } else if (CRIT != kCritRegs && r.role == 0) {
             // critical wave that gathers its dp + dq = 1 taps from LDS (several
             // channel tiles: the previous diagonal's channels sit in several
             // waves)
-            const f32x4 *R0 = reinterpret_cast<const f32x4 *>(R + rown);
-            auto run = [&](auto full) {
+            auto run = [&](auto full, auto pad) {
                 float4 av[G];
                 int ad[G];
                 addrs(ad, e_lo - gi);
@@ -1091,7 +1116,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                 for (; e <= e_hi; ++e) {
                     const int j = e - gi;
                     load(av, ad, full);
-                    const f32x4 rs = partial_sum(R0 + (e & 1) * (rstride / 4));
+                    const f32x4 rs = partial_sum((e & 1) * (rstride / 4), pad);
                     f32x4 x = mma(av, full);
                     x += rs;
                     const bool ok = wch && (unsigned)j < (unsigned)W;
@@ -1102,10 +1127,14 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                 for (; e < E; ++e)
                     __syncthreads();
             };
-            if (ngw == NG)
-                run(std::true_type{});
+            if (ngw == NG && !pl.compact)
+                run(std::true_type{}, std::true_type{});
+            else if (ngw == NG)
+                run(std::true_type{}, std::false_type{});
+            else if (!pl.compact)
+                run(std::false_type{}, std::true_type{});
             else
-                run(std::false_type{});
+                run(std::false_type{}, std::false_type{});
         } else {
             __syncthreads();
             for (int e = 0; e < E; ++e)

@@ -248,6 +248,33 @@ def test_unit_workload(orc, name):
     assert torch.equal(finc.unit_inverse(y[3:4].contiguous(), K4d)[0], xr[3])
 
 
+@pytest.mark.parametrize("shape", [(2, 2, 64, 64, 3), (1, 3, 48, 64, 3), (1, 2, 64, 40, 2)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_large_images(orc, shape):
+    """Images whose padded partial-tile layout does not fit in LDS (the
+    compact one is used): layer and unit, against the oracle."""
+    B, C, H, W, k = shape
+    print(f"large B={B} C={C} H={H} W={W} k={k}", flush=True)
+    rng = np.random.default_rng(C * 1000 + H + W)
+    x = rng.normal(size=(B, C, H, W))
+    K = synth.masked_kernel(C, k, 3, 55)
+    xd, Kd = dev(x), dev(K)
+    y = finc.forward(xd, Kd, 3)
+    yh = host(y)
+    assert_close(yh, orc.forward(f64(x), f64(K), 3), "forward")
+    xr = finc.inverse(y, Kd, 3, out=poisoned(x.shape))
+    assert_close(host(xr), orc.inverse(yh, f64(K), 3), "inverse")
+    assert_round_trip(host(xr), f64(x), "layer")
+    K4 = synth.unit_kernels(C, k, 4)
+    K4d = dev(K4)
+    yu = finc.unit_forward(xd, K4d)
+    yuh = host(yu)
+    assert_close(yuh, orc.unit_forward(f64(x), f64(K4)), "unit forward")
+    xu = finc.unit_inverse(yu, K4d, out=poisoned(x.shape))
+    assert_close(host(xu), orc.unit_inverse(yuh, f64(K4)), "unit inverse")
+    assert_round_trip(host(xu), f64(x), "unit")
+
+
 SPLIT_SHAPES = [
     # (B, C, H, W, k): quarters of 1 .. 16 channels, ragged sizes, k = 1 .. 5
     (2, 4, 5, 7, 3), (3, 8, 6, 4, 2), (2, 12, 13, 17, 3), (1, 16, 9, 6, 5), (2, 4, 3, 3, 1),

@@ -391,6 +391,14 @@ constexpr int kMaxGroups = 8;                       // quad groups (x4 quads) pe
 // its MODE), and kOneLayer: a single level of a single layer without actnorm
 // (the chain's loops and hand-overs compiled out)
 constexpr int kCritGather = 0, kCritRegs = 1, kCritBoth = 2, kOneLayer = 4;
+// kStream (with kOneLayer and kCritRegs): a single layer whose image does not
+// fit in LDS.  Solution and input live in per-row rings of kRing frame
+// columns; every kPhase diagonal steps the workgroup drains the solved
+// columns to HBM, writes the input of the next kPhase diagonals (loaded a
+// phase earlier into registers) and issues the loads of the phase after.
+constexpr int kStream = 8;
+constexpr int kRing = 32, kPhase = 16;
+constexpr int kStreamRegs = 8;   // prefetched input values per thread
 
 // Work split and LDS layout of one level (same for every layer of it).
 struct Plan {
@@ -402,6 +410,9 @@ struct Plan {
     // or S with one shared zero slot per parity (compact, when the padded
     // layout would not fit in LDS)
     int RS, compact;
+    // stream: X holds frame rows -P .. H-1 and Y rows 0 .. H-1, each as a
+    // ring of kRing frame columns (frame orientation, no border columns)
+    int stream;
     int ncq, nq, nq_crit;       // quads per tap, quads of a tile, quads of the critical wave
     int fq0, fq1;               // fresh quads [fq0, fq1); stale quads [fq1, nq)
     int FG, SG;                 // fresh and stale groups of a tile's helpers
@@ -413,7 +424,7 @@ struct Plan {
     int wave[kMaxWaves];        // per wave: role | mt << 2 | nt << 6 | h << 10 | groups << 14
     // divisions of the index arithmetic: CP / 4, W, H W / 4, H W, CP - C,
     // C, CP, W / 4, ncq (divisors below 1 are replaced by 1)
-    FastDiv d_cp4, d_W, d_hw4, d_HW, d_pad, d_C, d_CP, d_w4, d_ncq;
+    FastDiv d_cp4, d_W, d_hw4, d_HW, d_pad, d_C, d_CP, d_w4, d_ncq, d_H;
 };
 
 // Quad groups of the busiest wave of a plan.
@@ -423,7 +434,10 @@ inline int plan_groups(const Plan &p) {
 }
 
 // false if the shape needs more waves or registers than a workgroup has
-inline bool make_plan(int C, int H, int W, int K, Plan &p) {
+// (stream: the ring layout; also false when a phase's input does not fit in
+// the threads' prefetch registers)
+inline bool make_plan(int C, int H, int W, int K, Plan &p, bool stream = false) {
+    p.stream = stream ? 1 : 0;
     p.C = C;
     p.CP = round_up4(C);
     p.H = H;
@@ -459,8 +473,15 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p) {
     p.NW = p.T * (1 + p.S);
     p.S4 = round_up4(p.S);
     p.offX = 0;
-    p.offY = (H + 2 * p.P) * p.WP * p.CP;
-    p.offR = p.offY + H * W * p.CP;
+    if (stream) {
+        if (!p.regcrit || kPhase * H * C > kStreamRegs * p.NW * kWave)
+            return false;
+        p.offY = (H + p.P) * kRing * p.CP;
+        p.offR = p.offY + H * kRing * p.CP;
+    } else {
+        p.offY = (H + 2 * p.P) * p.WP * p.CP;
+        p.offR = p.offY + H * W * p.CP;
+    }
     for (p.compact = 0; p.compact < 2; ++p.compact) {
         p.RS = p.compact ? p.S : p.S4;
         p.offZ = p.offR + 2 * (p.T * p.RS + p.compact) * 256;
@@ -479,6 +500,7 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p) {
     p.d_CP = make_fastdiv(p.CP);
     p.d_w4 = make_fastdiv(imax(W / 4, 1));
     p.d_ncq = make_fastdiv(p.ncq);
+    p.d_H = make_fastdiv(H);
     // wave roles: critical waves of the tiles first, then S helpers per tile,
     // then idle waves; with the number of quad groups each one owns
     for (int w = 0; w < kMaxWaves; ++w) {
@@ -783,6 +805,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
     // the critical loop(s) its levels use)
     constexpr int CRIT = MODE & 3;
     constexpr bool kOne = (MODE & kOneLayer) != 0;
+    constexpr bool kStr = (MODE & kStream) != 0;
     const bool regc = CRIT == kCritRegs    ? r.role == 0
                       : CRIT == kCritGather ? false
                                             : pl.regcrit && r.role == 0;
@@ -826,7 +849,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
     // corner-free geometry of each group's quad: dp | dq << 4 | cq << 8, or
     // -1 where the quad does not exist (decoded while the input loads)
     int geo[G];
-    level_input(lv, top, up, sm, b, (a.vec & 1) != 0, [&] {
+    auto decode = [&] {
 #pragma unroll
         for (int g = 0; g < NG; ++g) {
             const int uq = quad_of(pl, r, g, kq);
@@ -839,7 +862,90 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                 geo[g] = dp | dq << 4 | cq << 8;
             }
         }
-    });
+    };
+    // --- stream form: input and output move between HBM and the rings in
+    // phases of kPhase diagonals.  Element t of the phase starting at
+    // diagonal d0: frame row i, channel c, diagonal d0 + t % kPhase
+    // (consecutive threads take consecutive columns of one row).
+    float ypre[kStreamRegs];
+    const int nph = kPhase * H * C;
+    const float *zin = lv.z + b * (size_t)C * HW;
+    float *zout = a.out + b * (size_t)C * HW;
+    const int scorner = corner_at(0);
+    const bool sfh = scorner == FINC_BL || scorner == FINC_BR;
+    const bool sfw = scorner == FINC_TR || scorner == FINC_BR;
+    auto selem = [&](int t, int d0, int &i, int &c, int &j) __attribute__((always_inline)) {
+        const int rc = t >> 4;
+        c = fdiv(rc, pl.d_H);
+        i = rc - c * H;
+        j = d0 + (t & (kPhase - 1)) - i;
+    };
+    // natural NCHW offset of frame pixel (i, j), channel c
+    auto snat = [&](int c, int i, int j) __attribute__((always_inline)) {
+        return c * HW + (sfh ? H - 1 - i : i) * W + (sfw ? W - 1 - j : j);
+    };
+    // loads of the input of diagonals d0 .. d0 + kPhase - 1 into registers
+    auto sissue = [&](int d0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < kStreamRegs; ++u) {
+            const int t = threadIdx.x + u * blockDim.x;
+            int i, c, j;
+            selem(t, d0, i, c, j);
+            const bool ok = t < nph && (unsigned)j < (unsigned)W;
+            ypre[u] = zin[ok ? snat(c, i, j) : 0];
+        }
+    };
+    // the loaded values into the input ring
+    auto sput = [&](int d0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < kStreamRegs; ++u) {
+            const int t = threadIdx.x + u * blockDim.x;
+            int i, c, j;
+            selem(t, d0, i, c, j);
+            if (t < nph && (unsigned)j < (unsigned)W)
+                sm[pl.offY + (i * kRing + (j & (kRing - 1))) * CP + c] = ypre[u];
+        }
+    };
+    // solved diagonals d0 .. d1 to HBM
+    auto sdrain = [&](int d0, int d1) __attribute__((always_inline)) {
+        for (int t = threadIdx.x; t < nph; t += blockDim.x) {
+            int i, c, j;
+            selem(t, d0, i, c, j);
+            if (d0 + (t & (kPhase - 1)) <= d1 && (unsigned)j < (unsigned)W)
+                zout[snat(c, i, j)] =
+                    sm[pl.offX + ((i + P) * kRing + (j & (kRing - 1))) * CP + c];
+        }
+    };
+    // end of diagonal step e: the barrier; in the stream form, at the end of
+    // a phase, the exchange with HBM and one more barrier
+    auto step_end = [&](int e) __attribute__((always_inline)) {
+        __syncthreads();
+        if constexpr (kStr) {
+            const bool pend = (e & (kPhase - 1)) == kPhase - 1;
+            if (pend || e == E - 1) {
+                if (pend)
+                    sput(e + 2);   // input of diagonals e + 2 .. e + 1 + kPhase
+                sdrain(e & ~(kPhase - 1), e);
+                if (pend)
+                    sissue(e + 2 + kPhase);
+                __syncthreads();
+            }
+        }
+    };
+    if constexpr (kStr) {
+        // diagonals 0 .. kPhase of the input; the next phase's loads in flight
+        sissue(1);
+        decode();
+        zero_floats(sm + pl.offX, pl.offT - pl.offX);   // rings, partial tiles, Z
+        __syncthreads();
+        sput(1);
+        if (threadIdx.x < C)
+            sm[pl.offY + threadIdx.x] = zin[snat(threadIdx.x, 0, 0)];
+        sissue(1 + kPhase);
+        __syncthreads();
+    } else {
+        level_input(lv, top, up, sm, b, (a.vec & 1) != 0, decode);
+    }
     for (int n = 0; n < nlayers; ++n) {
         const int u = kOne ? 0 : a.n_units - 1 - n / a.lpu, q = kOne ? 0 : a.lpu - 1 - n % a.lpu;
         if (!kOne && n > 0) {   // previous layer's solution is this layer's input
@@ -908,13 +1014,32 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
         auto colx = [&](int j) {   // natural column of frame column j (clamped), times CP
             return fwo + __mul24(imin(imax(j, 0), W - 1), dcol);
         };
+        // stream form: ring row base of each group's source and its column
+        // back-offset (the self tap reads the input ring)
+        int rbase[G], sdq[G];
+        if constexpr (kStr) {
+#pragma unroll
+            for (int g = 0; g < NG; ++g) {
+                const int dp = geo[g] & 15, dq = (geo[g] >> 4) & 15, cq4 = (geo[g] >> 8) << 2;
+                const bool self = geo[g] < 0 || (dp == 0 && dq == 0);
+                rbase[g] = self ? pl.offY + gic * kRing * CP + (geo[g] < 0 ? 0 : cq4)
+                                : pl.offX + (gic - dp + P) * kRing * CP + cq4;
+                sdq[g] = self ? 0 : dq;
+            }
+        }
         // Gather addresses of every group at frame column j.
         auto addrs = [&](int (&ad)[G], int j) {
-            const int cx = colx(j);
             const bool live = j >= 0 && gi < H;
+            if constexpr (kStr) {
 #pragma unroll
-            for (int g = 0; g < NG; ++g)
-                ad[g] = live ? gbase[g] + cx : zaddr;
+                for (int g = 0; g < NG; ++g)
+                    ad[g] = live ? rbase[g] + __mul24((j - sdq[g]) & (kRing - 1), CP) : zaddr;
+            } else {
+                const int cx = colx(j);
+#pragma unroll
+                for (int g = 0; g < NG; ++g)
+                    ad[g] = live ? gbase[g] + cx : zaddr;
+            }
         };
         // The wave's B operands, one 16-byte load per group, all in flight
         // together.  `full`: the wave owns every group of the instance (no
@@ -993,15 +1118,15 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                 __syncthreads();
                 int e = 0;
                 for (; e < lo; ++e)
-                    __syncthreads();
+                    step_end(e);
                 for (; e <= hi; ++e) {
                     load(av, ad, full);
                     Rw[((e + 1) & 1) * (rstride / 4)] = mma(av, full);
                     addrs(ad, e + 2 - gi);
-                    __syncthreads();
+                    step_end(e);
                 }
                 for (; e < E; ++e)
-                    __syncthreads();
+                    step_end(e);
             };
             if (ngw == NG)
                 run(std::true_type{});
@@ -1030,23 +1155,28 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                 const int uoi = fh ? H - 1 - imax(ui, 0) : imax(ui, 0);
                 int ju = e_lo - 16 * mt;   // frame column of row 16 mt (and of the row above it)
                 int ucol = pl.offX + ((uoi + P) * WP + P) * CP + fwo + 4 * kq + ju * dcol;
+                // (stream form: ring rows of the written row and of the row above)
+                const int wxs = pl.offX + (gic + P) * kRing * CP + nt * 16 + 4 * kq;
+                const int uxs = pl.offX + (imax(ui, 0) + P) * kRing * CP + 4 * kq;
                 const f32x4 *b1 = sbase(1, pad), *b2 = sbase(2, pad), *b3 = sbase(3, pad);
                 __syncthreads();
                 int e = 0;
                 for (; e < e_lo; ++e)
-                    __syncthreads();
+                    step_end(e);
                 for (; e <= e_hi; ++e) {
                     {
                         const int po = (e & 1) * (rstride / 4);
+                        const int ucur = kStr ? uxs + __mul24(ju & (kRing - 1), CP) : ucol;
+                        const int wcur = kStr ? wxs + __mul24(j & (kRing - 1), CP) : wcol;
                         f32x4 up = zero;
                         if (mt > 0)
                             up = *reinterpret_cast<const f32x4 *>(
-                                sm + ((li == 0 && 4 * kq < CP && (unsigned)ju < (unsigned)W) ? ucol
+                                sm + ((li == 0 && 4 * kq < CP && (unsigned)ju < (unsigned)W) ? ucur
                                                                                         : zaddr));
                         // the first four partial tiles in flight during the MFMAs
                         const f32x4 q0 = R0[po], q1 = b1[po], q2 = b2[po], q3 = b3[po];
                         const bool ok = wch && (unsigned)j < (unsigned)W;
-                        const int waddr = ok ? wcol : taddr;
+                        const int waddr = ok ? wcur : taddr;
                         __builtin_amdgcn_sched_barrier(0);
                         f32x4 p = pre;
                         // tap (0,1): own row, previous column; tap (1,0): row above,
@@ -1055,10 +1185,10 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                         // Elements are copied to scalars first: this compiler
                         // bit-casts a vector element lvalue as element 0.
                         if constexpr (G >= 2) {   // (instances with G < 2 never get regc)
-    #pragma unroll
+#pragma unroll
                             for (int e4 = kPre; e4 < 4; ++e4)
                                 p = mfma4(w[0][e4], dprev[e4], p);
-    #pragma unroll
+#pragma unroll
                             for (int e4 = 0; e4 < 4; ++e4) {
                                 const float de = dprev[e4], ue = up[e4];
                                 const float s1 = __int_as_float(__builtin_amdgcn_update_dpp(
@@ -1083,7 +1213,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                         // next diagonal's own-row MFMAs, overlapping the write
                         pre = zero;
                         if constexpr (G >= 2) {
-    #pragma unroll
+#pragma unroll
                             for (int e4 = 0; e4 < kPre; ++e4)
                                 pre = mfma4(w[0][e4], dprev[e4], pre);
                         }
@@ -1092,10 +1222,10 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                     wcol += dcol;
                     ju += 1;
                     ucol += dcol;
-                    __syncthreads();
+                    step_end(e);
                 }
                 for (; e < E; ++e)
-                    __syncthreads();
+                    step_end(e);
             };
             if (pl.compact)
                 crit(std::false_type{});
@@ -1112,7 +1242,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                 __syncthreads();
                 int e = 0;
                 for (; e < e_lo; ++e)
-                    __syncthreads();
+                    step_end(e);
                 for (; e <= e_hi; ++e) {
                     const int j = e - gi;
                     load(av, ad, full);
@@ -1122,10 +1252,10 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
                     const bool ok = wch && (unsigned)j < (unsigned)W;
                     *reinterpret_cast<f32x4 *>(sm + (ok ? wx0 + colx(j) : taddr)) = x;
                     addrs(ad, e + 1 - gi);
-                    __syncthreads();
+                    step_end(e);
                 }
                 for (; e < E; ++e)
-                    __syncthreads();
+                    step_end(e);
             };
             if (ngw == NG && !pl.compact)
                 run(std::true_type{}, std::true_type{});
@@ -1138,7 +1268,7 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
         } else {
             __syncthreads();
             for (int e = 0; e < E; ++e)
-                __syncthreads();
+                step_end(e);
         }
     }
 }
@@ -1180,6 +1310,8 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
             __syncthreads();
         }
     }
+    if constexpr ((MODE & kStream) != 0)
+        return;   // (the solution went out phase by phase)
     const Plan &p0 = lv.pl;   // the last level run
     const int HW0 = p0.H * p0.W, n0 = p0.C * HW0;
     float *dst = a.out + b * (size_t)n0;
@@ -1256,15 +1388,21 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
 
 // Inverse kernel instances, in groups of one workgroup size and one mode, by
 // quad groups per wave (1..kMaxGroups).  The host picks one by address.
-constexpr int kInverseGroups = 15;
-constexpr int kGroupThreads[kInverseGroups] = {256, 256, 256, 256, 256, 512, 512, 512,
-                                               512, 512, 1024, 1024, 1024, 1024, 1024};
-constexpr int kGroupModes[5] = {kCritGather, kCritRegs, kCritBoth, kCritGather | kOneLayer,
-                                kCritRegs | kOneLayer};
+constexpr int kInverseGroups = 18;
+constexpr int kModesPerSize = 6;
+constexpr int kGroupThreads[kInverseGroups] = {256, 256, 256, 256, 256, 256,
+                                               512, 512, 512, 512, 512, 512,
+                                               1024, 1024, 1024, 1024, 1024, 1024};
+constexpr int kGroupModes[kModesPerSize] = {kCritGather,
+                                            kCritRegs,
+                                            kCritBoth,
+                                            kCritGather | kOneLayer,
+                                            kCritRegs | kOneLayer,
+                                            kCritRegs | kOneLayer | kStream};
 constexpr int kGroupMode[kInverseGroups] = {
-    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4],
-    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4],
-    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4]};
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4], kGroupModes[5],
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4], kGroupModes[5],
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4], kGroupModes[5]};
 
 template <int MAXT, int MODE>
 const void *inverse_instance_of(int ng) {
@@ -1283,7 +1421,8 @@ const void *inverse_instance_of(int ng) {
 }  // namespace
 
 #define FINC_GROUPS(X) \
-    X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14)
+    X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) \
+    X(16) X(17)
 #define FINC_CAT2(a, b) a##b
 #define FINC_CAT(a, b) FINC_CAT2(a, b)
 
@@ -1715,22 +1854,61 @@ const void *inverse_instance(int threads, int mode, int ng) {
     static const void *(*const groups[kInverseGroups])(int) = {FINC_GROUPS(FINC_ENTRY)};
 #undef FINC_ENTRY
     int m = 2;   // kCritBoth stands for any other mode
-    for (int i = 0; i < 5; ++i)
+    for (int i = 0; i < kModesPerSize; ++i)
         if (kGroupModes[i] == mode)
             m = i;
     const int t = threads <= 256 ? 0 : threads <= 512 ? 1 : 2;
-    return groups[5 * t + m](ng);
+    return groups[kModesPerSize * t + m](ng);
+}
+
+// A single level of layers without actnorm whose image does not fit in LDS:
+// one stream-form launch per layer, in place on the output after the first
+// (each workgroup reads a pixel's input before it writes the pixel).
+int launch_streamed(const InvArgs &a, int B, hipStream_t stream) {
+    const Level &l0 = a.lv[0];
+    Plan p;
+    if (a.n_units * a.lpu < 1 || !make_plan(l0.pl.C, l0.pl.H, l0.pl.W, l0.pl.K, p, true))
+        return FINC_EUNSUPPORTED;
+    if (B == 0)
+        return FINC_OK;
+    const size_t lds = (size_t)p.lds_floats * sizeof(float);
+    int rc = check_lds(lds);
+    if (rc != FINC_OK)
+        return rc;
+    const int threads = p.NW * kWave;
+    const void *k = inverse_instance(threads, kCritRegs | kOneLayer | kStream, plan_groups(p));
+    if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+        hipSuccess)
+        (void)hipGetLastError();
+    for (int n = 0; n < a.n_units * a.lpu; ++n) {
+        const int u = a.n_units - 1 - n / a.lpu, q = a.lpu - 1 - n % a.lpu;
+        InvArgs s;
+        memset(&s, 0, sizeof(s));
+        s.L = s.n_units = s.lpu = 1;
+        s.corner0 = a.lpu == 1 ? a.corner0 : q;
+        s.out = a.out;
+        s.lv[0].z = n == 0 ? l0.z : a.out;
+        s.lv[0].prep = l0.prep + (size_t)(u * a.lpu + q) * p.lstride;
+        s.lv[0].pl = p;
+        void *args[] = {&s};
+        (void)hipLaunchKernel(k, dim3(B), dim3(threads), args, lds, stream);
+        rc = launched();
+        if (rc != FINC_OK)
+            return rc;
+    }
+    return FINC_OK;
 }
 
 int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     size_t lds = 0;
     int threads = 0;
     int rc = plan_inverse(a, &lds, &threads);
-    if (rc != FINC_OK)
-        return rc;
-    if (B == 0)
+    if (rc == FINC_OK && B == 0)
         return FINC_OK;
-    rc = check_lds(lds);
+    if (rc == FINC_OK)
+        rc = check_lds(lds);
+    if (rc == FINC_EUNSUPPORTED && a.L == 1 && !a.lv[0].scale && !a.split)
+        return launch_streamed(a, B, stream);   // the image does not fit in LDS
     if (rc != FINC_OK)
         return rc;
     int ng = 1, nreg = 0;

@@ -275,6 +275,37 @@ def test_large_images(orc, shape):
     assert_round_trip(host(xu), f64(x), "unit")
 
 
+@pytest.mark.parametrize("shape,corner", [((2, 2, 128, 128, 3), 0), ((1, 3, 16, 600, 3), 3),
+                                          ((2, 4, 40, 300, 2), 1), ((1, 2, 100, 130, 5), 2)],
+                         ids=lambda s: "x".join(map(str, s)) if isinstance(s, tuple) else str(s))
+def test_stream_images(orc, shape, corner):
+    """Images too large for LDS: the inverse streams them through column
+    rings (layer, in place, and the unit as four launches) -- against the
+    oracle."""
+    B, C, H, W, k = shape
+    print(f"stream B={B} C={C} H={H} W={W} k={k} corner={corner}", flush=True)
+    rng = np.random.default_rng(H * W + C)
+    x = rng.normal(size=(B, C, H, W))
+    K = synth.garbage_in_mask(synth.masked_kernel(C, k, corner, 31), corner)
+    Kd = dev(K)
+    y = finc.forward(dev(x), Kd, corner)
+    yh = host(y)
+    assert_close(yh, orc.forward(f64(x), f64(K), corner), "forward")
+    xr = finc.inverse(y, Kd, corner, out=poisoned(x.shape))
+    assert_close(host(xr), orc.inverse(yh, f64(K), corner), "inverse")
+    assert_round_trip(host(xr), f64(x), "layer")
+    z = rng.normal(size=x.shape)
+    zd = dev(z)
+    finc.inverse(zd, Kd, corner, out=zd)   # in place
+    assert_close(host(zd), orc.inverse(f64(z), f64(K), corner), "in-place inverse of z")
+    assert torch.equal(finc.inverse(y[-1:].contiguous(), Kd, corner)[0], xr[-1])
+    K4 = synth.unit_kernels(C, k, 8)
+    yu = orc.unit_forward(f64(x), f64(K4)).astype(np.float32)
+    xu = finc.unit_inverse(dev(yu), dev(K4), out=poisoned(x.shape))
+    assert_close(host(xu), orc.unit_inverse(f64(yu), f64(K4)), "unit inverse")
+    assert_round_trip(host(xu), f64(x), "unit", tol=1e-3)
+
+
 SPLIT_SHAPES = [
     # (B, C, H, W, k): quarters of 1 .. 16 channels, ragged sizes, k = 1 .. 5
     (2, 4, 5, 7, 3), (3, 8, 6, 4, 2), (2, 12, 13, 17, 3), (1, 16, 9, 6, 5), (2, 4, 3, 3, 1),

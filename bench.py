@@ -46,7 +46,7 @@ def parse():
     p.add_argument("--no-graph", action="store_true",
                    help="launch every step eagerly instead of replaying a HIP graph")
     p.add_argument("--no-configs", action="store_true",
-                   help="skip the per-configuration table (forward / inverse of every workload)")
+                   help="skip the per-configuration table (forward / inverse of every workload) and the scaling sweep")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                    help="only run a plain device copy of MIB MiB ten times (the known-size "
                         "reference for rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -250,6 +250,36 @@ def per_config(dev) -> list:
     return rows
 
 
+def scaling_sweep(dev) -> dict:
+    """Unit inverse (four layers, prepared weights) at C = 2, k = 3 over image
+    sizes and batches, after the paper's sampling-time sweep (Sec. 5, Fig. 3)."""
+    import numpy as np
+    import torch
+
+    from paper_2301_09266_amd import finc, synth
+
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    rows = []
+    for n in synth.SWEEP_SIZES:
+        for B in synth.SWEEP_BATCHES:
+            c = synth.sweep_case(n, B)
+            x, K4 = d(c["x"]), d(c["K4"])
+            y = x
+            for q in range(4):   # the unit's layers one by one (any image size)
+                y = finc.forward(y, K4[q].contiguous(), q)
+            prep = finc.prepare(K4, [0, 1, 2, 3])
+            out = torch.empty_like(x)
+            finc.unit_inverse_prepared(y, prep, c["k"], out=out)
+            err = float((out - x).abs().max())
+            per = 20 if n <= 32 else 5
+            us = graph_time_us(lambda: finc.unit_inverse_prepared(y, prep, c["k"], out=out), 3, per)
+            rows.append({"n": n, "B": B, "unit_inverse_us": us, "images_per_s": B / (us * 1e-6),
+                         "us_per_diagonal_step": us / (4 * (2 * n - 1)),
+                         "round_trip_max_abs": err})
+    return {"what": "FInC unit inverse (TL, TR, BL, BR), C = 2, k = 3, n x n images",
+            "rows": rows}
+
+
 def cpu_baseline(step, seconds: float):
     """The oracle, single-threaded, on whole batches of the same step until
     `seconds` of CPU time have been spent (at least one image)."""
@@ -403,6 +433,7 @@ def main():
     }
     if not args.no_configs:
         out["per_config"] = per_config(dev)
+        out["scaling_sweep"] = scaling_sweep(dev)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(st, args.cpu_seconds)
     print(json.dumps(out))

@@ -179,6 +179,17 @@ WORKLOADS = {
 }
 
 
+# Scaling sweep after the paper's sampling-time study (Sec. 5, Fig. 3): one
+# FInC unit at C = 2, k = 3, square images of 16 .. 128 pixels a side,
+# batches of 1 .. 128 (the larger images exceed LDS and stream).
+SWEEP_SIZES = (16, 32, 64, 128)
+SWEEP_BATCHES = (1, 8, 32, 128)
+
+
+def sweep_case(n: int, B: int, C: int = 2, k: int = 3, seed: int = 0) -> dict:
+    return unit_case(B, C, n, n, k, seed)
+
+
 def make(name: str, **override) -> dict:
     spec = dict(WORKLOADS[name])
     spec.update(override)

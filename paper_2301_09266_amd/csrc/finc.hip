@@ -1765,9 +1765,14 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B) {
     p.n = n;
     p.corner0 = corner0;
     if (n == 1) {
-        p.RB = imax(1, imin(H, ceil_div(64, W)));
-        while (p.RB > 1 && (long long)B * ceil_div(H, p.RB) < 512)
-            p.RB /= 2;
+        // row blocks of about 64 pixels, halved while the grid has fewer than
+        // 512 blocks, but never below a full 16-pixel tile: every block
+        // stages all of the layer's weights, so a block with a part-empty
+        // tile pays that in full for less work
+        const int rb_min = imin(H, ceil_div(16, W));
+        p.RB = imax(rb_min, imin(H, ceil_div(64, W)));
+        while (p.RB > rb_min && (long long)B * ceil_div(H, p.RB) < 512)
+            p.RB = imax(rb_min, p.RB / 2);
     } else {
         p.RB = H;
     }

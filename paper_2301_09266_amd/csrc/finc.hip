@@ -793,12 +793,14 @@ __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm
 // All layers of one level for one wave (NG quad groups).  Weights of the
 // next layer are fetched into registers while the current one runs.
 template <int NG, int MAXT, int MODE>
-__device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const Plan &up,
-                            const Plan &pl, const Role &r, float *sm, size_t b) {
+__device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, const Level &lv,
+                                                           bool top, const Plan &up,
+                                                           const Plan &pl, const Role &r,
+                                                           float *sm, size_t b) {
     constexpr int G = NG > 0 ? NG : 1;
     // weights of the next layer prefetched into registers when they fit (with
     // 16 waves a lane has 128 registers)
-    constexpr bool kPrefetch = NG <= 4 && MAXT <= 512;
+    constexpr bool kPrefetch = NG <= 4 && (MAXT <= 512 || NG <= 2);
     constexpr int GN = kPrefetch ? G : 1;
     // the register-fed critical wave owns the two dp + dq = 1 taps as groups
     // (MODE: kCritGather / kCritRegs / kCritBoth -- the instance carries only
@@ -1273,6 +1275,27 @@ __device__ void level_waves(const InvArgs &a, const Level &lv, bool top, const P
     }
 }
 
+// A wave of a multi-level chain runs the level loop compiled for its own
+// quad-group count at that level (G = the first count >= ng): a level whose
+// waves own fewer groups than the chain's widest level then runs as it does
+// on its own, without per-group tests and with the weight prefetch.  Every
+// variant passes the same barriers, so the waves of one workgroup may run
+// different ones.
+template <int G, int NG, int MAXT, int MODE>
+__device__ __attribute__((always_inline)) void level_waves_for(int ng, const InvArgs &a, const Level &lv, bool top,
+                                const Plan &up, const Plan &pl, const Role &r, float *sm,
+                                size_t b) {
+    if constexpr (G < NG) {
+        if (ng <= G) {
+            level_waves<G, MAXT, MODE>(a, lv, top, up, pl, r, sm, b);
+            return;
+        }
+        level_waves_for<G + 1, NG, MAXT, MODE>(ng, a, lv, top, up, pl, r, sm, b);
+    } else {
+        level_waves<NG, MAXT, MODE>(a, lv, top, up, pl, r, sm, b);
+    }
+}
+
 // Inverse of a whole chain with the image in LDS from the first load to the
 // last store.  Levels run in argument order (the top of a stack first);
 // between levels the solution of the level above is unsqueezed and the
@@ -1300,7 +1323,12 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
         const Plan &pl = lv.pl;
         const int CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
         float *Y = sm + pl.offY;
-        level_waves<NG, MAXT, MODE>(a, lv, i == 0, above, pl, role_of(a, i), sm, b);
+        if constexpr (!kOne && MAXT == 1024) {   // (chains whose levels differ most)
+            const Role r = role_of(a, i);
+            level_waves_for<1, NG, MAXT, MODE>(r.ng, a, lv, i == 0, above, pl, r, sm, b);
+        } else {
+            level_waves<NG, MAXT, MODE>(a, lv, i == 0, above, pl, role_of(a, i), sm, b);
+        }
         if (!kOne && a.n_units * a.lpu == 0) {   // no layers at this level: the input passes through
             for (int idx = threadIdx.x; idx < HW * CP; idx += blockDim.x) {
                 const int p = fdiv(idx, pl.d_CP), c = idx - p * CP;

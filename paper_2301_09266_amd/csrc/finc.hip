@@ -1505,6 +1505,7 @@ struct FwdArgs {
 };
 
 constexpr int kFwdThreads = 256;
+constexpr int kFwdMinBlocks = 256;   // a block per compute unit of the chip
 constexpr int kNoQuad = 1 << 30;   // quad offset marker: padding quad (zero weights)
 
 __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
@@ -1793,13 +1794,13 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B) {
     p.n = n;
     p.corner0 = corner0;
     if (n == 1) {
-        // row blocks of about 64 pixels, halved while the grid has fewer than
-        // 512 blocks, but never below a full 16-pixel tile: every block
-        // stages all of the layer's weights, so a block with a part-empty
-        // tile pays that in full for less work
+        // row blocks of about 128 pixels (a wave per 16-pixel tile), halved
+        // while the grid has fewer blocks than the chip has compute units, but
+        // never below a full tile: every block stages all of the layer's
+        // weights, so more and smaller blocks pay that again for less work
         const int rb_min = imin(H, ceil_div(16, W));
-        p.RB = imax(rb_min, imin(H, ceil_div(64, W)));
-        while (p.RB > rb_min && (long long)B * ceil_div(H, p.RB) < 512)
+        p.RB = imax(rb_min, imin(H, ceil_div(128, W)));
+        while (p.RB > rb_min && (long long)B * ceil_div(H, p.RB) < kFwdMinBlocks)
             p.RB = imax(rb_min, p.RB / 2);
     } else {
         p.RB = H;

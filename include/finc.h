@@ -176,7 +176,11 @@ int finc_split_inverse_prepared(const float *y, float *x, const void *prepared4,
  * the level's latent as the second half of the channels.
  *   z: host array of L device pointers; z[l] for l < L-1 is (B, C_l/2, H_l,
  *      W_l), z[L-1] is (B, C_{L-1}, H_{L-1}, W_{L-1}).
- *   x: device (B, C1, H1, W1) output.
+ *   x: device (B, C1, H1, W1) output.  When the levels need different
+ *      kernel instances they run as one launch each, and x also carries the
+ *      hand-over between them (each image's block of x holds the upper
+ *      levels' solutions until level 0 overwrites it): its contents are
+ *      undefined until the call's work on `stream` has finished.
  *   K: device, for l, u, block q (TL, TR, BL, BR): C_l*C_l*k*k floats each.
  *   scale, bias: device, for l, u: C_l floats each (scale must be nonzero).
  *   workspace: device, >= finc_stack_workspace_bytes(L, U, C1, k) bytes,

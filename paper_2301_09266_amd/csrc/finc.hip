@@ -545,6 +545,12 @@ struct InvArgs {
     // (the last level's W a multiple of 4, out 16-byte aligned)
     int vec;
     float *out;           // output of the last level: (B, C, H, W)
+    int out_stride;       // floats from one image's output to the next (C H W when packed)
+    // hin (chains that start below the top of a stack): the first level's
+    // input is concat(unsqueeze(h), z), h being the level above's solution,
+    // (2C, H/2, W/2) per image, hin_stride floats apart
+    const float *hin;
+    int hin_stride;
     Level lv[kMaxLevels]; // in the order they run
 };
 static_assert(sizeof(InvArgs) <= 4096, "kernel arguments are limited to 4 KB");
@@ -751,9 +757,9 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
 // the solution buffer (with its zero border) and the zero block are cleared.
 // `work` (register-only set-up) runs while the top level's input is on its
 // way.
-template <typename F>
+template <bool HIN, typename F>
 __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm, size_t b,
-                            bool vec4, F work) {
+                            bool vec4, const float *hin, int hin_stride, F work) {
     const Plan &pl = lv.pl;
     const int C = pl.C, CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
     float *Y = sm + pl.offY;
@@ -761,7 +767,43 @@ __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm
         zero_floats(sm + pl.offX, pl.offY - pl.offX);
         zero_floats(sm + pl.offR, pl.offZ + 256 - pl.offR);   // (Z stays 0)
     };
-    if (top) {
+    if (HIN && top && hin) {
+        // the level above ran in a launch of its own: its solution comes from
+        // HBM, unsqueezed (channel c < C/2 of pixel (i, j) is channel
+        // 4c + 2(i&1) + (j&1) of h at (i/2, j/2)), the latent behind it.
+        // All loads of a round in flight before its LDS stores.
+        work();
+        clear();
+        const int Ch = C / 2, Wu = W / 2, HWu = (pl.H / 2) * Wu, total = CP * HW;
+        const float *hb = hin + b * (size_t)hin_stride;
+        const float *lat = lv.z + b * (size_t)Ch * HW;
+        constexpr int U = 8;
+        for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
+            float v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int idx = imin(base + u * blockDim.x, total - 1);
+                const int c = fdiv(idx, pl.d_HW), p = idx - c * HW;
+                const int i = fdiv(p, pl.d_W), j = p - i * W;
+                const float *src =
+                    c < Ch ? hb + (size_t)(4 * c + 2 * (i & 1) + (j & 1)) * HWu + (i >> 1) * Wu +
+                                 (j >> 1)
+                           : lat + (size_t)imin(c - Ch, Ch - 1) * HW + p;
+                v[u] = *src;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                pin(v[u]);
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int idx = base + u * blockDim.x;
+                if (idx < total) {
+                    const int c = fdiv(idx, pl.d_HW), p = idx - c * HW;
+                    Y[p * CP + c] = c < C ? v[u] : 0.0f;
+                }
+            }
+        }
+    } else if (top) {
         // the solution buffer and the partial tiles are cleared while the
         // image is on its way
         load_input(sm, pl, lv.z + b * (size_t)C * HW, vec4, [&] {
@@ -946,7 +988,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
         sissue(1 + kPhase);
         __syncthreads();
     } else {
-        level_input(lv, top, up, sm, b, (a.vec & 1) != 0, decode);
+        level_input<!kOne>(lv, top, up, sm, b, (a.vec & 1) != 0, a.hin, a.hin_stride, decode);
     }
     for (int n = 0; n < nlayers; ++n) {
         const int u = kOne ? 0 : a.n_units - 1 - n / a.lpu, q = kOne ? 0 : a.lpu - 1 - n % a.lpu;
@@ -1342,7 +1384,7 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
         return;   // (the solution went out phase by phase)
     const Plan &p0 = lv.pl;   // the last level run
     const int HW0 = p0.H * p0.W, n0 = p0.C * HW0;
-    float *dst = a.out + b * (size_t)n0;
+    float *dst = a.out + b * (size_t)a.out_stride;
     // With vec bit 1, a thread takes four pixels of a row by one
     // channel quad: four 16-byte LDS reads, one per pixel, transposed in
     // registers into four 16-byte stores, one per channel, coalesced across
@@ -1954,8 +1996,11 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     int mode = nreg == a.L ? kCritRegs : nreg == 0 ? kCritGather : kCritBoth;
     {
         const Plan &top = a.lv[0].pl, &last = a.lv[a.L - 1].pl;
+        if (a.out_stride == 0)
+            a.out_stride = last.C * last.H * last.W;
         const bool in4 = (top.H * top.W) % 4 == 0 && ((uintptr_t)a.lv[0].z & 15u) == 0;
-        const bool out4 = last.W % 4 == 0 && ((uintptr_t)a.out & 15u) == 0;
+        const bool out4 =
+            last.W % 4 == 0 && ((uintptr_t)a.out & 15u) == 0 && a.out_stride % 4 == 0;
         a.vec = (in4 ? 1 : 0) | (out4 ? 2 : 0);
     }
     if (a.L == 1 && a.n_units * a.lpu == 1 && !a.lv[0].scale)
@@ -1967,6 +2012,22 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     void *args[] = {&a};
     (void)hipLaunchKernel(k, dim3(B), dim3(threads), args, lds, stream);
     return launched();
+}
+
+// true if the levels of a chain would each pick a different kernel instance
+// than the chain as a whole (work split, quad groups or critical form)
+bool levels_differ(const InvArgs &a) {
+    Plan p0;
+    for (int l = 0; l < a.L; ++l) {
+        Plan p = a.lv[l].pl;
+        if (!make_plan(p.C, p.H, p.W, p.K, p))
+            return false;   // (the chain launch reports it)
+        if (l == 0)
+            p0 = p;
+        else if (p.NW != p0.NW || plan_groups(p) != plan_groups(p0) || p.regcrit != p0.regcrit)
+            return true;
+    }
+    return false;
 }
 
 // Channels up to which the forward launch also prepares the inverse's
@@ -2407,7 +2468,38 @@ int finc_stack_inverse_prepared(const float *const *z, float *x, const void *pre
     a.n_units = U;
     a.lpu = 4;
     a.corner0 = FINC_TL;
-    return launch_inverse_chain(a, B, stream);
+    if (!levels_differ(a))
+        return launch_inverse_chain(a, B, stream);
+    // Levels whose kernel instances differ (work split, quad groups or
+    // critical form) run as launches of their own, each in its own instance:
+    // one instance for all would be sized for the widest level and run the
+    // others slower.  The hand-over goes through x, image by image: with
+    // N = C1 H1 W1 floats per image, level l > 0 writes its solution to
+    // [N / 2^l, N / 2^(l-1)) of its image's block and level 0 to all of it;
+    // level l reads the level above's from [N / 2^(l+1), N / 2^l).  A level
+    // reads only its own image's block and loads all of its input before its
+    // first store, so no region is overwritten while another reads it.
+    const int N = C1 * H1 * W1;
+    for (int i = 0; i < L; ++i) {   // top first
+        const int l = L - 1 - i;
+        InvArgs s;
+        memset(&s, 0, sizeof(s));
+        s.lv[0] = a.lv[i];
+        s.L = 1;
+        s.n_units = U;
+        s.lpu = 4;
+        s.corner0 = FINC_TL;
+        s.out = x + (l == 0 ? 0 : N >> l);
+        s.out_stride = N;
+        if (i > 0) {
+            s.hin = x + (N >> (l + 1));
+            s.hin_stride = N;
+        }
+        const int rc = launch_inverse_chain(s, B, stream);
+        if (rc != FINC_OK)
+            return rc;
+    }
+    return FINC_OK;
 }
 
 int finc_stack_inverse(const float *const *z, float *x, const float *K, const float *scale,

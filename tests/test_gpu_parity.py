@@ -391,6 +391,29 @@ def test_stack_small(orc):
     assert_close(host(x), want, "small stack")
 
 
+def test_stack_levels_in_own_launches(orc):
+    """Small stack whose levels need different kernel instances (12, 24 and
+    48 channels: one, two and three channel tiles), so each level runs in a
+    launch of its own and hands its solution to the next through the output
+    tensor: per image max|gpu - oracle| / max(1, max|oracle|) <= 1e-4 (the
+    stack workload's criterion), and each image independent of the batch."""
+    c = synth.stack_case(B=3, C1=12, H1=16, W1=16, levels=3, units=2, k=3)
+    Kf, sf, bf = _stack_flat(c)
+    zd = [dev(z) for z in c["z"]]
+    args = (dev(Kf), dev(sf), dev(bf), 3, 2, 12, 16, 16, 3)
+    x = finc.stack_inverse(zd, *args, out=poisoned((3, 12, 16, 16)))
+    want = orc.stack_inverse([f64(z) for z in c["z"]], [f64(a) for a in c["K"]],
+                             [f64(a) for a in c["scale"]], [f64(a) for a in c["bias"]],
+                             3, 2, 3, 12, 16, 16)
+    xh = host(x)
+    assert np.isfinite(xh).all()
+    for b in range(3):
+        err = np.max(np.abs(xh[b] - want[b])) / max(1.0, np.max(np.abs(want[b])))
+        assert err <= TOL, f"image {b}: inf-norm relative error {err:.3e}"
+    one = finc.stack_inverse([z[2:3].contiguous() for z in zd], *args)
+    assert torch.equal(one[0], x[2])
+
+
 def test_stack_workload(orc):
     """Three levels of eight units (12x32x32 -> 24x16x16 -> 48x8x8), batch 64:
     the oracle runs on four sampled images (results do not depend on the

@@ -313,6 +313,23 @@ SPLIT_SHAPES = [
 ]
 
 
+def test_unsupported_shapes_rejected():
+    """Shapes beyond what a workgroup can hold are rejected before any launch
+    with FINC_EUNSUPPORTED, the output untouched: 8 channels at 128 x 128
+    (the stream form's phase input exceeds its prefetch registers) and 129
+    rows (more row tiles than a workgroup has waves)."""
+    for C, H, W in [(8, 128, 128), (2, 129, 16)]:
+        K = dev(synth.masked_kernel(C, 3, 0, 1000))
+        prep = finc.prepare(K, [0])
+        y = torch.zeros((1, C, H, W), dtype=torch.float32, device=DEV)
+        out = poisoned((1, C, H, W))
+        with pytest.raises(finc.FincError) as err:
+            finc.inverse_prepared(y, prep, 3, 0, out=out)
+        assert err.value.code == finc.EUNSUPPORTED, (C, H, W)
+        torch.cuda.synchronize()
+        assert torch.isnan(out).all(), (C, H, W)
+
+
 @pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda s: "x".join(map(str, s)))
 def test_split_unit(orc, shape):
     """Channel-split unit (Sec. 4.3, Alg. 2): forward, log|det|, inverse and the

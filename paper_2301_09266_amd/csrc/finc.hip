@@ -1817,8 +1817,8 @@ int plan_inverse(InvArgs &a, size_t *lds_bytes, int *threads) {
 }
 
 // Work split and LDS layout of a forward launch: n = 1 splits each image into
-// blocks of rows (about 4 pixel tiles a block, and at least ~512 blocks when
-// the batch allows); a unit (n = 4) keeps whole images.
+// blocks of rows (up to eight 16-pixel tiles a block, and a block per compute
+// unit when the batch allows); a unit (n = 4) keeps whole images.
 FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B) {
     FwdPlan p;
     memset(&p, 0, sizeof(p));
@@ -1836,10 +1836,11 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B) {
     p.n = n;
     p.corner0 = corner0;
     if (n == 1) {
-        // row blocks of about 128 pixels (a wave per 16-pixel tile), halved
-        // while the grid has fewer blocks than the chip has compute units, but
-        // never below a full tile: every block stages all of the layer's
-        // weights, so more and smaller blocks pay that again for less work
+        // row blocks of about 128 pixels (eight 16-pixel tiles, two a wave),
+        // halved while the grid has fewer blocks than the chip has compute
+        // units, but never below a full tile: every block stages all of the
+        // layer's weights, so more and smaller blocks pay that again for less
+        // work
         const int rb_min = imin(H, ceil_div(16, W));
         p.RB = imax(rb_min, imin(H, ceil_div(128, W)));
         while (p.RB > rb_min && (long long)B * ceil_div(H, p.RB) < kFwdMinBlocks)

@@ -119,8 +119,11 @@ int finc_inverse_prepared(const float *y, float *x, const void *prepared, int B,
  * other; the inverse runs BR^-1, BL^-1, TR^-1, TL^-1 in one launch, as
  * Algorithm 2 inverts a whole unit at once.)  K4: device, 4 consecutive OIHW
  * tensors in the order TL, TR, BL, BR.  Activations stay in on-chip memory
- * between the four blocks.  finc_unit_forward allows x == y (each image is
- * read whole before it is written); the inverse's rules are as for one block.
+ * between the four blocks (a batch smaller than the GPU's compute units is
+ * split into bands of rows, each band recomputing the rows its neighbours'
+ * later blocks read).  finc_unit_forward allows x == y (then each image is
+ * one band, read whole before it is written); the inverse's rules are as for
+ * one block.
  * logdet (finc_unit_forward): NULL, or device double for the unit's log|det|;
  * prepared4: NULL, or device buffer of finc_workspace_bytes(C, k, 4) bytes
  * (rules as for finc_forward) for finc_unit_inverse_prepared.

@@ -1523,6 +1523,7 @@ struct FwdPlan {
     int C, CP, H, W, K, P, WP;
     int NT, ncq, nq, NG;         // channel tiles, quads per tile (all taps), quad groups
     int RB, nblk;                // rows per block, blocks per image
+    int HB;                      // halo rows staged above and below a block
     int offI, offO, offW, offD;  // LDS floats: input rows (RB + 2P) x WP x CP, output
                                  // (chains only), weight fragments, quad offsets (ints)
     int lds_floats;
@@ -1574,15 +1575,14 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     const int b = bid / fp.nblk, blk = bid - b * fp.nblk;
     const int corner0 = a.split ? (b & 3) : fp.corner0;   // this block's (first) corner
     const float *Kb = a.K + (a.split ? (size_t)(b & 3) * fp.C * fp.C * fp.K * fp.K : 0);
-    const int i0 = blk * fp.RB, rb = imin(H, i0 + fp.RB) - i0;
-    const int npix = rb * W, ntile = ceil_div(npix, 16), nitem = ntile * fp.NT;
+    const int i0 = blk * fp.RB, rb = imin(H, i0 + fp.RB) - i0, HB = fp.HB;
     float *X = sm + fp.offI;
     float4 *Wf = reinterpret_cast<float4 *>(sm + fp.offW);
     int *Dq = reinterpret_cast<int *>(sm + fp.offD);
     const size_t HW = (size_t)H * W;
     const float *xb = a.in + (size_t)b * C * HW;
     float *yb = a.out + (size_t)b * C * HW;
-    // zero-bordered input rows i0 - P .. i0 + rb + P - 1: every element of
+    // zero-bordered input rows i0 - HB .. i0 + rb + HB - 1: every element of
     // the block is written once, with x where the taps of this launch read
     // the image and zero elsewhere (outside the image, padding channels, and
     // for a single layer the halo side its corner never reads).  Loads are
@@ -1590,9 +1590,9 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     {
         int oh0, ow0;
         self_tap(corner0, K, oh0, ow0);
-        const int up = fp.n == 1 ? oh0 : P, down = fp.n == 1 ? P - oh0 : P;
+        const int up = fp.n == 1 ? oh0 : HB, down = fp.n == 1 ? P - oh0 : HB;
         const int lo = imax(0, i0 - up), hi = imin(H, i0 + rb + down);   // rows read
-        const int nrow = rb + 2 * P, plane = nrow * WP, total = CP * plane;
+        const int nrow = rb + 2 * HB, plane = nrow * WP, total = CP * plane;
         const FastDiv dpl = blk == fp.nblk - 1 ? fp.d_plane_last : fp.d_plane;
         constexpr int U = 8;
         for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
@@ -1604,7 +1604,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
                 const int idx = base + u * blockDim.x;
                 const int c = fdiv(idx, dpl), rem = idx - c * plane;
                 const int pr = fdiv(rem, fp.d_WP), pc = rem - pr * WP;
-                const int i = i0 - P + pr, j = pc - P;
+                const int i = i0 - HB + pr, j = pc - P;
                 inb[u] = idx < total && c < C && i >= lo && i < hi && j >= 0 && j < W;
                 v[u] = xb[inb[u] ? c * HW + (size_t)i * W + j : 0];
                 dst[u] = idx < total ? rem * CP + c : -1;
@@ -1713,13 +1713,24 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         }
         const bool last = q == fp.n - 1;
         float *Yo = sm + fp.offO;
+        // rows of this layer's output the block computes, rlo .. rhi - 1: its
+        // own, and in a band of a unit also those its later layers read
+        // (TL: k-1 above for TR; TL, TR: 2(k-1) below for BL and BR; BL:
+        // k-1 below for BR), within the image
+        int rlo = i0, rhi = i0 + rb;
+        if (fp.n > 1 && fp.nblk > 1) {
+            rlo = imax(0, i0 - (q == 0 ? P : 0));
+            rhi = imin(H, i0 + rb + (q < 2 ? 2 * P : q == 2 ? P : 0));
+        }
+        const int npix = (rhi - rlo) * W, nitem = ceil_div(npix, 16) * fp.NT;
+        const int xrow = rlo - i0 + HB;   // staged row of output row rlo
         for (int item = wave; item < nitem; item += nwaves) {
             const int tile = fdiv(item, fp.d_NT), nt = item - tile * fp.NT;
             const int p = tile * 16 + li;
             const bool valid = p < npix;
             const int pc = valid ? p : 0;
             const int il = fdiv(pc, fp.d_W), j = pc - il * W;
-            const int base = ((il + P) * WP + j + P) * CP;
+            const int base = ((il + xrow) * WP + j + P) * CP;
             const int zaddr = fp.offW;   // any valid address: its products meet zero weights
             // four accumulators over the quad groups (group g -> g mod 4), joined
             // pairwise: the rounding chain is a quarter as long as a single one
@@ -1750,7 +1761,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
 #pragma unroll
                     for (int r = 0; r < 4; ++r)
                         if (co0 + r < C)
-                            yb[(co0 + r) * HW + (size_t)(i0 + il) * W + j] = acc[r];
+                            yb[(co0 + r) * HW + (size_t)(rlo + il) * W + j] = acc[r];
                 }
             } else if (valid && co0 < CP) {
                 *reinterpret_cast<f32x4 *>(Yo + (size_t)p * CP + co0) = acc;
@@ -1761,7 +1772,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
             for (int idx = threadIdx.x; idx < npix * CP / 4; idx += blockDim.x) {
                 const int p = fdiv(idx, fp.d_cp4), c4 = idx - p * (CP / 4);
                 const int il = fdiv(p, fp.d_W), j = p - il * W;
-                reinterpret_cast<float4 *>(X)[((il + P) * WP + j + P) * (CP / 4) + c4] =
+                reinterpret_cast<float4 *>(X)[((il + xrow) * WP + j + P) * (CP / 4) + c4] =
                     reinterpret_cast<const float4 *>(Yo)[idx];
             }
             __syncthreads();
@@ -1819,7 +1830,9 @@ int plan_inverse(InvArgs &a, size_t *lds_bytes, int *threads) {
 // Work split and LDS layout of a forward launch: n = 1 splits each image into
 // blocks of rows (up to eight 16-pixel tiles a block, and a block per compute
 // unit when the batch allows); a unit (n = 4) keeps whole images.
-FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B) {
+// whole: a unit keeps whole images (in place: an image must be read whole
+// before any of it is written).
+FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B, bool whole) {
     FwdPlan p;
     memset(&p, 0, sizeof(p));
     p.C = C;
@@ -1846,17 +1859,25 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B) {
         while (p.RB > rb_min && (long long)B * ceil_div(H, p.RB) < kFwdMinBlocks)
             p.RB = imax(rb_min, p.RB / 2);
     } else {
+        // a unit keeps whole images, or, with fewer of them than compute
+        // units, bands of rows: TL and TR read k-1 rows up, BL and BR k-1
+        // rows down, so a band stages 2(k-1) rows each side and each layer
+        // also computes the rows of the halo its later layers read
+        const int rb_min = imin(H, imax(ceil_div(16, W), 2 * p.P));
         p.RB = H;
+        while (!whole && p.RB > rb_min && (long long)B * ceil_div(H, p.RB) < kFwdMinBlocks)
+            p.RB = imax(rb_min, p.RB / 2);
     }
     p.nblk = ceil_div(H, p.RB);
+    p.HB = n > 1 && p.nblk > 1 ? 2 * p.P : p.P;
     p.offI = 0;
-    p.offO = (p.RB + 2 * p.P) * p.WP * p.CP;
-    p.offW = p.offO + (n > 1 ? H * W * p.CP : 0);
+    p.offO = (p.RB + 2 * p.HB) * p.WP * p.CP;
+    p.offW = p.offO + (n > 1 ? imin(H, p.RB + 3 * p.P) * W * p.CP : 0);
     p.offD = p.offW + p.NT * p.NG * 256;
     p.lds_floats = p.offD + round_up4(4 * p.NG);
     const int rb_last = H - (p.nblk - 1) * p.RB;
-    p.d_plane = make_fastdiv((p.RB + 2 * p.P) * p.WP);
-    p.d_plane_last = make_fastdiv((rb_last + 2 * p.P) * p.WP);
+    p.d_plane = make_fastdiv((p.RB + 2 * p.HB) * p.WP);
+    p.d_plane_last = make_fastdiv((rb_last + 2 * p.HB) * p.WP);
     p.d_WP = make_fastdiv(p.WP);
     p.d_NG = make_fastdiv(p.NG);
     p.d_ncq = make_fastdiv(p.ncq);
@@ -2048,7 +2069,7 @@ int launch_forward(const float *x, float *y, const float *K, double *logdet, flo
     a.K = K;
     a.logdet = logdet;
     a.split = split;
-    a.fp = make_fwd_plan(C, H, W, k, n, corner0, B);
+    a.fp = make_fwd_plan(C, H, W, k, n, corner0, B, x == y);
     if (B == 0)
         return FINC_OK;
     const int nprep = split ? 4 : n;

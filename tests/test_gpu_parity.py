@@ -313,6 +313,23 @@ SPLIT_SHAPES = [
 ]
 
 
+@pytest.mark.parametrize("shape", [(3, 5, 37, 9, 3), (2, 12, 24, 20, 5), (1, 3, 9, 40, 2)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_unit_forward_bands(orc, shape):
+    """Unit forward of a batch smaller than the compute units: images split
+    into bands of rows, each recomputing the rows its neighbours' later
+    layers read, the last band ragged.  Against the oracle elementwise, and
+    in place (then whole images) bit for bit the same."""
+    B, C, H, W, k = shape
+    c = synth.unit_case(B, C, H, W, k)
+    x, K4 = c["x"], c["K4"]
+    y = finc.unit_forward(dev(x), dev(K4), out=poisoned(x.shape))
+    assert_close(host(y), orc.unit_forward(f64(x), f64(K4)), f"unit forward {shape}")
+    inplace = dev(x)
+    finc.unit_forward(inplace, dev(K4), out=inplace)
+    assert torch.equal(inplace, y)
+
+
 def test_unsupported_shapes_rejected():
     """Shapes beyond what a workgroup can hold are rejected before any launch
     with FINC_EUNSUPPORTED, the output untouched: 8 channels at 128 x 128

@@ -46,6 +46,7 @@ def load(path: str = LIB):
         "orc_forward": [_dp, _dp, _dp, L, I, I, I, I, I],
         "orc_inverse": [_dp, _dp, _dp, L, I, I, I, I, I],
         "orc_logdet": [_dp, I, I, I, I, I, _dp],
+        "orc_backward": [_dp, _dp, _dp, _dp, _dp, ctypes.c_double, L, I, I, I, I, I],
         "orc_unit_forward": [_dp, _dp, _dp, L, I, I, I, I],
         "orc_unit_inverse": [_dp, _dp, _dp, L, I, I, I, I],
         "orc_unit_logdet": [_dp, I, I, I, I, _dp],
@@ -113,6 +114,15 @@ class Oracle:
         _check(self.lib.orc_logdet(_p(K), K.shape[0], K.shape[-1], corner, H, W, _p(out)),
                allow_singular)
         return float(out[0])
+
+    def backward(self, x, dy, K, corner: int, gld: float = 0.0):
+        """(dx, dK) of one layer for the loss gradient dy (see orc_backward)."""
+        x, dy, K = _c(x), _c(dy), _c(K)
+        B, C, H, W = x.shape
+        dx, dK = np.empty_like(x), np.empty_like(K)
+        _check(self.lib.orc_backward(_p(x), _p(dy), _p(K), _p(dx), _p(dK), float(gld), B, C,
+                                     H, W, K.shape[-1], corner))
+        return dx, dK
 
     def unit_forward(self, x, K4) -> np.ndarray:
         x, K4 = _c(x), _c(K4)

@@ -493,3 +493,66 @@ int orc_stack_inverse(const double *const *z, double *x, const double *K,
     free(t);
     return rc;
 }
+
+/* Backward of one layer, for training on the negative log-likelihood (Sec. 2
+ * NLL equation; Sec. 6 training details).  Given x and dy = dL/dy for
+ * y = layer(x):
+ *   dx = J^T dy: every output gradient dy[co,i,j] is sent back along each tap
+ *        to the input pixel that tap read, with the weight the layer used;
+ *   dK[co,ci,a,b] = sum over images and output pixels of dy[co,i,j] times the
+ *        input the tap read (zero outside the image); the masked entries (self
+ *        tap, ci > co) get 0 -- the paper resets their gradients to zero after
+ *        every training step -- and the self diagonal also gets
+ *        gld * H * W / K[c,c,self], the gradient of gld * log|det|.
+ * dx or dK may be NULL (not computed). */
+int orc_backward(const double *x, const double *dy, const double *K, double *dx,
+                 double *dK, double gld, long B, int C, int H, int W, int k,
+                 int corner)
+{
+    if (bad_shape(B, C, H, W, k, corner) || !x || !dy || !K)
+        return ORC_EINVAL;
+    int oh, ow;
+    corner_offsets(corner, k, &oh, &ow);
+    const long plane = (long)H * W, img = (long)C * plane;
+    if (dx) {
+        for (long e = 0; e < B * img; ++e)
+            dx[e] = 0.0;
+        for (long n = 0; n < B; ++n)
+            for (int co = 0; co < C; ++co)
+                for (int i = 0; i < H; ++i)
+                    for (int j = 0; j < W; ++j) {
+                        const double g = dy[n * img + co * plane + (long)i * W + j];
+                        for (int ci = 0; ci < C; ++ci)
+                            for (int a = 0; a < k; ++a)
+                                for (int b = 0; b < k; ++b) {
+                                    int ii = i + a - oh, jj = j + b - ow;
+                                    if (ii < 0 || ii >= H || jj < 0 || jj >= W)
+                                        continue;
+                                    dx[n * img + ci * plane + (long)ii * W + jj] +=
+                                        kmasked(K, C, k, oh, ow, co, ci, a, b) * g;
+                                }
+                    }
+    }
+    if (dK) {
+        for (int co = 0; co < C; ++co)
+            for (int ci = 0; ci < C; ++ci)
+                for (int a = 0; a < k; ++a)
+                    for (int b = 0; b < k; ++b) {
+                        double s = 0.0;
+                        if (!(a == oh && b == ow && ci > co))
+                            for (long n = 0; n < B; ++n)
+                                for (int i = 0; i < H; ++i)
+                                    for (int j = 0; j < W; ++j) {
+                                        int ii = i + a - oh, jj = j + b - ow;
+                                        if (ii < 0 || ii >= H || jj < 0 || jj >= W)
+                                            continue;
+                                        s += dy[n * img + co * plane + (long)i * W + j] *
+                                             x[n * img + ci * plane + (long)ii * W + jj];
+                                    }
+                        if (a == oh && b == ow && ci == co)
+                            s += gld * (double)H * (double)W / kw(K, C, k, co, co, a, b);
+                        dK[(((long)co * C + ci) * k + a) * k + b] = s;
+                    }
+    }
+    return ORC_OK;
+}

@@ -469,10 +469,54 @@ def pin_stack(o):
     close(zf[0], h[:, 2:], 1e-12, "split keeps the first half")
 
 
+def pin_backward_autograd(o):
+    """Backward = torch autograd (fp64) of L = sum(y * dy) + gld * log|det|
+    with y = conv2d of the corner-padded input with K * mask: dx = x.grad,
+    dK = K.grad (the mask multiplies, so the masked entries get gradient 0 --
+    the paper's reset), for all corners, k in {1, 2, 3, 5}, H != W; masked
+    entries of the buffer hold junk that must be ignored."""
+    rng = np.random.default_rng(23)
+    for corner in range(4):
+        for (B, C, H, W, k) in [(2, 3, 5, 7, 3), (1, 2, 6, 4, 2), (2, 4, 3, 3, 1), (1, 2, 7, 6, 5)]:
+            x = rng.normal(size=(B, C, H, W))
+            dy = rng.normal(size=(B, C, H, W))
+            K = rand_kernel(rng, C, k, corner)
+            gld = float(rng.normal())
+            mask = np.ones_like(K)
+            sh, sw = SELF[corner](k)
+            for co in range(C):
+                mask[co, co + 1:, sh, sw] = 0.0
+            xt = torch.tensor(x, requires_grad=True)
+            Kt = torch.tensor(K, requires_grad=True)
+            Km = Kt * torch.tensor(mask)
+            y = F.conv2d(F.pad(xt, PADS[corner](k)), Km)
+            diag = torch.stack([Km[c, c, sh, sw] for c in range(C)])
+            loss = (y * torch.tensor(dy)).sum() + gld * H * W * torch.log(diag.abs()).sum()
+            loss.backward()
+            Kj = synth.garbage_in_mask(K, corner, seed=corner + 5)
+            dx, dK = o.backward(x, dy, Kj, corner, gld)
+            close(dx, xt.grad.numpy(), 1e-12, f"backward dx corner={corner} k={k}")
+            close(dK, Kt.grad.numpy(), 1e-12, f"backward dK corner={corner} k={k}")
+
+
+def pin_backward_dense(o):
+    """dx = J^T dy with the dense Jacobian of the layer (built column by
+    column from the forward), on one small image per corner."""
+    rng = np.random.default_rng(29)
+    C, H, W, k = 2, 4, 5, 3
+    for corner in range(4):
+        K = rand_kernel(rng, C, k, corner)
+        J = dense_jacobian(lambda v: o.forward(v, K, corner), C, H, W)
+        dy = rng.normal(size=(1, C, H, W))
+        dx, _ = o.backward(rng.normal(size=(1, C, H, W)), dy, K, corner)
+        close(dx.ravel(), J.T @ dy.ravel(), 1e-12, f"backward J^T corner={corner}")
+
+
 ALL_PINS = [
     pin_forward_conv2d, pin_fig1_matrix, pin_jacobian_triangular, pin_logdet_slogdet,
     pin_logdet_singular, pin_inverse_dense_solve, pin_inverse_triangular_solve,
     pin_round_trip, pin_k1_pixelwise, pin_impulse_geometric, pin_row_lfilter,
     pin_flip_equivalence, pin_wavefront_schedule, pin_unit_dense, pin_unit_round_trip,
     pin_split_dense, pin_split_round_trip, pin_squeeze_reshape, pin_actnorm, pin_stack,
+    pin_backward_autograd, pin_backward_dense,
 ]

@@ -48,6 +48,16 @@ MUTANTS = [
     ("stack inverse concatenates latent first",
      "memcpy(h + b * 2 * Cq * hw, t + b * Cq * hw, sizeof(double) * Cq * hw);",
      "memcpy(h + (b * 2 * Cq + Cq) * hw, t + b * Cq * hw, sizeof(double) * Cq * hw);", 0),
+    ("backward input gradient transposes channels",
+     "kmasked(K, C, k, oh, ow, co, ci, a, b) * g;", "kmasked(K, C, k, oh, ow, ci, co, a, b) * g;",
+     0),
+    ("backward keeps the masked weight gradients", "if (!(a == oh && b == ow && ci > co))",
+     "if (1)", 0),
+    ("backward forgets the log|det| term",
+     "s += gld * (double)H * (double)W / kw(K, C, k, co, co, a, b);", "s += 0.0;", 0),
+    ("backward weight gradient reads the mirrored tap",
+     "x[n * img + ci * plane + (long)ii * W + jj];",
+     "x[n * img + ci * plane + (long)(H - 1 - ii) * W + jj];", 0),
 ]
 
 

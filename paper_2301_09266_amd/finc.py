@@ -31,6 +31,8 @@ SIGNATURES = {
     "finc_logdet": (_i, [_vp, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "finc_backward": (_i, [_vp, _vp, _vp, _vp, _vp, ctypes.c_double, _i, _i, _i, _i, _i, _i,
+                           _vp]),
     "finc_unit_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "finc_unit_logdet": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
@@ -201,6 +203,30 @@ def inverse_prepared(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: in
     _check(L.finc_inverse_prepared(_ptr(y), _ptr(x), _ptr(prepared), B, C, H, W, k, corner,
                                    _stream()), "finc_inverse_prepared")
     return x
+
+
+def backward(x: torch.Tensor, dy: torch.Tensor, K: torch.Tensor, corner: int,
+             gld: float = 0.0, want_dx: bool = True, want_dK: bool = True,
+             dx: torch.Tensor | None = None, dK: torch.Tensor | None = None):
+    """(dx, dK) of one layer for the loss gradient dy (see finc_backward);
+    either is None when not wanted."""
+    L = _require_lib()
+    _dev(x, "x")
+    B, C, H, W = x.shape
+    _dev(dy, "dy", x.shape)
+    _dev(K, "K")
+    k = K.shape[-1]
+    if want_dx:
+        dx = torch.empty_like(x) if dx is None else _dev(dx, "dx", x.shape)
+    else:
+        dx = None
+    if want_dK:
+        dK = torch.empty_like(K) if dK is None else _dev(dK, "dK", K.shape)
+    else:
+        dK = None
+    _check(L.finc_backward(_ptr(x), _ptr(dy), _ptr(K), _ptr(dx), _ptr(dK), float(gld), B, C, H,
+                           W, k, corner, _stream()), "finc_backward")
+    return dx, dK
 
 
 def unit_forward(x: torch.Tensor, K4: torch.Tensor, out: torch.Tensor | None = None,

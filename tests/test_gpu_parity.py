@@ -330,6 +330,44 @@ def test_unit_forward_bands(orc, shape):
     assert torch.equal(inplace, y)
 
 
+@pytest.mark.parametrize("shape", [(2, 3, 5, 7, 3), (3, 12, 16, 16, 3), (1, 7, 9, 6, 5),
+                                   (2, 4, 6, 6, 1), (2, 5, 8, 11, 2), (1, 20, 9, 10, 7)],
+                         ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("corner", [0, 1, 2, 3])
+def test_backward(orc, shape, corner):
+    """Backward of one layer (dx = J^T dy; dK with the masked entries reset
+    and the log|det| term) against the oracle; junk in the masked weight
+    slots is ignored; the same bits on a second run."""
+    B, C, H, W, k = shape
+    rng = np.random.default_rng(100 + corner)
+    x = rng.normal(size=(B, C, H, W))
+    dy = rng.normal(size=(B, C, H, W))
+    K = synth.garbage_in_mask(synth.masked_kernel(C, k, corner, 1000 + corner), corner)
+    gld = -0.75
+    dx, dK = finc.backward(dev(x), dev(dy), dev(K), corner, gld, dx=poisoned(x.shape),
+                           dK=poisoned(K.shape))
+    want_dx, want_dK = orc.backward(f64(x), f64(dy), f64(K), corner, gld)
+    assert_close(host(dx), want_dx, f"backward dx {shape} corner {corner}")
+    assert_close(host(dK), want_dK, f"backward dK {shape} corner {corner}")
+    dx2, dK2 = finc.backward(dev(x), dev(dy), dev(K), corner, gld)
+    assert torch.equal(dx, dx2) and torch.equal(dK, dK2)
+
+
+def test_backward_workload(orc):
+    """Backward at the benchmark shape (64 images, 12 x 16 x 16, k = 3, TL):
+    dK sums 16,384 pixels per tap; dx checked on four sampled images."""
+    c = synth.make("layer_c12_16x16_b64_k3")
+    x, K = c["x"], c["K"]
+    dy = np.random.default_rng(5).normal(size=x.shape)
+    dx, dK = finc.backward(dev(x), dev(dy), dev(K), 0, -1.0)
+    want_dx, want_dK = orc.backward(f64(x), f64(dy), f64(K), 0, -1.0)
+    assert_close(host(dK), want_dK, "backward dK, batch 64")
+    pick = [0, 21, 63]
+    assert_close(host(dx)[pick], want_dx[pick], "backward dx, batch 64")
+    only_dk = finc.backward(dev(x), dev(dy), dev(K), 0, -1.0, want_dx=False)
+    assert only_dk[0] is None and torch.equal(only_dk[1], dK)
+
+
 def test_unsupported_shapes_rejected():
     """Shapes beyond what a workgroup can hold are rejected before any launch
     with FINC_EUNSUPPORTED, the output untouched: 8 channels at 128 x 128

@@ -197,6 +197,7 @@ def per_config(dev) -> list:
     for name, spec in synth.WORKLOADS.items():
         c = synth.make(name)
         kind = spec["kind"]
+        bwd = None
         if kind == "layer":
             B, C, H, W, k = (c[n] for n in "BCHWk")
             x, K = d(c["x"]), d(c["K"])
@@ -206,6 +207,11 @@ def per_config(dev) -> list:
             fwd = graph_time_us(lambda: finc.forward(x, K, c["corner"], out=out), 5, 20)
             inv = graph_time_us(lambda: finc.inverse_prepared(y, prep, k, c["corner"], out=out), 5, 20)
             act, wts, layers = 2 * C * H * W * 4, C * C * k * k * 4, 1
+            # training direction: dx and dK of the layer for a loss gradient dy
+            dyt = torch.randn_like(x)
+            dxo, dKo = torch.empty_like(x), torch.empty_like(K)
+            bwd = graph_time_us(lambda: finc.backward(x, dyt, K, c["corner"], -1.0, dx=dxo, dK=dKo),
+                                5, 20)
         elif kind == "unit":
             B, C, H, W, k = (c[n] for n in "BCHWk")
             x, K4 = d(c["x"]), d(c["K4"])
@@ -242,7 +248,7 @@ def per_config(dev) -> list:
         alg = B * act + wts
         gbs = alg / (inv * 1e-6) / 1e9
         rows.append({"workload": name, "B": B, "C": C, "H": H, "W": W, "k": k, "layers": layers,
-                     "forward_us": fwd, "inverse_us": inv,
+                     "forward_us": fwd, "inverse_us": inv, "backward_us": bwd,
                      "inverse_images_per_s": B / (inv * 1e-6),
                      "inverse_pixels_per_s": B * H * W / (inv * 1e-6),
                      "inverse_alg_bytes": alg, "inverse_hbm_gbs": gbs,

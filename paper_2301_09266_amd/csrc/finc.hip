@@ -1794,7 +1794,10 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
 constexpr int kBwdThreads = 256;
 
 // One thread per input pixel of one channel ci of one image (grid: pixel
-// blocks x C x B); the channel's masked weights K[.][ci][.][.] in LDS.
+// blocks x C x B); the channel's masked weights K[.][ci][.][.] in LDS.  Per
+// output channel, the k x k output gradients a pixel receives are loaded
+// together (unconditionally, from clamped addresses) before they are summed.
+template <int KMAX>
 __global__ __launch_bounds__(kBwdThreads) void backward_dx_kernel(const float *dy, const float *K,
                                                                   float *dx, int C, int H, int W,
                                                                   int k, int oh, int ow) {
@@ -1815,16 +1818,25 @@ __global__ __launch_bounds__(kBwdThreads) void backward_dx_kernel(const float *d
     const float *dyb = dy + (size_t)b * C * HW;
     float acc = 0.0f;
     for (int co = 0; co < C; ++co) {
-        for (int a = 0; a < k; ++a) {
+        const float *dyc = dyb + co * HW;
+        float v[KMAX][KMAX];
+#pragma unroll
+        for (int a = 0; a < KMAX; ++a) {
             const int i = s - a + oh;
-            if (i < 0 || i >= H)
-                continue;
-            for (int bb = 0; bb < k; ++bb) {
+#pragma unroll
+            for (int bb = 0; bb < KMAX; ++bb) {
                 const int j = t - bb + ow;
-                if (j >= 0 && j < W)
-                    acc = fmaf(kc[(co * k + a) * k + bb], dyb[co * HW + (size_t)i * W + j], acc);
+                const bool in = a < k && bb < k && i >= 0 && i < H && j >= 0 && j < W;
+                v[a][bb] = dyc[in ? (size_t)i * W + j : 0];
+                v[a][bb] = in ? v[a][bb] : 0.0f;
             }
         }
+#pragma unroll
+        for (int a = 0; a < KMAX; ++a)
+#pragma unroll
+            for (int bb = 0; bb < KMAX; ++bb)
+                if (a < k && bb < k)
+                    acc = fmaf(kc[(co * k + a) * k + bb], v[a][bb], acc);
     }
     dx[((size_t)b * C + ci) * HW + p] = acc;
 }
@@ -1846,25 +1858,41 @@ __global__ __launch_bounds__(kBwdThreads) void backward_dk_kernel(const float *x
 #pragma unroll
     for (int t = 0; t < KMAX * KMAX; ++t)
         acc[t] = 0.0f;
-    for (int n = 0; n < B; ++n) {
-        const float *dyn = dy + n * img + co * HW, *xn = x + n * img + ci * HW;
-        for (int p = tid; p < (int)HW; p += kBwdThreads) {
+    // U (image, pixel) positions a round, a workgroup's width apart: all
+    // their loads (unconditional, from clamped addresses) in flight before
+    // the multiply-adds, which run in position order
+    constexpr int U = KMAX <= 3 ? 4 : KMAX <= 5 ? 2 : 1;   // (registers: U k^2 + k^2)
+    const int HWi = (int)HW, total = B * HWi;   // (B C H W < 2^31)
+    for (int q0 = tid; q0 < total; q0 += U * kBwdThreads) {
+        float g[U], v[U][KMAX][KMAX];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int q = q0 + u * kBwdThreads;
+            const bool live = q < total;
+            const int qc = live ? q : 0, n = qc / HWi, p = qc - n * HWi;
             const int i = p / W, j = p - i * W;
-            const float g = dyn[p];
+            const float *xn = x + n * img + ci * HW;
+            g[u] = live ? dy[n * img + co * HW + p] : 0.0f;
 #pragma unroll
             for (int a = 0; a < KMAX; ++a) {
                 const int ii = i + a - oh;
-                if (a >= k || ii < 0 || ii >= H)
-                    continue;
 #pragma unroll
                 for (int bb = 0; bb < KMAX; ++bb) {
                     const int jj = j + bb - ow;
-                    if (bb < k && jj >= 0 && jj < W)
-                        acc[a * KMAX + bb] =
-                            fmaf(g, xn[(size_t)ii * W + jj], acc[a * KMAX + bb]);
+                    const bool in = a < k && bb < k && ii >= 0 && ii < H && jj >= 0 && jj < W;
+                    v[u][a][bb] = xn[in ? (size_t)ii * W + jj : 0];
+                    v[u][a][bb] = in ? v[u][a][bb] : 0.0f;
                 }
             }
         }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int a = 0; a < KMAX; ++a)
+#pragma unroll
+                for (int bb = 0; bb < KMAX; ++bb)
+                    if (a < k && bb < k)
+                        acc[a * KMAX + bb] = fmaf(g[u], v[u][a][bb], acc[a * KMAX + bb]);
     }
 #pragma unroll
     for (int t = 0; t < KMAX * KMAX; ++t)
@@ -2173,9 +2201,16 @@ int launch_backward(const float *x, const float *dy, const float *K, float *dx, 
     for (int b0 = 0; dx && b0 < B; b0 += 65535) {
         const dim3 grid((unsigned)ceil_div(H * W, kBwdThreads), (unsigned)C,
                         (unsigned)imin(B - b0, 65535));
-        hipLaunchKernelGGL(backward_dx_kernel, grid, dim3(kBwdThreads),
-                           (size_t)C * k * k * sizeof(float), stream, dy + b0 * img, K,
-                           dx + b0 * img, C, H, W, k, oh, ow);
+        const size_t lds = (size_t)C * k * k * sizeof(float);
+        if (k <= 3)
+            hipLaunchKernelGGL(backward_dx_kernel<3>, grid, dim3(kBwdThreads), lds, stream,
+                               dy + b0 * img, K, dx + b0 * img, C, H, W, k, oh, ow);
+        else if (k <= 5)
+            hipLaunchKernelGGL(backward_dx_kernel<5>, grid, dim3(kBwdThreads), lds, stream,
+                               dy + b0 * img, K, dx + b0 * img, C, H, W, k, oh, ow);
+        else
+            hipLaunchKernelGGL(backward_dx_kernel<7>, grid, dim3(kBwdThreads), lds, stream,
+                               dy + b0 * img, K, dx + b0 * img, C, H, W, k, oh, ow);
         const int rc = launched();
         if (rc != FINC_OK)
             return rc;

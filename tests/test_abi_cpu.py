@@ -84,6 +84,26 @@ def test_forward_rejects(args):
     assert finc.lib().finc_forward(*args, None) == finc.EINVAL
 
 
+FAKE3 = ctypes.c_void_p(0x1100000)
+FAKE4 = ctypes.c_void_p(0x1900000)
+
+
+@pytest.mark.parametrize("args", [
+    (NULL, FAKE2, FAKE3, FAKE4, NULL, 0.0, *SHAPE, 0),                       # no x
+    (FAKE, NULL, FAKE3, FAKE4, NULL, 0.0, *SHAPE, 0),                        # no dy
+    (FAKE, FAKE2, NULL, FAKE4, NULL, 0.0, *SHAPE, 0),                        # no K
+    (FAKE, FAKE2, FAKE3, FAKE4, NULL, 0.0, 2, 0, 16, 16, 3, 0),              # C = 0
+    (FAKE, FAKE2, FAKE3, FAKE4, NULL, 0.0, *SHAPE, 4),                       # bad corner
+    (FAKE, FAKE2, FAKE3, ctypes.c_void_p(0x100000 + 64), NULL, 0.0, *SHAPE, 0),   # dx over x
+    (FAKE, FAKE2, FAKE3, ctypes.c_void_p(0x900000 + 64), NULL, 0.0, *SHAPE, 0),   # dx over dy
+    (FAKE, FAKE2, FAKE3, NULL, ctypes.c_void_p(0x100000 + 64), 0.0, *SHAPE, 0),   # dK over x
+    (FAKE, FAKE2, FAKE3, NULL, FAKE3, 0.0, *SHAPE, 0),                        # dK over K
+    (FAKE, FAKE2, FAKE3, FAKE4, ctypes.c_void_p(0x1900000 + 64), 0.0, *SHAPE, 0),  # dK over dx
+])
+def test_backward_rejects(args):
+    assert finc.lib().finc_backward(*args, None) == finc.EINVAL
+
+
 def test_inverse_rejects():
     lib = finc.lib()
     ws = ctypes.c_void_p(0x4000000)

@@ -1841,75 +1841,69 @@ __global__ __launch_bounds__(kBwdThreads) void backward_dx_kernel(const float *d
     dx[((size_t)b * C + ci) * HW + p] = acc;
 }
 
-// One workgroup per (co, ci): each thread sums its share of the batch's
-// output pixels (a stride of the workgroup size) for all k x k taps, then
-// the taps are summed across the threads by a fixed tree in LDS: the same
-// bits on every run.  Masked entries get 0, the self diagonal also gets
-// gld H W / K[c][c][self] (in double).
+// One workgroup per (co, ci, kernel row a): each thread sums its share of
+// the batch's output pixels (a stride of the workgroup size) for the k taps
+// of row a, then the taps are summed across the threads by a fixed tree in
+// LDS: the same bits on every run.  Masked entries get 0, the self diagonal
+// also gets gld H W / K[c][c][self] (in double).
 template <int KMAX>
 __global__ __launch_bounds__(kBwdThreads) void backward_dk_kernel(const float *x, const float *dy,
                                                                   const float *K, float *dK,
                                                                   double gld, int B, int C, int H,
                                                                   int W, int k, int oh, int ow) {
-    __shared__ float red[KMAX * KMAX][kBwdThreads];
-    const int co = blockIdx.x, ci = blockIdx.y, tid = threadIdx.x, kk = k * k;
+    __shared__ float red[KMAX][kBwdThreads];
+    const int co = blockIdx.x, ci = blockIdx.y, a = blockIdx.z, tid = threadIdx.x;
     const size_t HW = (size_t)H * W, img = (size_t)C * HW;
-    float acc[KMAX * KMAX];
+    float acc[KMAX];
 #pragma unroll
-    for (int t = 0; t < KMAX * KMAX; ++t)
+    for (int t = 0; t < KMAX; ++t)
         acc[t] = 0.0f;
     // U (image, pixel) positions a round, a workgroup's width apart: all
     // their loads (unconditional, from clamped addresses) in flight before
     // the multiply-adds, which run in position order
-    constexpr int U = KMAX <= 3 ? 4 : KMAX <= 5 ? 2 : 1;   // (registers: U k^2 + k^2)
+    constexpr int U = 8;
     const int HWi = (int)HW, total = B * HWi;   // (B C H W < 2^31)
     for (int q0 = tid; q0 < total; q0 += U * kBwdThreads) {
-        float g[U], v[U][KMAX][KMAX];
+        float g[U], v[U][KMAX];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int q = q0 + u * kBwdThreads;
             const bool live = q < total;
             const int qc = live ? q : 0, n = qc / HWi, p = qc - n * HWi;
-            const int i = p / W, j = p - i * W;
+            const int i = p / W, j = p - i * W, ii = i + a - oh;
             const float *xn = x + n * img + ci * HW;
             g[u] = live ? dy[n * img + co * HW + p] : 0.0f;
 #pragma unroll
-            for (int a = 0; a < KMAX; ++a) {
-                const int ii = i + a - oh;
-#pragma unroll
-                for (int bb = 0; bb < KMAX; ++bb) {
-                    const int jj = j + bb - ow;
-                    const bool in = a < k && bb < k && ii >= 0 && ii < H && jj >= 0 && jj < W;
-                    v[u][a][bb] = xn[in ? (size_t)ii * W + jj : 0];
-                    v[u][a][bb] = in ? v[u][a][bb] : 0.0f;
-                }
+            for (int bb = 0; bb < KMAX; ++bb) {
+                const int jj = j + bb - ow;
+                const bool in = bb < k && ii >= 0 && ii < H && jj >= 0 && jj < W;
+                v[u][bb] = xn[in ? (size_t)ii * W + jj : 0];
+                v[u][bb] = in ? v[u][bb] : 0.0f;
             }
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int a = 0; a < KMAX; ++a)
-#pragma unroll
-                for (int bb = 0; bb < KMAX; ++bb)
-                    if (a < k && bb < k)
-                        acc[a * KMAX + bb] = fmaf(g[u], v[u][a][bb], acc[a * KMAX + bb]);
+            for (int bb = 0; bb < KMAX; ++bb)
+                if (bb < k)
+                    acc[bb] = fmaf(g[u], v[u][bb], acc[bb]);
     }
 #pragma unroll
-    for (int t = 0; t < KMAX * KMAX; ++t)
+    for (int t = 0; t < KMAX; ++t)
         red[t][tid] = acc[t];
     __syncthreads();
     for (int h = kBwdThreads / 2; h > 0; h >>= 1) {
         if (tid < h) {
 #pragma unroll
-            for (int t = 0; t < KMAX * KMAX; ++t)
+            for (int t = 0; t < KMAX; ++t)
                 red[t][tid] += red[t][tid + h];
         }
         __syncthreads();
     }
-    if (tid < kk) {
-        const int a = tid / k, bb = tid - a * k;
+    if (tid < k) {
+        const int bb = tid;
         const bool self = a == oh && bb == ow;
-        float v = red[a * KMAX + bb][0];
+        float v = red[bb][0];
         if (self && ci > co)
             v = 0.0f;   // masked: its gradient is reset to zero
         else if (self && ci == co)
@@ -2217,7 +2211,7 @@ int launch_backward(const float *x, const float *dy, const float *K, float *dx, 
     }
     if (!dK)
         return FINC_OK;
-    const dim3 grid((unsigned)C, (unsigned)C);
+    const dim3 grid((unsigned)C, (unsigned)C, (unsigned)k);
     if (k <= 3)
         hipLaunchKernelGGL(backward_dk_kernel<3>, grid, dim3(kBwdThreads), 0, stream, x, dy, K,
                            dK, gld, B, C, H, W, k, oh, ow);

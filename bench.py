@@ -286,6 +286,29 @@ def scaling_sweep(dev) -> dict:
             "rows": rows}
 
 
+def batch_scaling(dev) -> dict:
+    """The benchmark layer (12 x 16 x 16, k = 3, TL) at batches 1, 8 and 64:
+    one GPU's share of a batch of 64 sharded over 64, 8 and 1 GPUs."""
+    import numpy as np
+    import torch
+
+    from paper_2301_09266_amd import finc, synth
+
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    rows = []
+    for B in (1, 8, 64):
+        c = synth.layer_case(B, 12, 16, 16, 3)
+        x, K = d(c["x"]), d(c["K"])
+        y = finc.forward(x, K, 0)
+        prep = finc.prepare(K, [0])
+        out = torch.empty_like(x)
+        fwd = graph_time_us(lambda: finc.forward(x, K, 0, out=out), 5, 20)
+        inv = graph_time_us(lambda: finc.inverse_prepared(y, prep, 3, 0, out=out), 5, 20)
+        rows.append({"B": B, "forward_us": fwd, "inverse_us": inv,
+                     "inverse_images_per_s": B / (inv * 1e-6)})
+    return {"what": "layer 12 x 16 x 16, k = 3, TL, by batch", "rows": rows}
+
+
 def cpu_baseline(step, seconds: float):
     """The oracle, single-threaded, on whole batches of the same step until
     `seconds` of CPU time have been spent (at least one image)."""
@@ -440,6 +463,7 @@ def main():
     if not args.no_configs:
         out["per_config"] = per_config(dev)
         out["scaling_sweep"] = scaling_sweep(dev)
+        out["batch_scaling"] = batch_scaling(dev)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(st, args.cpu_seconds)
     print(json.dumps(out))

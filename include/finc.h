@@ -23,8 +23,11 @@
  *    enqueueing.  Nothing is allocated, freed or synchronised by the library.
  *  - Return value: FINC_OK or a negative finc_status.  Arguments are checked
  *    before any HIP call: a bad argument returns FINC_EINVAL and enqueues
- *    nothing.  FINC_EUNSUPPORTED: shape valid but outside what the kernels
- *    handle (per-image working set larger than one workgroup's LDS).
+ *    nothing.  FINC_EUNSUPPORTED (inverse calls only, also with B == 0):
+ *    the shape is valid but the per-image work split needs more waves or
+ *    more weight registers per wave than one workgroup has, or its LDS
+ *    layout exceeds 160 KB and the stream form (single layers of at most 16
+ *    channels) does not apply; finc_inverse_plan answers it for any shape.
  *    FINC_EHIP: a HIP runtime call failed (hipGetLastError after the launch).
  *    Device-side faults surface at the caller's next synchronisation.
  *  - A zero self-tap diagonal weight makes the layer singular: finc_logdet
@@ -65,6 +68,31 @@ int finc_version(void);
 
 /* Static text for a status code (never NULL). */
 const char *finc_strerror(int status);
+
+/* ---- Inverse kernel selection (host arithmetic only, no HIP call) --------
+ * The inverse of Algorithm 1 runs as one of a fixed set of compiled kernel
+ * instances, chosen on the host from the level shapes: workgroup size,
+ * critical-path form ("mode") and weight quad groups held in registers per
+ * wave.  finc_inverse_plan reports the instance(s) a call would launch, for
+ * tests that must reach every instance and for capacity planning:
+ *   kind FINC_PLAN_LAYER: finc_inverse(_prepared) on C x H x W, k;
+ *   kind FINC_PLAN_UNIT:  finc_unit_inverse(_prepared);
+ *   kind FINC_PLAN_SPLIT: finc_split_inverse(_prepared), C = the unit's
+ *                         channels (a multiple of 4);
+ *   kind FINC_PLAN_STACK: finc_stack_inverse(_prepared) with L levels of U
+ *                         units, C = C1, H = H1, W = W1.
+ * L and U are ignored except for FINC_PLAN_STACK.  For each distinct launch
+ * (one; or L for a stack whose levels run in launches of their own) it writes
+ * six ints to info: workgroup threads, mode bits (0 gathering critical wave,
+ * 1 register-fed; +4 single layer; +8 stream form, one launch per layer),
+ * quad groups per wave, 1 if streamed, LDS bytes, 1 if partial tiles are
+ * kept in the compact layout (the padded one would not fit).  The LDS
+ * budget is gfx950's 160 KB per workgroup.  Returns the number of launches
+ * written, FINC_EINVAL for bad arguments (or max_launches too small), or
+ * FINC_EUNSUPPORTED exactly when the corresponding call would return it. */
+enum { FINC_PLAN_LAYER = 0, FINC_PLAN_UNIT = 1, FINC_PLAN_SPLIT = 2, FINC_PLAN_STACK = 3 };
+int finc_inverse_plan(int kind, int L, int U, int C, int H, int W, int k, int *info,
+                      int max_launches);
 
 /* ---- Weight preparation (one-time per weight set) -----------------------
  * The inverse of one layer solves, per pixel, L x_p = y_p - sum_s K_s x_src

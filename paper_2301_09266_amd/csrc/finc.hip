@@ -390,7 +390,7 @@ constexpr int kMaxGroups = 8;                       // quad groups (x4 quads) pe
 // critical-wave forms an inverse instance is built with (low two bits of
 // its MODE), and kOneLayer: a single level of a single layer without actnorm
 // (the chain's loops and hand-overs compiled out)
-constexpr int kCritGather = 0, kCritRegs = 1, kCritBoth = 2, kOneLayer = 4;
+constexpr int kCritGather = 0, kCritRegs = 1, kOneLayer = 4;
 // kStream (with kOneLayer and kCritRegs): a single layer whose image does not
 // fit in LDS.  Solution and input live in per-row rings of kRing frame
 // columns; every kPhase diagonal steps the workgroup drains the solved
@@ -845,14 +845,12 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
     constexpr bool kPrefetch = NG <= 4 && (MAXT <= 512 || NG <= 2);
     constexpr int GN = kPrefetch ? G : 1;
     // the register-fed critical wave owns the two dp + dq = 1 taps as groups
-    // (MODE: kCritGather / kCritRegs / kCritBoth -- the instance carries only
-    // the critical loop(s) its levels use)
+    // (MODE: kCritGather / kCritRegs -- the instance carries only the
+    // critical loop its levels use)
     constexpr int CRIT = MODE & 3;
     constexpr bool kOne = (MODE & kOneLayer) != 0;
     constexpr bool kStr = (MODE & kStream) != 0;
-    const bool regc = CRIT == kCritRegs    ? r.role == 0
-                      : CRIT == kCritGather ? false
-                                            : pl.regcrit && r.role == 0;
+    const bool regc = CRIT == kCritRegs && r.role == 0;
     const int ngw = r.ng;
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int C = pl.C, CP = pl.CP, H = pl.H, W = pl.W, P = pl.P, WP = pl.WP;
@@ -1176,7 +1174,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                 run(std::true_type{});
             else
                 run(std::false_type{});
-        } else if (CRIT != kCritGather && r.role == 0 && regc) {
+        } else if (CRIT == kCritRegs && r.role == 0) {
             // register-fed critical wave.  dprev: lane (kq, li) holds channels
             // 4 kq .. +3 of row li's pixel of the previous diagonal (0 for rows
             // not started).  Its MFMA chain needs nothing from LDS but, in a
@@ -1275,7 +1273,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                 crit(std::false_type{});
             else
                 crit(std::true_type{});
-        } else if (CRIT != kCritRegs && r.role == 0) {
+        } else if (CRIT == kCritGather && r.role == 0) {
             // critical wave that gathers its dp + dq = 1 taps from LDS (several
             // channel tiles: the previous diagonal's channels sit in several
             // waves)
@@ -1458,21 +1456,19 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
 
 // Inverse kernel instances, in groups of one workgroup size and one mode, by
 // quad groups per wave (1..kMaxGroups).  The host picks one by address.
-constexpr int kInverseGroups = 18;
-constexpr int kModesPerSize = 6;
-constexpr int kGroupThreads[kInverseGroups] = {256, 256, 256, 256, 256, 256,
-                                               512, 512, 512, 512, 512, 512,
-                                               1024, 1024, 1024, 1024, 1024, 1024};
+constexpr int kInverseGroups = 15;
+constexpr int kModesPerSize = 5;
+constexpr int kGroupThreads[kInverseGroups] = {256,  256,  256,  256,  256,  512,  512, 512,
+                                               512,  512,  1024, 1024, 1024, 1024, 1024};
 constexpr int kGroupModes[kModesPerSize] = {kCritGather,
                                             kCritRegs,
-                                            kCritBoth,
                                             kCritGather | kOneLayer,
                                             kCritRegs | kOneLayer,
                                             kCritRegs | kOneLayer | kStream};
 constexpr int kGroupMode[kInverseGroups] = {
-    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4], kGroupModes[5],
-    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4], kGroupModes[5],
-    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4], kGroupModes[5]};
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4],
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4],
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4]};
 
 template <int MAXT, int MODE>
 const void *inverse_instance_of(int ng) {
@@ -1491,8 +1487,7 @@ const void *inverse_instance_of(int ng) {
 }  // namespace
 
 #define FINC_GROUPS(X) \
-    X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) \
-    X(16) X(17)
+    X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14)
 #define FINC_CAT2(a, b) a##b
 #define FINC_CAT(a, b) FINC_CAT2(a, b)
 
@@ -2083,30 +2078,86 @@ const void *inverse_instance(int threads, int mode, int ng) {
 #endif
     static const void *(*const groups[kInverseGroups])(int) = {FINC_GROUPS(FINC_ENTRY)};
 #undef FINC_ENTRY
-    int m = 2;   // kCritBoth stands for any other mode
+    int m = -1;
     for (int i = 0; i < kModesPerSize; ++i)
         if (kGroupModes[i] == mode)
             m = i;
+    if (m < 0)
+        return nullptr;
     const int t = threads <= 256 ? 0 : threads <= 512 ? 1 : 2;
     return groups[kModesPerSize * t + m](ng);
+}
+
+// How an inverse chain is launched: the kernel instance (workgroup size,
+// mode, quad groups per wave), its LDS, and whether the image is streamed
+// (one stream-form launch per layer) because it does not fit in LDS.
+struct InvChoice {
+    int streamed;
+    int threads, mode, ng;
+    int compact;   // some level keeps compact partial tiles
+    size_t lds;
+    Plan sp;   // the stream form's plan (streamed only)
+};
+
+// The choice for a chain whose workgroups may use lds_lim bytes of LDS:
+// FINC_EUNSUPPORTED when neither the LDS-resident chain nor (a single level of
+// layers without actnorm) the stream form fits.  Host arithmetic only.
+int choose_inverse(InvArgs &a, size_t lds_lim, InvChoice &c) {
+    memset(&c, 0, sizeof(c));
+    size_t lds = 0;
+    int threads = 0;
+    int rc = plan_inverse(a, &lds, &threads);
+    if (rc == FINC_OK && lds > lds_lim)
+        rc = FINC_EUNSUPPORTED;
+    if (rc == FINC_EUNSUPPORTED && a.L == 1 && !a.lv[0].scale && !a.split) {
+        const Level &l0 = a.lv[0];
+        if (a.n_units * a.lpu < 1 || !make_plan(l0.pl.C, l0.pl.H, l0.pl.W, l0.pl.K, c.sp, true))
+            return FINC_EUNSUPPORTED;
+        c.lds = (size_t)c.sp.lds_floats * sizeof(float);
+        if (c.lds > lds_lim)
+            return FINC_EUNSUPPORTED;
+        c.streamed = 1;
+        c.threads = c.sp.NW * kWave;
+        c.mode = kCritRegs | kOneLayer | kStream;
+        c.ng = plan_groups(c.sp);
+        c.compact = c.sp.compact;
+        return FINC_OK;
+    }
+    if (rc != FINC_OK)
+        return rc;
+    int ng = 1, nreg = 0;
+    for (int l = 0; l < a.L; ++l) {
+        const Plan &p = a.lv[l].pl;
+        ng = imax(ng, plan_groups(p));
+        nreg += p.regcrit;
+        c.compact |= p.compact;
+    }
+    // levels of one launch share the critical form: a stack whose levels
+    // differ in it runs them in launches of their own
+    if (nreg != 0 && nreg != a.L)
+        return FINC_EUNSUPPORTED;
+    int mode = nreg == a.L ? kCritRegs : kCritGather;
+    if (a.L == 1 && a.n_units * a.lpu == 1 && !a.lv[0].scale)
+        mode |= kOneLayer;   // (a single level has one critical form)
+    c.threads = threads;
+    c.mode = mode;
+    c.ng = ng;
+    c.lds = lds;
+    return FINC_OK;
 }
 
 // A single level of layers without actnorm whose image does not fit in LDS:
 // one stream-form launch per layer, in place on the output after the first
 // (each workgroup reads a pixel's input before it writes the pixel).
-int launch_streamed(const InvArgs &a, int B, hipStream_t stream) {
+int launch_streamed(const InvArgs &a, const InvChoice &ch, int B, hipStream_t stream) {
     const Level &l0 = a.lv[0];
-    Plan p;
-    if (a.n_units * a.lpu < 1 || !make_plan(l0.pl.C, l0.pl.H, l0.pl.W, l0.pl.K, p, true))
+    const Plan &p = ch.sp;
+    const size_t lds = ch.lds;
+    const int threads = ch.threads;
+    int rc = FINC_OK;
+    const void *k = inverse_instance(threads, ch.mode, ch.ng);
+    if (!k)
         return FINC_EUNSUPPORTED;
-    if (B == 0)
-        return FINC_OK;
-    const size_t lds = (size_t)p.lds_floats * sizeof(float);
-    int rc = check_lds(lds);
-    if (rc != FINC_OK)
-        return rc;
-    const int threads = p.NW * kWave;
-    const void *k = inverse_instance(threads, kCritRegs | kOneLayer | kStream, plan_groups(p));
     if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
         hipSuccess)
         (void)hipGetLastError();
@@ -2130,24 +2181,22 @@ int launch_streamed(const InvArgs &a, int B, hipStream_t stream) {
 }
 
 int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
-    size_t lds = 0;
-    int threads = 0;
-    int rc = plan_inverse(a, &lds, &threads);
-    if (rc == FINC_OK && B == 0)
-        return FINC_OK;
-    if (rc == FINC_OK)
-        rc = check_lds(lds);
-    if (rc == FINC_EUNSUPPORTED && a.L == 1 && !a.lv[0].scale && !a.split)
-        return launch_streamed(a, B, stream);   // the image does not fit in LDS
+    size_t lim = kLdsBytes;
+    if (B > 0) {
+        const int lrc = lds_limit(&lim);
+        if (lrc != FINC_OK)
+            return lrc;
+    }
+    InvChoice ch;
+    const int rc = choose_inverse(a, lim, ch);
     if (rc != FINC_OK)
         return rc;
-    int ng = 1, nreg = 0;
-    for (int l = 0; l < a.L; ++l) {
-        const Plan &p = a.lv[l].pl;
-        ng = imax(ng, plan_groups(p));
-        nreg += p.regcrit;
-    }
-    int mode = nreg == a.L ? kCritRegs : nreg == 0 ? kCritGather : kCritBoth;
+    if (B == 0)
+        return FINC_OK;
+    if (ch.streamed)
+        return launch_streamed(a, ch, B, stream);   // the image does not fit in LDS
+    const int threads = ch.threads, mode = ch.mode, ng = ch.ng;
+    const size_t lds = ch.lds;
     {
         const Plan &top = a.lv[0].pl, &last = a.lv[a.L - 1].pl;
         if (a.out_stride == 0)
@@ -2157,9 +2206,9 @@ int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
             last.W % 4 == 0 && ((uintptr_t)a.out & 15u) == 0 && a.out_stride % 4 == 0;
         a.vec = (in4 ? 1 : 0) | (out4 ? 2 : 0);
     }
-    if (a.L == 1 && a.n_units * a.lpu == 1 && !a.lv[0].scale)
-        mode |= kOneLayer;   // (a single level has one critical form)
     const void *k = inverse_instance(threads, mode, ng);
+    if (!k)
+        return FINC_EUNSUPPORTED;
     if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
         hipSuccess)
         (void)hipGetLastError();   // not needed on every runtime; the launch check decides
@@ -2295,6 +2344,12 @@ size_t stack_level_bytes(int l, int U, int C1, int k) {
     return (size_t)U * 4 * prep_layer_floats(C1 << l, k) * sizeof(float);
 }
 
+// Channel-split unit: C a multiple of 4; seen as (4B, C/4, H, W).
+bool valid_split(int B, int C, int H, int W, int k) {
+    return C >= 4 && C % 4 == 0 && B >= 0 && B <= (1 << 28) &&
+           valid_shape(4 * B, C / 4, H, W, k);
+}
+
 bool valid_stack(int B, int L, int U, int C1, int H1, int W1, int k) {
     if (L < 1 || L > kMaxLevels || U < 0 || B < 0 || C1 < 1 || H1 < 1 || W1 < 1)
         return false;
@@ -2343,6 +2398,77 @@ const char *finc_strerror(int status) {
     case FINC_EHIP: return "HIP runtime error";
     default: return "unknown status";
     }
+}
+
+static void put_choice(const InvChoice &c, int *dst) {
+    dst[0] = c.threads;
+    dst[1] = c.mode;
+    dst[2] = c.ng;
+    dst[3] = c.streamed;
+    dst[4] = (int)c.lds;
+    dst[5] = c.compact;
+}
+
+int finc_inverse_plan(int kind, int L, int U, int C, int H, int W, int k, int *info,
+                      int max_launches) {
+    if (!info || max_launches < 1)
+        return FINC_EINVAL;
+    static const float dummy[1] = {0.0f};   // stands for a non-null scale / bias
+    InvArgs a;
+    memset(&a, 0, sizeof(a));
+    a.L = 1;
+    a.n_units = 1;
+    a.lpu = 1;
+    if (kind == FINC_PLAN_LAYER) {
+        if (!valid_shape(1, C, H, W, k))
+            return FINC_EINVAL;
+        a.lv[0] = level(dummy, nullptr, nullptr, nullptr, C, H, W, k);
+    } else if (kind == FINC_PLAN_UNIT) {
+        if (!valid_shape(1, C, H, W, k))
+            return FINC_EINVAL;
+        a.lv[0] = level(dummy, nullptr, nullptr, nullptr, C, H, W, k);
+        a.lpu = 4;
+    } else if (kind == FINC_PLAN_SPLIT) {
+        if (!valid_split(1, C, H, W, k))
+            return FINC_EINVAL;
+        a.lv[0] = level(dummy, nullptr, nullptr, nullptr, C / 4, H, W, k);
+        a.split = 1;
+    } else if (kind == FINC_PLAN_STACK) {
+        if (!valid_stack(1, L, U, C, H, W, k))
+            return FINC_EINVAL;
+        for (int l = 0; l < L; ++l)
+            a.lv[L - 1 - l] = level(dummy, nullptr, dummy, dummy, C << l, H >> l, W >> l, k);
+        a.L = L;
+        a.n_units = U;
+        a.lpu = 4;
+        if (levels_differ(a)) {
+            if (max_launches < L)
+                return FINC_EINVAL;
+            for (int i = 0; i < L; ++i) {
+                InvArgs s;
+                memset(&s, 0, sizeof(s));
+                s.lv[0] = a.lv[i];
+                s.L = 1;
+                s.n_units = U;
+                s.lpu = 4;
+                s.hin = i > 0 ? dummy : nullptr;
+                InvChoice c;
+                const int rc = choose_inverse(s, kLdsBytes, c);
+                if (rc != FINC_OK)
+                    return rc;
+                put_choice(c, info + 6 * i);
+            }
+            return L;
+        }
+    } else {
+        return FINC_EINVAL;
+    }
+    InvChoice c;
+    const int rc = choose_inverse(a, kLdsBytes, c);
+    if (rc != FINC_OK)
+        return rc;
+    put_choice(c, info);
+    return 1;
 }
 
 size_t finc_workspace_bytes(int C, int k, int n_layers) {
@@ -2454,8 +2580,8 @@ int finc_inverse(const float *y, float *x, const float *K, int B, int C, int H, 
         overlap(workspace, wsb, y, bytes) ||
         overlap(workspace, wsb, K, (size_t)C * C * k * k * sizeof(float)))
         return FINC_EINVAL;
-    if (B == 0)
-        return FINC_OK;
+    if (B == 0)   // nothing to launch; the shape is still checked
+        return finc_inverse_prepared(y, x, workspace, 0, C, H, W, k, corner, stream);
     const int rc = finc_prepare(K, 1, &corner, C, k, workspace, stream);
     if (rc != FINC_OK)
         return rc;
@@ -2493,12 +2619,6 @@ int finc_unit_logdet(const float *K4, int C, int k, int H, int W, double *out,
     hipLaunchKernelGGL(logdet_kernel, dim3(1), dim3(kWave), 0, stream, K4, 4, FINC_TL, C, k,
                        H, W, out);
     return launched();
-}
-
-// Channel-split unit: C a multiple of 4; seen as (4B, C/4, H, W).
-static bool valid_split(int B, int C, int H, int W, int k) {
-    return C >= 4 && C % 4 == 0 && B >= 0 && B <= (1 << 28) &&
-           valid_shape(4 * B, C / 4, H, W, k);
 }
 
 int finc_split_logdet(const float *Kq4, int C, int k, int H, int W, double *out,
@@ -2566,8 +2686,8 @@ int finc_split_inverse(const float *y, float *x, const float *Kq4, int B, int C,
         overlap(workspace, wsb, y, bytes) ||
         overlap(workspace, wsb, Kq4, (size_t)4 * Cq * Cq * k * k * sizeof(float)))
         return FINC_EINVAL;
-    if (B == 0)
-        return FINC_OK;
+    if (B == 0)   // nothing to launch; the shape is still checked
+        return finc_split_inverse_prepared(y, x, workspace, 0, C, H, W, k, stream);
     const int corners[4] = {FINC_TL, FINC_TR, FINC_BL, FINC_BR};
     const int rc = finc_prepare(Kq4, 4, corners, Cq, k, workspace, stream);
     if (rc != FINC_OK)
@@ -2606,8 +2726,8 @@ int finc_unit_inverse(const float *y, float *x, const float *K4, int B, int C, i
         overlap(workspace, wsb, y, bytes) ||
         overlap(workspace, wsb, K4, (size_t)4 * C * C * k * k * sizeof(float)))
         return FINC_EINVAL;
-    if (B == 0)
-        return FINC_OK;
+    if (B == 0)   // nothing to launch; the shape is still checked
+        return finc_unit_inverse_prepared(y, x, workspace, 0, C, H, W, k, stream);
     static const int corners[4] = {FINC_TL, FINC_TR, FINC_BL, FINC_BR};
     const int rc = finc_prepare(K4, 4, corners, C, k, workspace, stream);
     if (rc != FINC_OK)
@@ -2720,8 +2840,9 @@ int finc_stack_inverse(const float *const *z, float *x, const float *K, const fl
     const size_t wsb = finc_stack_workspace_bytes(L, U, C1, k);
     if (overlap(workspace, wsb, x, (size_t)B * C1 * H1 * W1 * sizeof(float)))
         return FINC_EINVAL;
-    if (B == 0)
-        return FINC_OK;
+    if (B == 0)   // nothing to launch; the shape is still checked
+        return finc_stack_inverse_prepared(z, x, workspace, scale, bias, 0, L, U, C1, H1, W1, k,
+                                           stream);
     const int rc = finc_stack_prepare(K, L, U, C1, k, workspace, stream);
     if (rc != FINC_OK)
         return rc;

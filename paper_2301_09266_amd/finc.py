@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "csrc", "lib
 
 TL, TR, BL, BR = 0, 1, 2, 3
 OK, EINVAL, ESINGULAR, EUNSUPPORTED, EHIP = 0, -1, -2, -3, -4
+PLAN_LAYER, PLAN_UNIT, PLAN_SPLIT, PLAN_STACK = 0, 1, 2, 3
 
 _vp = ctypes.c_void_p
 _i = ctypes.c_int
@@ -25,6 +26,7 @@ _sz = ctypes.c_size_t
 SIGNATURES = {
     "finc_version": (_i, []),
     "finc_strerror": (ctypes.c_char_p, [_i]),
+    "finc_inverse_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i), _i]),
     "finc_workspace_bytes": (_sz, [_i, _i, _i]),
     "finc_prepare": (_i, [_vp, _i, ctypes.POINTER(_i), _i, _i, _vp, _vp]),
     "finc_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
@@ -126,6 +128,18 @@ def _workspace(nbytes: int, device, ws):
 
 def version() -> int:
     return _require_lib().finc_version()
+
+
+def inverse_plan(kind: int, C: int, H: int, W: int, k: int, L: int = 1, U: int = 1):
+    """The inverse kernel launches a call would make (finc_inverse_plan): a
+    list of dicts (threads, mode, groups, streamed, lds, compact), one per
+    distinct launch, or the negative status (EUNSUPPORTED, EINVAL)."""
+    info = (ctypes.c_int * (6 * 8))()
+    n = _require_lib().finc_inverse_plan(kind, L, U, C, H, W, k, info, 8)
+    if n < 0:
+        return n
+    keys = ("threads", "mode", "groups", "streamed", "lds", "compact")
+    return [dict(zip(keys, info[6 * i:6 * i + 6])) for i in range(n)]
 
 
 def workspace_bytes(C: int, k: int, n_layers: int = 1) -> int:

@@ -1,0 +1,116 @@
+"""The inverse's kernel selection, on the host (no GPU): every kernel
+instance reachable inside the library's domain is reached by a shape of the
+GPU sweep, the selection query agrees with what the entry points return, and
+the supported channel counts are those stated for the library."""
+import ctypes
+
+import pytest
+
+import domain
+from paper_2301_09266_amd import finc
+
+FAKE = ctypes.c_void_p(0x100000)     # never dereferenced: B == 0 enqueues nothing
+FAKE2 = ctypes.c_void_p(0x900000)
+WS = ctypes.c_void_p(0x4000000)      # 256-byte aligned
+
+# Largest C the inverse supports for an image of 16 m rows (m = 1 .. 8) and
+# width 8, per kernel size k, for a single layer and a unit (the channel-split
+# unit: four times the layer's value, at most 64).  Every C up to the value
+# is supported; none above it.
+SUPPORT_MAX_C = {
+    1: (64, 64, 32, 32, 16, 16, 16, 16),
+    2: (64, 60, 32, 28, 16, 16, 16, 12),
+    3: (52, 32, 16, 16, 16, 16, 12, 12),
+    4: (36, 24, 16, 16, 16, 8, 8, 8),
+    5: (32, 16, 16, 16, 8, 4, 4, 4),
+    6: (24, 16, 12, 8, 4, 0, 0, 0),
+    7: (16, 16, 8, 8, 4, 0, 0, 0),
+}
+
+
+def test_cover_reaches_every_instance():
+    found = domain.reachable()
+    covered = {domain.instance(*c) for c in domain.COVER}
+    assert not any(isinstance(c, int) for c in covered), "a cover shape is not supported"
+    missing = set(found) - covered
+    assert not missing, {m: found[m] for m in missing}
+    # every mode the library compiles is used: gathering and register-fed
+    # critical waves, chains and single layers, and the stream form
+    assert {key[1] for key in found} == {0, 1, 4, 5, 13}
+    assert {key[3] for key in found} == {0, 1}   # padded and compact partial tiles
+
+
+def test_random_cases_are_supported_and_seeded():
+    for seed in domain.RANDOM_SEEDS:
+        cases = domain.random_cases(seed)
+        assert cases == domain.random_cases(seed)
+        assert len(cases) == domain.RANDOM_PER_SEED
+        for kind, B, C, H, W, k, corner in cases:
+            assert not isinstance(domain.instance(kind, C, H, W, k), int)
+
+
+@pytest.mark.parametrize("kind", ["layer", "unit", "split"])
+def test_supported_channels(kind):
+    for k, row in SUPPORT_MAX_C.items():
+        for m, cmax in enumerate(row, start=1):
+            if kind == "split":
+                cmax = min(64, 4 * cmax)
+            for C in domain._channels(kind):
+                ok = not isinstance(domain.instance(kind, C, 16 * m, 8, k), int)
+                assert ok == (C <= cmax), (kind, C, 16 * m, k)
+    for C in (1, 12, 64):   # more than 128 rows: never
+        assert domain.instance("layer", C, 129, 4, 3) == finc.EUNSUPPORTED
+
+
+SHAPES = [(C, H, W, k) for C in (1, 4, 12, 16, 17, 24, 32, 36, 48, 52, 53, 64)
+          for H, W in ((1, 1), (8, 8), (16, 16), (40, 30), (64, 64), (128, 200), (129, 8))
+          for k in (1, 3, 5, 7)]
+
+
+def test_plan_matches_inverse_entry_points():
+    lib = finc.lib()
+    for C, H, W, k in SHAPES:
+        want = domain.instance("layer", C, H, W, k)
+        want = want if isinstance(want, int) else finc.OK
+        assert lib.finc_inverse_prepared(FAKE, FAKE2, WS, 0, C, H, W, k, 2, None) == want
+        assert lib.finc_inverse(FAKE, FAKE2, FAKE, 0, C, H, W, k, 2, WS, None) == want
+        want = domain.instance("unit", C, H, W, k)
+        want = want if isinstance(want, int) else finc.OK
+        assert lib.finc_unit_inverse_prepared(FAKE, FAKE2, WS, 0, C, H, W, k, None) == want
+        if C % 4 == 0:
+            want = domain.instance("split", C, H, W, k)
+            want = want if isinstance(want, int) else finc.OK
+            assert lib.finc_split_inverse_prepared(FAKE, FAKE2, WS, 0, C, H, W, k, None) == want
+
+
+def test_plan_of_stacks():
+    lib = finc.lib()
+    z = (ctypes.c_void_p * 4)(0x100000, 0x200000, 0x300000, 0x400000)
+    # the sampling stack: three levels that need different instances, so
+    # three launches
+    p = finc.inverse_plan(finc.PLAN_STACK, 12, 32, 32, 3, L=3, U=8)
+    assert len(p) == 3 and len({(q["threads"], q["groups"]) for q in p}) == 3
+    # levels sharing one plan: the whole stack in one launch
+    p = finc.inverse_plan(finc.PLAN_STACK, 2, 16, 16, 3, L=2, U=2)
+    assert len(p) == 1
+    for L, C1, H1, k in [(3, 12, 32, 3), (2, 2, 16, 3), (3, 16, 32, 3), (2, 32, 64, 3),
+                         (4, 4, 64, 5), (1, 64, 16, 3)]:
+        p = finc.inverse_plan(finc.PLAN_STACK, C1, H1, H1, k, L=L, U=2)
+        want = p if isinstance(p, int) else finc.OK
+        got = lib.finc_stack_inverse_prepared(z, FAKE2, WS, FAKE, FAKE, 0, L, 2, C1, H1, H1, k,
+                                              None)
+        assert got == want, (L, C1, H1, k)
+    assert finc.inverse_plan(finc.PLAN_STACK, 3, 16, 16, 3, L=2, U=1) == finc.EINVAL   # odd C1
+
+
+def test_plan_rejects_bad_arguments():
+    lib = finc.lib()
+    info = (ctypes.c_int * 6)()
+    assert lib.finc_inverse_plan(0, 1, 1, 12, 16, 16, 3, None, 1) == finc.EINVAL
+    assert lib.finc_inverse_plan(0, 1, 1, 12, 16, 16, 3, info, 0) == finc.EINVAL
+    assert lib.finc_inverse_plan(7, 1, 1, 12, 16, 16, 3, info, 1) == finc.EINVAL
+    assert lib.finc_inverse_plan(0, 1, 1, 65, 16, 16, 3, info, 1) == finc.EINVAL
+    assert lib.finc_inverse_plan(2, 1, 1, 6, 16, 16, 3, info, 1) == finc.EINVAL
+    assert lib.finc_inverse_plan(3, 3, 8, 12, 32, 32, 3, info, 2) == finc.EINVAL   # 3 launches
+    assert lib.finc_inverse_plan(0, 1, 1, 12, 16, 16, 3, info, 1) == 1
+    assert info[0] == 256 and info[1] == 5 and info[2] == 2 and info[3] == 0

@@ -23,11 +23,13 @@
  *    enqueueing.  Nothing is allocated, freed or synchronised by the library.
  *  - Return value: FINC_OK or a negative finc_status.  Arguments are checked
  *    before any HIP call: a bad argument returns FINC_EINVAL and enqueues
- *    nothing.  FINC_EUNSUPPORTED (inverse calls only, also with B == 0):
- *    the shape is valid but the per-image work split needs more waves or
- *    more weight registers per wave than one workgroup has, or its LDS
- *    layout exceeds 160 KB and the stream form (single layers of at most 16
- *    channels) does not apply; finc_inverse_plan answers it for any shape.
+ *    nothing.  FINC_EUNSUPPORTED: the shape is valid but does not fit the
+ *    kernels.  Inverse calls (also with B == 0): the per-image work split
+ *    needs more waves or more weight registers per wave than one workgroup
+ *    has, or its LDS layout exceeds 160 KB and the stream form (single layers
+ *    of at most 16 channels) does not apply; finc_inverse_plan answers it for
+ *    any shape.  Forward calls (B > 0): one block of rows with its halo does
+ *    not fit in LDS (very wide rows); finc_forward_plan answers it.
  *    FINC_EHIP: a HIP runtime call failed (hipGetLastError after the launch).
  *    Device-side faults surface at the caller's next synchronisation.
  *  - A zero self-tap diagonal weight makes the layer singular: finc_logdet
@@ -93,6 +95,19 @@ const char *finc_strerror(int status);
 enum { FINC_PLAN_LAYER = 0, FINC_PLAN_UNIT = 1, FINC_PLAN_SPLIT = 2, FINC_PLAN_STACK = 3 };
 int finc_inverse_plan(int kind, int L, int U, int C, int H, int W, int k, int *info,
                       int max_launches);
+
+/* The forward's work split (host arithmetic only): an image is cut into
+ * blocks of rows, each staged in LDS with its halo rows and the layer's
+ * weights; a unit keeps whole images, or bands of rows when the batch is
+ * smaller than the GPU's compute units or an image does not fit (in place,
+ * in_place != 0, a unit keeps whole images).  For finc_forward (kind
+ * FINC_PLAN_LAYER), finc_unit_forward (FINC_PLAN_UNIT) and finc_split_forward
+ * (FINC_PLAN_SPLIT, C = the unit's channels) on a batch of B images it writes
+ * info[0] = blocks per image, info[1] = rows per block, info[2] = LDS bytes
+ * per block, and returns FINC_OK, or FINC_EUNSUPPORTED when even the
+ * smallest block does not fit in gfx950's 160 KB (the forward call then
+ * returns it too), or FINC_EINVAL. */
+int finc_forward_plan(int kind, int B, int C, int H, int W, int k, int in_place, int *info);
 
 /* ---- Weight preparation (one-time per weight set) -----------------------
  * The inverse of one layer solves, per pixel, L x_p = y_p - sum_s K_s x_src

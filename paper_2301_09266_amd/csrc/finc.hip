@@ -1975,13 +1975,14 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B, boo
     p.NG = ceil_div(p.nq, 4);
     p.n = n;
     p.corner0 = corner0;
+    int rb_min;
     if (n == 1) {
         // row blocks of about 128 pixels (eight 16-pixel tiles, two a wave),
         // halved while the grid has fewer blocks than the chip has compute
         // units, but never below a full tile: every block stages all of the
         // layer's weights, so more and smaller blocks pay that again for less
         // work
-        const int rb_min = imin(H, ceil_div(16, W));
+        rb_min = imin(H, ceil_div(16, W));
         p.RB = imax(rb_min, imin(H, ceil_div(128, W)));
         while (p.RB > rb_min && (long long)B * ceil_div(H, p.RB) < kFwdMinBlocks)
             p.RB = imax(rb_min, p.RB / 2);
@@ -1990,18 +1991,28 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B, boo
         // units, bands of rows: TL and TR read k-1 rows up, BL and BR k-1
         // rows down, so a band stages 2(k-1) rows each side and each layer
         // also computes the rows of the halo its later layers read
-        const int rb_min = imin(H, imax(ceil_div(16, W), 2 * p.P));
+        rb_min = imin(H, imax(ceil_div(16, W), 2 * p.P));
         p.RB = H;
         while (!whole && p.RB > rb_min && (long long)B * ceil_div(H, p.RB) < kFwdMinBlocks)
             p.RB = imax(rb_min, p.RB / 2);
     }
-    p.nblk = ceil_div(H, p.RB);
-    p.HB = n > 1 && p.nblk > 1 ? 2 * p.P : p.P;
-    p.offI = 0;
-    p.offO = (p.RB + 2 * p.HB) * p.WP * p.CP;
-    p.offW = p.offO + (n > 1 ? imin(H, p.RB + 3 * p.P) * W * p.CP : 0);
-    p.offD = p.offW + p.NT * p.NG * 256;
-    p.lds_floats = p.offD + round_up4(4 * p.NG);
+    // LDS layout for the rows of a block; blocks (bands, for a unit not
+    // computed in place) are halved further while it does not fit
+    auto layout = [&] {
+        p.nblk = ceil_div(H, p.RB);
+        p.HB = n > 1 && p.nblk > 1 ? 2 * p.P : p.P;
+        p.offI = 0;
+        p.offO = (p.RB + 2 * p.HB) * p.WP * p.CP;
+        p.offW = p.offO + (n > 1 ? imin(H, p.RB + 3 * p.P) * W * p.CP : 0);
+        p.offD = p.offW + p.NT * p.NG * 256;
+        p.lds_floats = p.offD + round_up4(4 * p.NG);
+    };
+    layout();
+    while ((size_t)p.lds_floats * sizeof(float) > kLdsBytes && p.RB > rb_min &&
+           !(n > 1 && whole)) {
+        p.RB = imax(rb_min, p.RB / 2);
+        layout();
+    }
     const int rb_last = H - (p.nblk - 1) * p.RB;
     p.d_plane = make_fastdiv((p.RB + 2 * p.HB) * p.WP);
     p.d_plane_last = make_fastdiv((rb_last + 2 * p.HB) * p.WP);
@@ -2398,6 +2409,22 @@ const char *finc_strerror(int status) {
     case FINC_EHIP: return "HIP runtime error";
     default: return "unknown status";
     }
+}
+
+int finc_forward_plan(int kind, int B, int C, int H, int W, int k, int in_place, int *info) {
+    if (!info || (kind != FINC_PLAN_LAYER && kind != FINC_PLAN_UNIT && kind != FINC_PLAN_SPLIT))
+        return FINC_EINVAL;
+    if (kind == FINC_PLAN_SPLIT ? !valid_split(B, C, H, W, k) : !valid_shape(B, C, H, W, k))
+        return FINC_EINVAL;
+    const bool unit = kind == FINC_PLAN_UNIT;
+    const FwdPlan fp = kind == FINC_PLAN_SPLIT
+                           ? make_fwd_plan(C / 4, H, W, k, 1, FINC_TL, 4 * B, false)
+                           : make_fwd_plan(C, H, W, k, unit ? 4 : 1, FINC_TL, B,
+                                           unit && in_place);
+    info[0] = fp.nblk;
+    info[1] = fp.RB;
+    info[2] = fp.lds_floats * (int)sizeof(float);
+    return (size_t)info[2] <= kLdsBytes ? FINC_OK : FINC_EUNSUPPORTED;
 }
 
 static void put_choice(const InvChoice &c, int *dst) {

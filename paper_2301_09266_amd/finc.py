@@ -27,6 +27,7 @@ SIGNATURES = {
     "finc_version": (_i, []),
     "finc_strerror": (ctypes.c_char_p, [_i]),
     "finc_inverse_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i), _i]),
+    "finc_forward_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i)]),
     "finc_workspace_bytes": (_sz, [_i, _i, _i]),
     "finc_prepare": (_i, [_vp, _i, ctypes.POINTER(_i), _i, _i, _vp, _vp]),
     "finc_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
@@ -140,6 +141,16 @@ def inverse_plan(kind: int, C: int, H: int, W: int, k: int, L: int = 1, U: int =
         return n
     keys = ("threads", "mode", "groups", "streamed", "lds", "compact")
     return [dict(zip(keys, info[6 * i:6 * i + 6])) for i in range(n)]
+
+
+def forward_plan(kind: int, B: int, C: int, H: int, W: int, k: int, in_place: bool = False):
+    """The forward's row blocks (finc_forward_plan): dict(blocks, rows, lds),
+    or the negative status (EUNSUPPORTED when a block does not fit)."""
+    info = (ctypes.c_int * 3)()
+    rc = _require_lib().finc_forward_plan(kind, B, C, H, W, k, int(in_place), info)
+    if rc < 0:
+        return rc
+    return dict(blocks=info[0], rows=info[1], lds=info[2])
 
 
 def workspace_bytes(C: int, k: int, n_layers: int = 1) -> int:

@@ -114,3 +114,33 @@ def test_plan_rejects_bad_arguments():
     assert lib.finc_inverse_plan(3, 3, 8, 12, 32, 32, 3, info, 2) == finc.EINVAL   # 3 launches
     assert lib.finc_inverse_plan(0, 1, 1, 12, 16, 16, 3, info, 1) == 1
     assert info[0] == 256 and info[1] == 5 and info[2] == 2 and info[3] == 0
+
+
+def test_forward_plan():
+    """The forward's row blocks: about 128 pixels, halved until the grid has
+    a block per compute unit; units in bands when the batch is small or an
+    image does not fit; EUNSUPPORTED only when one block of rows with its
+    halo exceeds LDS."""
+    L, U, S = finc.PLAN_LAYER, finc.PLAN_UNIT, finc.PLAN_SPLIT
+    assert finc.forward_plan(L, 64, 12, 16, 16, 3) == dict(blocks=4, rows=4, lds=finc.forward_plan(
+        L, 64, 12, 16, 16, 3)["lds"])
+    assert finc.forward_plan(U, 256, 12, 16, 16, 3)["blocks"] == 1      # whole images
+    assert finc.forward_plan(U, 64, 12, 32, 32, 3)["blocks"] == 4       # bands of 8 rows
+    assert finc.forward_plan(U, 64, 12, 32, 32, 3, in_place=True)["blocks"] == 1
+    assert finc.forward_plan(S, 64, 48, 16, 16, 3)["lds"] <= 160 * 1024
+    # a unit at 12 x 128 x 128: too large whole, bands fit
+    p = finc.forward_plan(U, 512, 12, 128, 128, 3)
+    assert p["blocks"] > 1 and p["lds"] <= 160 * 1024
+    assert finc.forward_plan(U, 512, 12, 128, 128, 3, in_place=True) == finc.EUNSUPPORTED
+    # one row of 16384 pixels and 64 channels does not fit
+    assert finc.forward_plan(L, 1, 64, 2, 16384, 3) == finc.EUNSUPPORTED
+    assert finc.forward_plan(L, 1, 65, 2, 16, 3) == finc.EINVAL
+    # every block stages all of a layer's weights (C^2 k^2 floats, padded):
+    # the largest C per k for 8 x 8 and 32 x 32 images at batch 64 -- every
+    # smaller C fits, no larger one does
+    for kind, n, row in ((L, 8, (64, 64, 60, 44, 32, 28, 20)), (L, 32, (64, 64, 52, 36, 32, 24, 16)),
+                         (U, 8, (64, 64, 48, 36, 32, 24, 16)), (U, 32, (64, 64, 32, 24, 16, 12, 12))):
+        for k, cmax in enumerate(row, start=1):
+            for C in range(1, 65):
+                ok = not isinstance(finc.forward_plan(kind, 64, C, n, n, k), int)
+                assert ok == (C <= cmax), (kind, C, n, k)

@@ -2374,21 +2374,36 @@ bool valid_stack(int B, int L, int U, int C1, int H1, int W1, int k) {
                                                         W1 >> (L - 1), k);
 }
 
+// Arguments of a stack call.  x (written) must be clear of every buffer the
+// call reads: the latents, scale, bias, and K or the prepared weights (wb);
+// a workspace the call writes (wb_written) must be clear of all of them too.
 bool stack_call_ok(const float *const *z, const float *x, const float *scale,
-                   const float *bias, int B, int L, int U, int C1, int H1, int W1, int k) {
-    if (!valid_stack(B, L, U, C1, H1, W1, k) || !z || !x || !scale || !bias)
+                   const float *bias, int B, int L, int U, int C1, int H1, int W1, int k,
+                   const float *K, const void *wb, bool wb_written) {
+    if (!valid_stack(B, L, U, C1, H1, W1, k) || !z || !x || !scale || !bias || !wb)
         return false;
     for (int l = 0; l < L; ++l)
         if (!z[l])
             return false;
+    size_t sb = 0, kb = 0;   // bytes of scale (= of bias), of K
+    for (int l = 0; l < L; ++l) {
+        sb += (size_t)U * (C1 << l) * sizeof(float);
+        kb += (size_t)U * 4 * (C1 << l) * (C1 << l) * k * k * sizeof(float);
+    }
+    const size_t wbytes = finc_stack_workspace_bytes(L, U, C1, k);
     const size_t xbytes = (size_t)B * C1 * H1 * W1 * sizeof(float);
+    auto clear = [&](const void *p, size_t n) {
+        return !overlap(p, n, x, xbytes) && !(wb_written && overlap(p, n, wb, wbytes));
+    };
     for (int l = 0; l < L; ++l) {
         const int C = C1 << l, H = H1 >> l, W = W1 >> l;
         const size_t zb = (size_t)B * (l == L - 1 ? C : C / 2) * H * W * sizeof(float);
-        if (overlap(z[l], zb, x, xbytes))
+        if (!clear(z[l], zb))
             return false;
     }
-    return true;
+    if (!clear(scale, sb) || !clear(bias, sb) || (K && !clear(K, kb)))
+        return false;
+    return !overlap(wb, wbytes, x, xbytes);
 }
 
 }  // namespace
@@ -2806,7 +2821,7 @@ int finc_stack_inverse_prepared(const float *const *z, float *x, const void *pre
                                 const float *scale, const float *bias, int B, int L, int U,
                                 int C1, int H1, int W1, int k, hipStream_t stream) {
     if (!prepared || !aligned256(prepared) ||
-        !stack_call_ok(z, x, scale, bias, B, L, U, C1, H1, W1, k))
+        !stack_call_ok(z, x, scale, bias, B, L, U, C1, H1, W1, k, nullptr, prepared, false))
         return FINC_EINVAL;
     InvArgs a;
     memset(&a, 0, sizeof(a));
@@ -2862,10 +2877,7 @@ int finc_stack_inverse(const float *const *z, float *x, const float *K, const fl
                        const float *bias, int B, int L, int U, int C1, int H1, int W1, int k,
                        void *workspace, hipStream_t stream) {
     if (!K || !workspace || !aligned256(workspace) ||
-        !stack_call_ok(z, x, scale, bias, B, L, U, C1, H1, W1, k))
-        return FINC_EINVAL;
-    const size_t wsb = finc_stack_workspace_bytes(L, U, C1, k);
-    if (overlap(workspace, wsb, x, (size_t)B * C1 * H1 * W1 * sizeof(float)))
+        !stack_call_ok(z, x, scale, bias, B, L, U, C1, H1, W1, k, K, workspace, true))
         return FINC_EINVAL;
     if (B == 0)   // nothing to launch; the shape is still checked
         return finc_stack_inverse_prepared(z, x, workspace, scale, bias, 0, L, U, C1, H1, W1, k,

@@ -117,12 +117,21 @@ def _logdet_out(t: torch.Tensor | None):
     return t
 
 
+def _bytes_buf(t: torch.Tensor, nbytes: int, name: str):
+    """A device buffer of at least nbytes (prepared weights, workspaces)."""
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.numel() * t.element_size() < nbytes:
+        raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes, needs {nbytes}")
+    return t
+
+
 def _workspace(nbytes: int, device, ws):
     if ws is None:
         return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
-    if ws.numel() * ws.element_size() < nbytes:
-        raise ValueError("workspace too small")
-    return ws
+    return _bytes_buf(ws, nbytes, "workspace")
 
 
 # ---------------------------------------------------------------------------
@@ -224,6 +233,7 @@ def inverse_prepared(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: in
     L = _require_lib()
     _dev(y, "y")
     B, C, H, W = y.shape
+    _bytes_buf(prepared, workspace_bytes(C, k, 1), "prepared")
     x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
     _check(L.finc_inverse_prepared(_ptr(y), _ptr(x), _ptr(prepared), B, C, H, W, k, corner,
                                    _stream()), "finc_inverse_prepared")
@@ -298,6 +308,7 @@ def unit_inverse_prepared(y: torch.Tensor, prepared4: torch.Tensor, k: int,
     L = _require_lib()
     _dev(y, "y")
     B, C, H, W = y.shape
+    _bytes_buf(prepared4, workspace_bytes(C, k, 4), "prepared4")
     x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
     _check(L.finc_unit_inverse_prepared(_ptr(y), _ptr(x), _ptr(prepared4), B, C, H, W, k,
                                         _stream()), "finc_unit_inverse_prepared")
@@ -352,24 +363,46 @@ def split_inverse_prepared(y: torch.Tensor, prepared4: torch.Tensor, k: int,
     L = _require_lib()
     _dev(y, "y")
     B, C, H, W = y.shape
+    _bytes_buf(prepared4, workspace_bytes(C // 4, k, 4), "prepared4")
     x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
     _check(L.finc_split_inverse_prepared(_ptr(y), _ptr(x), _ptr(prepared4), B, C, H, W, k,
                                          _stream()), "finc_split_inverse_prepared")
     return x
 
 
-def _stack_args(z, L_levels):
+def _stack_args(z, L_levels, C1, H1, W1):
+    """Latents z[l]: (B, C_l / 2, H_l, W_l) below the top, (B, C_top, H_top,
+    W_top) at the top, C_l = C1 2^l, H_l = H1 / 2^l."""
     if len(z) != L_levels:
         raise ValueError("one latent per level")
-    for i, t in enumerate(z):
-        _dev(t, f"z[{i}]")
+    B = z[0].shape[0] if z[0].dim() == 4 else -1
+    for l, t in enumerate(z):
+        C = C1 << l
+        _dev(t, f"z[{l}]", (B, C if l == L_levels - 1 else C // 2, H1 >> l, W1 >> l))
     return (ctypes.c_void_p * L_levels)(*[t.data_ptr() for t in z])
+
+
+def _stack_params(L_levels, U, C1, k, scale, bias, K=None):
+    """scale, bias: U * sum_l C_l floats; K: U * 4 * sum_l C_l^2 k^2 floats."""
+    chans = sum(C1 << l for l in range(L_levels))
+    for name, t in (("scale", scale), ("bias", bias)):
+        _dev(t, name)
+        if t.numel() != U * chans:
+            raise ValueError(f"{name} has {t.numel()} elements, expected {U * chans}")
+    if K is not None:
+        _dev(K, "K")
+        n = U * 4 * sum((C1 << l) ** 2 for l in range(L_levels)) * k * k
+        if K.numel() != n:
+            raise ValueError(f"K has {K.numel()} elements, expected {n}")
 
 
 def stack_prepare(K: torch.Tensor, L: int, U: int, C1: int, k: int,
                   out: torch.Tensor | None = None):
     lb = _require_lib()
     _dev(K, "K")
+    n = U * 4 * sum((C1 << l) ** 2 for l in range(L)) * k * k
+    if K.numel() != n:
+        raise ValueError(f"K has {K.numel()} elements, expected {n}")
     out = _workspace(stack_workspace_bytes(L, U, C1, k), K.device, out)
     _check(lb.finc_stack_prepare(_ptr(K), L, U, C1, k, _ptr(out), _stream()),
            "finc_stack_prepare")
@@ -381,9 +414,8 @@ def stack_inverse(z, K: torch.Tensor, scale: torch.Tensor, bias: torch.Tensor, L
                   workspace: torch.Tensor | None = None):
     """z: list of L latents (see finc.h); K, scale, bias: flat device tensors."""
     lb = _require_lib()
-    zp = _stack_args(z, L)
-    for name, t in (("K", K), ("scale", scale), ("bias", bias)):
-        _dev(t, name)
+    zp = _stack_args(z, L, C1, H1, W1)
+    _stack_params(L, U, C1, k, scale, bias, K)
     B = z[0].shape[0]
     x = (torch.empty((B, C1, H1, W1), dtype=torch.float32, device=z[0].device)
          if out is None else _dev(out, "out", (B, C1, H1, W1)))
@@ -397,7 +429,9 @@ def stack_inverse_prepared(z, prepared: torch.Tensor, scale: torch.Tensor,
                            bias: torch.Tensor, L: int, U: int, C1: int, H1: int, W1: int,
                            k: int, out: torch.Tensor | None = None):
     lb = _require_lib()
-    zp = _stack_args(z, L)
+    zp = _stack_args(z, L, C1, H1, W1)
+    _stack_params(L, U, C1, k, scale, bias)
+    _bytes_buf(prepared, stack_workspace_bytes(L, U, C1, k), "prepared")
     B = z[0].shape[0]
     x = (torch.empty((B, C1, H1, W1), dtype=torch.float32, device=z[0].device)
          if out is None else _dev(out, "out", (B, C1, H1, W1)))

@@ -180,6 +180,43 @@ def test_stack_rejects():
                                   None) == finc.EINVAL
 
 
+def test_stack_overlaps_rejected():
+    """The output x is written, so every buffer the stack reads (latents,
+    scale, bias, K or the prepared weights) must be clear of it; the
+    workspace is written too and must be clear of all of them."""
+    lib = finc.lib()
+    x, ws = 0x50000000, 0x40000000     # x: 3 MB, workspace: 3.4 MB
+    zs = [0x1000000, 0x2000000, 0x3000000]
+    K, S, Bi = 0x60000000, 0x61000000, 0x62000000
+    shape = (64, 3, 8, 12, 32, 32, 3)
+
+    def full(z=zs, K=K, S=S, Bi=Bi, x=x, ws=ws):
+        zz = (ctypes.c_void_p * 3)(*z)
+        return lib.finc_stack_inverse(zz, ctypes.c_void_p(x), ctypes.c_void_p(K),
+                                      ctypes.c_void_p(S), ctypes.c_void_p(Bi), *shape,
+                                      ctypes.c_void_p(ws), None)
+
+    def prepared(z=zs, S=S, Bi=Bi, x=x, p=ws, B=64):
+        # (B = 64 only where the checks reject the call before any HIP call)
+        zz = (ctypes.c_void_p * 3)(*z)
+        return lib.finc_stack_inverse_prepared(zz, ctypes.c_void_p(x), ctypes.c_void_p(p),
+                                               ctypes.c_void_p(S), ctypes.c_void_p(Bi), B,
+                                               *shape[1:], None)
+
+    assert prepared(B=0) == finc.OK                           # (B = 0: checks only)
+    assert full(S=x + 64) == finc.EINVAL                      # scale inside x
+    assert full(Bi=x + 4096) == finc.EINVAL                   # bias inside x
+    assert full(K=x + 1024) == finc.EINVAL                    # K inside x
+    assert full(K=ws + 1024) == finc.EINVAL                   # K inside the workspace
+    assert full(S=ws + 64) == finc.EINVAL                     # scale inside the workspace
+    assert full(z=[zs[0], ws + 512, zs[2]]) == finc.EINVAL    # a latent inside the workspace
+    assert full(z=[x + 4, zs[1], zs[2]]) == finc.EINVAL       # a latent inside x
+    assert prepared(p=x) == finc.EINVAL                       # prepared weights inside x
+    assert prepared(S=x + 64) == finc.EINVAL
+    assert prepared(Bi=x + 64) == finc.EINVAL
+    assert prepared(S=ws, Bi=ws + 8, B=0) == finc.OK          # read-only buffers may share
+
+
 def test_empty_batch_enqueues_nothing():
     lib = finc.lib()
     ws = ctypes.c_void_p(0x4000000)

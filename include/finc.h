@@ -157,6 +157,24 @@ int finc_inverse_prepared(const float *y, float *x, const void *prepared, int B,
                           int C, int H, int W, int k, int corner,
                           hipStream_t stream);
 
+/* ---- The inverse for callers that cannot allocate ------------------------
+ * finc_inverse_noalloc: finc_inverse without a workspace argument, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  The prepared
+ * weights go to a 1 MiB device array of the library's own, one per device,
+ * held until the process ends; the largest layer the library accepts
+ * (C = 64, k = 7) needs 803,072 bytes of it, so every valid shape fits
+ * (FINC_EUNSUPPORTED would report one that did not).  The call allocates and
+ * frees nothing.  Its first call on a device looks up that device's array
+ * address (a HIP runtime query).  Every call on one device shares that
+ * device's array and rewrites all of it that the inverse reads: calls that
+ * overlap on one device -- concurrently from several host threads, or on
+ * several streams without ordering between them -- race and must not be
+ * made.  Arguments, aliasing (x == y allowed) and results as finc_inverse:
+ * bit for bit the same output. */
+int finc_inverse_noalloc(const float *y, float *x, const float *K, int B, int C, int H,
+                         int W, int k, int corner, hipStream_t stream);
+
 /* ---- FInC unit: four PCBs TL, TR, BL, BR applied in sequence -----------
  * (Sec. 4.3 and Fig. 2a, read as four full-channel blocks one after the
  * other; the inverse runs BR^-1, BL^-1, TR^-1, TL^-1 in one launch, as

@@ -23,6 +23,7 @@
 //    deterministic and independent of the batch size.
 
 #include <hip/hip_runtime.h>
+#include <mutex>
 #include <type_traits>
 
 #include <stdint.h>
@@ -2406,6 +2407,35 @@ bool stack_call_ok(const float *const *z, const float *x, const float *scale,
     return !overlap(wb, wbytes, x, xbytes);
 }
 
+// Prepared weights of finc_inverse_noalloc: one layer at the largest shape
+// the library accepts (C = 64, k = 7: 803,072 bytes), in a device array of
+// the library's own.  Each device holds its copy (at its own address) until
+// the process ends.  In host code `scratch` names a host-side stand-in; the
+// device address comes from hipGetSymbolAddress, once per device.
+constexpr size_t kScratchBytes = 1u << 20;
+static __device__ __align__(256) float scratch[kScratchBytes / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void *scratch_ptr[kMaxDevices];
+
+// Device address of this device's scratch array (looked up on the first call
+// on the device, with that device current).
+int scratch_of_device(void **out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return FINC_EHIP;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (!scratch_ptr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p)
+            return FINC_EHIP;
+        scratch_ptr[dev] = p;
+    }
+    *out = scratch_ptr[dev];
+    return FINC_OK;
+}
+
 }  // namespace
 
 // ===========================================================================
@@ -2628,6 +2658,27 @@ int finc_inverse(const float *y, float *x, const float *K, int B, int C, int H, 
     if (rc != FINC_OK)
         return rc;
     return finc_inverse_prepared(y, x, workspace, B, C, H, W, k, corner, stream);
+}
+
+int finc_inverse_noalloc(const float *y, float *x, const float *K, int B, int C, int H, int W,
+                         int k, int corner, hipStream_t stream) {
+    if (!valid_shape(B, C, H, W, k) || !valid_corner(corner) || !x || !y || !K)
+        return FINC_EINVAL;
+    if (finc_workspace_bytes(C, k, 1) > kScratchBytes)
+        return FINC_EUNSUPPORTED;   // (no shape the library accepts gets here)
+    const size_t bytes = (size_t)B * C * H * W * sizeof(float);
+    if (!inverse_alias_ok(y, x, bytes))
+        return FINC_EINVAL;
+    if (B == 0) {   // nothing to launch; the shape is still checked
+        int info[6];
+        const int n = finc_inverse_plan(FINC_PLAN_LAYER, 1, 1, C, H, W, k, info, 1);
+        return n < 0 ? n : FINC_OK;
+    }
+    void *ws = nullptr;
+    const int rc = scratch_of_device(&ws);
+    if (rc != FINC_OK)
+        return rc;
+    return finc_inverse(y, x, K, B, C, H, W, k, corner, ws, stream);
 }
 
 int finc_unit_forward(const float *x, float *y, const float *K4, double *logdet,

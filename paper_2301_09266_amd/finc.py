@@ -34,6 +34,7 @@ SIGNATURES = {
     "finc_logdet": (_i, [_vp, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "finc_inverse_noalloc": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "finc_backward": (_i, [_vp, _vp, _vp, _vp, _vp, ctypes.c_double, _i, _i, _i, _i, _i, _i,
                            _vp]),
     "finc_unit_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
@@ -225,6 +226,21 @@ def inverse(y: torch.Tensor, K: torch.Tensor, corner: int, out: torch.Tensor | N
     ws = _workspace(workspace_bytes(C, k, 1), y.device, workspace)
     _check(L.finc_inverse(_ptr(y), _ptr(x), _ptr(K), B, C, H, W, k, corner, _ptr(ws),
                           _stream()), "finc_inverse")
+    return x
+
+
+def inverse_noalloc(y: torch.Tensor, K: torch.Tensor, corner: int,
+                    out: torch.Tensor | None = None):
+    """finc_inverse with the library's own device array for the prepared
+    weights (no workspace); calls on one device must not overlap."""
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    k = K.shape[-1]
+    _dev(K, "K", (C, C, k, k))
+    x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
+    _check(L.finc_inverse_noalloc(_ptr(y), _ptr(x), _ptr(K), B, C, H, W, k, corner, _stream()),
+           "finc_inverse_noalloc")
     return x
 
 

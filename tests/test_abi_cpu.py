@@ -217,6 +217,21 @@ def test_stack_overlaps_rejected():
     assert prepared(S=ws, Bi=ws + 8, B=0) == finc.OK          # read-only buffers may share
 
 
+def test_noalloc_rejects_before_any_hip_call():
+    lib = finc.lib()
+    assert lib.finc_inverse_noalloc(NULL, FAKE2, FAKE, 2, 12, 16, 16, 3, 0, None) == finc.EINVAL
+    assert lib.finc_inverse_noalloc(FAKE, FAKE2, NULL, 2, 12, 16, 16, 3, 0, None) == finc.EINVAL
+    assert lib.finc_inverse_noalloc(FAKE, FAKE2, FAKE, 2, 65, 16, 16, 3, 0, None) == finc.EINVAL
+    assert lib.finc_inverse_noalloc(FAKE, FAKE2, FAKE, 2, 12, 16, 16, 3, 4, None) == finc.EINVAL
+    # x overlapping y other than exactly (in place) is rejected
+    assert lib.finc_inverse_noalloc(FAKE, ctypes.c_void_p(0x100000 + 64), FAKE, 2, 12, 16, 16, 3,
+                                    0, None) == finc.EINVAL
+    # an empty batch checks the shape and enqueues nothing
+    assert lib.finc_inverse_noalloc(FAKE, FAKE2, FAKE, 0, 12, 16, 16, 3, 0, None) == finc.OK
+    assert lib.finc_inverse_noalloc(FAKE, FAKE2, FAKE, 0, 64, 16, 16, 7, 0,
+                                    None) == finc.EUNSUPPORTED
+
+
 def test_empty_batch_enqueues_nothing():
     lib = finc.lib()
     ws = ctypes.c_void_p(0x4000000)

@@ -59,11 +59,23 @@ def load(path: str = LIB):
         "orc_unsqueeze": [_dp, _dp, L, I, I, I],
         "orc_stack_forward": [_dp, ctypes.POINTER(_dp), _dp, _dp, _dp, L, I, I, I, I, I, I],
         "orc_stack_inverse": [ctypes.POINTER(_dp), _dp, _dp, _dp, _dp, L, I, I, I, I, I, I],
+        "orc_conv1x1_forward": [_dp, _dp, _dp, L, I, I, I],
+        "orc_conv1x1_inverse": [_dp, _dp, _dp, L, I, I, I],
+        "orc_conv1x1_logdet": [_dp, I, I, I, _dp],
+        "orc_coupling_net": [_dp, _dp, _dp, L, I, I, I, I],
+        "orc_coupling_forward": [_dp, _dp, _dp, L, I, I, I, I, _dp],
+        "orc_coupling_inverse": [_dp, _dp, _dp, L, I, I, I, I],
+        "orc_step_forward": [_dp, _dp, _dp, L, I, I, I, I, I, _dp],
+        "orc_step_inverse": [_dp, _dp, _dp, L, I, I, I, I, I],
+        "orc_flow_params": [I, I, I, I, I],
+        "orc_flow_forward": [_dp, ctypes.POINTER(_dp), _dp, L, I, I, I, I, I, I, I, _dp],
+        "orc_flow_sample": [ctypes.POINTER(_dp), _dp, _dp, L, I, I, I, I, I, I, I],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
         fn.argtypes = args
         fn.restype = None if name.startswith(("orc_actnorm", "orc_squeeze", "orc_unsqueeze")) else I
+    lib.orc_flow_params.restype = L
     if path == LIB:
         _lib = lib
     return lib
@@ -221,6 +233,92 @@ class Oracle:
         zp = (_dp * levels)(*[_p(a) for a in z])
         _check(self.lib.orc_stack_inverse(zp, _p(x), _p(Kf), _p(sf), _p(bf), B, levels,
                                           units, C1, H1, W1, k))
+        return x
+
+
+    # ---- the full FInC Flow: 1x1 convolution, coupling, Step, multi-scale
+    # flow (parameter layout: see finc_oracle.c)
+    def conv1x1_forward(self, x, Wm) -> np.ndarray:
+        x, Wm = _c(x), _c(Wm)
+        y = np.empty_like(x)
+        _check(self.lib.orc_conv1x1_forward(_p(x), _p(y), _p(Wm), *x.shape))
+        return y
+
+    def conv1x1_inverse(self, y, Wm) -> np.ndarray:
+        y, Wm = _c(y), _c(Wm)
+        x = np.empty_like(y)
+        _check(self.lib.orc_conv1x1_inverse(_p(y), _p(x), _p(Wm), *y.shape))
+        return x
+
+    def conv1x1_logdet(self, Wm, H: int, W: int) -> float:
+        Wm = _c(Wm)
+        out = np.zeros(1)
+        _check(self.lib.orc_conv1x1_logdet(_p(Wm), Wm.shape[0], H, W, _p(out)))
+        return float(out[0])
+
+    def coupling_net(self, xa, cp, hid: int) -> np.ndarray:
+        xa, cp = _c(xa), _c(cp)
+        B, Ch, H, W = xa.shape
+        h = np.empty((B, 2 * Ch, H, W))
+        _check(self.lib.orc_coupling_net(_p(xa), _p(h), _p(cp), B, 2 * Ch, H, W, hid))
+        return h
+
+    def coupling_forward(self, x, cp, hid: int):
+        """(y, logdet per image)."""
+        x, cp = _c(x), _c(cp)
+        y, ld = np.empty_like(x), np.zeros(x.shape[0])
+        _check(self.lib.orc_coupling_forward(_p(x), _p(y), _p(cp), *x.shape, hid, _p(ld)))
+        return y, ld
+
+    def coupling_inverse(self, y, cp, hid: int) -> np.ndarray:
+        y, cp = _c(y), _c(cp)
+        x = np.empty_like(y)
+        _check(self.lib.orc_coupling_inverse(_p(y), _p(x), _p(cp), *y.shape, hid))
+        return x
+
+    def step_forward(self, x, sp, k: int, hid: int):
+        """(y, logdet per image) of one FInC Flow Step."""
+        x, sp = _c(x), _c(sp)
+        y, ld = np.empty_like(x), np.zeros(x.shape[0])
+        _check(self.lib.orc_step_forward(_p(x), _p(y), _p(sp), *x.shape, k, hid, _p(ld)))
+        return y, ld
+
+    def step_inverse(self, y, sp, k: int, hid: int) -> np.ndarray:
+        y, sp = _c(y), _c(sp)
+        x = np.empty_like(y)
+        _check(self.lib.orc_step_inverse(_p(y), _p(x), _p(sp), *y.shape, k, hid))
+        return x
+
+    def flow_params(self, L: int, K: int, C0: int, k: int, hid: int) -> int:
+        return int(self.lib.orc_flow_params(L, K, C0, k, hid))
+
+    @staticmethod
+    def flow_latent_shapes(B, L, C0, H0, W0):
+        out = []
+        for l in range(L):
+            C, H, W = (4 * C0) << l, H0 >> (l + 1), W0 >> (l + 1)
+            out.append((B, C if l == L - 1 else C // 2, H, W))
+        return out
+
+    def flow_forward(self, x, params, L: int, K: int, k: int, hid: int):
+        """(latents z[0..L-1], logdet per image)."""
+        x, params = _c(x), _c(params)
+        B, C0, H0, W0 = x.shape
+        z = [np.empty(s) for s in self.flow_latent_shapes(B, L, C0, H0, W0)]
+        ld = np.zeros(B)
+        zp = (_dp * L)(*[_p(a) for a in z])
+        _check(self.lib.orc_flow_forward(_p(x), zp, _p(params), B, L, K, C0, H0, W0, k, hid,
+                                         _p(ld)))
+        return z, ld
+
+    def flow_sample(self, z, params, L: int, K: int, C0: int, H0: int, W0: int, k: int,
+                    hid: int) -> np.ndarray:
+        z = [_c(a) for a in z]
+        params = _c(params)
+        B = z[0].shape[0]
+        x = np.empty((B, C0, H0, W0))
+        zp = (_dp * L)(*[_p(a) for a in z])
+        _check(self.lib.orc_flow_sample(zp, _p(x), _p(params), B, L, K, C0, H0, W0, k, hid))
         return x
 
 

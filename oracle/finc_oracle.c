@@ -556,3 +556,531 @@ int orc_backward(const double *x, const double *dy, const double *K, double *dx,
     }
     return ORC_OK;
 }
+
+/* ==========================================================================
+ * The full FInC Flow (Sec. 4.4 "Architecture", Fig. 2b and 2c).
+ *
+ * A FInC Flow Step is, in the forward direction, a FInC unit (the
+ * channel-split unit above, Sec. 4.3), an actnorm, an invertible 1x1
+ * convolution and an affine coupling layer, in that order.  Readings taken
+ * where the paper only names the layers (it follows Glow for all three):
+ *  - 1x1 convolution: y = Wm x at every pixel, Wm a C x C matrix; its
+ *    log|det| is H W log|det Wm|.
+ *  - Coupling (RealNVP / Glow): x = [xa, xb] (channel halves); the network
+ *    h = NN(xa) has C output channels, its first half the shift t, its
+ *    second half the raw scale r; scale = sigmoid(r + 2);
+ *    yb = (xb + t) * scale, ya = xa; log|det| = sum log scale (per image).
+ *    NN is a 3x3 convolution, ReLU, a 1x1 convolution, ReLU, and a 3x3
+ *    convolution whose output channel c is multiplied by exp(3 ls[c]) (the
+ *    "modified" zero-initialised 3x3 convolution of Glow / Emerging); every
+ *    convolution has a bias and zero "same" padding.
+ *  - Multi-scale (Fig. 2c): per level, squeeze, K steps, then (below the
+ *    top) split: the first half h1 goes on; the second half h2 becomes the
+ *    latent z = (h2 - mean) * exp(-logsd) with (mean, logsd) = the halves of
+ *    a prior network on h1, a 3x3 convolution with bias and exp(3 ls)
+ *    output scale (Glow's split prior; its log|det| is -sum logsd).  The
+ *    top level's output is the last latent.
+ *
+ * Parameter layout (doubles; C the level's channels, Ch = C/2, q = C/4,
+ * hid the coupling network's width, k the unit kernel size):
+ *   step:  Kq4 (4 q q k k) | an_s (C) | an_b (C) | Wm (C C) |
+ *          W1 (hid Ch 3 3) | b1 (hid) | W2 (hid hid) | b2 (hid) |
+ *          W3 (C hid 3 3) | b3 (C) | ls3 (C)
+ *   prior: Wp (C Ch 3 3) | bp (C) | lsp (C)
+ *   flow:  for level l = 0 .. L-1: K steps, then (l < L-1) the prior.
+ * Convolution weights are OIHW.  Level l has C_l = 4 C0 2^l channels and
+ * H0 / 2^(l+1) x W0 / 2^(l+1) pixels.
+ * ========================================================================== */
+
+/* y = Wm x at every pixel. */
+int orc_conv1x1_forward(const double *x, double *y, const double *Wm, long B, int C, int H,
+                        int W)
+{
+    if (B < 0 || C < 1 || H < 1 || W < 1 || !x || !y || !Wm)
+        return ORC_EINVAL;
+    const long plane = (long)H * W;
+    for (long n = 0; n < B; ++n)
+        for (int co = 0; co < C; ++co)
+            for (long p = 0; p < plane; ++p) {
+                double s = 0.0;
+                for (int ci = 0; ci < C; ++ci)
+                    s += Wm[(long)co * C + ci] * x[(n * C + ci) * plane + p];
+                y[(n * C + co) * plane + p] = s;
+            }
+    return ORC_OK;
+}
+
+/* LU factorisation with partial pivoting of a C x C matrix (row-major, in
+ * place); perm receives the row order.  Returns the log|det| and its sign in
+ * *sign (0 if singular). */
+static double lu_factor(double *A, int *perm, int C, int *sign)
+{
+    double ld = 0.0;
+    int sg = 1;
+    for (int i = 0; i < C; ++i)
+        perm[i] = i;
+    for (int c = 0; c < C; ++c) {
+        int piv = c;
+        for (int r = c + 1; r < C; ++r)
+            if (fabs(A[(long)r * C + c]) > fabs(A[(long)piv * C + c]))
+                piv = r;
+        if (A[(long)piv * C + c] == 0.0) {
+            *sign = 0;
+            return -INFINITY;
+        }
+        if (piv != c) {
+            for (int j = 0; j < C; ++j) {
+                double t = A[(long)c * C + j];
+                A[(long)c * C + j] = A[(long)piv * C + j];
+                A[(long)piv * C + j] = t;
+            }
+            int t = perm[c];
+            perm[c] = perm[piv];
+            perm[piv] = t;
+            sg = -sg;
+        }
+        double d = A[(long)c * C + c];
+        if (d < 0)
+            sg = -sg;
+        ld += log(fabs(d));
+        for (int r = c + 1; r < C; ++r) {
+            double f = A[(long)r * C + c] / d;
+            A[(long)r * C + c] = f;
+            for (int j = c + 1; j < C; ++j)
+                A[(long)r * C + j] -= f * A[(long)c * C + j];
+        }
+    }
+    *sign = sg;
+    return ld;
+}
+
+/* x = Wm^-1 y at every pixel, by LU with partial pivoting and substitution. */
+int orc_conv1x1_inverse(const double *y, double *x, const double *Wm, long B, int C, int H,
+                        int W)
+{
+    if (B < 0 || C < 1 || H < 1 || W < 1 || !x || !y || !Wm)
+        return ORC_EINVAL;
+    double *A = (double *)malloc(sizeof(double) * C * C);
+    double *v = (double *)malloc(sizeof(double) * C);
+    int *perm = (int *)malloc(sizeof(int) * C);
+    if (!A || !v || !perm) {
+        free(A);
+        free(v);
+        free(perm);
+        return ORC_ENOMEM;
+    }
+    memcpy(A, Wm, sizeof(double) * C * C);
+    int sign;
+    lu_factor(A, perm, C, &sign);
+    int rc = sign == 0 ? ORC_ESINGULAR : ORC_OK;
+    const long plane = (long)H * W;
+    for (long n = 0; n < B && rc == ORC_OK; ++n)
+        for (long p = 0; p < plane; ++p) {
+            for (int r = 0; r < C; ++r) { /* L v = P y */
+                double s = y[(n * C + perm[r]) * plane + p];
+                for (int j = 0; j < r; ++j)
+                    s -= A[(long)r * C + j] * v[j];
+                v[r] = s;
+            }
+            for (int r = C - 1; r >= 0; --r) { /* U x = v */
+                double s = v[r];
+                for (int j = r + 1; j < C; ++j)
+                    s -= A[(long)r * C + j] * v[j];
+                v[r] = s / A[(long)r * C + r];
+            }
+            for (int c = 0; c < C; ++c)
+                x[(n * C + c) * plane + p] = v[c];
+        }
+    free(A);
+    free(v);
+    free(perm);
+    return rc;
+}
+
+/* H W log|det Wm|. */
+int orc_conv1x1_logdet(const double *Wm, int C, int H, int W, double *out)
+{
+    if (C < 1 || H < 1 || W < 1 || !Wm || !out)
+        return ORC_EINVAL;
+    double *A = (double *)malloc(sizeof(double) * C * C);
+    int *perm = (int *)malloc(sizeof(int) * C);
+    if (!A || !perm) {
+        free(A);
+        free(perm);
+        return ORC_ENOMEM;
+    }
+    memcpy(A, Wm, sizeof(double) * C * C);
+    int sign;
+    double ld = lu_factor(A, perm, C, &sign);
+    free(A);
+    free(perm);
+    *out = (double)H * (double)W * ld;
+    return sign == 0 ? ORC_ESINGULAR : ORC_OK;
+}
+
+/* Same-padded r x r convolution (r odd), cross-correlation with zero padding
+ * (r-1)/2 on every side, plus bias; then ReLU (relu != 0), then multiplied by
+ * exp(3 ls[co]) (ls != NULL).  x (B, Ci, H, W), y (B, Co, H, W). */
+static void conv_same(const double *x, double *y, const double *Wt, const double *bias,
+                      const double *ls, long B, int Ci, int Co, int H, int W, int r, int relu)
+{
+    const long plane = (long)H * W;
+    const int pad = (r - 1) / 2;
+    for (long n = 0; n < B; ++n)
+        for (int co = 0; co < Co; ++co)
+            for (int i = 0; i < H; ++i)
+                for (int j = 0; j < W; ++j) {
+                    double s = bias[co];
+                    for (int ci = 0; ci < Ci; ++ci)
+                        for (int a = 0; a < r; ++a)
+                            for (int b = 0; b < r; ++b) {
+                                int ii = i + a - pad, jj = j + b - pad;
+                                if (ii < 0 || ii >= H || jj < 0 || jj >= W)
+                                    continue;
+                                s += Wt[(((long)co * Ci + ci) * r + a) * r + b] *
+                                     x[(n * Ci + ci) * plane + (long)ii * W + jj];
+                            }
+                    if (relu && s < 0.0)
+                        s = 0.0;
+                    if (ls)
+                        s *= exp(3.0 * ls[co]);
+                    y[(n * Co + co) * plane + (long)i * W + j] = s;
+                }
+}
+
+static long coupling_params(int C, int hid)
+{
+    const long Ch = C / 2;
+    return (long)hid * Ch * 9 + hid + (long)hid * hid + hid + (long)C * hid * 9 + 2L * C;
+}
+
+static long step_params(int C, int k, int hid)
+{
+    const long q = C / 4;
+    return 4 * q * q * k * k + 2L * C + (long)C * C + coupling_params(C, hid);
+}
+
+static long prior_params(int C) { return (long)C * (C / 2) * 9 + 2L * C; }
+
+/* The coupling network on xa (B, C/2, H, W) -> h (B, C, H, W); cp points at
+ * W1 of the layout above. */
+int orc_coupling_net(const double *xa, double *h, const double *cp, long B, int C, int H,
+                     int W, int hid)
+{
+    if (B < 0 || C < 2 || (C & 1) || H < 1 || W < 1 || hid < 1 || !xa || !h || !cp)
+        return ORC_EINVAL;
+    const int Ch = C / 2;
+    const long plane = (long)H * W;
+    const double *W1 = cp, *b1 = W1 + (long)hid * Ch * 9, *W2 = b1 + hid, *b2 = W2 + (long)hid * hid;
+    const double *W3 = b2 + hid, *b3 = W3 + (long)C * hid * 9, *ls3 = b3 + C;
+    double *t1 = (double *)malloc(sizeof(double) * (B * hid * plane > 0 ? B * hid * plane : 1));
+    double *t2 = (double *)malloc(sizeof(double) * (B * hid * plane > 0 ? B * hid * plane : 1));
+    if (!t1 || !t2) {
+        free(t1);
+        free(t2);
+        return ORC_ENOMEM;
+    }
+    conv_same(xa, t1, W1, b1, NULL, B, Ch, hid, H, W, 3, 1);
+    conv_same(t1, t2, W2, b2, NULL, B, hid, hid, H, W, 1, 1);
+    conv_same(t2, h, W3, b3, ls3, B, hid, C, H, W, 3, 0);
+    free(t1);
+    free(t2);
+    return ORC_OK;
+}
+
+static double sigmoid(double v) { return 1.0 / (1.0 + exp(-v)); }
+
+/* Affine coupling, forward: ya = xa, yb = (xb + t) sigmoid(r + 2); logdet[n]
+ * += sum over the image of log sigmoid(r + 2) (logdet may be NULL). */
+int orc_coupling_forward(const double *x, double *y, const double *cp, long B, int C, int H,
+                         int W, int hid, double *logdet)
+{
+    if (B < 0 || C < 2 || (C & 1) || H < 1 || W < 1 || !x || !y || !cp)
+        return ORC_EINVAL;
+    const int Ch = C / 2;
+    const long plane = (long)H * W, half = Ch * plane;
+    double *xa = (double *)malloc(sizeof(double) * (B * half > 0 ? B * half : 1));
+    double *h = (double *)malloc(sizeof(double) * (B * 2 * half > 0 ? B * 2 * half : 1));
+    if (!xa || !h) {
+        free(xa);
+        free(h);
+        return ORC_ENOMEM;
+    }
+    for (long n = 0; n < B; ++n)
+        memcpy(xa + n * half, x + n * 2 * half, sizeof(double) * half);
+    int rc = orc_coupling_net(xa, h, cp, B, C, H, W, hid);
+    for (long n = 0; n < B && rc == ORC_OK; ++n) {
+        double ld = 0.0;
+        for (long e = 0; e < half; ++e) {
+            double t = h[n * 2 * half + e], r = h[n * 2 * half + half + e];
+            double s = sigmoid(r + 2.0);
+            y[n * 2 * half + e] = x[n * 2 * half + e];
+            y[n * 2 * half + half + e] = (x[n * 2 * half + half + e] + t) * s;
+            ld += log(s);
+        }
+        if (logdet)
+            logdet[n] += ld;
+    }
+    free(xa);
+    free(h);
+    return rc;
+}
+
+/* Affine coupling, inverse: xa = ya, xb = yb / sigmoid(r + 2) - t with
+ * (t, r) = NN(ya). */
+int orc_coupling_inverse(const double *y, double *x, const double *cp, long B, int C, int H,
+                         int W, int hid)
+{
+    if (B < 0 || C < 2 || (C & 1) || H < 1 || W < 1 || !x || !y || !cp)
+        return ORC_EINVAL;
+    const int Ch = C / 2;
+    const long plane = (long)H * W, half = Ch * plane;
+    double *ya = (double *)malloc(sizeof(double) * (B * half > 0 ? B * half : 1));
+    double *h = (double *)malloc(sizeof(double) * (B * 2 * half > 0 ? B * 2 * half : 1));
+    if (!ya || !h) {
+        free(ya);
+        free(h);
+        return ORC_ENOMEM;
+    }
+    for (long n = 0; n < B; ++n)
+        memcpy(ya + n * half, y + n * 2 * half, sizeof(double) * half);
+    int rc = orc_coupling_net(ya, h, cp, B, C, H, W, hid);
+    for (long n = 0; n < B && rc == ORC_OK; ++n)
+        for (long e = 0; e < half; ++e) {
+            double t = h[n * 2 * half + e], r = h[n * 2 * half + half + e];
+            x[n * 2 * half + e] = y[n * 2 * half + e];
+            x[n * 2 * half + half + e] = y[n * 2 * half + half + e] / sigmoid(r + 2.0) - t;
+        }
+    free(ya);
+    free(h);
+    return rc;
+}
+
+/* One FInC Flow Step, forward: unit (channel-split), actnorm, 1x1, coupling.
+ * logdet (B values, may be NULL) is incremented by the step's log|det| per
+ * image. */
+int orc_step_forward(const double *x, double *y, const double *sp, long B, int C, int H, int W,
+                     int k, int hid, double *logdet)
+{
+    if (B < 0 || C < 4 || (C & 3) || H < 1 || W < 1 || k < 1 || !x || !y || !sp)
+        return ORC_EINVAL;
+    const int q = C / 4;
+    const long n_el = B * (long)C * H * W;
+    const double *Kq4 = sp, *s = Kq4 + 4L * q * q * k * k, *b = s + C, *Wm = b + C;
+    const double *cp = Wm + (long)C * C;
+    double *t1 = (double *)malloc(sizeof(double) * (n_el > 0 ? n_el : 1));
+    double *t2 = (double *)malloc(sizeof(double) * (n_el > 0 ? n_el : 1));
+    if (!t1 || !t2) {
+        free(t1);
+        free(t2);
+        return ORC_ENOMEM;
+    }
+    int rc = orc_split_forward(x, t1, Kq4, B, C, H, W, k);
+    if (rc == ORC_OK) {
+        orc_actnorm_forward(t1, t2, s, b, B, C, H, W);
+        rc = orc_conv1x1_forward(t2, t1, Wm, B, C, H, W);
+    }
+    if (rc == ORC_OK)
+        rc = orc_coupling_forward(t1, y, cp, B, C, H, W, hid, logdet);
+    if (rc == ORC_OK && logdet) {
+        double lu, lw, la = 0.0;
+        rc = orc_split_logdet(Kq4, C, k, H, W, &lu);
+        if (rc == ORC_OK)
+            rc = orc_conv1x1_logdet(Wm, C, H, W, &lw);
+        for (int c = 0; c < C; ++c)
+            la += log(fabs(s[c]));
+        la *= (double)H * W;
+        for (long n = 0; n < B && rc == ORC_OK; ++n)
+            logdet[n] += lu + la + lw;
+    }
+    free(t1);
+    free(t2);
+    return rc;
+}
+
+/* One FInC Flow Step, inverse: coupling^-1, 1x1^-1, actnorm^-1, unit^-1. */
+int orc_step_inverse(const double *y, double *x, const double *sp, long B, int C, int H, int W,
+                     int k, int hid)
+{
+    if (B < 0 || C < 4 || (C & 3) || H < 1 || W < 1 || k < 1 || !x || !y || !sp)
+        return ORC_EINVAL;
+    const int q = C / 4;
+    const long n_el = B * (long)C * H * W;
+    const double *Kq4 = sp, *s = Kq4 + 4L * q * q * k * k, *b = s + C, *Wm = b + C;
+    const double *cp = Wm + (long)C * C;
+    double *t1 = (double *)malloc(sizeof(double) * (n_el > 0 ? n_el : 1));
+    double *t2 = (double *)malloc(sizeof(double) * (n_el > 0 ? n_el : 1));
+    if (!t1 || !t2) {
+        free(t1);
+        free(t2);
+        return ORC_ENOMEM;
+    }
+    int rc = orc_coupling_inverse(y, t1, cp, B, C, H, W, hid);
+    if (rc == ORC_OK)
+        rc = orc_conv1x1_inverse(t1, t2, Wm, B, C, H, W);
+    if (rc == ORC_OK) {
+        orc_actnorm_inverse(t2, t1, s, b, B, C, H, W);
+        rc = orc_split_inverse(t1, x, Kq4, B, C, H, W, k);
+    }
+    free(t1);
+    free(t2);
+    return rc;
+}
+
+/* Floats of a flow's parameters (layout above). */
+long orc_flow_params(int L, int K, int C0, int k, int hid)
+{
+    long n = 0;
+    for (int l = 0; l < L; ++l) {
+        const int C = (4 * C0) << l;
+        n += (long)K * step_params(C, k, hid);
+        if (l < L - 1)
+            n += prior_params(C);
+    }
+    return n;
+}
+
+/* Split prior of a level: (mean, logsd) = halves of a 3x3 convolution of h1
+ * (B, C/2, H, W) with bias and exp(3 ls) output scale. */
+static int prior_net(const double *h1, double *ms, const double *pp, long B, int C, int H, int W)
+{
+    const int Ch = C / 2;
+    conv_same(h1, ms, pp, pp + (long)C * Ch * 9, pp + (long)C * Ch * 9 + C, B, Ch, C, H, W, 3,
+              0);
+    return ORC_OK;
+}
+
+/* Multi-scale flow, forward (density direction): x (B, C0, H0, W0) -> the
+ * latents z[l] (l < L-1: (B, C_l/2, H_l, W_l); z[L-1]: (B, C_{L-1}, H_{L-1},
+ * W_{L-1})) and logdet[n] (B values, overwritten): the sum of every step's
+ * log|det| and of -sum logsd of every split. */
+int orc_flow_forward(const double *x, double *const *z, const double *params, long B, int L,
+                     int K, int C0, int H0, int W0, int k, int hid, double *logdet)
+{
+    if (B < 0 || L < 1 || K < 0 || C0 < 1 || k < 1 || hid < 1 || !x || !z || !params ||
+        !logdet || (H0 % (2 << (L - 1))) || (W0 % (2 << (L - 1))))
+        return ORC_EINVAL;
+    const long tot = B * (long)C0 * H0 * W0;
+    double *h = (double *)malloc(sizeof(double) * (tot > 0 ? tot : 1));
+    double *t = (double *)malloc(sizeof(double) * (tot > 0 ? tot : 1));
+    double *ms = (double *)malloc(sizeof(double) * (tot > 0 ? tot : 1));
+    if (!h || !t || !ms) {
+        free(h);
+        free(t);
+        free(ms);
+        return ORC_ENOMEM;
+    }
+    for (long n = 0; n < B; ++n)
+        logdet[n] = 0.0;
+    memcpy(h, x, sizeof(double) * tot);
+    int C = C0, H = H0, W = W0, rc = ORC_OK;
+    const double *p = params;
+    for (int l = 0; l < L && rc == ORC_OK; ++l) {
+        orc_squeeze(h, t, B, C, H, W);
+        C *= 4;
+        H /= 2;
+        W /= 2;
+        for (int s = 0; s < K && rc == ORC_OK; ++s) {
+            rc = orc_step_forward(t, h, p, B, C, H, W, k, hid, logdet);
+            memcpy(t, h, sizeof(double) * tot);
+            p += step_params(C, k, hid);
+        }
+        if (rc != ORC_OK)
+            break;
+        const long plane = (long)H * W;
+        if (l == L - 1) {
+            memcpy(z[l], t, sizeof(double) * B * C * plane);
+            break;
+        }
+        const int Ch = C / 2;
+        for (long n = 0; n < B; ++n) /* h1 */
+            memcpy(h + n * Ch * plane, t + n * C * plane, sizeof(double) * Ch * plane);
+        prior_net(h, ms, p, B, C, H, W);
+        for (long n = 0; n < B; ++n) {
+            double ld = 0.0;
+            for (long e = 0; e < Ch * plane; ++e) {
+                double mean = ms[n * C * plane + e], logsd = ms[n * C * plane + Ch * plane + e];
+                z[l][n * Ch * plane + e] = (t[n * C * plane + Ch * plane + e] - mean) * exp(-logsd);
+                ld -= logsd;
+            }
+            logdet[n] += ld;
+        }
+        p += prior_params(C);
+        C = Ch;
+    }
+    free(h);
+    free(t);
+    free(ms);
+    return rc;
+}
+
+/* Multi-scale flow, sampling direction: from the latents to x. */
+int orc_flow_sample(const double *const *z, double *x, const double *params, long B, int L,
+                    int K, int C0, int H0, int W0, int k, int hid)
+{
+    if (B < 0 || L < 1 || K < 0 || C0 < 1 || k < 1 || hid < 1 || !x || !z || !params ||
+        (H0 % (2 << (L - 1))) || (W0 % (2 << (L - 1))))
+        return ORC_EINVAL;
+    const long tot = B * (long)C0 * H0 * W0;
+    double *h = (double *)malloc(sizeof(double) * (tot > 0 ? tot : 1));
+    double *t = (double *)malloc(sizeof(double) * (tot > 0 ? tot : 1));
+    double *ms = (double *)malloc(sizeof(double) * (tot > 0 ? tot : 1));
+    const double **sp = (const double **)malloc(sizeof(double *) * (L * (K + 1) + 1));
+    if (!h || !t || !ms || !sp) {
+        free(h);
+        free(t);
+        free(ms);
+        free(sp);
+        return ORC_ENOMEM;
+    }
+    /* where each level's steps and prior start */
+    const double *p = params;
+    for (int l = 0; l < L; ++l) {
+        const int C = (4 * C0) << l;
+        for (int s = 0; s < K; ++s) {
+            sp[l * (K + 1) + s] = p;
+            p += step_params(C, k, hid);
+        }
+        sp[l * (K + 1) + K] = p;
+        if (l < L - 1)
+            p += prior_params(C);
+    }
+    int rc = ORC_OK;
+    int C = (4 * C0) << (L - 1), H = H0 >> L, W = W0 >> L;
+    memcpy(h, z[L - 1], sizeof(double) * B * C * H * W);
+    for (int l = L - 1; l >= 0 && rc == ORC_OK; --l) {
+        const long plane = (long)H * W;
+        if (l < L - 1) {
+            /* h holds h1 (B, C/2, H, W): the prior gives h2 = mean + exp(logsd) z */
+            const int Ch = C / 2;
+            prior_net(h, ms, sp[l * (K + 1) + K], B, C, H, W);
+            for (long n = 0; n < B; ++n) {
+                memcpy(t + n * C * plane, h + n * Ch * plane, sizeof(double) * Ch * plane);
+                for (long e = 0; e < Ch * plane; ++e) {
+                    double mean = ms[n * C * plane + e], logsd = ms[n * C * plane + Ch * plane + e];
+                    t[n * C * plane + Ch * plane + e] = mean + exp(logsd) * z[l][n * Ch * plane + e];
+                }
+            }
+            memcpy(h, t, sizeof(double) * B * C * plane);
+        }
+        for (int s = K - 1; s >= 0 && rc == ORC_OK; --s) {
+            rc = orc_step_inverse(h, t, sp[l * (K + 1) + s], B, C, H, W, k, hid);
+            memcpy(h, t, sizeof(double) * B * C * plane);
+        }
+        orc_unsqueeze(h, t, B, C, H, W);
+        C /= 4;
+        H *= 2;
+        W *= 2;
+        memcpy(h, t, sizeof(double) * B * C * H * W);
+        /* the level below kept h (now the first half of its channels) */
+        if (l > 0)
+            C = C * 2; /* below: C_{l-1} = C_l / 2 channels, of which h is the half */
+    }
+    if (rc == ORC_OK)
+        memcpy(x, h, sizeof(double) * tot);
+    free(h);
+    free(t);
+    free(ms);
+    free(sp);
+    return rc;
+}

@@ -201,3 +201,113 @@ def make(name: str, **override) -> dict:
     if kind == "split":
         return split_case(**spec)
     return stack_case(**spec)
+
+
+# ---------------------------------------------------------------------------
+# The full FInC Flow (Sec. 4.4, Fig. 2b/2c): Steps of [channel-split unit,
+# actnorm, invertible 1x1 convolution, affine coupling] in a multi-scale
+# architecture with split priors.  The paper times untrained models; these
+# are random untrained weights, drawn in the parameter layout below, all from
+# one default_rng(seed) stream in layout order:
+#   step:  Kq4 (4, C/4, C/4, k, k) masked as above but std 0.02 (diagonal
+#          1 + U(-0.1, 0.1)) | actnorm scale exp(N(0, 0.1^2)) (C) | bias
+#          N(0, 0.1^2) (C) | Wm (C, C): a random rotation (Q of the QR of a
+#          N(0, 1) matrix, columns' signs fixed by R's diagonal, as Glow
+#          initialises it) | coupling network: W1 (hid, C/2, 3, 3) He-normal
+#          (std sqrt(2 / fan_in)), b1 (hid) N(0, 0.01^2), W2 (hid, hid, 1, 1)
+#          He-normal, b2 (hid) N(0, 0.01^2), W3 (C, hid, 3, 3) N(0, (0.02 /
+#          sqrt(fan_in))^2) (Glow starts it at zero; small and nonzero here so
+#          that the coupling does something), b3 (C) N(0, 0.01^2) with 2 added
+#          to its scale half (scale = sigmoid(r + 2) near 0.98), ls3 (C)
+#          N(0, 0.01^2)
+#   prior (levels below the top): Wp (C, C/2, 3, 3) N(0, (0.02 /
+#          sqrt(fan_in))^2), bp (C) N(0, 0.01^2), lsp (C) N(0, 0.01^2)
+# With the single layer's std 0.05, Glow's fixed coupling scale
+# sigmoid(2) = 0.88 and larger output weights, the inverse of 84 random Steps
+# grows by about 1.17 a Step and the split prior's exp(logsd) overflows; the
+# scales above keep the sampled images finite (rms about 7 from N(0, 1)
+# latents at the CIFAR-10 setting).
+#   flow:  for level l: K steps, then (l < L-1) the prior; level l has
+#          C_l = 4 C0 2^l channels at H0 / 2^(l+1) x W0 / 2^(l+1).
+# ---------------------------------------------------------------------------
+
+def _flow_step(rng, C, k, hid, unit_std=0.02, out_std=0.02, rbias=2.0):
+    q = C // 4
+    Kq4 = np.empty((4, q, q, k, k))
+    for g in range(4):
+        K = rng.normal(0.0, unit_std, size=(q, q, k, k))
+        sh, sw = self_tap(g, k)
+        for co in range(q):
+            K[co, co + 1:, sh, sw] = 0.0
+        K[np.arange(q), np.arange(q), sh, sw] = 1.0 + rng.uniform(-0.1, 0.1, size=q)
+        Kq4[g] = K
+    an_s = np.exp(rng.normal(0.0, 0.1, size=C))
+    an_b = rng.normal(0.0, 0.1, size=C)
+    Q, R = np.linalg.qr(rng.normal(size=(C, C)))
+    Wm = Q * np.sign(np.diag(R))[None, :]
+    Ch = C // 2
+    W1 = rng.normal(0.0, np.sqrt(2.0 / (Ch * 9)), size=(hid, Ch, 3, 3))
+    b1 = rng.normal(0.0, 0.01, size=hid)
+    W2 = rng.normal(0.0, np.sqrt(2.0 / hid), size=(hid, hid, 1, 1))
+    b2 = rng.normal(0.0, 0.01, size=hid)
+    W3 = rng.normal(0.0, out_std / np.sqrt(hid * 9), size=(C, hid, 3, 3))
+    b3 = rng.normal(0.0, 0.01, size=C)
+    b3[C // 2:] += rbias
+    ls3 = rng.normal(0.0, 0.01, size=C)
+    return [Kq4, an_s, an_b, Wm, W1, b1, W2, b2, W3, b3, ls3]
+
+
+def _flow_prior(rng, C, prior_std=0.02):
+    Wp = rng.normal(0.0, prior_std / np.sqrt(C // 2 * 9), size=(C, C // 2, 3, 3))
+    bp = rng.normal(0.0, 0.01, size=C)
+    lsp = rng.normal(0.0, 0.01, size=C)
+    return [Wp, bp, lsp]
+
+
+def step_params(C: int, k: int, hid: int, seed: int = 3000) -> np.ndarray:
+    """One Step's parameters, flat, in the layout above."""
+    rng = np.random.default_rng(seed)
+    return np.concatenate([a.ravel() for a in _flow_step(rng, C, k, hid)])
+
+
+def flow_params(L: int, K: int, C0: int, k: int, hid: int, seed: int = 3000,
+                unit_std: float = 0.02, out_std: float = 0.02, rbias: float = 2.0,
+                prior_std: float = 0.02) -> np.ndarray:
+    """All parameters of an L-level flow of K Steps per level, flat."""
+    rng = np.random.default_rng(seed)
+    parts = []
+    for l in range(L):
+        C = (4 * C0) << l
+        for _ in range(K):
+            parts += _flow_step(rng, C, k, hid, unit_std, out_std, rbias)
+        if l < L - 1:
+            parts += _flow_prior(rng, C, prior_std)
+    return np.concatenate([a.ravel() for a in parts])
+
+
+def flow_latent_shapes(B: int, L: int, C0: int, H0: int, W0: int):
+    out = []
+    for l in range(L):
+        C, H, W = (4 * C0) << l, H0 >> (l + 1), W0 >> (l + 1)
+        out.append((B, C if l == L - 1 else C // 2, H, W))
+    return out
+
+
+def flow_case(B: int, L: int, K: int, C0: int, H0: int, W0: int, k: int = 3, hid: int = 512,
+              seed: int = 0) -> dict:
+    """Images x ~ N(0, 1) (seed) and latents z[l] ~ N(0, 1) (seed + 1, level 0
+    first) for a flow, with its parameters."""
+    x = gaussian(np.random.default_rng(seed), (B, C0, H0, W0))
+    rz = np.random.default_rng(seed + 1)
+    z = [gaussian(rz, s) for s in flow_latent_shapes(B, L, C0, H0, W0)]
+    return dict(x=x, z=z, params=flow_params(L, K, C0, k, hid), B=B, L=L, K=K, C0=C0, H0=H0,
+                W0=W0, k=k, hid=hid)
+
+
+# The paper's CIFAR-10 model (Table 3: setting [28, 28, 28], i.e. three
+# levels of 28 Steps on 3 x 32 x 32 images; its sampling time is for n = 100
+# images), and a small one the oracle runs in a blink.
+FLOWS = {
+    "flow_cifar10_L3_K28_b100": dict(B=100, L=3, K=28, C0=3, H0=32, W0=32, k=3, hid=512),
+    "flow_small_L2_K2_b4": dict(B=4, L=2, K=2, C0=1, H0=8, W0=8, k=3, hid=16),
+}

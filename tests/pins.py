@@ -512,11 +512,159 @@ def pin_backward_dense(o):
         close(dx.ravel(), J.T @ dy.ravel(), 1e-12, f"backward J^T corner={corner}")
 
 
+# --------------------------------------------------------------------------
+# The full FInC Flow (Sec. 4.4, Fig. 2b/2c): 1x1 convolution, coupling, Step,
+# multi-scale flow
+# --------------------------------------------------------------------------
+
+def fd_jacobian(f, x, h=1e-6):
+    """Central-difference Jacobian of f (array -> array) at x, one image."""
+    x = np.asarray(x, dtype=np.float64)
+    n = x.size
+    cols = []
+    for i in range(n):
+        e = np.zeros(n)
+        e[i] = h
+        cols.append((f((x.ravel() + e).reshape(x.shape)) -
+                     f((x.ravel() - e).reshape(x.shape))).ravel() / (2 * h))
+    return np.stack(cols, axis=1)
+
+
+def pin_conv1x1(o):
+    """y = Wm x per pixel (einsum); inverse = numpy solve per pixel; log|det|
+    = H W slogdet(Wm); a singular Wm is reported."""
+    rng = np.random.default_rng(31)
+    for C in (1, 3, 6):
+        Wm = rng.normal(size=(C, C)) + 2 * np.eye(C)
+        x = rng.normal(size=(2, C, 3, 5))
+        close(o.conv1x1_forward(x, Wm), np.einsum("oi,bihw->bohw", Wm, x), 1e-13,
+              f"1x1 forward C={C}")
+        y = rng.normal(size=(2, C, 3, 5))
+        want = np.linalg.solve(Wm, y.transpose(1, 0, 2, 3).reshape(C, -1))
+        close(o.conv1x1_inverse(y, Wm), want.reshape(C, 2, 3, 5).transpose(1, 0, 2, 3), 1e-12,
+              f"1x1 inverse C={C}")
+        close(o.conv1x1_logdet(Wm, 3, 5), 15 * np.linalg.slogdet(Wm)[1], 1e-11,
+              f"1x1 logdet C={C}")
+    # a permutation with a sign flip: partial pivoting must swap rows
+    P = np.array([[0.0, 1.0, 0.0], [0.0, 0.0, -2.0], [3.0, 0.0, 0.0]])
+    y = rng.normal(size=(1, 3, 2, 2))
+    close(o.conv1x1_forward(o.conv1x1_inverse(y, P), P), y, 1e-14, "1x1 pivoting")
+    close(o.conv1x1_logdet(P, 2, 2), 4 * np.log(6.0), 1e-14, "1x1 logdet of a permutation")
+    try:
+        o.conv1x1_logdet(np.ones((2, 2)), 2, 2)
+    except Exception as e:   # OracleError -2
+        assert getattr(e, "code", None) == -2
+    else:
+        raise AssertionError("singular 1x1 weight not reported")
+
+
+def _coupling_parts(cp, C, hid):
+    Ch = C // 2
+    sizes = [hid * Ch * 9, hid, hid * hid, hid, C * hid * 9, C, C]
+    parts = np.split(np.asarray(cp), np.cumsum(sizes)[:-1])
+    W1, b1, W2, b2, W3, b3, ls3 = parts
+    return (W1.reshape(hid, Ch, 3, 3), b1, W2.reshape(hid, hid, 1, 1), b2,
+            W3.reshape(C, hid, 3, 3), b3, ls3)
+
+
+def torch_coupling_net(xa, cp, C, hid):
+    """Library route: conv2d (padding 1) + bias, ReLU, 1x1 conv2d + bias,
+    ReLU, conv2d (padding 1) + bias times exp(3 ls)."""
+    W1, b1, W2, b2, W3, b3, ls3 = [torch.from_numpy(np.ascontiguousarray(a))
+                                    for a in _coupling_parts(cp, C, hid)]
+    t = torch.from_numpy(np.ascontiguousarray(xa))
+    t = F.relu(F.conv2d(t, W1, b1, padding=1))
+    t = F.relu(F.conv2d(t, W2, b2))
+    t = F.conv2d(t, W3, b3, padding=1) * torch.exp(3 * ls3)[None, :, None, None]
+    return t.numpy()
+
+
+def pin_coupling(o):
+    """Coupling network = the torch route; forward = the closed form
+    [xa, (xb + t) sigmoid(r + 2)] with log|det| = sum log sigmoid(r + 2),
+    equal to the slogdet of its finite-difference Jacobian; inverse round
+    trip."""
+    rng = np.random.default_rng(32)
+    C, hid, H, W = 6, 5, 4, 3
+    cp = rng.normal(0.0, 0.4, size=hid * 3 * 9 + hid + hid * hid + hid + C * hid * 9 + 2 * C)
+    x = rng.normal(size=(2, C, H, W))
+    h = torch_coupling_net(x[:, :3], cp, C, hid)
+    close(o.coupling_net(x[:, :3], cp, hid), h, 1e-12, "coupling network vs conv2d")
+    t, r = h[:, :3], h[:, 3:]
+    sc = 1.0 / (1.0 + np.exp(-(r + 2.0)))
+    y, ld = o.coupling_forward(x, cp, hid)
+    close(y, np.concatenate([x[:, :3], (x[:, 3:] + t) * sc], axis=1), 1e-12, "coupling forward")
+    close(ld, np.log(sc).sum(axis=(1, 2, 3)), 1e-12, "coupling logdet closed form")
+    close(o.coupling_inverse(y, cp, hid), x, 1e-12, "coupling round trip")
+    J = fd_jacobian(lambda a: o.coupling_forward(a[None], cp, hid)[0], x[0])
+    close(ld[0], np.linalg.slogdet(J)[1], 1e-6, "coupling logdet vs Jacobian")
+
+
+def pin_step(o):
+    """One Step (channel-split unit, actnorm, 1x1, coupling) = the torch /
+    numpy route of those four pieces; its log|det| is the slogdet of its
+    finite-difference Jacobian; inverse round trip."""
+    C, k, hid, H, W = 8, 2, 3, 3, 3
+    sp = synth.step_params(C, k, hid, seed=78)
+    q = C // 4
+    n = [4 * q * q * k * k, C, C, C * C]
+    Kq4, s, b, Wm = np.split(sp[:sum(n)], np.cumsum(n)[:-1])
+    Kq4, Wm, cp = Kq4.reshape(4, q, q, k, k), Wm.reshape(C, C), sp[sum(n):]
+    x = np.random.default_rng(33).normal(size=(2, C, H, W))
+    u = _split_torch(x, Kq4) * s[None, :, None, None] + b[None, :, None, None]
+    v = np.einsum("oi,bihw->bohw", Wm, u)
+    hh = torch_coupling_net(v[:, :C // 2], cp, C, hid)
+    sc = 1.0 / (1.0 + np.exp(-(hh[:, C // 2:] + 2.0)))
+    want = np.concatenate([v[:, :C // 2], (v[:, C // 2:] + hh[:, :C // 2]) * sc], axis=1)
+    y, ld = o.step_forward(x, sp, k, hid)
+    close(y, want, 1e-11, "step forward vs composition of library routes")
+    close(o.step_inverse(y, sp, k, hid), x, 1e-11, "step round trip")
+    J = fd_jacobian(lambda a: o.step_forward(a[None], sp, k, hid)[0], x[0])
+    close(ld[0], np.linalg.slogdet(J)[1], 1e-6, "step logdet vs Jacobian")
+
+
+def _squeeze_np(x):
+    B, C, H, W = x.shape
+    return x.reshape(B, C, H // 2, 2, W // 2, 2).transpose(0, 1, 3, 5, 2, 4).reshape(
+        B, 4 * C, H // 2, W // 2)
+
+
+def pin_flow(o):
+    """Multi-scale flow: with no Steps it is squeeze, split (first half
+    goes on) and the split prior z = (h2 - mean) exp(-logsd), (mean, logsd)
+    from a conv2d of h1 -- against the numpy / torch route; with Steps, its
+    log|det| is the slogdet of its finite-difference Jacobian and sampling
+    inverts it."""
+    rng = np.random.default_rng(34)
+    # no Steps: L = 2 levels, 1 channel, 8 x 8 -> (4, 4, 4) -> split -> (8, 2, 2)
+    params = synth.flow_params(2, 0, 1, 3, 4, seed=79)
+    Wp = params[:4 * 2 * 9].reshape(4, 2, 3, 3)
+    bp, lsp = params[72:76], params[76:80]
+    x = rng.normal(size=(2, 1, 8, 8))
+    z, ld = o.flow_forward(x, params, 2, 0, 3, 4)
+    h = _squeeze_np(x)
+    ms = F.conv2d(torch.from_numpy(h[:, :2].copy()), torch.from_numpy(Wp),
+                  torch.from_numpy(bp), padding=1).numpy() * np.exp(3 * lsp)[None, :, None, None]
+    close(z[0], (h[:, 2:] - ms[:, :2]) * np.exp(-ms[:, 2:]), 1e-12, "split prior latent")
+    close(z[1], _squeeze_np(h[:, :2]), 0.0, "top latent")
+    close(ld, -ms[:, 2:].sum(axis=(1, 2, 3)), 1e-12, "split prior logdet")
+    # two Steps per level
+    L, K, C0, k, hid = 2, 2, 1, 2, 3
+    params = synth.flow_params(L, K, C0, k, hid, seed=80)
+    x = rng.normal(size=(1, C0, 4, 4))
+    z, ld = o.flow_forward(x, params, L, K, k, hid)
+    close(o.flow_sample(z, params, L, K, C0, 4, 4, k, hid), x, 1e-10, "flow round trip")
+    flat = lambda a: np.concatenate([t.ravel() for t in o.flow_forward(a[None], params, L, K,
+                                                                        k, hid)[0]])
+    J = fd_jacobian(flat, x[0])
+    close(ld[0], np.linalg.slogdet(J)[1], 1e-6, "flow logdet vs Jacobian")
+
+
 ALL_PINS = [
     pin_forward_conv2d, pin_fig1_matrix, pin_jacobian_triangular, pin_logdet_slogdet,
     pin_logdet_singular, pin_inverse_dense_solve, pin_inverse_triangular_solve,
     pin_round_trip, pin_k1_pixelwise, pin_impulse_geometric, pin_row_lfilter,
     pin_flip_equivalence, pin_wavefront_schedule, pin_unit_dense, pin_unit_round_trip,
     pin_split_dense, pin_split_round_trip, pin_squeeze_reshape, pin_actnorm, pin_stack,
-    pin_backward_autograd, pin_backward_dense,
+    pin_backward_autograd, pin_backward_dense, pin_conv1x1, pin_coupling, pin_step, pin_flow,
 ]

@@ -58,6 +58,32 @@ MUTANTS = [
     ("backward weight gradient reads the mirrored tap",
      "x[n * img + ci * plane + (long)ii * W + jj];",
      "x[n * img + ci * plane + (long)(H - 1 - ii) * W + jj];", 0),
+    ("1x1 forward transposes the matrix", "s += Wm[(long)co * C + ci] * x[(n * C + ci) * plane + p];",
+     "s += Wm[(long)ci * C + co] * x[(n * C + ci) * plane + p];", 0),
+    ("1x1 inverse forgets the row order", "double s = y[(n * C + perm[r]) * plane + p];",
+     "double s = y[(n * C + r) * plane + p];", 0),
+    ("1x1 logdet drops a pivot", "ld += log(fabs(d));", "ld += c ? log(fabs(d)) : 0.0;", 0),
+    ("coupling network pads on one side only", "int ii = i + a - pad, jj = j + b - pad;",
+     "int ii = i + a - 2 * pad, jj = j + b - pad;", 0),
+    ("coupling network skips a ReLU", "conv_same(t1, t2, W2, b2, NULL, B, hid, hid, H, W, 1, 1);",
+     "conv_same(t1, t2, W2, b2, NULL, B, hid, hid, H, W, 1, 0);", 0),
+    ("coupling scale without the +2", "double s = sigmoid(r + 2.0);", "double s = sigmoid(r);", 0),
+    ("coupling adds the shift after scaling",
+     "y[n * 2 * half + half + e] = (x[n * 2 * half + half + e] + t) * s;",
+     "y[n * 2 * half + half + e] = x[n * 2 * half + half + e] * s + t;", 0),
+    ("coupling inverse multiplies by the scale",
+     "y[n * 2 * half + half + e] / sigmoid(r + 2.0) - t;",
+     "y[n * 2 * half + half + e] * sigmoid(r + 2.0) - t;", 0),
+    ("step inverse undoes actnorm before the 1x1",
+     "rc = orc_conv1x1_inverse(t1, t2, Wm, B, C, H, W);",
+     "rc = orc_conv1x1_inverse(t1, t2, Wm, B, C, H, W); orc_actnorm_inverse(t2, t1, s, b, B, C, H, W); orc_conv1x1_inverse(t1, t2, Wm, B, C, H, W);", 0),
+    ("step logdet forgets the actnorm", "logdet[n] += lu + la + lw;", "logdet[n] += lu + lw;", 0),
+    ("split prior latent uses exp(+logsd)",
+     "z[l][n * Ch * plane + e] = (t[n * C * plane + Ch * plane + e] - mean) * exp(-logsd);",
+     "z[l][n * Ch * plane + e] = (t[n * C * plane + Ch * plane + e] - mean) * exp(logsd);", 0),
+    ("split prior forgets its log|det|", "ld -= logsd;", "ld -= 0.0;", 0),
+    ("flow sample runs the steps forwards", "for (int s = K - 1; s >= 0 && rc == ORC_OK; --s) {",
+     "for (int s = 0; s < K && rc == ORC_OK; ++s) {", 0),
 ]
 
 

@@ -283,6 +283,82 @@ int finc_stack_inverse_prepared(const float *const *z, float *x,
                                 const float *bias, int B, int L, int U, int C1,
                                 int H1, int W1, int k, hipStream_t stream);
 
+/* ---- The full FInC Flow (Sec. 4.4 "Architecture", Fig. 2b and 2c) ------
+ * A Step is, forward: the channel-split FInC unit (as finc_split_forward),
+ * actnorm u = s x + b, the invertible 1x1 convolution v = Wm u (Glow), and an
+ * affine coupling: with v = [va, vb] (channel halves) and h = NN(va),
+ * t = h[0 .. C/2), r = h[C/2 .. C), sc = sigmoid(r + 2): y = [va,
+ * (vb + t) sc], log|det| += sum log sc.  NN is a 3x3 convolution (C/2 ->
+ * hid), ReLU, a 1x1 convolution (hid -> hid), ReLU, and a 3x3 convolution
+ * (hid -> C) times exp(3 ls[c]) per output channel; every convolution has a
+ * bias and zero "same" padding.  (Readings: the paper names these layers
+ * after Glow; the shift/scale halves, sigmoid(r + 2) and the exp(3 ls)
+ * output scale are Glow's.)
+ * Step parameters, one flat fp32 array (C = channels, q = C/4, Ch = C/2):
+ *   Kq4 (4, q, q, k, k) | s (C) | b (C) | Wm (C, C) | W1 (hid, Ch, 3, 3) |
+ *   b1 (hid) | W2 (hid, hid) | b2 (hid) | W3 (C, hid, 3, 3) | b3 (C) | ls3 (C)
+ * The multi-scale flow of L levels, K Steps each, on (B, C0, H0, W0) images:
+ * per level squeeze (as the stack), K Steps, then below the top a split
+ * whose second half becomes the latent z_l = (h2 - mean) exp(-logsd), with
+ * (mean, logsd) the halves of a 3x3 convolution of the first half (C/2 -> C,
+ * bias, exp(3 ls) scale; Glow's split prior; log|det| -sum logsd); the top
+ * level's output is the last latent.  Level l has C_l = 4 C0 2^l channels at
+ * H0/2^(l+1) x W0/2^(l+1); z[l] is (B, C_l/2, ...) below the top and
+ * (B, C_l, ...) at it.  Flow parameters: per level its K Steps, then (below
+ * the top) the prior Wp (C_l, C_l/2, 3, 3) | bp (C_l) | lsp (C_l).
+ * Requirements: every Step's C a multiple of 4, at most 64; its unit's
+ * inverse supported (finc_inverse_plan, FINC_PLAN_SPLIT); H0, W0 divisible
+ * by 2^L; L <= 6; hid <= 4096.
+ * Prepared weights (finc_*_prepare, device, 256-byte aligned, private
+ * layout): per Step the unit's inverse weights and, in fp64 then rounded,
+ * the 1x1 convolution folded with the actnorm in both directions and the
+ * Step's per-pixel constant log|det|.  The calls read params (device) for
+ * the coupling and prior networks and prepared for the rest.
+ * Workspace (device, 256-byte aligned, overwritten): scratch activations.
+ * log|det| outputs are device doubles, one per image.  Aliasing: outputs
+ * must not overlap inputs, params, prepared or the workspace (EINVAL).
+ * Deterministic: fixed summation orders, no atomics. */
+size_t finc_step_param_count(int C, int k, int hid);
+size_t finc_step_prepared_bytes(int C, int k);
+size_t finc_step_workspace_bytes(int B, int C, int H, int W, int hid);
+int finc_step_prepare(const float *sp, int C, int k, int hid, void *prepared,
+                      hipStream_t stream);
+/* y = Step(x); logdet (B doubles, or NULL): += the Step's log|det|. */
+int finc_step_forward(const float *x, float *y, double *logdet, const float *sp,
+                      const void *prepared, int B, int C, int H, int W, int k, int hid,
+                      void *workspace, hipStream_t stream);
+/* x = Step^-1(y): coupling^-1, 1x1^-1 and actnorm^-1 (one prepared map),
+ * then the unit's wavefront inverse (Algorithm 2). */
+int finc_step_inverse(const float *y, float *x, const float *sp, const void *prepared, int B,
+                      int C, int H, int W, int k, int hid, void *workspace,
+                      hipStream_t stream);
+
+size_t finc_flow_param_count(int L, int K, int C0, int k, int hid);
+size_t finc_flow_prepared_bytes(int L, int K, int C0, int k);
+size_t finc_flow_workspace_bytes(int B, int L, int C0, int H0, int W0, int hid);
+int finc_flow_prepare(const float *params, int L, int K, int C0, int k, int hid,
+                      void *prepared, hipStream_t stream);
+/* Density direction: x (B, C0, H0, W0) -> latents z[0 .. L-1] (host array of
+ * device pointers) and logdet (B doubles, overwritten). */
+int finc_flow_forward(const float *x, float *const *z, double *logdet, const float *params,
+                      const void *prepared, int B, int L, int K, int C0, int H0, int W0,
+                      int k, int hid, void *workspace, hipStream_t stream);
+/* Sampling direction: latents -> x. */
+int finc_flow_sample(const float *const *z, float *x, const float *params,
+                     const void *prepared, int B, int L, int K, int C0, int H0, int W0,
+                     int k, int hid, void *workspace, hipStream_t stream);
+
+/* The invertible 1x1 convolution alone (Sec. 4.4): y = Wm x at every pixel
+ * (Wm (C, C), C <= 64); logdet (device double, or NULL) = H W log|det Wm|
+ * (-inf if singular).  The inverse applies Wm^-1, formed in fp64 by LU with
+ * partial pivoting.  workspace: finc_conv1x1_workspace_bytes(C), 256-byte
+ * aligned. */
+size_t finc_conv1x1_workspace_bytes(int C);
+int finc_conv1x1_forward(const float *x, float *y, const float *Wm, double *logdet, int B,
+                         int C, int H, int W, void *workspace, hipStream_t stream);
+int finc_conv1x1_inverse(const float *y, float *x, const float *Wm, int B, int C, int H, int W,
+                         void *workspace, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,8 +1,8 @@
 """Build the HIP library in-tree for gfx950: paper_2301_09266_amd/csrc/libfinc.so.
 
 finc.hip compiles as several translation units in parallel (FINC_PART: one
-per group of inverse kernel instances, and one with everything else), which
-are then linked into the one shared library.
+per group of inverse kernel instances, and one with everything else), flow.hip
+as one more; all are linked into the one shared library.
 """
 from __future__ import annotations
 
@@ -15,6 +15,7 @@ import tempfile
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "finc.hip")
+FLOW_SRC = os.path.join(PKG, "csrc", "flow.hip")
 LIB = os.path.join(PKG, "csrc", "libfinc.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
@@ -39,12 +40,14 @@ def build(out: str = LIB, extra: list[str] | None = None) -> str:
     """Compile every part of finc.hip and link them into `out`."""
     tmpdir = tempfile.mkdtemp(prefix="finc_build_")
     try:
-        parts = [-2] + list(range(INVERSE_GROUPS))
-        objs = [os.path.join(tmpdir, f"part{p + 2}.o") for p in parts]
+        # finc.hip in parts (FINC_PART), then flow.hip
+        parts = [-2] + list(range(INVERSE_GROUPS)) + [None]
+        objs = [os.path.join(tmpdir, f"part{i}.o") for i in range(len(parts))]
 
         def compile_part(i: int) -> None:
-            cmd = [HIPCC, *FLAGS, *(extra or []), f"-DFINC_PART={parts[i]}",
-                   "-I", os.path.join(ROOT, "include"), "-c", "-o", objs[i], SRC]
+            src, defs = (FLOW_SRC, []) if parts[i] is None else (SRC, [f"-DFINC_PART={parts[i]}"])
+            cmd = [HIPCC, *FLAGS, *(extra or []), *defs,
+                   "-I", os.path.join(ROOT, "include"), "-c", "-o", objs[i], src]
             subprocess.run(cmd, check=True)
 
         with concurrent.futures.ThreadPoolExecutor(_jobs()) as pool:

@@ -51,6 +51,23 @@ SIGNATURES = {
     "finc_stack_prepare": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
     "finc_stack_inverse_prepared": (_i, [ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _i, _i,
                                          _i, _i, _i, _i, _i, _vp]),
+    "finc_step_param_count": (_sz, [_i, _i, _i]),
+    "finc_step_prepared_bytes": (_sz, [_i, _i]),
+    "finc_step_workspace_bytes": (_sz, [_i, _i, _i, _i, _i]),
+    "finc_step_prepare": (_i, [_vp, _i, _i, _i, _vp, _vp]),
+    "finc_step_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
+    "finc_step_inverse": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
+    "finc_flow_param_count": (_sz, [_i, _i, _i, _i, _i]),
+    "finc_flow_prepared_bytes": (_sz, [_i, _i, _i, _i]),
+    "finc_flow_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
+    "finc_flow_prepare": (_i, [_vp, _i, _i, _i, _i, _i, _vp, _vp]),
+    "finc_flow_forward": (_i, [_vp, ctypes.POINTER(_vp), _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                               _i, _i, _vp, _vp]),
+    "finc_flow_sample": (_i, [ctypes.POINTER(_vp), _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i,
+                              _i, _vp, _vp]),
+    "finc_conv1x1_workspace_bytes": (_sz, [_i]),
+    "finc_conv1x1_forward": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp]),
+    "finc_conv1x1_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _vp, _vp]),
 }
 
 
@@ -454,4 +471,145 @@ def stack_inverse_prepared(z, prepared: torch.Tensor, scale: torch.Tensor,
     _check(lb.finc_stack_inverse_prepared(zp, _ptr(x), _ptr(prepared), _ptr(scale),
                                           _ptr(bias), B, L, U, C1, H1, W1, k, _stream()),
            "finc_stack_inverse_prepared")
+    return x
+
+
+# ---------------------------------------------------------------------------
+# The full FInC Flow (Step and multi-scale flow; parameter layout in finc.h)
+
+def conv1x1_forward(x: torch.Tensor, Wm: torch.Tensor, out: torch.Tensor | None = None,
+                    logdet: torch.Tensor | None = None, workspace: torch.Tensor | None = None):
+    lb = _require_lib()
+    _dev(x, "x")
+    B, C, H, W = x.shape
+    _dev(Wm, "Wm", (C, C))
+    y = torch.empty_like(x) if out is None else _dev(out, "out", x.shape)
+    ws = _workspace(int(lb.finc_conv1x1_workspace_bytes(C)), x.device, workspace)
+    _check(lb.finc_conv1x1_forward(_ptr(x), _ptr(y), _ptr(Wm), _ptr(_logdet_out(logdet)), B, C,
+                                   H, W, _ptr(ws), _stream()), "finc_conv1x1_forward")
+    return y
+
+
+def conv1x1_inverse(y: torch.Tensor, Wm: torch.Tensor, out: torch.Tensor | None = None,
+                    workspace: torch.Tensor | None = None):
+    lb = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    _dev(Wm, "Wm", (C, C))
+    x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
+    ws = _workspace(int(lb.finc_conv1x1_workspace_bytes(C)), y.device, workspace)
+    _check(lb.finc_conv1x1_inverse(_ptr(y), _ptr(x), _ptr(Wm), B, C, H, W, _ptr(ws), _stream()),
+           "finc_conv1x1_inverse")
+    return x
+
+
+def step_param_count(C: int, k: int, hid: int) -> int:
+    return int(_require_lib().finc_step_param_count(C, k, hid))
+
+
+def step_prepare(sp: torch.Tensor, C: int, k: int, hid: int, out: torch.Tensor | None = None):
+    lb = _require_lib()
+    _dev(sp, "sp")
+    if sp.numel() != step_param_count(C, k, hid):
+        raise ValueError(f"sp has {sp.numel()} elements, expected {step_param_count(C, k, hid)}")
+    pp = _workspace(int(lb.finc_step_prepared_bytes(C, k)), sp.device, out)
+    _check(lb.finc_step_prepare(_ptr(sp), C, k, hid, _ptr(pp), _stream()), "finc_step_prepare")
+    return pp
+
+
+def _step_call(name, a, sp, prepared, k, hid, out, workspace, logdet=None):
+    lb = _require_lib()
+    _dev(a, "input")
+    B, C, H, W = a.shape
+    _dev(sp, "sp")
+    if sp.numel() != step_param_count(C, k, hid):
+        raise ValueError("sp does not match (C, k, hid)")
+    _bytes_buf(prepared, int(lb.finc_step_prepared_bytes(C, k)), "prepared")
+    b = torch.empty_like(a) if out is None else _dev(out, "out", a.shape)
+    ws = _workspace(int(lb.finc_step_workspace_bytes(B, C, H, W, hid)), a.device, workspace)
+    if name == "finc_step_forward":
+        if logdet is not None and (not logdet.is_cuda or logdet.dtype != torch.float64 or
+                                   logdet.numel() < B):
+            raise ValueError("logdet must be a device float64 tensor of B elements")
+        rc = lb.finc_step_forward(_ptr(a), _ptr(b), _ptr(logdet), _ptr(sp), _ptr(prepared), B, C,
+                                  H, W, k, hid, _ptr(ws), _stream())
+    else:
+        rc = lb.finc_step_inverse(_ptr(a), _ptr(b), _ptr(sp), _ptr(prepared), B, C, H, W, k, hid,
+                                  _ptr(ws), _stream())
+    _check(rc, name)
+    return b
+
+
+def step_forward(x, sp, prepared, k: int, hid: int, out=None, logdet=None, workspace=None):
+    """y = Step(x); logdet (B float64, device) is incremented if given."""
+    return _step_call("finc_step_forward", x, sp, prepared, k, hid, out, workspace, logdet)
+
+
+def step_inverse(y, sp, prepared, k: int, hid: int, out=None, workspace=None):
+    return _step_call("finc_step_inverse", y, sp, prepared, k, hid, out, workspace)
+
+
+def flow_param_count(L: int, K: int, C0: int, k: int, hid: int) -> int:
+    return int(_require_lib().finc_flow_param_count(L, K, C0, k, hid))
+
+
+def flow_latent_shapes(B: int, L: int, C0: int, H0: int, W0: int):
+    return [(B, ((4 * C0) << l) // (1 if l == L - 1 else 2), H0 >> (l + 1), W0 >> (l + 1))
+            for l in range(L)]
+
+
+def flow_prepare(params: torch.Tensor, L: int, K: int, C0: int, k: int, hid: int,
+                 out: torch.Tensor | None = None):
+    lb = _require_lib()
+    _dev(params, "params")
+    if params.numel() != flow_param_count(L, K, C0, k, hid):
+        raise ValueError("params does not match (L, K, C0, k, hid)")
+    pp = _workspace(int(lb.finc_flow_prepared_bytes(L, K, C0, k)), params.device, out)
+    _check(lb.finc_flow_prepare(_ptr(params), L, K, C0, k, hid, _ptr(pp), _stream()),
+           "finc_flow_prepare")
+    return pp
+
+
+def _flow_common(params, prepared, L, K, C0, k, hid):
+    lb = _require_lib()
+    _dev(params, "params")
+    if params.numel() != flow_param_count(L, K, C0, k, hid):
+        raise ValueError("params does not match (L, K, C0, k, hid)")
+    _bytes_buf(prepared, int(lb.finc_flow_prepared_bytes(L, K, C0, k)), "prepared")
+    return lb
+
+
+def flow_forward(x: torch.Tensor, params: torch.Tensor, prepared: torch.Tensor, L: int, K: int,
+                 k: int, hid: int, workspace: torch.Tensor | None = None):
+    """(latents z[0..L-1], logdet per image) of images x."""
+    _dev(x, "x")
+    B, C0, H0, W0 = x.shape
+    lb = _flow_common(params, prepared, L, K, C0, k, hid)
+    z = [torch.empty(s, dtype=torch.float32, device=x.device)
+         for s in flow_latent_shapes(B, L, C0, H0, W0)]
+    ld = torch.empty(B, dtype=torch.float64, device=x.device)
+    ws = _workspace(int(lb.finc_flow_workspace_bytes(B, L, C0, H0, W0, hid)), x.device, workspace)
+    zp = (ctypes.c_void_p * L)(*[t.data_ptr() for t in z])
+    _check(lb.finc_flow_forward(_ptr(x), zp, _ptr(ld), _ptr(params), _ptr(prepared), B, L, K, C0,
+                                H0, W0, k, hid, _ptr(ws), _stream()), "finc_flow_forward")
+    return z, ld
+
+
+def flow_sample(z, params: torch.Tensor, prepared: torch.Tensor, L: int, K: int, C0: int,
+                H0: int, W0: int, k: int, hid: int, out: torch.Tensor | None = None,
+                workspace: torch.Tensor | None = None):
+    """Images from latents z[0..L-1] (shapes as flow_latent_shapes)."""
+    if len(z) != L:
+        raise ValueError("one latent per level")
+    B = z[0].shape[0]
+    for l, (t, shp) in enumerate(zip(z, flow_latent_shapes(B, L, C0, H0, W0))):
+        _dev(t, f"z[{l}]", shp)
+    lb = _flow_common(params, prepared, L, K, C0, k, hid)
+    x = (torch.empty((B, C0, H0, W0), dtype=torch.float32, device=z[0].device)
+         if out is None else _dev(out, "out", (B, C0, H0, W0)))
+    ws = _workspace(int(lb.finc_flow_workspace_bytes(B, L, C0, H0, W0, hid)), z[0].device,
+                    workspace)
+    zp = (ctypes.c_void_p * L)(*[t.data_ptr() for t in z])
+    _check(lb.finc_flow_sample(zp, _ptr(x), _ptr(params), _ptr(prepared), B, L, K, C0, H0, W0, k,
+                               hid, _ptr(ws), _stream()), "finc_flow_sample")
     return x

@@ -47,6 +47,8 @@ def parse():
                    help="launch every step eagerly instead of replaying a HIP graph")
     p.add_argument("--no-configs", action="store_true",
                    help="skip the per-configuration table (forward / inverse of every workload) and the scaling sweep")
+    p.add_argument("--no-flow", action="store_true",
+                   help="skip the full-flow sampling at the CIFAR-10 setting")
     p.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                    help="only run a plain device copy of MIB MiB ten times (the known-size "
                         "reference for rocprofv3 FETCH_SIZE / WRITE_SIZE) and exit")
@@ -247,13 +249,52 @@ def per_config(dev) -> list:
             layers = 4 * U * L
         alg = B * act + wts
         gbs = alg / (inv * 1e-6) / 1e9
-        rows.append({"workload": name, "B": B, "C": C, "H": H, "W": W, "k": k, "layers": layers,
-                     "forward_us": fwd, "inverse_us": inv, "backward_us": bwd,
-                     "inverse_images_per_s": B / (inv * 1e-6),
-                     "inverse_pixels_per_s": B * H * W / (inv * 1e-6),
-                     "inverse_alg_bytes": alg, "inverse_hbm_gbs": gbs,
-                     "inverse_hbm_frac": gbs / HBM_PEAK_GBS})
+        steps = (H + W - 1) * layers if kind != "stack" else None
+        row = {"workload": name, "B": B, "C": C, "H": H, "W": W, "k": k, "layers": layers,
+               "forward_us": fwd, "inverse_us": inv, "backward_us": bwd,
+               "inverse_images_per_s": B / (inv * 1e-6),
+               "inverse_pixels_per_s": B * H * W / (inv * 1e-6),
+               "inverse_alg_bytes": alg, "inverse_hbm_gbs": gbs,
+               "inverse_hbm_frac": gbs / HBM_PEAK_GBS,
+               "us_per_diagonal_step": inv / steps if steps else None}
+        row.update(oracle_row(c, kind, zd if kind == "stack" else y, out))
+        rows.append(row)
     return rows
+
+
+def oracle_row(c, kind, gpu_in, gpu_out):
+    """The oracle's inverse on image 0 of a workload: its images/s on the
+    host cores (at most 16 threads, each inverting image 0, about two
+    seconds), and max |gpu - oracle| / max(1, max |oracle|) for that image
+    (gpu_out: the last timed inverse; gpu_in: its input, or the latents of
+    the stack)."""
+    import numpy as np
+
+    import oracle
+
+    orc = oracle.default()
+    f64 = lambda a: np.asarray(a, dtype=np.float32).astype(np.float64)
+    h = lambda t: t.detach().cpu().numpy().astype(np.float64)
+    if kind == "stack":
+        zs = [h(z[:1]) for z in gpu_in]
+        Ks, ss, bs = ([f64(a) for a in c[n]] for n in ("K", "scale", "bias"))
+        inv = lambda: orc.stack_inverse(zs, Ks, ss, bs, c["levels"], c["units"], c["k"], c["C1"],
+                                        c["H1"], c["W1"])
+    else:
+        y = h(gpu_in[:1])
+        if kind == "layer":
+            inv = lambda: orc.inverse(y, f64(c["K"]), c["corner"])
+        elif kind == "unit":
+            inv = lambda: orc.unit_inverse(y, f64(c["K4"]))
+        else:
+            inv = lambda: orc.split_inverse(y, f64(c["Kq4"]))
+    n = oracle_threads()
+    rate, _, _ = cpu_rate(lambda i: inv(), 2.0, n)
+    want = inv()[0]
+    g = h(gpu_out[0])
+    return {"oracle_images_per_s": rate, "oracle_cores": n,
+            "parity_image0_inf_rel": float(np.abs(g - want).max() / max(1.0, np.abs(want).max())),
+            "parity_image0_max_abs": float(np.abs(g - want).max())}
 
 
 def scaling_sweep(dev) -> dict:
@@ -286,6 +327,132 @@ def scaling_sweep(dev) -> dict:
             "rows": rows}
 
 
+def protocol_runs(fn, runs: int = 11) -> dict:
+    """The paper's timing protocol (appendix, run-time and confidence
+    intervals): `runs` runs, the first dropped, mean, standard deviation and
+    the 95% confidence interval of the mean (Student t, runs - 2 degrees of
+    freedom).  fn() returns one run's time in milliseconds."""
+    import statistics
+
+    t = [fn() for _ in range(runs)][1:]
+    m = statistics.mean(t)
+    sd = statistics.stdev(t) if len(t) > 1 else 0.0
+    tq = {9: 2.262, 4: 2.776, 19: 2.093}.get(len(t) - 1, 1.96)
+    half = tq * sd / (len(t) ** 0.5)
+    return {"runs": runs, "dropped": 1, "mean_ms": m, "std_ms": sd,
+            "ci95_ms": [m - half, m + half]}
+
+
+def event_ms(fn) -> float:
+    import torch
+
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    a.record()
+    fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b)
+
+
+def step_cost(dev) -> dict:
+    """Where an inverse launch's time goes, from shipped kernels only.
+    t_step: the inverse of the same batch and channels at two image widths
+    (e.g. H + W - 1 = 31 and 63 diagonal steps for 16 x 16 and 16 x 48), the
+    time difference over the extra steps (it also carries those columns' share
+    of the load and store); fixed: the 16 x 16 time less 31 t_step (launch,
+    argument and weight loads, staging, the store).  t_barrier: a kernel
+    doing nothing but the steps' synchronisation (each thread writes an LDS
+    value, a barrier, each reads another wave's), 64 workgroups of 256
+    threads, per step from 31 and 1031 steps."""
+    import ctypes
+
+    import numpy as np
+    import torch
+
+    from paper_2301_09266_amd import build, finc, synth
+
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    rows = []
+    # (second widths: the widest that keeps the first's kernel instance and
+    # partial-tile layout, per finc_inverse_plan)
+    for C, H, W1, W2, k in ((12, 16, 16, 48, 3), (12, 32, 32, 40, 3), (48, 8, 8, 32, 3),
+                            (24, 16, 16, 32, 3)):
+        inst = lambda W: [{key: v for key, v in p.items() if key != "lds"}
+                          for p in finc.inverse_plan(finc.PLAN_LAYER, C, H, W, k)]
+        assert inst(W1) == inst(W2), (C, H, W1, W2)
+        t = []
+        for W in (W1, W2):
+            c = synth.layer_case(64, C, H, W, k)
+            y, K = d(c["x"]), d(c["K"])
+            prep = finc.prepare(K, [0])
+            out = torch.empty_like(y)
+            t.append(graph_time_us(lambda: finc.inverse_prepared(y, prep, k, 0, out=out), 5, 20))
+        ts = (t[1] - t[0]) / (W2 - W1)
+        rows.append({"C": C, "H": H, "W": [W1, W2], "k": k, "B": 64, "inverse_us": t,
+                     "t_step_us": ts, "fixed_us": t[0] - (H + W1 - 1) * ts})
+    lib = ctypes.CDLL(build.CALIB_LIB)
+    lib.finc_calib_barrier_chain.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_int,
+                                             ctypes.c_void_p]
+    buf = torch.empty(64 * 256, dtype=torch.float32, device=dev)
+    tb = []
+    for steps in (31, 1031):
+        # (the stream is taken at each call: graph capture runs on its own)
+        run = lambda: lib.finc_calib_barrier_chain(
+            ctypes.c_void_p(buf.data_ptr()), 64, steps,
+            ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        tb.append(graph_time_us(run, 5, 20))
+    return {"rows": rows, "t_barrier_us": (tb[1] - tb[0]) / 1000,
+            "barrier_kernel_us": {"31": tb[0], "1031": tb[1]}}
+
+
+def flow_sampling(dev, name: str = "flow_cifar10_L3_K28_b100") -> dict:
+    """The whole FInC Flow at the paper's CIFAR-10 setting (Table 3: three
+    levels of 28 Steps, 3 x 32 x 32, 512-wide coupling networks, n = 100
+    images): sampling (latents to images) and the forward (images to latents
+    and log|det|), each timed by the paper's protocol; weights prepared once
+    outside the timed region."""
+    import numpy as np
+    import torch
+
+    from paper_2301_09266_amd import finc, synth
+
+    c = synth.flow_case(**synth.FLOWS[name])
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    a = dict(L=c["L"], K=c["K"], k=c["k"], hid=c["hid"])
+    geo = dict(C0=c["C0"], H0=c["H0"], W0=c["W0"])
+    params = d(c["params"])
+    prep = finc.flow_prepare(params, c["L"], c["K"], c["C0"], c["k"], c["hid"])
+    zs = [d(t) for t in c["z"]]
+    x = torch.empty((c["B"], c["C0"], c["H0"], c["W0"]), device=dev)
+    ws = torch.empty(finc.lib().finc_flow_workspace_bytes(c["B"], c["L"], c["C0"], c["H0"],
+                                                          c["W0"], c["hid"]),
+                     dtype=torch.uint8, device=dev)
+    sample = lambda: finc.flow_sample(zs, params, prep, out=x, workspace=ws, **geo, **a)
+    forward = lambda: finc.flow_forward(x, params, prep, workspace=ws, **a)
+    sample()
+    torch.cuda.synchronize()
+    st = protocol_runs(lambda: event_ms(sample))
+    ft = protocol_runs(lambda: event_ms(forward))
+    # conv flops of the coupling and prior networks (2 per multiply-add), per image
+    fl = 0
+    for l in range(c["L"]):
+        C, hw = (4 * c["C0"]) << l, (c["H0"] >> (l + 1)) * (c["W0"] >> (l + 1))
+        hid = c["hid"]
+        fl += c["K"] * 2 * hw * (hid * C // 2 * 9 + hid * hid + C * hid * 9)
+        if l < c["L"] - 1:
+            fl += 2 * hw * C * C // 2 * 9
+    B = c["B"]
+    return {"workload": name, "B": B, "params": int(params.numel()),
+            "sample": st, "sample_images_per_s": B / (st["mean_ms"] * 1e-3),
+            "forward": ft, "forward_images_per_s": B / (ft["mean_ms"] * 1e-3),
+            "network_gflop_per_image": fl / 1e9,
+            "sample_network_tflops": fl * B / (st["mean_ms"] * 1e-3) / 1e12,
+            "paper_context": "FInC Flow, CIFAR-10 [28,28,28], 39.46M parameters: ST 0.41 s, "
+                             "FT 0.37 s for 100 images on a GTX 1080Ti (Table 3); untrained "
+                             "models in both"}
+
+
 def batch_scaling(dev) -> dict:
     """The benchmark layer (12 x 16 x 16, k = 3, TL) at batches 1, 8 and 64:
     one GPU's share of a batch of 64 sharded over 64, 8 and 1 GPUs."""
@@ -309,26 +476,60 @@ def batch_scaling(dev) -> dict:
     return {"what": "layer 12 x 16 x 16, k = 3, TL, by batch", "rows": rows}
 
 
+def host_info() -> dict:
+    """CPU model and the cores this process may use."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": len(os.sched_getaffinity(0)),
+            "os_cpu_count": os.cpu_count()}
+
+
+def oracle_threads() -> int:
+    # at most 16: a one-GPU box's share of the host, whatever nproc shows
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def cpu_rate(work, seconds: float, threads: int):
+    """Images per second of `work(i)` (one image each, i counting up) run on
+    `threads` threads until `seconds` have passed (at least one round).  The
+    oracle's C calls release the interpreter lock, so threads run in parallel."""
+    import concurrent.futures
+
+    done = 0
+    t0 = time.perf_counter()
+    with concurrent.futures.ThreadPoolExecutor(threads) as pool:
+        while True:
+            list(pool.map(work, range(done, done + threads)))
+            done += threads
+            el = time.perf_counter() - t0
+            if el >= seconds:
+                break
+    return done / el, done, el
+
+
 def cpu_baseline(step, seconds: float):
-    """The oracle, single-threaded, on whole batches of the same step until
-    `seconds` of CPU time have been spent (at least one image)."""
+    """The oracle on the same step (forward, log|det|, raster-order inverse,
+    fp64), image by image: on all the host cores this process may use (at
+    most 16), and on one thread, each for about `seconds`."""
     import oracle
 
     orc = oracle.default()
-    B = step.B
-    done = 0
-    t0 = time.perf_counter()
-    while True:
-        n = min(B, 8)
-        imgs = [(done + i) % B for i in range(n)]
-        step.cpu_step(orc, imgs)
-        done += n
-        el = time.perf_counter() - t0
-        if el >= seconds:
-            break
-    return dict(value=done / el, unit="images/s", cores=1, kind="oracle",
-                sample=f"{done} images of the same step (forward, logdet, raster-order "
-                       f"inverse) in fp64, {el:.1f} s, one thread")
+    work = lambda i: step.cpu_step(orc, [i % step.B])
+    n = oracle_threads()
+    rate, done, el = cpu_rate(work, seconds, n)
+    rate1, done1, el1 = cpu_rate(work, seconds / 2, 1)
+    return dict(value=rate, unit="images/s", cores=n, kind="oracle",
+                sample=f"{done} images of the same step (forward, logdet, raster-order inverse) "
+                       f"in fp64 on {n} threads, {el:.1f} s",
+                single_thread={"value": rate1, "unit": "images/s", "cores": 1,
+                               "sample": f"{done1} images, {el1:.1f} s"},
+                host=host_info())
 
 
 def main():
@@ -460,10 +661,27 @@ def main():
         "wall_s_timed": wall,
         "round_trip_max_abs": err,
     }
+    # the paper's protocol on the dominant kernel: 11 runs of a graph of 20
+    # inverse launches, the first dropped
+    if graph is not None:
+        g20 = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g20):
+            for _ in range(20):
+                st.inverse()
+        torch.cuda.synchronize()
+        pr = protocol_runs(lambda: event_ms(g20.replay))
+        out["inverse"]["protocol"] = {k: (v / 20 * 1e3 if k == "mean_ms" or k == "std_ms" else
+                                          ([w / 20 * 1e3 for w in v] if k == "ci95_ms" else v))
+                                      for k, v in pr.items()}
+        out["inverse"]["protocol"]["unit"] = "us per launch (graph of 20)"
     if not args.no_configs:
         out["per_config"] = per_config(dev)
         out["scaling_sweep"] = scaling_sweep(dev)
         out["batch_scaling"] = batch_scaling(dev)
+    if not args.no_configs:
+        out["step_cost"] = step_cost(dev)
+    if not args.no_flow:
+        out["flow_sampling"] = flow_sampling(dev)
     if args.cpu_seconds > 0:
         out["cpu_baseline"] = cpu_baseline(st, args.cpu_seconds)
     print(json.dumps(out))

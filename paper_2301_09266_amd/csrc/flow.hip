@@ -99,6 +99,11 @@ struct ConvArgs {
     int B, Ci, Co, H, W, K;   // K = Ci R^2
     long long xs, ys;         // floats from one image to the next
     Div d_HW, d_W;
+    // split over K (blockIdx.z = part): part z sums chunks [z cps, (z+1) cps)
+    // and writes its raw sums to partial + z Co Q (c_out-major); a second
+    // kernel adds the parts in order and applies bias, ReLU and scale
+    float *partial;
+    int cps;
 };
 
 constexpr int kConvThreads = 256;
@@ -183,15 +188,17 @@ __global__ __launch_bounds__(kConvThreads) void conv_kernel(ConvArgs a) {
 #pragma unroll
     for (int s = 0; s < NS; ++s)
         acc[s] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    const int nchunk = (a.K + kKc - 1) / kKc;
-    load_chunk(0);
+    const int nall = (a.K + kKc - 1) / kKc;
+    const int cbeg = a.partial ? blockIdx.z * a.cps : 0;
+    const int nchunk = a.partial ? min(a.cps, nall - cbeg) : nall;
+    load_chunk(cbeg * kKc);
     store_chunk();
     __syncthreads();
     const float *arow = &As[(wco * 16 + li) * kSK + 4 * kq];
     const float *brow = &Bs[(wpx * 16 * NS + li) * kSK + 4 * kq];
     for (int c = 0; c < nchunk; ++c) {
         if (c + 1 < nchunk)
-            load_chunk((c + 1) * kKc);   // in flight during the MFMAs
+            load_chunk((cbeg + c + 1) * kKc);   // in flight during the MFMAs
 #pragma unroll
         for (int blk = 0; blk < kKc / 16; ++blk) {
             const float4 w4 = *reinterpret_cast<const float4 *>(arow + 16 * blk);
@@ -209,6 +216,20 @@ __global__ __launch_bounds__(kConvThreads) void conv_kernel(ConvArgs a) {
             store_chunk();
             __syncthreads();
         }
+    }
+    if (a.partial) {   // raw sums of this part of K
+        float *pz = a.partial + (long long)blockIdx.z * a.Co * Q;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const int qo = n0 + wpx * 16 * NS + 16 * s + li;
+#pragma unroll
+            for (int rr = 0; rr < 4; ++rr) {
+                const int co = co0 + wco * 16 + 4 * kq + rr;
+                if (qo < Q && co < a.Co)
+                    pz[(long long)co * Q + qo] = acc[s][rr];
+            }
+        }
+        return;
     }
     // epilogue: lane (kq, li) holds c_out 4 kq + rr of pixel li of each slot
     float bv[4], sv[4];
@@ -239,6 +260,26 @@ __global__ __launch_bounds__(kConvThreads) void conv_kernel(ConvArgs a) {
     }
 }
 
+
+// The parts of a K-split convolution added in order (part 0 first), then
+// bias, ReLU and the output scale, as the unsplit kernel's epilogue does.
+__global__ __launch_bounds__(256) void conv_reduce_kernel(ConvArgs a, int parts) {
+    const int Q = a.B * a.H * a.W, HW = a.H * a.W;
+    const long long n = (long long)a.Co * Q;
+    for (long long e = blockIdx.x * 256ll + threadIdx.x; e < n; e += (long long)gridDim.x * 256) {
+        const int co = (int)(e / Q), q = (int)(e - (long long)co * Q);
+        float v = 0.0f;
+        for (int z = 0; z < parts; ++z)
+            v += a.partial[(long long)z * n + e];
+        v += a.bias[co];
+        if (a.relu)
+            v = fmaxf(v, 0.0f);
+        if (a.ls)
+            v *= expf(3.0f * a.ls[co]);
+        const int b = divi(q, a.d_HW), p = q - b * HW;
+        a.y[(long long)b * a.ys + (long long)co * HW + p] = v;
+    }
+}
 
 // ---------------------------------------------------------------------------
 // The 1x1 convolution with its actnorm, prepared in fp64 (one workgroup per
@@ -549,9 +590,13 @@ bool valid_step(int C, int k, int hid) {
            hid <= 4096;
 }
 
+// Parts a narrow convolution's K is split into (at most; their partial sums
+// take kMaxParts Co B H W floats).
+constexpr int kMaxParts = 8;
+
 int launch_conv(const float *x, long long xs, float *y, long long ys, const float *Wt,
                 const float *bias, const float *ls, int relu, int B, int Ci, int Co, int H, int W,
-                int R, hipStream_t st) {
+                int R, hipStream_t st, float *partial = nullptr) {
     if (B == 0)
         return FINC_OK;
     ConvArgs a;
@@ -580,11 +625,32 @@ int launch_conv(const float *x, long long xs, float *y, long long ys, const floa
         else
             hipLaunchKernelGGL((conv_kernel<3, 4, 4>), grid, dim3(kConvThreads), 0, st, a);
     } else {
-        const dim3 grid(cdiv(Q, 128), cdiv(Co, 16));
+        // narrow outputs (the coupling's last convolution, C_out = C) have
+        // few tiles: a long K is split into parts of at least 8 chunks so
+        // that the grid covers the chip.  The parts depend on K only, not on
+        // the batch, and are added in order: results stay deterministic and
+        // independent of B.
+        const int nchunk = cdiv(a.K, kKc);
+        int parts = 1;
+        if (partial)
+            while (parts < kMaxParts && nchunk >= 16 * parts)
+                parts *= 2;
+        a.cps = cdiv(nchunk, parts);
+        parts = cdiv(nchunk, a.cps);
+        a.partial = parts > 1 ? partial : nullptr;
+        const dim3 grid(cdiv(Q, 128), cdiv(Co, 16), parts);
         if (R == 1)
             hipLaunchKernelGGL((conv_kernel<1, 1, 2>), grid, dim3(kConvThreads), 0, st, a);
         else
             hipLaunchKernelGGL((conv_kernel<3, 1, 2>), grid, dim3(kConvThreads), 0, st, a);
+        if (parts > 1) {
+            const int rc = launched();
+            if (rc != FINC_OK)
+                return rc;
+            const long long n = (long long)Co * Q;
+            hipLaunchKernelGGL(conv_reduce_kernel, dim3((unsigned)(n / 256 + 1 < 8192 ? n / 256 + 1 : 8192)),
+                               dim3(256), 0, st, a, parts);
+        }
     }
     return launched();
 }
@@ -623,13 +689,15 @@ int launch_squeeze(const float *in, float *out, int B, int C, int H, int W, long
 }
 
 // Scratch of a Step at (B, C, H, W): u (B C HW), hh (B C HW), t1, t2
-// (B hid HW each), floats, each 256-byte aligned.
+// (B hid HW each), the partial sums of the coupling's last convolution
+// (kMaxParts B C HW), floats, each 256-byte aligned.
 struct StepScratch {
-    float *u, *hh, *t1, *t2;
+    float *u, *hh, *t1, *t2, *part;
 };
 size_t step_scratch_bytes(int B, int C, int H, int W, int hid) {
     const size_t hw = (size_t)H * W;
-    return 2 * up256((size_t)B * C * hw * 4) + 2 * up256((size_t)B * hid * hw * 4);
+    return 2 * up256((size_t)B * C * hw * 4) + 2 * up256((size_t)B * hid * hw * 4) +
+           up256((size_t)kMaxParts * B * C * hw * 4);
 }
 StepScratch carve(void *ws, int B, int C, int H, int W, int hid) {
     const size_t hw = (size_t)H * W;
@@ -642,6 +710,8 @@ StepScratch carve(void *ws, int B, int C, int H, int W, int hid) {
     s.t1 = (float *)p;
     p += up256((size_t)B * hid * hw * 4);
     s.t2 = (float *)p;
+    p += up256((size_t)B * hid * hw * 4);
+    s.part = (float *)p;
     return s;
 }
 
@@ -656,7 +726,7 @@ int coupling_net(const float *v, long long vs, const float *sp, const StepLayout
                          sp + L.b2, nullptr, 1, B, L.hid, L.hid, H, W, 1, st);
     if (rc == FINC_OK)
         rc = launch_conv(s.t2, (long long)L.hid * hw, s.hh, (long long)L.C * hw, sp + L.w3,
-                         sp + L.b3, sp + L.ls3, 0, B, L.hid, L.C, H, W, 3, st);
+                         sp + L.b3, sp + L.ls3, 0, B, L.hid, L.C, H, W, 3, st, s.part);
     return rc;
 }
 

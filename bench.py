@@ -212,8 +212,10 @@ def per_config(dev) -> list:
             # training direction: dx and dK of the layer for a loss gradient dy
             dyt = torch.randn_like(x)
             dxo, dKo = torch.empty_like(x), torch.empty_like(K)
-            bwd = graph_time_us(lambda: finc.backward(x, dyt, K, c["corner"], -1.0, dx=dxo, dK=dKo),
-                                5, 20)
+            bws = torch.empty(finc.lib().finc_backward_workspace_bytes(B, C, H, W, k),
+                              dtype=torch.uint8, device=dev)
+            bwd = graph_time_us(lambda: finc.backward(x, dyt, K, c["corner"], -1.0, dx=dxo, dK=dKo,
+                                                      workspace=bws), 5, 20)
         elif kind == "unit":
             B, C, H, W, k = (c[n] for n in "BCHWk")
             x, K4 = d(c["x"]), d(c["K4"])

@@ -231,8 +231,9 @@ int finc_split_inverse_prepared(const float *y, float *x, const void *prepared4,
 
 /* ---- Backward of one layer (training) -------------------------------------
  * The paper trains on the negative log-likelihood (Sec. 2, NLL equation) and
- * resets the masked weights' gradients to zero after every step (Sec. 6).
- * For y = finc_forward(x, K, corner) and dy = dL/dy of a loss L:
+ * resets the masked weights' gradients to zero after every step (appendix,
+ * training details).  For y = finc_forward(x, K, corner) and dy = dL/dy of a
+ * loss L:
  *   dx: device (B, C, H, W), or NULL to skip: J^T dy, the gradient of L with
  *       respect to x;
  *   dK: device OIHW (C*C*k*k floats), or NULL to skip: the gradient of L
@@ -240,12 +241,17 @@ int finc_split_inverse_prepared(const float *y, float *x, const void *prepared4,
  *       (self tap, c_in > c_out) set to 0, plus gld * H * W / K[c,c,self] on
  *       the self diagonal -- the gradient of gld * log|det| (gld = 0 for the
  *       convolution alone, -1 for the log|det| part of the NLL of one image).
- * x, dy, K are read only; dx and dK overwritten, overlapping none of the
- * inputs nor each other (else FINC_EINVAL).  With B = 0 only the log|det|
- * term remains in dK.  Deterministic: no atomics, a fixed summation order. */
+ *   workspace: device, >= finc_backward_workspace_bytes(B, C, H, W, k) bytes,
+ *       256-byte aligned, overwritten (the partial sums of dK over parts of
+ *       the batch's pixels).
+ * x, dy, K are read only; dx, dK and the workspace overwritten, overlapping
+ * none of the inputs nor each other (else FINC_EINVAL).  With B = 0 only the
+ * log|det| term remains in dK (x, dy may then be NULL).  Deterministic: no atomics, a fixed summation
+ * order (dK depends on B through that order, as any sum over the batch). */
+size_t finc_backward_workspace_bytes(int B, int C, int H, int W, int k);
 int finc_backward(const float *x, const float *dy, const float *K, float *dx,
                   float *dK, double gld, int B, int C, int H, int W, int k,
-                  int corner, hipStream_t stream);
+                  int corner, void *workspace, hipStream_t stream);
 
 /* ---- Multi-scale sampling stack (Sec. 4.4, Fig. 2c) ---------------------
  * L levels of U units; level l has C_l = C1 << l channels and spatial size

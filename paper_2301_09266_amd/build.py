@@ -16,6 +16,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "finc.hip")
 FLOW_SRC = os.path.join(PKG, "csrc", "flow.hip")
+BACKWARD_SRC = os.path.join(PKG, "csrc", "backward.hip")
 LIB = os.path.join(PKG, "csrc", "libfinc.so")
 CALIB_SRC = os.path.join(PKG, "csrc", "calib.hip")
 CALIB_LIB = os.path.join(PKG, "csrc", "libfinc_calib.so")
@@ -42,12 +43,13 @@ def build(out: str = LIB, extra: list[str] | None = None) -> str:
     """Compile every part of finc.hip and link them into `out`."""
     tmpdir = tempfile.mkdtemp(prefix="finc_build_")
     try:
-        # finc.hip in parts (FINC_PART), then flow.hip
-        parts = [-2] + list(range(INVERSE_GROUPS)) + [None]
+        # finc.hip in parts (FINC_PART), then flow.hip and backward.hip
+        parts = [-2] + list(range(INVERSE_GROUPS)) + [FLOW_SRC, BACKWARD_SRC]
         objs = [os.path.join(tmpdir, f"part{i}.o") for i in range(len(parts))]
 
         def compile_part(i: int) -> None:
-            src, defs = (FLOW_SRC, []) if parts[i] is None else (SRC, [f"-DFINC_PART={parts[i]}"])
+            src, defs = ((parts[i], []) if isinstance(parts[i], str)
+                         else (SRC, [f"-DFINC_PART={parts[i]}"]))
             cmd = [HIPCC, *FLAGS, *(extra or []), *defs,
                    "-I", os.path.join(ROOT, "include"), "-c", "-o", objs[i], src]
             subprocess.run(cmd, check=True)

@@ -1779,138 +1779,6 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Backward of one layer (training on the negative log-likelihood, Sec. 2 and
-// Sec. 6).  y = layer(x) sends x[ci, i + a - oh, j + b - ow] to y[co, i, j]
-// with weight K[co][ci][a][b] (masked at the self tap), so
-//   dx[ci, s, t] = sum over co, a, b of K[co][ci][a][b] dy[co, s - a + oh, t - b + ow]
-//                  (output pixels inside the image),
-//   dK[co][ci][a][b] = sum over images and output pixels of dy[co, i, j] times
-//                  the input the tap read (zero outside the image).
-// ---------------------------------------------------------------------------
-constexpr int kBwdThreads = 256;
-
-// One thread per input pixel of one channel ci of one image (grid: pixel
-// blocks x C x B); the channel's masked weights K[.][ci][.][.] in LDS.  Per
-// output channel, the k x k output gradients a pixel receives are loaded
-// together (unconditionally, from clamped addresses) before they are summed.
-template <int KMAX>
-__global__ __launch_bounds__(kBwdThreads) void backward_dx_kernel(const float *dy, const float *K,
-                                                                  float *dx, int C, int H, int W,
-                                                                  int k, int oh, int ow) {
-    extern __shared__ float kc[];   // kc[(co k + a) k + b] = K[co][ci][a][b], masked
-    const int ci = blockIdx.y, b = blockIdx.z, kk = k * k;
-    for (int idx = threadIdx.x; idx < C * kk; idx += blockDim.x) {
-        const int co = idx / kk, t = idx - co * kk, a = t / k, bb = t - a * k;
-        kc[idx] = (a == oh && bb == ow && ci > co)
-                      ? 0.0f
-                      : K[((size_t)(co * C + ci) * k + a) * k + bb];
-    }
-    __syncthreads();
-    const size_t HW = (size_t)H * W;
-    const int p = blockIdx.x * blockDim.x + threadIdx.x;
-    if (p >= (int)HW)
-        return;
-    const int s = p / W, t = p - s * W;
-    const float *dyb = dy + (size_t)b * C * HW;
-    float acc = 0.0f;
-    for (int co = 0; co < C; ++co) {
-        const float *dyc = dyb + co * HW;
-        float v[KMAX][KMAX];
-#pragma unroll
-        for (int a = 0; a < KMAX; ++a) {
-            const int i = s - a + oh;
-#pragma unroll
-            for (int bb = 0; bb < KMAX; ++bb) {
-                const int j = t - bb + ow;
-                const bool in = a < k && bb < k && i >= 0 && i < H && j >= 0 && j < W;
-                v[a][bb] = dyc[in ? (size_t)i * W + j : 0];
-                v[a][bb] = in ? v[a][bb] : 0.0f;
-            }
-        }
-#pragma unroll
-        for (int a = 0; a < KMAX; ++a)
-#pragma unroll
-            for (int bb = 0; bb < KMAX; ++bb)
-                if (a < k && bb < k)
-                    acc = fmaf(kc[(co * k + a) * k + bb], v[a][bb], acc);
-    }
-    dx[((size_t)b * C + ci) * HW + p] = acc;
-}
-
-// One workgroup per (co, ci, kernel row a): each thread sums its share of
-// the batch's output pixels (a stride of the workgroup size) for the k taps
-// of row a, then the taps are summed across the threads by a fixed tree in
-// LDS: the same bits on every run.  Masked entries get 0, the self diagonal
-// also gets gld H W / K[c][c][self] (in double).
-template <int KMAX>
-__global__ __launch_bounds__(kBwdThreads) void backward_dk_kernel(const float *x, const float *dy,
-                                                                  const float *K, float *dK,
-                                                                  double gld, int B, int C, int H,
-                                                                  int W, int k, int oh, int ow) {
-    __shared__ float red[KMAX][kBwdThreads];
-    const int co = blockIdx.x, ci = blockIdx.y, a = blockIdx.z, tid = threadIdx.x;
-    const size_t HW = (size_t)H * W, img = (size_t)C * HW;
-    float acc[KMAX];
-#pragma unroll
-    for (int t = 0; t < KMAX; ++t)
-        acc[t] = 0.0f;
-    // U (image, pixel) positions a round, a workgroup's width apart: all
-    // their loads (unconditional, from clamped addresses) in flight before
-    // the multiply-adds, which run in position order
-    constexpr int U = 8;
-    const int HWi = (int)HW, total = B * HWi;   // (B C H W < 2^31)
-    for (int q0 = tid; q0 < total; q0 += U * kBwdThreads) {
-        float g[U], v[U][KMAX];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int q = q0 + u * kBwdThreads;
-            const bool live = q < total;
-            const int qc = live ? q : 0, n = qc / HWi, p = qc - n * HWi;
-            const int i = p / W, j = p - i * W, ii = i + a - oh;
-            const float *xn = x + n * img + ci * HW;
-            g[u] = live ? dy[n * img + co * HW + p] : 0.0f;
-#pragma unroll
-            for (int bb = 0; bb < KMAX; ++bb) {
-                const int jj = j + bb - ow;
-                const bool in = bb < k && ii >= 0 && ii < H && jj >= 0 && jj < W;
-                v[u][bb] = xn[in ? (size_t)ii * W + jj : 0];
-                v[u][bb] = in ? v[u][bb] : 0.0f;
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int bb = 0; bb < KMAX; ++bb)
-                if (bb < k)
-                    acc[bb] = fmaf(g[u], v[u][bb], acc[bb]);
-    }
-#pragma unroll
-    for (int t = 0; t < KMAX; ++t)
-        red[t][tid] = acc[t];
-    __syncthreads();
-    for (int h = kBwdThreads / 2; h > 0; h >>= 1) {
-        if (tid < h) {
-#pragma unroll
-            for (int t = 0; t < KMAX; ++t)
-                red[t][tid] += red[t][tid + h];
-        }
-        __syncthreads();
-    }
-    if (tid < k) {
-        const int bb = tid;
-        const bool self = a == oh && bb == ow;
-        float v = red[bb][0];
-        if (self && ci > co)
-            v = 0.0f;   // masked: its gradient is reset to zero
-        else if (self && ci == co)
-            v = (float)((double)v +
-                        gld * (double)H * (double)W /
-                            (double)K[((size_t)(co * C + co) * k + a) * k + bb]);
-        dK[((size_t)(co * C + ci) * k + a) * k + bb] = v;
-    }
-}
-
-// ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
 bool valid_shape(int B, int C, int H, int W, int k) {
@@ -2245,46 +2113,6 @@ bool levels_differ(const InvArgs &a) {
     return false;
 }
 
-// Backward of one layer: dx (batches of up to 65535 images per launch: the
-// grid's third dimension) and dK.
-int launch_backward(const float *x, const float *dy, const float *K, float *dx, float *dK,
-                    double gld, int B, int C, int H, int W, int k, int corner,
-                    hipStream_t stream) {
-    int oh, ow;
-    self_tap(corner, k, oh, ow);
-    const size_t img = (size_t)C * H * W;
-    for (int b0 = 0; dx && b0 < B; b0 += 65535) {
-        const dim3 grid((unsigned)ceil_div(H * W, kBwdThreads), (unsigned)C,
-                        (unsigned)imin(B - b0, 65535));
-        const size_t lds = (size_t)C * k * k * sizeof(float);
-        if (k <= 3)
-            hipLaunchKernelGGL(backward_dx_kernel<3>, grid, dim3(kBwdThreads), lds, stream,
-                               dy + b0 * img, K, dx + b0 * img, C, H, W, k, oh, ow);
-        else if (k <= 5)
-            hipLaunchKernelGGL(backward_dx_kernel<5>, grid, dim3(kBwdThreads), lds, stream,
-                               dy + b0 * img, K, dx + b0 * img, C, H, W, k, oh, ow);
-        else
-            hipLaunchKernelGGL(backward_dx_kernel<7>, grid, dim3(kBwdThreads), lds, stream,
-                               dy + b0 * img, K, dx + b0 * img, C, H, W, k, oh, ow);
-        const int rc = launched();
-        if (rc != FINC_OK)
-            return rc;
-    }
-    if (!dK)
-        return FINC_OK;
-    const dim3 grid((unsigned)C, (unsigned)C, (unsigned)k);
-    if (k <= 3)
-        hipLaunchKernelGGL(backward_dk_kernel<3>, grid, dim3(kBwdThreads), 0, stream, x, dy, K,
-                           dK, gld, B, C, H, W, k, oh, ow);
-    else if (k <= 5)
-        hipLaunchKernelGGL(backward_dk_kernel<5>, grid, dim3(kBwdThreads), 0, stream, x, dy, K,
-                           dK, gld, B, C, H, W, k, oh, ow);
-    else
-        hipLaunchKernelGGL(backward_dk_kernel<7>, grid, dim3(kBwdThreads), 0, stream, x, dy, K,
-                           dK, gld, B, C, H, W, k, oh, ow);
-    return launched();
-}
-
 // Channels up to which the forward launch also prepares the inverse's
 // weights in its own blocks (their LDS is small); wider layers get a
 // separate preparation launch.
@@ -2594,21 +2422,6 @@ int finc_forward(const float *x, float *y, const float *K, double *logdet, void 
     }
     return launch_forward(x, y, K, logdet, (float *)prepared, B, C, H, W, k, 1, corner, 0,
                           stream);
-}
-
-int finc_backward(const float *x, const float *dy, const float *K, float *dx, float *dK,
-                  double gld, int B, int C, int H, int W, int k, int corner,
-                  hipStream_t stream) {
-    if (!valid_shape(B, C, H, W, k) || !valid_corner(corner) || !x || !dy || !K)
-        return FINC_EINVAL;
-    const size_t act = (size_t)B * C * H * W * sizeof(float);
-    const size_t wts = (size_t)C * C * k * k * sizeof(float);
-    if (dx && (overlap(dx, act, x, act) || overlap(dx, act, dy, act) || overlap(dx, act, K, wts) ||
-               (dK && overlap(dx, act, dK, wts))))
-        return FINC_EINVAL;
-    if (dK && (overlap(dK, wts, x, act) || overlap(dK, wts, dy, act) || overlap(dK, wts, K, wts)))
-        return FINC_EINVAL;
-    return launch_backward(x, dy, K, dx, dK, gld, B, C, H, W, k, corner, stream);
 }
 
 int finc_logdet(const float *K, int C, int k, int corner, int H, int W, double *out,

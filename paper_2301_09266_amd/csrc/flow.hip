@@ -40,246 +40,10 @@
 #include <stdint.h>
 #include <string.h>
 
+#include "conv_gemm.h"
 #include "finc.h"
 
 namespace {
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-
-__device__ inline f32x4 mfma4(float a, float b, f32x4 c) {
-    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
-}
-
-inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
-
-// Division of a non-negative int by a divisor fixed on the host (multiply-
-// high and shifts, Granlund and Montgomery's round-up method).
-struct Div {
-    unsigned m;
-    int s1, s2;
-};
-inline Div make_div(int d) {
-    int l = 0;
-    while ((1ull << l) < (unsigned long long)d)
-        ++l;
-    Div f;
-    f.m = (unsigned)((((1ull << l) - (unsigned long long)d) << 32) / (unsigned long long)d + 1);
-    f.s1 = l < 1 ? l : 1;
-    f.s2 = l > 1 ? l - 1 : 0;
-    return f;
-}
-__device__ inline int divi(int x, const Div &f) {
-    const unsigned t = __umulhi(f.m, (unsigned)x);
-    return (int)((t + (((unsigned)x - t) >> f.s1)) >> f.s2);
-}
-
-// ---------------------------------------------------------------------------
-// Same-padded R x R convolution as an MFMA implicit GEMM.
-//   y[b][co][i][j] = act(bias[co] + sum_{ci,a,c} Wt[co][ci][a][c] *
-//                        x[b][ci][i + a - P][j + c - P]) * oscale[co]
-// with P = (R - 1) / 2, zeros outside the image, act = ReLU or identity,
-// oscale = exp(3 ls[co]) or 1.  Weights are OIHW, so W[co][k] with
-// k = ci R^2 + a R + c is contiguous in k.  Pixels are flattened over the
-// batch (q = b H W + p), so a block's tile may span images.
-//
-// Block: 256 threads, 4 waves arranged WCO (along c_out) x 4 / WCO (along
-// pixels); each wave computes 16 c_out x 16 NS pixels (NS accumulators).
-// K is staged 64 at a time: A[co][k] (weights) and B[px][k] (the gathered
-// input window, im2col on the fly), rows padded to 68 floats.  Within one
-// 16-wide slice of k, lane group kq takes k = 4 kq .. 4 kq + 3 as the four
-// MFMAs' k (one float4 LDS read each for A and B).
-// ---------------------------------------------------------------------------
-struct ConvArgs {
-    const float *x;
-    float *y;
-    const float *Wt;     // (Co, Ci, R, R)
-    const float *bias;   // (Co)
-    const float *ls;     // (Co) or null
-    int relu;
-    int B, Ci, Co, H, W, K;   // K = Ci R^2
-    long long xs, ys;         // floats from one image to the next
-    Div d_HW, d_W;
-    // split over K (blockIdx.z = part): part z sums chunks [z cps, (z+1) cps)
-    // and writes its raw sums to partial + z Co Q (c_out-major); a second
-    // kernel adds the parts in order and applies bias, ReLU and scale
-    float *partial;
-    int cps;
-};
-
-constexpr int kConvThreads = 256;
-constexpr int kKc = 64;     // k values staged at a time
-constexpr int kSK = 68;     // LDS row stride (floats)
-
-template <int R, int WCO, int NS>
-__global__ __launch_bounds__(kConvThreads) void conv_kernel(ConvArgs a) {
-    constexpr int BM = 16 * WCO, BN = 16 * NS * (4 / WCO);
-    constexpr int TPP = kConvThreads / BN;   // threads per staged pixel
-    constexpr int QPT = 16 / TPP;            // k quads per thread (B)
-    constexpr int AQ = BM * 16 / kConvThreads;   // weight quads per thread
-    constexpr int P = (R - 1) / 2;
-    __shared__ __attribute__((aligned(16))) float As[BM * kSK];
-    __shared__ __attribute__((aligned(16))) float Bs[BN * kSK];
-    const int tid = threadIdx.x, lane = tid & 63, kq = lane >> 4, li = lane & 15;
-    const int wave = tid >> 6, wco = wave % WCO, wpx = wave / WCO;
-    const int co0 = blockIdx.y * BM;
-    const int n0 = blockIdx.x * BN;
-    const int HW = a.H * a.W, Q = a.B * HW;
-
-    // this thread's staged pixel and its window's validity per tap
-    const int spx = tid % BN, sk0 = tid / BN;   // pixel slot; first k quad
-    const int q = n0 + spx;
-    const bool qok = q < Q;
-    const int qb = qok ? divi(q, a.d_HW) : 0, qp = qok ? q - qb * HW : 0;
-    const int qi = divi(qp, a.d_W), qj = qp - qi * a.W;
-    unsigned tapok = 0;
-#pragma unroll
-    for (int t = 0; t < R * R; ++t) {
-        const int ii = qi + t / R - P, jj = qj + t % R - P;
-        if (qok && ii >= 0 && ii < a.H && jj >= 0 && jj < a.W)
-            tapok |= 1u << t;
-    }
-    const float *xq = a.x + (long long)qb * a.xs + qp;
-
-    float ra[AQ][4], rb[QPT][4];
-    auto load_chunk = [&](int k0) {
-#pragma unroll
-        for (int u = 0; u < AQ; ++u) {
-            const int idx = tid + u * kConvThreads;
-            const int col = idx >> 4, kk = k0 + 4 * (idx & 15);
-            const int co = co0 + col;
-            const float *w = a.Wt + (long long)(co < a.Co ? co : 0) * a.K;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const bool ok = co < a.Co && kk + e < a.K;
-                const float v = w[ok ? kk + e : 0];
-                ra[u][e] = ok ? v : 0.0f;
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < QPT; ++u) {
-            const int kk = k0 + 4 * (sk0 + u * TPP);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int k = kk + e;
-                const int ci = (int)((unsigned)k / (R * R));
-                const int t = k - ci * R * R;
-                const int ta = t / R, tb = t - ta * R;
-                const bool ok = k < a.K && ((tapok >> t) & 1u);
-                const long long off = (long long)ci * HW + (ta - P) * a.W + (tb - P);
-                const float v = xq[ok ? off : 0];
-                rb[u][e] = ok ? v : 0.0f;
-            }
-        }
-    };
-    auto store_chunk = [&] {
-#pragma unroll
-        for (int u = 0; u < AQ; ++u) {
-            const int idx = tid + u * kConvThreads;
-            *reinterpret_cast<float4 *>(&As[(idx >> 4) * kSK + 4 * (idx & 15)]) =
-                make_float4(ra[u][0], ra[u][1], ra[u][2], ra[u][3]);
-        }
-#pragma unroll
-        for (int u = 0; u < QPT; ++u)
-            *reinterpret_cast<float4 *>(&Bs[spx * kSK + 4 * (sk0 + u * TPP)]) =
-                make_float4(rb[u][0], rb[u][1], rb[u][2], rb[u][3]);
-    };
-
-    f32x4 acc[NS];
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-        acc[s] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    const int nall = (a.K + kKc - 1) / kKc;
-    const int cbeg = a.partial ? blockIdx.z * a.cps : 0;
-    const int nchunk = a.partial ? min(a.cps, nall - cbeg) : nall;
-    load_chunk(cbeg * kKc);
-    store_chunk();
-    __syncthreads();
-    const float *arow = &As[(wco * 16 + li) * kSK + 4 * kq];
-    const float *brow = &Bs[(wpx * 16 * NS + li) * kSK + 4 * kq];
-    for (int c = 0; c < nchunk; ++c) {
-        if (c + 1 < nchunk)
-            load_chunk((cbeg + c + 1) * kKc);   // in flight during the MFMAs
-#pragma unroll
-        for (int blk = 0; blk < kKc / 16; ++blk) {
-            const float4 w4 = *reinterpret_cast<const float4 *>(arow + 16 * blk);
-#pragma unroll
-            for (int s = 0; s < NS; ++s) {
-                const float4 b4 = *reinterpret_cast<const float4 *>(brow + 16 * s * kSK + 16 * blk);
-                acc[s] = mfma4(w4.x, b4.x, acc[s]);
-                acc[s] = mfma4(w4.y, b4.y, acc[s]);
-                acc[s] = mfma4(w4.z, b4.z, acc[s]);
-                acc[s] = mfma4(w4.w, b4.w, acc[s]);
-            }
-        }
-        if (c + 1 < nchunk) {
-            __syncthreads();
-            store_chunk();
-            __syncthreads();
-        }
-    }
-    if (a.partial) {   // raw sums of this part of K
-        float *pz = a.partial + (long long)blockIdx.z * a.Co * Q;
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            const int qo = n0 + wpx * 16 * NS + 16 * s + li;
-#pragma unroll
-            for (int rr = 0; rr < 4; ++rr) {
-                const int co = co0 + wco * 16 + 4 * kq + rr;
-                if (qo < Q && co < a.Co)
-                    pz[(long long)co * Q + qo] = acc[s][rr];
-            }
-        }
-        return;
-    }
-    // epilogue: lane (kq, li) holds c_out 4 kq + rr of pixel li of each slot
-    float bv[4], sv[4];
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-        const int co = co0 + wco * 16 + 4 * kq + rr;
-        const int cc = co < a.Co ? co : 0;
-        bv[rr] = a.bias[cc];
-        sv[rr] = a.ls ? expf(3.0f * a.ls[cc]) : 1.0f;
-    }
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-        const int qo = n0 + wpx * 16 * NS + 16 * s + li;
-        if (qo >= Q)
-            continue;
-        const int b = divi(qo, a.d_HW), p = qo - b * HW;
-        float *yq = a.y + (long long)b * a.ys + p;
-#pragma unroll
-        for (int rr = 0; rr < 4; ++rr) {
-            const int co = co0 + wco * 16 + 4 * kq + rr;
-            if (co < a.Co) {
-                float v = acc[s][rr] + bv[rr];
-                if (a.relu)
-                    v = fmaxf(v, 0.0f);
-                yq[(long long)co * HW] = v * sv[rr];
-            }
-        }
-    }
-}
-
-
-// The parts of a K-split convolution added in order (part 0 first), then
-// bias, ReLU and the output scale, as the unsplit kernel's epilogue does.
-__global__ __launch_bounds__(256) void conv_reduce_kernel(ConvArgs a, int parts) {
-    const int Q = a.B * a.H * a.W, HW = a.H * a.W;
-    const long long n = (long long)a.Co * Q;
-    for (long long e = blockIdx.x * 256ll + threadIdx.x; e < n; e += (long long)gridDim.x * 256) {
-        const int co = (int)(e / Q), q = (int)(e - (long long)co * Q);
-        float v = 0.0f;
-        for (int z = 0; z < parts; ++z)
-            v += a.partial[(long long)z * n + e];
-        v += a.bias[co];
-        if (a.relu)
-            v = fmaxf(v, 0.0f);
-        if (a.ls)
-            v *= expf(3.0f * a.ls[co]);
-        const int b = divi(q, a.d_HW), p = q - b * HW;
-        a.y[(long long)b * a.ys + (long long)co * HW + p] = v;
-    }
-}
 
 // ---------------------------------------------------------------------------
 // The 1x1 convolution with its actnorm, prepared in fp64 (one workgroup per
@@ -543,6 +307,18 @@ inline bool overlap(const void *a, size_t na, const void *b, size_t nb) {
 }
 int launched() { return hipGetLastError() == hipSuccess ? FINC_OK : FINC_EHIP; }
 
+// The flow's convolutions: 3 x 3 "same" (coupling and prior networks) and
+// 1 x 1 (the coupling's middle convolution, the 1x1 / actnorm map).
+int launch_conv(const float *x, long long xs, float *y, long long ys, const float *Wt,
+                const float *bias, const float *ls, int relu, int B, int Ci, int Co, int H, int W,
+                int R, hipStream_t st, float *partial = nullptr) {
+    if (R == 1)
+        return launch_conv_r<1>(x, xs, y, ys, Wt, bias, ls, relu, B, Ci, Co, H, W, -1, -1, st,
+                                partial);
+    return launch_conv_r<3>(x, xs, y, ys, Wt, bias, ls, relu, B, Ci, Co, H, W, -1, -1, st,
+                            partial);
+}
+
 // Offsets (floats) of one Step's parameters.
 struct StepLayout {
     int C, q, Ch, k, hid;
@@ -588,71 +364,6 @@ StepPrep step_prep(int C, int k) {
 bool valid_step(int C, int k, int hid) {
     return C >= 4 && C % 4 == 0 && C <= kFlowMaxC && k >= 1 && k <= FINC_MAX_K && hid >= 1 &&
            hid <= 4096;
-}
-
-// Parts a narrow convolution's K is split into (at most; their partial sums
-// take kMaxParts Co B H W floats).
-constexpr int kMaxParts = 8;
-
-int launch_conv(const float *x, long long xs, float *y, long long ys, const float *Wt,
-                const float *bias, const float *ls, int relu, int B, int Ci, int Co, int H, int W,
-                int R, hipStream_t st, float *partial = nullptr) {
-    if (B == 0)
-        return FINC_OK;
-    ConvArgs a;
-    memset(&a, 0, sizeof(a));
-    a.x = x;
-    a.y = y;
-    a.Wt = Wt;
-    a.bias = bias;
-    a.ls = ls;
-    a.relu = relu;
-    a.B = B;
-    a.Ci = Ci;
-    a.Co = Co;
-    a.H = H;
-    a.W = W;
-    a.K = Ci * R * R;
-    a.xs = xs;
-    a.ys = ys;
-    a.d_HW = make_div(H * W);
-    a.d_W = make_div(W);
-    const long long Q = (long long)B * H * W;
-    if (Co >= 64) {
-        const dim3 grid(cdiv(Q, 64), cdiv(Co, 64));
-        if (R == 1)
-            hipLaunchKernelGGL((conv_kernel<1, 4, 4>), grid, dim3(kConvThreads), 0, st, a);
-        else
-            hipLaunchKernelGGL((conv_kernel<3, 4, 4>), grid, dim3(kConvThreads), 0, st, a);
-    } else {
-        // narrow outputs (the coupling's last convolution, C_out = C) have
-        // few tiles: a long K is split into parts of at least 8 chunks so
-        // that the grid covers the chip.  The parts depend on K only, not on
-        // the batch, and are added in order: results stay deterministic and
-        // independent of B.
-        const int nchunk = cdiv(a.K, kKc);
-        int parts = 1;
-        if (partial)
-            while (parts < kMaxParts && nchunk >= 16 * parts)
-                parts *= 2;
-        a.cps = cdiv(nchunk, parts);
-        parts = cdiv(nchunk, a.cps);
-        a.partial = parts > 1 ? partial : nullptr;
-        const dim3 grid(cdiv(Q, 128), cdiv(Co, 16), parts);
-        if (R == 1)
-            hipLaunchKernelGGL((conv_kernel<1, 1, 2>), grid, dim3(kConvThreads), 0, st, a);
-        else
-            hipLaunchKernelGGL((conv_kernel<3, 1, 2>), grid, dim3(kConvThreads), 0, st, a);
-        if (parts > 1) {
-            const int rc = launched();
-            if (rc != FINC_OK)
-                return rc;
-            const long long n = (long long)Co * Q;
-            hipLaunchKernelGGL(conv_reduce_kernel, dim3((unsigned)(n / 256 + 1 < 8192 ? n / 256 + 1 : 8192)),
-                               dim3(256), 0, st, a, parts);
-        }
-    }
-    return launched();
 }
 
 int launch_elt(int mode, float *v, long long vs, const float *vin, long long vins, const float *h,

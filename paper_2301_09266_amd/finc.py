@@ -35,8 +35,9 @@ SIGNATURES = {
     "finc_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_inverse_prepared": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
     "finc_inverse_noalloc": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
+    "finc_backward_workspace_bytes": (_sz, [_i, _i, _i, _i, _i]),
     "finc_backward": (_i, [_vp, _vp, _vp, _vp, _vp, ctypes.c_double, _i, _i, _i, _i, _i, _i,
-                           _vp]),
+                           _vp, _vp]),
     "finc_unit_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "finc_unit_logdet": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
@@ -275,7 +276,8 @@ def inverse_prepared(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: in
 
 def backward(x: torch.Tensor, dy: torch.Tensor, K: torch.Tensor, corner: int,
              gld: float = 0.0, want_dx: bool = True, want_dK: bool = True,
-             dx: torch.Tensor | None = None, dK: torch.Tensor | None = None):
+             dx: torch.Tensor | None = None, dK: torch.Tensor | None = None,
+             workspace: torch.Tensor | None = None):
     """(dx, dK) of one layer for the loss gradient dy (see finc_backward);
     either is None when not wanted."""
     L = _require_lib()
@@ -292,8 +294,9 @@ def backward(x: torch.Tensor, dy: torch.Tensor, K: torch.Tensor, corner: int,
         dK = torch.empty_like(K) if dK is None else _dev(dK, "dK", K.shape)
     else:
         dK = None
+    ws = _workspace(int(L.finc_backward_workspace_bytes(B, C, H, W, k)), x.device, workspace)
     _check(L.finc_backward(_ptr(x), _ptr(dy), _ptr(K), _ptr(dx), _ptr(dK), float(gld), B, C, H,
-                           W, k, corner, _stream()), "finc_backward")
+                           W, k, corner, _ptr(ws), _stream()), "finc_backward")
     return dx, dK
 
 

@@ -101,7 +101,21 @@ FAKE4 = ctypes.c_void_p(0x1900000)
     (FAKE, FAKE2, FAKE3, FAKE4, ctypes.c_void_p(0x1900000 + 64), 0.0, *SHAPE, 0),  # dK over dx
 ])
 def test_backward_rejects(args):
-    assert finc.lib().finc_backward(*args, None) == finc.EINVAL
+    ws = ctypes.c_void_p(0x40000000)
+    assert finc.lib().finc_backward(*args, ws, None) == finc.EINVAL
+
+
+def test_backward_workspace_rules():
+    lib = finc.lib()
+    args = (FAKE, FAKE2, FAKE3, FAKE4, NULL, 0.0, *SHAPE, 0)
+    assert lib.finc_backward(*args, NULL, None) == finc.EINVAL                         # none
+    assert lib.finc_backward(*args, ctypes.c_void_p(0x40000010), None) == finc.EINVAL  # misaligned
+    assert lib.finc_backward(*args, ctypes.c_void_p(0x1900000), None) == finc.EINVAL   # over dx
+    assert lib.finc_backward(*args, ctypes.c_void_p(0x1100000), None) == finc.EINVAL   # over K
+    B, C, H, W, k = SHAPE
+    n = lib.finc_backward_workspace_bytes(B, C, H, W, k)
+    assert n >= C * C * k * k * 4 and n % 256 == 0
+    assert lib.finc_backward_workspace_bytes(B, 65, H, W, k) == 0
 
 
 def test_inverse_rejects():

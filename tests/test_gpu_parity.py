@@ -300,7 +300,8 @@ def test_unit_forward_bands(orc, shape):
 
 
 @pytest.mark.parametrize("shape", [(2, 3, 5, 7, 3), (3, 12, 16, 16, 3), (1, 7, 9, 6, 5),
-                                   (2, 4, 6, 6, 1), (2, 5, 8, 11, 2), (1, 20, 9, 10, 7)],
+                                   (2, 4, 6, 6, 1), (2, 5, 8, 11, 2), (1, 20, 9, 10, 7),
+                                   (2, 64, 5, 6, 3), (1, 33, 7, 5, 4), (3, 2, 11, 4, 6)],
                          ids=lambda s: "x".join(map(str, s)))
 @pytest.mark.parametrize("corner", [0, 1, 2, 3])
 def test_backward(orc, shape, corner):
@@ -322,19 +323,40 @@ def test_backward(orc, shape, corner):
     assert torch.equal(dx, dx2) and torch.equal(dK, dK2)
 
 
-def test_backward_workload(orc):
-    """Backward at the benchmark shape (64 images, 12 x 16 x 16, k = 3, TL):
-    dK sums 16,384 pixels per tap; dx checked on four sampled images."""
-    c = synth.make("layer_c12_16x16_b64_k3")
-    x, K = c["x"], c["K"]
+@pytest.mark.parametrize("name", ["layer_c12_16x16_b64_k3", "layer_c12_32x32_b64_k3",
+                                  "layer_c12_32x32_b64_k5"])
+def test_backward_workload(orc, name):
+    """Backward at the single-layer workloads' shapes (64 images of 12
+    channels, 16 x 16 or 32 x 32, k = 3 or 5): dK sums 16,384 or 65,536
+    pixels per tap, each entry held to the size of its terms (the root sum
+    of squares of the products it adds, from the oracle's dK of x^2 and
+    dy^2); dx checked on three sampled images; dx alone and dK alone give
+    the same bits as both together."""
+    c = synth.make(name)
+    x, K, corner = c["x"], c["K"], c["corner"]
     dy = np.random.default_rng(5).normal(size=x.shape)
-    dx, dK = finc.backward(dev(x), dev(dy), dev(K), 0, -1.0)
-    want_dx, want_dK = orc.backward(f64(x), f64(dy), f64(K), 0, -1.0)
-    assert_close(host(dK), want_dK, "backward dK, batch 64")
+    dx, dK = finc.backward(dev(x), dev(dy), dev(K), corner, -1.0)
+    want_dx, want_dK = orc.backward(f64(x), f64(dy), f64(K), corner, -1.0)
+    _, sq = orc.backward(f64(x) ** 2, f64(dy) ** 2, f64(K), corner, 0.0)
+    assert_close(host(dK), want_dK, f"backward dK, {name}", scale=np.sqrt(sq))
     pick = [0, 21, 63]
-    assert_close(host(dx)[pick], want_dx[pick], "backward dx, batch 64")
-    only_dk = finc.backward(dev(x), dev(dy), dev(K), 0, -1.0, want_dx=False)
+    assert_close(host(dx)[pick], want_dx[pick], f"backward dx, {name}")
+    only_dk = finc.backward(dev(x), dev(dy), dev(K), corner, -1.0, want_dx=False)
     assert only_dk[0] is None and torch.equal(only_dk[1], dK)
+    only_dx = finc.backward(dev(x), dev(dy), dev(K), corner, -1.0, want_dK=False)
+    assert only_dx[1] is None and torch.equal(only_dx[0], dx)
+
+
+def test_backward_empty_batch(orc):
+    """No images: dx is empty and dK holds only the log|det| term (masked
+    entries 0), as the oracle gives it."""
+    C, H, W, k, corner = 5, 6, 7, 3, 2
+    K = synth.masked_kernel(C, k, corner, 77)
+    x = np.zeros((0, C, H, W))
+    dx, dK = finc.backward(dev(x), dev(x), dev(K), corner, -1.0, dK=poisoned(K.shape))
+    want_dx, want_dK = orc.backward(f64(x), f64(x), f64(K), corner, -1.0)
+    assert dx.shape == (0, C, H, W)
+    assert_close(host(dK), want_dK, "backward dK, no images")
 
 
 def test_unsupported_shapes_rejected():

@@ -47,6 +47,10 @@ def load(path: str = LIB):
         "orc_inverse": [_dp, _dp, _dp, L, I, I, I, I, I],
         "orc_logdet": [_dp, I, I, I, I, I, _dp],
         "orc_backward": [_dp, _dp, _dp, _dp, _dp, ctypes.c_double, L, I, I, I, I, I],
+        "orc_unit_backward": [_dp, _dp, _dp, _dp, _dp, ctypes.c_double, L, I, I, I, I],
+        "orc_split_backward": [_dp, _dp, _dp, _dp, _dp, ctypes.c_double, L, I, I, I, I],
+        "orc_actnorm_backward": [_dp, _dp, _dp, _dp, _dp, _dp, ctypes.c_double, L, I, I, I],
+        "orc_gauss_nll": [ctypes.POINTER(_dp), ctypes.POINTER(L), I, L, _dp, _dp, _dp],
         "orc_unit_forward": [_dp, _dp, _dp, L, I, I, I, I],
         "orc_unit_inverse": [_dp, _dp, _dp, L, I, I, I, I],
         "orc_unit_logdet": [_dp, I, I, I, I, _dp],
@@ -74,7 +78,8 @@ def load(path: str = LIB):
     for name, args in sig.items():
         fn = getattr(lib, name)
         fn.argtypes = args
-        fn.restype = None if name.startswith(("orc_actnorm", "orc_squeeze", "orc_unsqueeze")) else I
+        fn.restype = None if name.startswith(("orc_actnorm_f", "orc_actnorm_i", "orc_squeeze",
+                                              "orc_unsqueeze")) else I
     lib.orc_flow_params.restype = L
     if path == LIB:
         _lib = lib
@@ -135,6 +140,45 @@ class Oracle:
         _check(self.lib.orc_backward(_p(x), _p(dy), _p(K), _p(dx), _p(dK), float(gld), B, C,
                                      H, W, K.shape[-1], corner))
         return dx, dK
+
+    def unit_backward(self, x, dy, K4, gld: float = 0.0):
+        """(dx, dK4) of the sequential unit (see orc_unit_backward)."""
+        x, dy, K4 = _c(x), _c(dy), _c(K4)
+        B, C, H, W = x.shape
+        dx, dK4 = np.empty_like(x), np.empty_like(K4)
+        _check(self.lib.orc_unit_backward(_p(x), _p(dy), _p(K4), _p(dx), _p(dK4), float(gld),
+                                          B, C, H, W, K4.shape[-1]))
+        return dx, dK4
+
+    def split_backward(self, x, dy, Kq4, gld: float = 0.0):
+        """(dx, dKq4) of the channel-split unit (see orc_split_backward)."""
+        x, dy, Kq4 = _c(x), _c(dy), _c(Kq4)
+        B, C, H, W = x.shape
+        dx, dKq4 = np.empty_like(x), np.empty_like(Kq4)
+        _check(self.lib.orc_split_backward(_p(x), _p(dy), _p(Kq4), _p(dx), _p(dKq4),
+                                           float(gld), B, C, H, W, Kq4.shape[-1]))
+        return dx, dKq4
+
+    def actnorm_backward(self, x, dy, s, gld: float = 0.0):
+        """(dx, ds, db) of actnorm (see orc_actnorm_backward)."""
+        x, dy, s = _c(x), _c(dy), _c(s)
+        B, C, H, W = x.shape
+        dx, ds, db = np.empty_like(x), np.empty(C), np.empty(C)
+        _check(self.lib.orc_actnorm_backward(_p(x), _p(dy), _p(s), _p(dx), _p(ds), _p(db),
+                                             float(gld), B, C, H, W))
+        return dx, ds, db
+
+    def gauss_nll(self, zs, logdet):
+        """(nll, bpd) per image for latents zs (arrays with the batch first)
+        and per-image log|det| (see orc_gauss_nll)."""
+        zs = [_c(z) for z in zs]
+        logdet = _c(logdet)
+        B = logdet.shape[0]
+        n = (ctypes.c_long * len(zs))(*[int(np.prod(z.shape[1:])) for z in zs])
+        ptrs = (_dp * len(zs))(*[_p(z) for z in zs])
+        nll, bpd = np.empty(B), np.empty(B)
+        _check(self.lib.orc_gauss_nll(ptrs, n, len(zs), B, _p(logdet), _p(nll), _p(bpd)))
+        return nll, bpd
 
     def unit_forward(self, x, K4) -> np.ndarray:
         x, K4 = _c(x), _c(K4)

@@ -557,6 +557,137 @@ int orc_backward(const double *x, const double *dy, const double *K, double *dx,
     return ORC_OK;
 }
 
+/* Backward of the FInC unit (the four blocks TL, TR, BL, BR in sequence):
+ * the inputs of the last three blocks, h1 = TL(x), h2 = TR(h1),
+ * h3 = BL(h2), are recomputed by the forward; then the chain rule takes the
+ * blocks in reverse, each block's orc_backward receiving the input gradient
+ * of the block after it.  The unit's log|det| is the sum of its blocks', so
+ * each block takes the same gld.  dx or dK4 may be NULL. */
+int orc_unit_backward(const double *x, const double *dy, const double *K4, double *dx,
+                      double *dK4, double gld, long B, int C, int H, int W, int k)
+{
+    if (bad_shape(B, C, H, W, k, 0) || !x || !dy || !K4)
+        return ORC_EINVAL;
+    const long n = B * (long)C * H * W, ksz = (long)C * C * k * k;
+    const size_t bytes = sizeof(double) * (n > 0 ? n : 1);
+    double *h[4] = {(double *)x, malloc(bytes), malloc(bytes), malloc(bytes)};
+    double *g = malloc(bytes), *gn = malloc(bytes);
+    int rc = (h[1] && h[2] && h[3] && g && gn) ? ORC_OK : ORC_ENOMEM;
+    for (int q = 0; q < 3 && rc == ORC_OK; ++q)
+        rc = orc_forward(h[q], h[q + 1], K4 + q * ksz, B, C, H, W, k, UNIT_ORDER[q]);
+    if (rc == ORC_OK)
+        memcpy(g, dy, sizeof(double) * n);
+    for (int q = 3; q >= 0 && rc == ORC_OK; --q) {
+        rc = orc_backward(h[q], g, K4 + q * ksz, gn, dK4 ? dK4 + q * ksz : NULL, gld, B, C, H,
+                          W, k, UNIT_ORDER[q]);
+        memcpy(g, gn, sizeof(double) * n);
+    }
+    if (rc == ORC_OK && dx)
+        memcpy(dx, g, sizeof(double) * n);
+    free(h[1]);
+    free(h[2]);
+    free(h[3]);
+    free(g);
+    free(gn);
+    return rc;
+}
+
+/* Backward of the channel-split unit: quarter g (channels g C/4 .. (g+1) C/4
+ * of every image) is one block with corner g and its own weights, so its
+ * gradients come from orc_backward on that quarter alone, over the whole
+ * batch; gld multiplies the unit's log|det| (the quarters' sum).  dx or
+ * dKq4 may be NULL. */
+int orc_split_backward(const double *x, const double *dy, const double *Kq4, double *dx,
+                       double *dKq4, double gld, long B, int C, int H, int W, int k)
+{
+    if (bad_shape(B, C, H, W, k, 0) || C % 4 != 0 || !x || !dy || !Kq4)
+        return ORC_EINVAL;
+    const int Cq = C / 4;
+    const long part = (long)Cq * H * W, ksz = (long)Cq * Cq * k * k;
+    const size_t bytes = sizeof(double) * (B * part > 0 ? B * part : 1);
+    double *xq = malloc(bytes), *gq = malloc(bytes), *dq = malloc(bytes);
+    int rc = (xq && gq && dq) ? ORC_OK : ORC_ENOMEM;
+    for (int g = 0; g < 4 && rc == ORC_OK; ++g) {
+        for (long b = 0; b < B; ++b) {
+            const long off = (b * C + (long)g * Cq) * H * W;
+            memcpy(xq + b * part, x + off, sizeof(double) * part);
+            memcpy(gq + b * part, dy + off, sizeof(double) * part);
+        }
+        rc = orc_backward(xq, gq, Kq4 + g * ksz, dq, dKq4 ? dKq4 + g * ksz : NULL, gld, B, Cq,
+                          H, W, k, g);
+        for (long b = 0; dx && rc == ORC_OK && b < B; ++b)
+            memcpy(dx + (b * C + (long)g * Cq) * H * W, dq + b * part, sizeof(double) * part);
+    }
+    free(xq);
+    free(gq);
+    free(dq);
+    return rc;
+}
+
+/* Backward of actnorm y = s x + b (per channel), whose log|det| is
+ * H W sum_c log|s_c| per image:
+ *   dx = s dy;  ds[c] = sum over images and pixels of dy x, plus
+ *   gld H W / s[c];  db[c] = sum over images and pixels of dy.
+ * dx, ds or db may be NULL. */
+int orc_actnorm_backward(const double *x, const double *dy, const double *s, double *dx,
+                         double *ds, double *db, double gld, long B, int C, int H, int W)
+{
+    if (B < 0 || C < 1 || H < 1 || W < 1 || !s || (B > 0 && (!x || !dy)))
+        return ORC_EINVAL;
+    const long plane = (long)H * W;
+    for (int c = 0; c < C; ++c) {
+        double sx = 0.0, sy = 0.0;
+        for (long n = 0; n < B; ++n)
+            for (long p = 0; p < plane; ++p) {
+                const long o = (n * C + c) * plane + p;
+                sx += dy[o] * x[o];
+                sy += dy[o];
+                if (dx)
+                    dx[o] = s[c] * dy[o];
+            }
+        if (ds)
+            ds[c] = sx + gld * (double)plane / s[c];
+        if (db)
+            db[c] = sy;
+    }
+    return ORC_OK;
+}
+
+/* Negative log-likelihood of each image (Sec. 2, the log-probability
+ * equation, negated): the flow maps the image to latents whose values z
+ * are standard normal, and the layers' log|det| (summed per image in
+ * logdet) corrects the density, so
+ *   nll[b] = sum over the image's latent values of (z^2 + log 2 pi) / 2
+ *            - logdet[b],
+ * and bits per dimension (Sec. 6, BPD equation) bpd[b] = nll[b] log2(e) / D
+ * with D the image's values (the latents' total, n[0] + ... + n[L-1]).
+ * z[l] holds B blocks of n[l] values, one per image.  bpd may be NULL. */
+int orc_gauss_nll(const double *const *z, const long *n, int L, long B, const double *logdet,
+                  double *nll, double *bpd)
+{
+    if (L < 1 || B < 0 || !z || !n || !logdet || !nll)
+        return ORC_EINVAL;
+    long D = 0;
+    for (int l = 0; l < L; ++l) {
+        if (n[l] < 1 || (B > 0 && !z[l]))
+            return ORC_EINVAL;
+        D += n[l];
+    }
+    const double log2pi = log(2.0 * 3.14159265358979323846);
+    for (long b = 0; b < B; ++b) {
+        double q = 0.0;
+        for (int l = 0; l < L; ++l)
+            for (long e = 0; e < n[l]; ++e) {
+                const double v = z[l][b * n[l] + e];
+                q += 0.5 * (v * v + log2pi);
+            }
+        nll[b] = q - logdet[b];
+        if (bpd)
+            bpd[b] = nll[b] / ((double)D * log(2.0));
+    }
+    return ORC_OK;
+}
+
 /* ==========================================================================
  * The full FInC Flow (Sec. 4.4 "Architecture", Fig. 2b and 2c).
  *

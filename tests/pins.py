@@ -512,6 +512,103 @@ def pin_backward_dense(o):
         close(dx.ravel(), J.T @ dy.ravel(), 1e-12, f"backward J^T corner={corner}")
 
 
+def _torch_layer(xt, Kt, corner):
+    """One masked block in torch (fp64): the mask multiplies K, so autograd
+    gives the masked entries gradient 0; also its diagonal log|det| per
+    image, H W sum_c log|K[c, c, self]|."""
+    k = Kt.shape[-1]
+    sh, sw = SELF[corner](k)
+    mask = torch.ones_like(Kt)
+    for co in range(Kt.shape[0]):
+        mask[co, co + 1:, sh, sw] = 0.0
+    Km = Kt * mask
+    y = F.conv2d(F.pad(xt, PADS[corner](k)), Km)
+    diag = torch.stack([Km[c, c, sh, sw] for c in range(Kt.shape[0])])
+    return y, xt.shape[2] * xt.shape[3] * torch.log(diag.abs()).sum()
+
+
+def pin_unit_backward_autograd(o):
+    """Backward of the sequential unit (TL, TR, BL, BR) = torch autograd of
+    L = sum(y dy) + gld log|det| through the four blocks, for k in {1, 2, 3}
+    and H != W; junk in the masked slots of every block is ignored."""
+    rng = np.random.default_rng(31)
+    for (B, C, H, W, k) in [(2, 3, 5, 6, 3), (1, 2, 4, 7, 2), (2, 3, 3, 4, 1)]:
+        K4 = np.stack([rand_kernel(rng, C, k, q) for q in range(4)])
+        x = rng.normal(size=(B, C, H, W))
+        dy = rng.normal(size=(B, C, H, W))
+        gld = float(rng.normal())
+        xt = torch.tensor(x, requires_grad=True)
+        Kt = torch.tensor(K4, requires_grad=True)
+        h, ld = xt, 0.0
+        for q in range(4):
+            h, l1 = _torch_layer(h, Kt[q], q)
+            ld = ld + l1
+        ((h * torch.tensor(dy)).sum() + gld * ld).backward()
+        Kj = np.stack([synth.garbage_in_mask(K4[q], q, seed=q + 9) for q in range(4)])
+        dx, dK4 = o.unit_backward(x, dy, Kj, gld)
+        close(dx, xt.grad.numpy(), 1e-11, f"unit backward dx k={k}")
+        close(dK4, Kt.grad.numpy(), 1e-11, f"unit backward dK k={k}")
+
+
+def pin_split_backward_autograd(o):
+    """Backward of the channel-split unit = torch autograd of the four
+    quarters (corner g on channels g C/4 .. (g+1) C/4, concatenated)."""
+    rng = np.random.default_rng(37)
+    for (B, C, H, W, k) in [(2, 8, 5, 6, 3), (3, 4, 4, 3, 2)]:
+        q = C // 4
+        Kq4 = np.stack([rand_kernel(rng, q, k, g) for g in range(4)])
+        x = rng.normal(size=(B, C, H, W))
+        dy = rng.normal(size=(B, C, H, W))
+        gld = float(rng.normal())
+        xt = torch.tensor(x, requires_grad=True)
+        Kt = torch.tensor(Kq4, requires_grad=True)
+        outs, ld = [], 0.0
+        for g in range(4):
+            y, l1 = _torch_layer(xt[:, g * q:(g + 1) * q], Kt[g], g)
+            outs.append(y)
+            ld = ld + l1
+        ((torch.cat(outs, 1) * torch.tensor(dy)).sum() + gld * ld).backward()
+        dx, dKq4 = o.split_backward(x, dy, Kq4, gld)
+        close(dx, xt.grad.numpy(), 1e-11, f"split backward dx C={C}")
+        close(dKq4, Kt.grad.numpy(), 1e-11, f"split backward dK C={C}")
+
+
+def pin_actnorm_backward_autograd(o):
+    """Actnorm backward = torch autograd of sum(y dy) + gld H W sum log|s|."""
+    rng = np.random.default_rng(41)
+    B, C, H, W = 3, 5, 4, 6
+    x, dy = rng.normal(size=(B, C, H, W)), rng.normal(size=(B, C, H, W))
+    s = rng.uniform(0.5, 1.5, size=C) * rng.choice([-1.0, 1.0], size=C)
+    b = rng.normal(size=C)
+    gld = -0.7
+    xt = torch.tensor(x, requires_grad=True)
+    st = torch.tensor(s, requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    y = st[None, :, None, None] * xt + bt[None, :, None, None]
+    ((y * torch.tensor(dy)).sum() + gld * H * W * torch.log(st.abs()).sum()).backward()
+    dx, ds, db = o.actnorm_backward(x, dy, s, gld)
+    close(dx, xt.grad.numpy(), 1e-12, "actnorm backward dx")
+    close(ds, st.grad.numpy(), 1e-11, "actnorm backward ds")
+    close(db, bt.grad.numpy(), 1e-11, "actnorm backward db")
+
+
+def pin_gauss_nll(o):
+    """NLL per image = -(sum of scipy's standard normal log-density over all
+    its latents) - log|det|; bits per dimension = NLL log2(e) / D; with
+    latents of different sizes and images that differ."""
+    import scipy.stats
+    rng = np.random.default_rng(43)
+    B = 3
+    zs = [rng.normal(size=(B, 6, 4, 4)), rng.normal(size=(B, 12, 2, 2)) * 2.0]
+    logdet = rng.normal(size=B) * 10.0
+    nll, bpd = o.gauss_nll(zs, logdet)
+    D = 6 * 16 + 12 * 4
+    want = np.array([-sum(scipy.stats.norm.logpdf(z[i]).sum() for z in zs) - logdet[i]
+                     for i in range(B)])
+    close(nll, want, 1e-10, "gauss nll")
+    close(bpd, want / (D * np.log(2.0)), 1e-12, "bits per dimension")
+
+
 # --------------------------------------------------------------------------
 # The full FInC Flow (Sec. 4.4, Fig. 2b/2c): 1x1 convolution, coupling, Step,
 # multi-scale flow
@@ -666,5 +763,7 @@ ALL_PINS = [
     pin_round_trip, pin_k1_pixelwise, pin_impulse_geometric, pin_row_lfilter,
     pin_flip_equivalence, pin_wavefront_schedule, pin_unit_dense, pin_unit_round_trip,
     pin_split_dense, pin_split_round_trip, pin_squeeze_reshape, pin_actnorm, pin_stack,
-    pin_backward_autograd, pin_backward_dense, pin_conv1x1, pin_coupling, pin_step, pin_flow,
+    pin_backward_autograd, pin_backward_dense, pin_unit_backward_autograd,
+    pin_split_backward_autograd, pin_actnorm_backward_autograd, pin_gauss_nll, pin_conv1x1,
+    pin_coupling, pin_step, pin_flow,
 ]

@@ -55,6 +55,19 @@ MUTANTS = [
      "if (1)", 0),
     ("backward forgets the log|det| term",
      "s += gld * (double)H * (double)W / kw(K, C, k, co, co, a, b);", "s += 0.0;", 0),
+    ("unit backward feeds each block its own output",
+     "rc = orc_backward(h[q], g, K4 + q * ksz, gn,",
+     "rc = orc_backward(h[q < 3 ? q + 1 : 3], g, K4 + q * ksz, gn,", 0),
+    ("unit backward gives the log|det| term to the last block only",
+     "dK4 ? dK4 + q * ksz : NULL, gld, B, C, H,", "dK4 ? dK4 + q * ksz : NULL, q == 3 ? gld : 0.0, B, C, H,", 0),
+    ("split backward gives every quarter the first corner",
+     "H, W, k, g);\n        for (long b = 0; dx", "H, W, k, 0);\n        for (long b = 0; dx", 0),
+    ("actnorm backward forgets the log|det| term", "ds[c] = sx + gld * (double)plane / s[c];",
+     "ds[c] = sx;", 0),
+    ("actnorm backward scales dx by 1/s", "dx[o] = s[c] * dy[o];", "dx[o] = dy[o] / s[c];", 0),
+    ("nll drops the normalising constant", "q += 0.5 * (v * v + log2pi);", "q += 0.5 * v * v;", 0),
+    ("nll adds the log|det|", "nll[b] = q - logdet[b];", "nll[b] = q + logdet[b];", 0),
+    ("bpd in nats", "bpd[b] = nll[b] / ((double)D * log(2.0));", "bpd[b] = nll[b] / (double)D;", 0),
     ("backward weight gradient reads the mirrored tap",
      "x[n * img + ci * plane + (long)ii * W + jj];",
      "x[n * img + ci * plane + (long)(H - 1 - ii) * W + jj];", 0),

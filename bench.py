@@ -225,6 +225,12 @@ def per_config(dev) -> list:
             fwd = graph_time_us(lambda: finc.unit_forward(x, K4, out=out), 5, 10)
             inv = graph_time_us(lambda: finc.unit_inverse_prepared(y, prep, k, out=out), 5, 10)
             act, wts, layers = 2 * C * H * W * 4, 4 * C * C * k * k * 4, 4
+            # training direction: recompute of the blocks' inputs, four layer backwards
+            dyt, dxo, dKo = torch.randn_like(x), torch.empty_like(x), torch.empty_like(K4)
+            bws = torch.empty(finc.lib().finc_unit_backward_workspace_bytes(B, C, H, W, k),
+                              dtype=torch.uint8, device=dev)
+            bwd = graph_time_us(lambda: finc.unit_backward(x, dyt, K4, -1.0, dx=dxo, dK4=dKo,
+                                                           workspace=bws), 5, 10)
         elif kind == "split":
             B, C, H, W, k = (c[n] for n in "BCHWk")
             x, Kq4 = d(c["x"]), d(c["Kq4"])
@@ -234,6 +240,11 @@ def per_config(dev) -> list:
             fwd = graph_time_us(lambda: finc.split_forward(x, Kq4, out=out), 5, 20)
             inv = graph_time_us(lambda: finc.split_inverse_prepared(y, prep, k, out=out), 5, 20)
             act, wts, layers = 2 * C * H * W * 4, 4 * (C // 4) ** 2 * k * k * 4, 1
+            dyt, dxo, dKo = torch.randn_like(x), torch.empty_like(x), torch.empty_like(Kq4)
+            bws = torch.empty(finc.lib().finc_split_backward_workspace_bytes(B, C, H, W, k),
+                              dtype=torch.uint8, device=dev)
+            bwd = graph_time_us(lambda: finc.split_backward(x, dyt, Kq4, -1.0, dx=dxo, dKq4=dKo,
+                                                            workspace=bws), 5, 20)
         else:
             B, C1, H1, W1, k, L, U = (c[n] for n in ("B", "C1", "H1", "W1", "k", "levels", "units"))
             Kf = d(np.concatenate([a.ravel() for a in c["K"]]))

@@ -230,7 +230,7 @@ int finc_split_inverse_prepared(const float *y, float *x, const void *prepared4,
                                 hipStream_t stream);
 
 /* ---- Backward of one layer (training) -------------------------------------
- * The paper trains on the negative log-likelihood (Sec. 2, NLL equation) and
+ * The paper trains on the negative log-likelihood (Sec. 3, NLL equation) and
  * resets the masked weights' gradients to zero after every step (appendix,
  * training details).  For y = finc_forward(x, K, corner) and dy = dL/dy of a
  * loss L:
@@ -252,6 +252,57 @@ size_t finc_backward_workspace_bytes(int B, int C, int H, int W, int k);
 int finc_backward(const float *x, const float *dy, const float *K, float *dx,
                   float *dK, double gld, int B, int C, int H, int W, int k,
                   int corner, void *workspace, hipStream_t stream);
+
+/* Backward of the FInC units, by the chain rule over their blocks (same
+ * gradient conventions as finc_backward; gld multiplies the unit's log|det|,
+ * the sum of its four blocks', so each block takes the same gld).
+ * finc_unit_backward: the unit of finc_unit_forward (blocks TL, TR, BL, BR
+ *   in sequence, K4 = 4 OIHW tensors).  The inputs of blocks 2..4 are
+ *   recomputed by the forward into the workspace, then the blocks run in
+ *   reverse.  dK4: 4 C*C*k*k floats or NULL; dx may be NULL.  workspace:
+ *   >= finc_unit_backward_workspace_bytes(B, C, H, W, k) bytes (four
+ *   activations and dK's partial sums).  The forward's limits apply
+ *   (FINC_EUNSUPPORTED where finc_forward_plan reports them).
+ * finc_split_backward: the channel-split unit of finc_split_forward
+ *   (Sec. 4.3): quarter g of the C channels is one block of C/4 channels
+ *   with corner g; Kq4 / dKq4 = 4 (C/4, C/4, k, k) tensors.  workspace:
+ *   >= finc_split_backward_workspace_bytes(B, C, H, W, k) bytes.
+ * Aliasing and errors as for finc_backward. */
+size_t finc_unit_backward_workspace_bytes(int B, int C, int H, int W, int k);
+int finc_unit_backward(const float *x, const float *dy, const float *K4, float *dx,
+                       float *dK4, double gld, int B, int C, int H, int W, int k,
+                       void *workspace, hipStream_t stream);
+size_t finc_split_backward_workspace_bytes(int B, int C, int H, int W, int k);
+int finc_split_backward(const float *x, const float *dy, const float *Kq4, float *dx,
+                        float *dKq4, double gld, int B, int C, int H, int W, int k,
+                        void *workspace, hipStream_t stream);
+
+/* Backward of actnorm y = s x + b (per channel c; log|det| H W sum_c
+ * log|s_c| per image, Sec. 4.4): dx = s dy; ds[c] = sum over the batch's
+ * pixels of dy x, plus gld H W / s[c]; db[c] = sum of dy.  x, dy, dx:
+ * device (B, C, H, W); s, ds, db: device C floats; dx, ds or db may be
+ * NULL.  workspace: >= finc_actnorm_backward_workspace_bytes(B, C, H, W)
+ * bytes, 256-byte aligned (per-channel partial sums).  Sums in fp64, in a
+ * fixed order.  Outputs overlapping any input or each other: FINC_EINVAL. */
+size_t finc_actnorm_backward_workspace_bytes(int B, int C, int H, int W);
+int finc_actnorm_backward(const float *x, const float *dy, const float *s, float *dx,
+                          float *ds, float *db, double gld, int B, int C, int H, int W,
+                          void *workspace, hipStream_t stream);
+
+/* Negative log-likelihood of each image under a standard normal latent
+ * (Sec. 3, the log-probability equation negated) and its bits per dimension
+ * (Sec. 5, BPD equation):
+ *   nll[b] = sum over image b's latent values v of (v^2 + log 2 pi) / 2
+ *            - logdet[b];   bpd[b] = nll[b] / (D log 2),
+ * D = n[0] + ... + n[L-1] values per image.  z: host array of L device
+ * pointers, z[l] holding B blocks of n[l] floats (one per image), 1 <= L
+ * <= 16; logdet, nll, bpd: device doubles, B each (bpd may be NULL).  The
+ * gradient of sum_b nll[b] with respect to z is z itself.  For data
+ * quantised to 2^8 levels and scaled to [0, 1), add D log 256 to nll
+ * before dividing (not done here: the equation has no such term).  Fixed
+ * summation order (fp64). */
+int finc_gauss_nll(const float *const *z, const long long *n, int L, int B,
+                   const double *logdet, double *nll, double *bpd, hipStream_t stream);
 
 /* ---- Multi-scale sampling stack (Sec. 4.4, Fig. 2c) ---------------------
  * L levels of U units; level l has C_l = C1 << l channels and spatial size

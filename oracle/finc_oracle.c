@@ -494,8 +494,8 @@ int orc_stack_inverse(const double *const *z, double *x, const double *K,
     return rc;
 }
 
-/* Backward of one layer, for training on the negative log-likelihood (Sec. 2
- * NLL equation; Sec. 6 training details).  Given x and dy = dL/dy for
+/* Backward of one layer, for training on the negative log-likelihood (Sec. 3
+ * NLL equation; the appendix's training details).  Given x and dy = dL/dy for
  * y = layer(x):
  *   dx = J^T dy: every output gradient dy[co,i,j] is sent back along each tap
  *        to the input pixel that tap read, with the weight the layer used;
@@ -653,13 +653,13 @@ int orc_actnorm_backward(const double *x, const double *dy, const double *s, dou
     return ORC_OK;
 }
 
-/* Negative log-likelihood of each image (Sec. 2, the log-probability
+/* Negative log-likelihood of each image (Sec. 3, the log-probability
  * equation, negated): the flow maps the image to latents whose values z
  * are standard normal, and the layers' log|det| (summed per image in
  * logdet) corrects the density, so
  *   nll[b] = sum over the image's latent values of (z^2 + log 2 pi) / 2
  *            - logdet[b],
- * and bits per dimension (Sec. 6, BPD equation) bpd[b] = nll[b] log2(e) / D
+ * and bits per dimension (Sec. 5, BPD equation) bpd[b] = nll[b] log2(e) / D
  * with D the image's values (the latents' total, n[0] + ... + n[L-1]).
  * z[l] holds B blocks of n[l] values, one per image.  bpd may be NULL. */
 int orc_gauss_nll(const double *const *z, const long *n, int L, long B, const double *logdet,

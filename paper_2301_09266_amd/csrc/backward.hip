@@ -1,5 +1,5 @@
 // backward.hip -- backward of the masked k x k convolution layer on gfx950,
-// for training on the negative log-likelihood (Sec. 2 NLL equation; the
+// for training on the negative log-likelihood (Sec. 3 NLL equation; the
 // appendix's training details reset the masked weights' gradients to zero
 // after every step), behind finc_backward of include/finc.h.
 //
@@ -45,6 +45,7 @@ inline bool overlapb(const void *a, size_t na, const void *b, size_t nb) {
 struct DkArgs {
     const float *x, *dy;
     float *partial;
+    long long img;   // floats from one image to the next (x and dy)
     int B, C, H, W, k, oh, ow, N, cpp, nchunk;
     Div d_HW, d_W, d_kk, d_k;
 };
@@ -57,7 +58,7 @@ __device__ __forceinline__ void dk_tile(const DkArgs &a, int bx, int by, int bz,
     const int tid = threadIdx.x, lane = tid & 63, kq = lane >> 4, li = lane & 15, wave = tid >> 6;
     const int col0 = bx * 64, co0 = by * 16;
     const int HW = a.H * a.W, P = a.B * HW, kk = a.k * a.k;
-    const long long img = (long long)a.C * HW;
+    const long long img = a.img;
     // staging roles: A: thread -> (co 16 x position quad 16); B: thread -> (col, 4 quads)
     const int aco = co0 + (tid >> 4), aq = tid & 15;
     const int bcol = col0 + (tid & 63), bq0 = tid >> 6;
@@ -236,39 +237,15 @@ void launch_fused_r(const ConvArgs &ca, int cfg, int ndx, int gx, const DkArgs &
         launch_fused<R, 1, 1>(ca, ndx, gx, da, dgx, dgy, ndk, st);
 }
 
-}  // namespace
-
-extern "C" {
-
-size_t finc_backward_workspace_bytes(int B, int C, int H, int W, int k) {
-    if (!valid_bwd_shape(B, C, H, W, k))
-        return 0;
-    const int parts = dk_parts(B, C, H, W, k);
-    return up256b((size_t)parts * C * C * k * k * sizeof(float));
-}
-
-int finc_backward(const float *x, const float *dy, const float *K, float *dx, float *dK,
-                  double gld, int B, int C, int H, int W, int k, int corner, void *workspace,
-                  hipStream_t stream) {
-    if (!valid_bwd_shape(B, C, H, W, k) || corner < FINC_TL || corner > FINC_BR ||
-        (B > 0 && (!x || !dy)) || !K || !workspace || ((uintptr_t)workspace & 255u))
-        return FINC_EINVAL;
-    const size_t act = (size_t)B * C * H * W * sizeof(float);
-    const size_t wts = (size_t)C * C * k * k * sizeof(float);
-    const size_t wsb = finc_backward_workspace_bytes(B, C, H, W, k);
-    if (dx && (overlapb(dx, act, x, act) || overlapb(dx, act, dy, act) ||
-               overlapb(dx, act, K, wts) || (dK && overlapb(dx, act, dK, wts)) ||
-               overlapb(dx, act, workspace, wsb)))
-        return FINC_EINVAL;
-    if (dK && (overlapb(dK, wts, x, act) || overlapb(dK, wts, dy, act) ||
-               overlapb(dK, wts, K, wts) || overlapb(dK, wts, workspace, wsb)))
-        return FINC_EINVAL;
-    if (overlapb(workspace, wsb, x, act) || overlapb(workspace, wsb, dy, act) ||
-        overlapb(workspace, wsb, K, wts))
-        return FINC_EINVAL;
+// Both gradients of one layer whose images lie img floats apart in x, dy and
+// dx (C H W for a whole tensor, more for a channel slice of a wider one);
+// partial: dk_parts(B, C, H, W, k) C^2 k^2 floats.  Arguments checked by
+// the caller.
+int launch_layer_backward(const float *x, const float *dy, const float *K, float *dx, float *dK,
+                          double gld, int B, int C, int H, int W, int k, int corner,
+                          long long img, float *partial, hipStream_t stream) {
     const int oh = (corner == FINC_TL || corner == FINC_TR) ? k - 1 : 0;
     const int ow = (corner == FINC_TL || corner == FINC_BL) ? k - 1 : 0;
-    float *partial = (float *)workspace;
     const int n = C * C * k * k;
     const long long Q = (long long)B * H * W;
     // the input gradient: the convolution of dy with K transposed and flipped
@@ -287,7 +264,7 @@ int finc_backward(const float *x, const float *dy, const float *K, float *dx, fl
         ca.K = C * k * k;
         ca.ph = k - 1 - oh;
         ca.pw = k - 1 - ow;
-        ca.xs = ca.ys = (long long)C * H * W;
+        ca.xs = ca.ys = img;
         ca.d_HW = make_div(H * W);
         ca.d_W = make_div(W);
         ca.flip = 1;
@@ -306,6 +283,7 @@ int finc_backward(const float *x, const float *dy, const float *K, float *dx, fl
         da.x = x;
         da.dy = dy;
         da.partial = partial;
+        da.img = img;
         da.B = B;
         da.C = C;
         da.H = H;
@@ -343,6 +321,327 @@ int finc_backward(const float *x, const float *dy, const float *K, float *dx, fl
         return FINC_OK;
     hipLaunchKernelGGL(dk_reduce_kernel, dim3((n + 7) / 8), dim3(256), 0, stream, partial, parts,
                        K, dK, gld, C, k, H, W, oh, ow);
+    return conv_launched();
+}
+
+
+
+// ---- actnorm backward -----------------------------------------------------
+// y = s x + b per channel: dx = s dy; ds[c] = sum dy x + gld H W / s[c];
+// db[c] = sum dy.  Block (c, part) covers images [part bpp, (part+1) bpp) of
+// channel c: it writes dx there and its two sums (fp64, each thread's
+// elements in order, then a fixed tree) to partial[(c parts + part) 2 + .];
+// actnorm_reduce_kernel adds the parts in order.
+constexpr int kAnThreads = 256;
+
+__global__ __launch_bounds__(kAnThreads) void actnorm_bwd_kernel(const float *x, const float *dy,
+                                                                 const float *s, float *dx,
+                                                                 double *partial, int B, int C,
+                                                                 int HW, int bpp, int parts) {
+    __shared__ double red[2][kAnThreads];
+    const int c = blockIdx.x, part = blockIdx.y, tid = threadIdx.x;
+    const int b0 = part * bpp, b1 = min(b0 + bpp, B);
+    const float sc = s[c];
+    double sx = 0.0, sy = 0.0;
+    for (int b = b0; b < b1; ++b) {
+        const long long base = ((long long)b * C + c) * HW;
+        for (int p = tid; p < HW; p += kAnThreads) {
+            const float g = dy[base + p];
+            sx += (double)g * (double)x[base + p];
+            sy += (double)g;
+            if (dx)
+                dx[base + p] = sc * g;
+        }
+    }
+    red[0][tid] = sx;
+    red[1][tid] = sy;
+    __syncthreads();
+    for (int h = kAnThreads / 2; h > 0; h >>= 1) {
+        if (tid < h) {
+            red[0][tid] += red[0][tid + h];
+            red[1][tid] += red[1][tid + h];
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        partial[((long long)c * parts + part) * 2] = red[0][0];
+        partial[((long long)c * parts + part) * 2 + 1] = red[1][0];
+    }
+}
+
+__global__ __launch_bounds__(64) void actnorm_reduce_kernel(const double *partial, int parts,
+                                                            const float *s, float *ds, float *db,
+                                                            double gld, int C, int HW) {
+    const int c = blockIdx.x * 64 + threadIdx.x;
+    if (c >= C)
+        return;
+    double sx = 0.0, sy = 0.0;
+    for (int z = 0; z < parts; ++z) {
+        sx += partial[((long long)c * parts + z) * 2];
+        sy += partial[((long long)c * parts + z) * 2 + 1];
+    }
+    if (ds)
+        ds[c] = (float)(sx + gld * (double)HW / (double)s[c]);
+    if (db)
+        db[c] = (float)sy;
+}
+
+// Parts of the batch per channel: about 512 blocks over the chip, at least
+// 16 K values per block.
+int actnorm_parts(int B, int C, int HW) {
+    long long parts = 512 / C;
+    const long long per = (16384 + HW - 1) / HW;   // images per block at minimum
+    if (parts > (B + per - 1) / per)
+        parts = (B + per - 1) / per;
+    return (int)(parts < 1 ? 1 : parts);
+}
+
+// ---- negative log-likelihood ----------------------------------------------
+// One block per image: each latent's values in a fixed order (thread t takes
+// t, t + 256, ...; fp64), a fixed tree over the threads, the latents in order.
+constexpr int kNllMaxL = 16;
+struct NllArgs {
+    const float *z[kNllMaxL];
+    long long n[kNllMaxL];
+    int L;
+    long long D;
+    const double *logdet;
+    double *nll, *bpd;
+};
+
+__global__ __launch_bounds__(256) void gauss_nll_kernel(NllArgs a) {
+    __shared__ double red[256];
+    const int b = blockIdx.x, tid = threadIdx.x;
+    double total = 0.0;
+    for (int l = 0; l < a.L; ++l) {
+        const float *zb = a.z[l] + (long long)b * a.n[l];
+        double q = 0.0;
+        for (long long e = tid; e < a.n[l]; e += 256) {
+            const double v = zb[e];
+            q += v * v;
+        }
+        red[tid] = q;
+        __syncthreads();
+        for (int h = 128; h > 0; h >>= 1) {
+            if (tid < h)
+                red[tid] += red[tid + h];
+            __syncthreads();
+        }
+        total += red[0];
+        __syncthreads();
+    }
+    if (tid == 0) {
+        const double log2pi = 1.8378770664093454836;   // log(2 pi)
+        const double nll = 0.5 * (total + (double)a.D * log2pi) - a.logdet[b];
+        a.nll[b] = nll;
+        if (a.bpd)
+            a.bpd[b] = nll / ((double)a.D * 0.69314718055994530942);   // / (D log 2)
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t finc_backward_workspace_bytes(int B, int C, int H, int W, int k) {
+    if (!valid_bwd_shape(B, C, H, W, k))
+        return 0;
+    const int parts = dk_parts(B, C, H, W, k);
+    return up256b((size_t)parts * C * C * k * k * sizeof(float));
+}
+
+int finc_backward(const float *x, const float *dy, const float *K, float *dx, float *dK,
+                  double gld, int B, int C, int H, int W, int k, int corner, void *workspace,
+                  hipStream_t stream) {
+    if (!valid_bwd_shape(B, C, H, W, k) || corner < FINC_TL || corner > FINC_BR ||
+        (B > 0 && (!x || !dy)) || !K || !workspace || ((uintptr_t)workspace & 255u))
+        return FINC_EINVAL;
+    const size_t act = (size_t)B * C * H * W * sizeof(float);
+    const size_t wts = (size_t)C * C * k * k * sizeof(float);
+    const size_t wsb = finc_backward_workspace_bytes(B, C, H, W, k);
+    if (dx && (overlapb(dx, act, x, act) || overlapb(dx, act, dy, act) ||
+               overlapb(dx, act, K, wts) || (dK && overlapb(dx, act, dK, wts)) ||
+               overlapb(dx, act, workspace, wsb)))
+        return FINC_EINVAL;
+    if (dK && (overlapb(dK, wts, x, act) || overlapb(dK, wts, dy, act) ||
+               overlapb(dK, wts, K, wts) || overlapb(dK, wts, workspace, wsb)))
+        return FINC_EINVAL;
+    if (overlapb(workspace, wsb, x, act) || overlapb(workspace, wsb, dy, act) ||
+        overlapb(workspace, wsb, K, wts))
+        return FINC_EINVAL;
+    return launch_layer_backward(x, dy, K, dx, dK, gld, B, C, H, W, k, corner,
+                                 (long long)C * H * W, (float *)workspace, stream);
+}
+
+
+// ---- backward of the FInC units ---------------------------------------------
+
+size_t finc_unit_backward_workspace_bytes(int B, int C, int H, int W, int k) {
+    if (!valid_bwd_shape(B, C, H, W, k))
+        return 0;
+    return 4 * up256b((size_t)B * C * H * W * sizeof(float)) +
+           finc_backward_workspace_bytes(B, C, H, W, k);
+}
+
+int finc_unit_backward(const float *x, const float *dy, const float *K4, float *dx, float *dK4,
+                       double gld, int B, int C, int H, int W, int k, void *workspace,
+                       hipStream_t stream) {
+    if (!valid_bwd_shape(B, C, H, W, k) || (B > 0 && (!x || !dy)) || !K4 || !workspace ||
+        ((uintptr_t)workspace & 255u))
+        return FINC_EINVAL;
+    const size_t act = (size_t)B * C * H * W * sizeof(float);
+    const size_t wts = 4 * (size_t)C * C * k * k * sizeof(float);
+    const size_t wsb = finc_unit_backward_workspace_bytes(B, C, H, W, k);
+    const void *ins[3] = {x, dy, K4};
+    const size_t insz[3] = {act, act, wts};
+    for (int i = 0; i < 3; ++i)
+        if (overlapb(workspace, wsb, ins[i], insz[i]) || (dx && overlapb(dx, act, ins[i], insz[i])) ||
+            (dK4 && overlapb(dK4, wts, ins[i], insz[i])))
+            return FINC_EINVAL;
+    if ((dx && (overlapb(dx, act, workspace, wsb) || (dK4 && overlapb(dx, act, dK4, wts)))) ||
+        (dK4 && overlapb(dK4, wts, workspace, wsb)))
+        return FINC_EINVAL;
+    const size_t ksz = (size_t)C * C * k * k;
+    char *w = (char *)workspace;
+    const size_t slot = up256b(act);
+    float *h[4] = {(float *)x, (float *)w, (float *)(w + slot), (float *)(w + 2 * slot)};
+    float *g = (float *)(w + 3 * slot);
+    float *partial = (float *)(w + 4 * slot);
+    // the inputs of blocks TR, BL, BR, recomputed: h[q + 1] = block q (h[q])
+    for (int q = 0; q < 3 && B > 0; ++q) {
+        const int rc = finc_forward(h[q], h[q + 1], K4 + q * ksz, nullptr, nullptr, B, C, H, W,
+                                    k, q, stream);
+        if (rc != FINC_OK)
+            return rc;
+    }
+    // blocks in reverse; the gradient alternates between g and the freed slots
+    const float *gin = dy;
+    float *gout[4] = {dx, g, h[3], g};   // block q writes its input gradient to gout[q]
+    for (int q = 3; q >= 0; --q) {
+        const int rc = launch_layer_backward(h[q], gin, K4 + q * ksz, gout[q],
+                                             dK4 ? dK4 + q * ksz : nullptr, gld, B, C, H, W, k,
+                                             q, (long long)C * H * W, partial, stream);
+        if (rc != FINC_OK)
+            return rc;
+        gin = gout[q];
+    }
+    return FINC_OK;
+}
+
+size_t finc_split_backward_workspace_bytes(int B, int C, int H, int W, int k) {
+    if (C % 4 != 0 || !valid_bwd_shape(B, C / 4, H, W, k))
+        return 0;
+    return finc_backward_workspace_bytes(B, C / 4, H, W, k);
+}
+
+int finc_split_backward(const float *x, const float *dy, const float *Kq4, float *dx,
+                        float *dKq4, double gld, int B, int C, int H, int W, int k,
+                        void *workspace, hipStream_t stream) {
+    if (C % 4 != 0 || !valid_bwd_shape(B, C / 4, H, W, k) || (B > 0 && (!x || !dy)) || !Kq4 ||
+        !workspace || ((uintptr_t)workspace & 255u))
+        return FINC_EINVAL;
+    const int q = C / 4;
+    const size_t act = (size_t)B * C * H * W * sizeof(float);
+    const size_t wts = 4 * (size_t)q * q * k * k * sizeof(float);
+    const size_t wsb = finc_split_backward_workspace_bytes(B, C, H, W, k);
+    const void *ins[3] = {x, dy, Kq4};
+    const size_t insz[3] = {act, act, wts};
+    for (int i = 0; i < 3; ++i)
+        if (overlapb(workspace, wsb, ins[i], insz[i]) || (dx && overlapb(dx, act, ins[i], insz[i])) ||
+            (dKq4 && overlapb(dKq4, wts, ins[i], insz[i])))
+            return FINC_EINVAL;
+    if ((dx && (overlapb(dx, act, workspace, wsb) || (dKq4 && overlapb(dx, act, dKq4, wts)))) ||
+        (dKq4 && overlapb(dKq4, wts, workspace, wsb)))
+        return FINC_EINVAL;
+    const long long img = (long long)C * H * W, plane = (long long)q * H * W;
+    const size_t ksz = (size_t)q * q * k * k;
+    for (int g = 0; g < 4; ++g) {   // quarter g: corner g on channels [g q, (g+1) q)
+        const int rc = launch_layer_backward(
+            B > 0 ? x + g * plane : x, B > 0 ? dy + g * plane : dy, Kq4 + g * ksz,
+            dx && B > 0 ? dx + g * plane : nullptr, dKq4 ? dKq4 + g * ksz : nullptr, gld, B, q,
+            H, W, k, g, img, (float *)workspace, stream);
+        if (rc != FINC_OK)
+            return rc;
+    }
+    return FINC_OK;
+}
+
+// ---- actnorm backward and the negative log-likelihood -----------------------
+
+size_t finc_actnorm_backward_workspace_bytes(int B, int C, int H, int W) {
+    if (B < 0 || C < 1 || H < 1 || W < 1 || (long long)B * C * H * W >= (1ll << 31))
+        return 0;
+    return up256b((size_t)2 * C * actnorm_parts(B, C, H * W) * sizeof(double));
+}
+
+int finc_actnorm_backward(const float *x, const float *dy, const float *s, float *dx, float *ds,
+                          float *db, double gld, int B, int C, int H, int W, void *workspace,
+                          hipStream_t stream) {
+    const size_t wsb = finc_actnorm_backward_workspace_bytes(B, C, H, W);
+    if (wsb == 0 || (B > 0 && (!x || !dy)) || !s || !workspace || ((uintptr_t)workspace & 255u))
+        return FINC_EINVAL;
+    const size_t act = (size_t)B * C * H * W * sizeof(float), vec = (size_t)C * sizeof(float);
+    const void *ins[3] = {x, dy, s};
+    const size_t insz[3] = {act, act, vec};
+    void *outs[4] = {dx, ds, db, workspace};
+    const size_t outsz[4] = {act, vec, vec, wsb};
+    for (int o = 0; o < 4; ++o) {
+        if (!outs[o])
+            continue;
+        for (int i = 0; i < 3; ++i)
+            if (overlapb(outs[o], outsz[o], ins[i], insz[i]))
+                return FINC_EINVAL;
+        for (int o2 = o + 1; o2 < 4; ++o2)
+            if (outs[o2] && overlapb(outs[o], outsz[o], outs[o2], outsz[o2]))
+                return FINC_EINVAL;
+    }
+    const int HW = H * W, parts = actnorm_parts(B, C, HW);
+    const int bpp = B > 0 ? cdiv(B, parts) : 0;
+    double *partial = (double *)workspace;
+    const int np = B > 0 ? cdiv(B, bpp) : 0;   // parts that hold images
+    if (np > 0) {
+        hipLaunchKernelGGL(actnorm_bwd_kernel, dim3(C, np), dim3(kAnThreads), 0, stream, x, dy, s,
+                           dx, partial, B, C, HW, bpp, np);
+        const int rc = conv_launched();
+        if (rc != FINC_OK)
+            return rc;
+    }
+    if (!ds && !db)
+        return FINC_OK;
+    hipLaunchKernelGGL(actnorm_reduce_kernel, dim3((C + 63) / 64), dim3(64), 0, stream, partial,
+                       np, s, ds, db, gld, C, HW);
+    return conv_launched();
+}
+
+int finc_gauss_nll(const float *const *z, const long long *n, int L, int B, const double *logdet,
+                   double *nll, double *bpd, hipStream_t stream) {
+    if (L < 1 || L > kNllMaxL || B < 0 || !z || !n || !logdet || !nll)
+        return FINC_EINVAL;
+    NllArgs a;
+    memset(&a, 0, sizeof(a));
+    a.L = L;
+    for (int l = 0; l < L; ++l) {
+        if (n[l] < 1 || (B > 0 && !z[l]))
+            return FINC_EINVAL;
+        a.z[l] = z[l];
+        a.n[l] = n[l];
+        a.D += n[l];
+    }
+    const size_t per = (size_t)B * sizeof(double);
+    if (overlapb(nll, per, logdet, per) || (bpd && (overlapb(bpd, per, logdet, per) ||
+                                                    overlapb(bpd, per, nll, per))))
+        return FINC_EINVAL;
+    for (int l = 0; l < L; ++l) {
+        const size_t zb = (size_t)B * n[l] * sizeof(float);
+        if (overlapb(nll, per, z[l], zb) || (bpd && overlapb(bpd, per, z[l], zb)))
+            return FINC_EINVAL;
+    }
+    a.logdet = logdet;
+    a.nll = nll;
+    a.bpd = bpd;
+    if (B == 0)
+        return FINC_OK;
+    hipLaunchKernelGGL(gauss_nll_kernel, dim3(B), dim3(256), 0, stream, a);
     return conv_launched();
 }
 

@@ -8,6 +8,7 @@ fails, FincError is raised.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 
 import torch
@@ -38,6 +39,17 @@ SIGNATURES = {
     "finc_backward_workspace_bytes": (_sz, [_i, _i, _i, _i, _i]),
     "finc_backward": (_i, [_vp, _vp, _vp, _vp, _vp, ctypes.c_double, _i, _i, _i, _i, _i, _i,
                            _vp, _vp]),
+    "finc_unit_backward_workspace_bytes": (_sz, [_i, _i, _i, _i, _i]),
+    "finc_unit_backward": (_i, [_vp, _vp, _vp, _vp, _vp, ctypes.c_double, _i, _i, _i, _i, _i,
+                                _vp, _vp]),
+    "finc_split_backward_workspace_bytes": (_sz, [_i, _i, _i, _i, _i]),
+    "finc_split_backward": (_i, [_vp, _vp, _vp, _vp, _vp, ctypes.c_double, _i, _i, _i, _i, _i,
+                                 _vp, _vp]),
+    "finc_actnorm_backward_workspace_bytes": (_sz, [_i, _i, _i, _i]),
+    "finc_actnorm_backward": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_double, _i, _i, _i,
+                                   _i, _vp, _vp]),
+    "finc_gauss_nll": (_i, [ctypes.POINTER(_vp), ctypes.POINTER(ctypes.c_longlong), _i, _i, _vp,
+                            _vp, _vp, _vp]),
     "finc_unit_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "finc_unit_logdet": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
@@ -284,8 +296,8 @@ def backward(x: torch.Tensor, dy: torch.Tensor, K: torch.Tensor, corner: int,
     _dev(x, "x")
     B, C, H, W = x.shape
     _dev(dy, "dy", x.shape)
-    _dev(K, "K")
     k = K.shape[-1]
+    _dev(K, "K", (C, C, k, k))
     if want_dx:
         dx = torch.empty_like(x) if dx is None else _dev(dx, "dx", x.shape)
     else:
@@ -298,6 +310,81 @@ def backward(x: torch.Tensor, dy: torch.Tensor, K: torch.Tensor, corner: int,
     _check(L.finc_backward(_ptr(x), _ptr(dy), _ptr(K), _ptr(dx), _ptr(dK), float(gld), B, C, H,
                            W, k, corner, _ptr(ws), _stream()), "finc_backward")
     return dx, dK
+
+
+def _unit_grads(fn, wsfn, x, dy, Kw, wshape, gld, want_dx, want_dK, dx, dKw, workspace):
+    L = _require_lib()
+    _dev(x, "x")
+    B, C, H, W = x.shape
+    _dev(dy, "dy", x.shape)
+    k = Kw.shape[-1]
+    _dev(Kw, "K", wshape(C, k))
+    dx = (torch.empty_like(x) if dx is None else _dev(dx, "dx", x.shape)) if want_dx else None
+    dKw = ((torch.empty_like(Kw) if dKw is None else _dev(dKw, "dK", Kw.shape))
+           if want_dK else None)
+    nbytes = int(getattr(L, wsfn)(B, C, H, W, k))
+    if nbytes == 0:
+        raise FincError(EINVAL, fn)
+    ws = _workspace(nbytes, x.device, workspace)
+    _check(getattr(L, fn)(_ptr(x), _ptr(dy), _ptr(Kw), _ptr(dx), _ptr(dKw), float(gld), B, C, H,
+                          W, k, _ptr(ws), _stream()), fn)
+    return dx, dKw
+
+
+def unit_backward(x, dy, K4, gld: float = 0.0, want_dx: bool = True, want_dK: bool = True,
+                  dx=None, dK4=None, workspace=None):
+    """(dx, dK4) of the sequential unit (see finc_unit_backward); K4 is
+    (4, C, C, k, k)."""
+    return _unit_grads("finc_unit_backward", "finc_unit_backward_workspace_bytes", x, dy, K4,
+                       lambda C, k: (4, C, C, k, k), gld, want_dx, want_dK, dx, dK4, workspace)
+
+
+def split_backward(x, dy, Kq4, gld: float = 0.0, want_dx: bool = True, want_dK: bool = True,
+                   dx=None, dKq4=None, workspace=None):
+    """(dx, dKq4) of the channel-split unit (see finc_split_backward); Kq4 is
+    (4, C/4, C/4, k, k)."""
+    return _unit_grads("finc_split_backward", "finc_split_backward_workspace_bytes", x, dy,
+                       Kq4, lambda C, k: (4, C // 4, C // 4, k, k), gld, want_dx, want_dK, dx,
+                       dKq4, workspace)
+
+
+def actnorm_backward(x, dy, s, gld: float = 0.0, workspace=None):
+    """(dx, ds, db) of actnorm y = s x + b (see finc_actnorm_backward)."""
+    L = _require_lib()
+    _dev(x, "x")
+    B, C, H, W = x.shape
+    _dev(dy, "dy", x.shape)
+    _dev(s, "s", (C,))
+    dx, ds, db = torch.empty_like(x), torch.empty_like(s), torch.empty_like(s)
+    nbytes = int(L.finc_actnorm_backward_workspace_bytes(B, C, H, W))
+    if nbytes == 0:
+        raise FincError(EINVAL, "finc_actnorm_backward")
+    ws = _workspace(nbytes, x.device, workspace)
+    _check(L.finc_actnorm_backward(_ptr(x), _ptr(dy), _ptr(s), _ptr(dx), _ptr(ds), _ptr(db),
+                                   float(gld), B, C, H, W, _ptr(ws), _stream()),
+           "finc_actnorm_backward")
+    return dx, ds, db
+
+
+def gauss_nll(zs, logdet):
+    """(nll, bpd) per image (device float64, B each) for latents zs (float32
+    tensors with the batch first) and per-image log|det| (float64, B); see
+    finc_gauss_nll."""
+    L = _require_lib()
+    if not logdet.is_cuda or logdet.dtype != torch.float64 or logdet.dim() != 1:
+        raise ValueError("logdet must be a 1-d float64 device tensor")
+    B = logdet.shape[0]
+    for z in zs:
+        _dev(z, "z")
+        if z.shape[0] != B:
+            raise ValueError(f"latent has batch {z.shape[0]}, expected {B}")
+    n = (ctypes.c_longlong * len(zs))(*[math.prod(z.shape[1:]) for z in zs])
+    ptrs = (_vp * len(zs))(*[z.data_ptr() for z in zs])
+    nll = torch.empty(B, dtype=torch.float64, device=logdet.device)
+    bpd = torch.empty_like(nll)
+    _check(L.finc_gauss_nll(ptrs, n, len(zs), B, _ptr(logdet), _ptr(nll), _ptr(bpd), _stream()),
+           "finc_gauss_nll")
+    return nll, bpd
 
 
 def unit_forward(x: torch.Tensor, K4: torch.Tensor, out: torch.Tensor | None = None,

@@ -118,6 +118,54 @@ def test_backward_workspace_rules():
     assert lib.finc_backward_workspace_bytes(B, 65, H, W, k) == 0
 
 
+def test_unit_split_backward_rejects():
+    lib = finc.lib()
+    ws = ctypes.c_void_p(0x40000000)
+    B, C, H, W, k = SHAPE
+    args = (FAKE, FAKE2, FAKE3, FAKE4, NULL, 0.0)
+    assert lib.finc_unit_backward(*args, B, C, H, W, k, NULL, None) == finc.EINVAL    # no ws
+    assert lib.finc_unit_backward(*args, B, C, H, W, k, ctypes.c_void_p(0x40000010),
+                                  None) == finc.EINVAL                                # misaligned
+    assert lib.finc_unit_backward(FAKE, FAKE2, FAKE3, ctypes.c_void_p(0x100000 + 64), NULL, 0.0,
+                                  B, C, H, W, k, ws, None) == finc.EINVAL            # dx over x
+    assert lib.finc_unit_backward(*args, B, 65, H, W, k, ws, None) == finc.EINVAL
+    assert lib.finc_unit_backward(NULL, FAKE2, FAKE3, FAKE4, NULL, 0.0, B, C, H, W, k, ws,
+                                  None) == finc.EINVAL                                # no x
+    assert lib.finc_split_backward(*args, B, 6, H, W, k, ws, None) == finc.EINVAL     # C % 4
+    assert lib.finc_split_backward(*args, B, 8, H, W, 8, ws, None) == finc.EINVAL     # k > 7
+    assert lib.finc_split_backward_workspace_bytes(B, 6, H, W, k) == 0
+    assert lib.finc_split_backward_workspace_bytes(B, 8, H, W, k) >= 4 * 4 * k * k
+    n = lib.finc_unit_backward_workspace_bytes(B, C, H, W, k)
+    assert n >= 4 * B * C * H * W * 4 and n % 256 == 0
+
+
+def test_actnorm_backward_and_nll_reject():
+    lib = finc.lib()
+    ws = ctypes.c_void_p(0x40000000)
+    B, C, H, W = 2, 3, 4, 5
+    S = ctypes.c_void_p(0x2000000)
+    assert lib.finc_actnorm_backward(FAKE, FAKE2, S, FAKE4, NULL, NULL, 0.0, B, C, H, W, NULL,
+                                     None) == finc.EINVAL                            # no ws
+    assert lib.finc_actnorm_backward(FAKE, FAKE2, S, ctypes.c_void_p(0x100000 + 8), NULL, NULL,
+                                     0.0, B, C, H, W, ws, None) == finc.EINVAL       # dx over x
+    assert lib.finc_actnorm_backward(FAKE, FAKE2, S, NULL, S, NULL, 0.0, B, C, H, W, ws,
+                                     None) == finc.EINVAL                            # ds over s
+    assert lib.finc_actnorm_backward(FAKE, FAKE2, S, NULL, FAKE4, FAKE4, 0.0, B, C, H, W, ws,
+                                     None) == finc.EINVAL                            # ds over db
+    assert lib.finc_actnorm_backward_workspace_bytes(B, 0, H, W) == 0
+    z = (ctypes.c_void_p * 2)(0x100000, 0x900000)
+    n = (ctypes.c_longlong * 2)(16, 8)
+    LD, OUT = ctypes.c_void_p(0x3000000), ctypes.c_void_p(0x3100000)
+    assert lib.finc_gauss_nll(z, n, 0, B, LD, OUT, NULL, None) == finc.EINVAL        # L = 0
+    assert lib.finc_gauss_nll(z, n, 17, B, LD, OUT, NULL, None) == finc.EINVAL       # L > 16
+    assert lib.finc_gauss_nll(z, n, 2, B, LD, LD, NULL, None) == finc.EINVAL         # nll over logdet
+    assert lib.finc_gauss_nll(z, n, 2, B, LD, OUT, OUT, None) == finc.EINVAL         # bpd over nll
+    assert lib.finc_gauss_nll(z, n, 2, B, LD, ctypes.c_void_p(0x100000), NULL,
+                              None) == finc.EINVAL                                   # nll over z
+    n0 = (ctypes.c_longlong * 2)(16, 0)
+    assert lib.finc_gauss_nll(z, n0, 2, B, LD, OUT, NULL, None) == finc.EINVAL       # empty latent
+
+
 def test_inverse_rejects():
     lib = finc.lib()
     ws = ctypes.c_void_p(0x4000000)

@@ -1,0 +1,161 @@
+"""Training-side gradients on the GPU against the oracle, through the C ABI:
+the backward of the sequential and channel-split FInC units (chain rule over
+their blocks), actnorm's backward, and the per-image negative log-likelihood
+and bits per dimension (Sec. 3 NLL equation, Sec. 5 BPD equation).
+
+Bar: 1e-4 * max(1, |oracle|) elementwise (gpu_util.assert_close); a weight
+gradient that sums many pixels is held to the root sum of squares of its
+terms where that is larger (fp32 rounding scales with the terms, not with a
+sum that cancels).  Every result is also bitwise the same on a second run.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2301_09266_amd import finc, synth
+
+pytestmark = pytest.mark.gpu
+
+from gpu_util import assert_close, dev, f64, host, poisoned  # noqa: E402
+
+
+@pytest.fixture(scope="module")
+def orc():
+    return oracle.default()
+
+
+def unit_kernels(C, k, seed):
+    """Four blocks TL, TR, BL, BR with junk in their masked slots."""
+    return np.stack([synth.garbage_in_mask(synth.masked_kernel(C, k, q, seed + q), q,
+                                           seed=seed + 10 + q) for q in range(4)])
+
+
+def term_scale_unit(orc, x, dy, K4):
+    """Per weight-gradient entry of each block, the root sum of squares of
+    the products it adds: the oracle's dK of the squared block input and
+    squared incoming gradient (the block inputs and gradients themselves from
+    the oracle's forward and per-block backward)."""
+    hs = [x]
+    for q in range(3):
+        hs.append(orc.forward(hs[-1], K4[q], q))
+    g, out = dy, [None] * 4
+    for q in range(3, -1, -1):
+        _, sq = orc.backward(hs[q] ** 2, g ** 2, K4[q], q, 0.0)
+        out[q] = np.sqrt(sq)
+        g, _ = orc.backward(hs[q], g, K4[q], q, 0.0)
+    return np.stack(out)
+
+
+UNIT_SHAPES = [(2, 3, 5, 7, 3), (3, 12, 16, 16, 3), (1, 5, 9, 6, 2), (2, 4, 6, 6, 1),
+               (1, 7, 6, 5, 5), (2, 20, 8, 9, 3)]
+
+
+@pytest.mark.parametrize("shape", UNIT_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_unit_backward(orc, shape):
+    B, C, H, W, k = shape
+    rng = np.random.default_rng(B * 1000 + C)
+    x, dy = rng.normal(size=(B, C, H, W)), rng.normal(size=(B, C, H, W))
+    K4 = unit_kernels(C, k, 300 + C)
+    gld = -0.5
+    dx, dK4 = finc.unit_backward(dev(x), dev(dy), dev(K4), gld, dx=poisoned(x.shape),
+                                 dK4=poisoned(K4.shape))
+    want_dx, want_dK4 = orc.unit_backward(f64(x), f64(dy), f64(K4), gld)
+    assert_close(host(dx), want_dx, f"unit backward dx {shape}")
+    assert_close(host(dK4), want_dK4, f"unit backward dK {shape}",
+                 scale=term_scale_unit(orc, f64(x), f64(dy), f64(K4)))
+    dx2, dK42 = finc.unit_backward(dev(x), dev(dy), dev(K4), gld)
+    assert torch.equal(dx, dx2) and torch.equal(dK4, dK42)
+
+
+def test_unit_backward_workload(orc):
+    """The unit workload's shape (256 images of 12 x 16 x 16, k = 3): dK4
+    sums 65,536 pixels per tap; dx on three sampled images; dx alone and dK
+    alone give the same bits."""
+    c = synth.unit_case(256, 12, 16, 16, 3)
+    x, K4 = c["x"], c["K4"]
+    dy = np.random.default_rng(8).normal(size=x.shape)
+    print("unit backward 256 x 12 x 16 x 16", flush=True)
+    dx, dK4 = finc.unit_backward(dev(x), dev(dy), dev(K4), -1.0)
+    want_dx, want_dK4 = orc.unit_backward(f64(x), f64(dy), f64(K4), -1.0)
+    assert_close(host(dK4), want_dK4, "unit backward dK, 256 images",
+                 scale=term_scale_unit(orc, f64(x), f64(dy), f64(K4)))
+    pick = [0, 100, 255]
+    assert_close(host(dx)[pick], want_dx[pick], "unit backward dx, 256 images")
+    only_dk = finc.unit_backward(dev(x), dev(dy), dev(K4), -1.0, want_dx=False)
+    assert only_dk[0] is None and torch.equal(only_dk[1], dK4)
+    only_dx = finc.unit_backward(dev(x), dev(dy), dev(K4), -1.0, want_dK=False)
+    assert only_dx[1] is None and torch.equal(only_dx[0], dx)
+
+
+SPLIT_SHAPES = [(2, 8, 5, 7, 3), (3, 48, 8, 8, 3), (1, 4, 9, 6, 5), (2, 16, 16, 16, 2),
+                (2, 12, 7, 4, 7), (1, 64, 6, 6, 3)]
+
+
+@pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_split_backward(orc, shape):
+    B, C, H, W, k = shape
+    q = C // 4
+    rng = np.random.default_rng(B * 100 + C + k)
+    x, dy = rng.normal(size=(B, C, H, W)), rng.normal(size=(B, C, H, W))
+    Kq4 = np.stack([synth.garbage_in_mask(synth.masked_kernel(q, k, g, 500 + g), g, seed=g + 3)
+                    for g in range(4)])
+    gld = 0.8
+    dx, dKq4 = finc.split_backward(dev(x), dev(dy), dev(Kq4), gld, dx=poisoned(x.shape),
+                                   dKq4=poisoned(Kq4.shape))
+    want_dx, want_dKq4 = orc.split_backward(f64(x), f64(dy), f64(Kq4), gld)
+    assert_close(host(dx), want_dx, f"split backward dx {shape}")
+    _, sq = orc.split_backward(f64(x) ** 2, f64(dy) ** 2, f64(Kq4), 0.0)
+    assert_close(host(dKq4), want_dKq4, f"split backward dK {shape}", scale=np.sqrt(sq))
+    dx2, dKq42 = finc.split_backward(dev(x), dev(dy), dev(Kq4), gld)
+    assert torch.equal(dx, dx2) and torch.equal(dKq4, dKq42)
+
+
+def test_unit_backward_empty_batch(orc):
+    """No images: dx empty, each block's dK only its log|det| term."""
+    C, H, W, k = 5, 6, 7, 3
+    K4 = unit_kernels(C, k, 90)
+    x = np.zeros((0, C, H, W))
+    _, dK4 = finc.unit_backward(dev(x), dev(x), dev(K4), -1.0, dK4=poisoned(K4.shape))
+    assert_close(host(dK4), orc.unit_backward(f64(x), f64(x), f64(K4), -1.0)[1],
+                 "unit backward dK, no images")
+    Kq4 = np.stack([synth.masked_kernel(2, k, g, 60 + g) for g in range(4)])
+    x8 = np.zeros((0, 8, H, W))
+    _, dKq4 = finc.split_backward(dev(x8), dev(x8), dev(Kq4), -1.0, dKq4=poisoned(Kq4.shape))
+    assert_close(host(dKq4), orc.split_backward(f64(x8), f64(x8), f64(Kq4), -1.0)[1],
+                 "split backward dK, no images")
+
+
+@pytest.mark.parametrize("shape", [(3, 5, 4, 6), (64, 12, 16, 16), (1, 96, 3, 5), (0, 4, 4, 4),
+                                   (300, 3, 8, 8)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_actnorm_backward(orc, shape):
+    B, C, H, W = shape
+    rng = np.random.default_rng(C + H)
+    x, dy = rng.normal(size=shape), rng.normal(size=shape)
+    s = rng.uniform(0.5, 1.5, size=C) * rng.choice([-1.0, 1.0], size=C)
+    gld = -0.25
+    dx, ds, db = finc.actnorm_backward(dev(x), dev(dy), dev(s), gld)
+    want = orc.actnorm_backward(f64(x), f64(dy), f64(s), gld)
+    assert_close(host(dx), want[0], f"actnorm dx {shape}")
+    assert_close(host(ds), want[1], f"actnorm ds {shape}")
+    assert_close(host(db), want[2], f"actnorm db {shape}")
+    again = finc.actnorm_backward(dev(x), dev(dy), dev(s), gld)
+    assert all(torch.equal(a, b) for a, b in zip((dx, ds, db), again))
+
+
+@pytest.mark.parametrize("B", [1, 3, 100])
+def test_gauss_nll(orc, B):
+    """Three latents of the CIFAR-10 flow's shapes ([28, 28, 28] with L = 3
+    on 3 x 32 x 32 images: 6 x 16 x 16, 12 x 8 x 8, 48 x 4 x 4); fp64 sums
+    of the fp32 latents on both sides, so the bar is 1e-12 relative."""
+    rng = np.random.default_rng(B)
+    zs = [rng.normal(size=(B, 6, 16, 16)), rng.normal(size=(B, 12, 8, 8)),
+          rng.normal(size=(B, 48, 4, 4)) * 1.5]
+    logdet = rng.normal(size=B) * 100.0
+    nll, bpd = finc.gauss_nll([dev(z) for z in zs],
+                              torch.tensor(logdet, dtype=torch.float64, device="cuda:0"))
+    want_nll, want_bpd = orc.gauss_nll([f64(z) for z in zs], logdet)
+    g_nll, g_bpd = nll.cpu().numpy(), bpd.cpu().numpy()
+    assert np.max(np.abs(g_nll - want_nll) / np.abs(want_nll)) < 1e-12
+    assert np.max(np.abs(g_bpd - want_bpd) / np.abs(want_bpd)) < 1e-12

@@ -96,6 +96,21 @@ enum { FINC_PLAN_LAYER = 0, FINC_PLAN_UNIT = 1, FINC_PLAN_SPLIT = 2, FINC_PLAN_S
 int finc_inverse_plan(int kind, int L, int U, int C, int H, int W, int k, int *info,
                       int max_launches);
 
+/* Diagnostic of Theorem 2's step count: the inverse of finc_inverse_prepared
+ * (kind FINC_PLAN_LAYER, one layer with corner `corner`) or of
+ * finc_split_inverse_prepared (kind FINC_PLAN_SPLIT, corner ignored), which
+ * also writes, for every wave w of the launch's workgroup b (b = image, or
+ * 4 * image + quarter for the channel-split unit), steps[b * waves + w] = the
+ * number of diagonal steps that wave ran, each ended by the workgroup's step
+ * barrier (waves = the plan's threads / 64).  Every wave of every
+ * workgroup runs H + W - 1 of them.  steps: device ints, at least that many
+ * (max_steps; FINC_EINVAL if fewer), not overlapping x, y or prepared.
+ * Returns the number of ints written, or an error as the inverse call would.
+ * For tests and tools; the product calls do not count. */
+int finc_inverse_steps(int kind, const float *y, float *x, const void *prepared, int B,
+                       int C, int H, int W, int k, int corner, int *steps, int max_steps,
+                       hipStream_t stream);
+
 /* The forward's work split (host arithmetic only): an image is cut into
  * blocks of rows, each staged in LDS with its halo rows and the layer's
  * weights; a unit keeps whole images, or bands of rows when the batch is

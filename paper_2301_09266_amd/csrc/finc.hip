@@ -553,6 +553,10 @@ struct InvArgs {
     const float *hin;
     int hin_stride;
     Level lv[kMaxLevels]; // in the order they run
+    // steps (diagnostic, single-level calls only; null otherwise): lane 0 of
+    // wave w of workgroup b writes steps[b * waves + w] = the number of
+    // diagonal steps (each ended by the step barrier) that wave ran
+    int *steps;
 };
 static_assert(sizeof(InvArgs) <= 4096, "kernel arguments are limited to 4 KB");
 
@@ -961,7 +965,9 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
     };
     // end of diagonal step e: the barrier; in the stream form, at the end of
     // a phase, the exchange with HBM and one more barrier
+    int nsteps = 0;   // diagonal steps this wave ran (the steps diagnostic)
     auto step_end = [&](int e) __attribute__((always_inline)) {
+        ++nsteps;
         __syncthreads();
         if constexpr (kStr) {
             const bool pend = (e & (kPhase - 1)) == kPhase - 1;
@@ -1314,6 +1320,8 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                 step_end(e);
         }
     }
+    if (a.steps && (threadIdx.x & 63) == 0)
+        a.steps[b * (blockDim.x >> 6) + (threadIdx.x >> 6)] = nsteps;
 }
 
 // A wave of a multi-level chain runs the level loop compiled for its own
@@ -2051,6 +2059,7 @@ int launch_streamed(const InvArgs &a, const InvChoice &ch, int B, hipStream_t st
         s.lv[0].z = n == 0 ? l0.z : a.out;
         s.lv[0].prep = l0.prep + (size_t)(u * a.lpu + q) * p.lstride;
         s.lv[0].pl = p;
+        s.steps = a.steps;   // (set for single layers only)
         void *args[] = {&s};
         (void)hipLaunchKernel(k, dim3(B), dim3(threads), args, lds, stream);
         rc = launched();
@@ -2579,6 +2588,46 @@ int finc_split_inverse_prepared(const float *y, float *x, const void *prepared4,
     a.corner0 = FINC_TL;
     a.split = 1;
     return launch_inverse_chain(a, 4 * B, stream);
+}
+
+int finc_inverse_steps(int kind, const float *y, float *x, const void *prepared, int B, int C,
+                       int H, int W, int k, int corner, int *steps, int max_steps,
+                       hipStream_t stream) {
+    if ((kind != FINC_PLAN_LAYER && kind != FINC_PLAN_SPLIT) || !steps || max_steps < 0 ||
+        !valid_corner(corner))
+        return FINC_EINVAL;
+    const bool split = kind == FINC_PLAN_SPLIT;
+    if (split ? !valid_split(B, C, H, W, k) : !valid_shape(B, C, H, W, k))
+        return FINC_EINVAL;
+    if (!x || !y || !prepared || !aligned256(prepared))
+        return FINC_EINVAL;
+    const int Cl = split ? C / 4 : C;
+    const size_t bytes = (size_t)B * C * H * W * sizeof(float);
+    const size_t pb = finc_workspace_bytes(Cl, k, split ? 4 : 1);
+    int info[6];
+    const int n = finc_inverse_plan(kind, 1, 1, C, H, W, k, info, 1);
+    if (n < 0)
+        return n;
+    const long long count = (long long)(split ? 4 * B : B) * (info[0] / 64);
+    if (count > max_steps)
+        return FINC_EINVAL;
+    if (!inverse_alias_ok(y, x, bytes) || overlap(x, bytes, prepared, pb) ||
+        overlap(steps, (size_t)count * sizeof(int), x, bytes) ||
+        overlap(steps, (size_t)count * sizeof(int), y, bytes) ||
+        overlap(steps, (size_t)count * sizeof(int), prepared, pb))
+        return FINC_EINVAL;
+    InvArgs a;
+    memset(&a, 0, sizeof(a));
+    a.lv[0] = level(y, prepared, nullptr, nullptr, Cl, H, W, k);
+    a.out = x;
+    a.L = 1;
+    a.n_units = 1;
+    a.lpu = 1;
+    a.corner0 = split ? FINC_TL : corner;
+    a.split = split ? 1 : 0;
+    a.steps = steps;
+    const int rc = launch_inverse_chain(a, split ? 4 * B : B, stream);
+    return rc == FINC_OK ? (int)count : rc;
 }
 
 int finc_split_inverse(const float *y, float *x, const float *Kq4, int B, int C, int H, int W,

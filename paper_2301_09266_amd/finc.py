@@ -29,6 +29,7 @@ SIGNATURES = {
     "finc_strerror": (ctypes.c_char_p, [_i]),
     "finc_inverse_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i), _i]),
     "finc_forward_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i)]),
+    "finc_inverse_steps": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp]),
     "finc_workspace_bytes": (_sz, [_i, _i, _i]),
     "finc_prepare": (_i, [_vp, _i, ctypes.POINTER(_i), _i, _i, _vp, _vp]),
     "finc_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
@@ -284,6 +285,32 @@ def inverse_prepared(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: in
     _check(L.finc_inverse_prepared(_ptr(y), _ptr(x), _ptr(prepared), B, C, H, W, k, corner,
                                    _stream()), "finc_inverse_prepared")
     return x
+
+
+def inverse_steps(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: int = TL,
+                  split: bool = False):
+    """(x, steps): the inverse of a prepared layer (or, split=True, of a
+    prepared channel-split unit) and the number of diagonal steps every wave
+    of every workgroup ran, as (workgroups, waves) int32 (see
+    finc_inverse_steps)."""
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    kind = PLAN_SPLIT if split else PLAN_LAYER
+    _bytes_buf(prepared, workspace_bytes(C // 4 if split else C, k, 4 if split else 1),
+               "prepared")
+    info = inverse_plan(kind, C, H, W, k)
+    if isinstance(info, int):
+        _check(info, "finc_inverse_steps")
+    waves = info[0]["threads"] // 64
+    nwg = (4 * B if split else B)
+    steps = torch.full((nwg, waves), -1, dtype=torch.int32, device=y.device)
+    x = torch.empty_like(y)
+    n = L.finc_inverse_steps(kind, _ptr(y), _ptr(x), _ptr(prepared), B, C, H, W, k, corner,
+                             _ptr(steps), steps.numel(), _stream())
+    if n < 0:
+        _check(n, "finc_inverse_steps")
+    return x, steps
 
 
 def backward(x: torch.Tensor, dy: torch.Tensor, K: torch.Tensor, corner: int,

@@ -308,3 +308,23 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(finc, "_lib", None)
     with pytest.raises(RuntimeError, match="not built"):
         finc.lib(str(tmp_path / "missing.so"))
+
+
+def test_inverse_steps_rejects():
+    lib = finc.lib()
+    S = ctypes.c_void_p(0x2000000)
+    P = ctypes.c_void_p(0x40000000)
+    B, C, H, W, k = SHAPE
+    # unit kind, too small a buffer, steps over y, misaligned prepared, bad corner
+    assert lib.finc_inverse_steps(finc.PLAN_UNIT, FAKE, FAKE2, P, B, C, H, W, k, 0, S, 100,
+                                  None) == finc.EINVAL
+    assert lib.finc_inverse_steps(finc.PLAN_LAYER, FAKE, FAKE2, P, B, C, H, W, k, 0, S, 1,
+                                  None) == finc.EINVAL
+    assert lib.finc_inverse_steps(finc.PLAN_LAYER, FAKE, FAKE2, P, B, C, H, W, k, 0, FAKE, 100,
+                                  None) == finc.EINVAL
+    assert lib.finc_inverse_steps(finc.PLAN_LAYER, FAKE, FAKE2, ctypes.c_void_p(0x40000010), B,
+                                  C, H, W, k, 0, S, 100, None) == finc.EINVAL
+    assert lib.finc_inverse_steps(finc.PLAN_LAYER, FAKE, FAKE2, P, B, C, H, W, k, 4, S, 100,
+                                  None) == finc.EINVAL
+    assert lib.finc_inverse_steps(finc.PLAN_SPLIT, FAKE, FAKE2, P, B, 6, H, W, k, 0, S, 100,
+                                  None) == finc.EINVAL

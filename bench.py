@@ -335,9 +335,52 @@ def scaling_sweep(dev) -> dict:
             us = graph_time_us(lambda: finc.unit_inverse_prepared(y, prep, c["k"], out=out), 3, per)
             rows.append({"n": n, "B": B, "unit_inverse_us": us, "images_per_s": B / (us * 1e-6),
                          "us_per_diagonal_step": us / (4 * (2 * n - 1)),
-                         "round_trip_max_abs": err})
-    return {"what": "FInC unit inverse (TL, TR, BL, BR), C = 2, k = 3, n x n images",
+                         "round_trip_max_abs": err, "form": "one workgroup per image"})
+    # beyond one workgroup: the banded stream form (bands of rows in
+    # workgroups of their own, pipelined)
+    for n in synth.SWEEP_BANDED_SIZES:
+        for B in synth.SWEEP_BATCHES:
+            c = synth.sweep_case(n, B)
+            x, K4 = d(c["x"]), d(c["K4"])
+            y = x
+            for q in range(4):
+                y = finc.forward(y, K4[q].contiguous(), q)
+            out, ws = finc.unit_inverse_banded(y, K4)
+            err = float((out - x).abs().max())
+            us = graph_time_us(lambda: finc.unit_inverse_banded(y, K4, out=out, workspace=ws), 2, 3)
+            plan = finc.banded_plan(2, n, n, c["k"])
+            rows.append({"n": n, "B": B, "unit_inverse_us": us, "images_per_s": B / (us * 1e-6),
+                         "us_per_diagonal_step": us / (4 * (2 * n - 1)),
+                         "round_trip_max_abs": err,
+                         "form": f"banded: {plan['bands']} bands of {plan['rows']} rows"})
+    return {"what": "FInC unit inverse (TL, TR, BL, BR), C = 2, k = 3, n x n images "
+                    "(the banded unit call includes its weight preparation)",
             "rows": rows}
+
+
+def banded_layers(dev) -> list:
+    """Single layers beyond one workgroup (banded stream form): 12 x 128 x 128
+    and 16 x 256 x 64 at k = 3, batch 8, weights prepared inside the call."""
+    import numpy as np
+    import torch
+
+    from paper_2301_09266_amd import finc, synth
+
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    rows = []
+    for (B, C, H, W, k) in ((8, 12, 128, 128, 3), (8, 16, 256, 64, 3)):
+        c = synth.layer_case(B, C, H, W, k)
+        x, K = d(c["x"]), d(c["K"])
+        y = finc.forward(x, K, 0)
+        out, ws = finc.inverse_banded(y, K, 0)
+        err = float((out - x).abs().max())
+        us = graph_time_us(lambda: finc.inverse_banded(y, K, 0, out=out, workspace=ws), 3, 5)
+        plan = finc.banded_plan(C, H, W, k)
+        rows.append({"B": B, "C": C, "H": H, "W": W, "k": k, "inverse_us": us,
+                     "images_per_s": B / (us * 1e-6), "us_per_diagonal_step": us / (H + W - 1),
+                     "bands": plan["bands"], "band_rows": plan["rows"],
+                     "threads": plan["threads"], "round_trip_max_abs": err})
+    return rows
 
 
 def protocol_runs(fn, runs: int = 11) -> dict:
@@ -690,6 +733,7 @@ def main():
     if not args.no_configs:
         out["per_config"] = per_config(dev)
         out["scaling_sweep"] = scaling_sweep(dev)
+        out["banded_layers"] = banded_layers(dev)
         out["batch_scaling"] = batch_scaling(dev)
     if not args.no_configs:
         out["step_cost"] = step_cost(dev)

@@ -96,6 +96,38 @@ enum { FINC_PLAN_LAYER = 0, FINC_PLAN_UNIT = 1, FINC_PLAN_SPLIT = 2, FINC_PLAN_S
 int finc_inverse_plan(int kind, int L, int U, int C, int H, int W, int k, int *info,
                       int max_launches);
 
+/* ---- Images whose level does not fit one workgroup (Sec. 5, Fig. 3's
+ * large images) ---------------------------------------------------------------
+ * The banded stream form: the image's rows (in the corner's frame) are cut
+ * into bands of R rows, one workgroup each, every band running the column-
+ * streaming diagonal wavefront of its own rows.  A band reads the k - 1 rows
+ * above it -- the band above's solution -- from the output as that band
+ * drains them, waiting on a per-band count of drained diagonals in the
+ * workspace; the bands run pipelined, each about R + 16 diagonals behind the
+ * one above (Thm. 2's H + W - 1 steps plus that lag per band).  A workgroup
+ * takes its (image, band) from a ticket at its start, so it only ever waits
+ * on a band that started before it.  Every wait is bounded: after about a
+ * second the band sets the workspace's timeout flag (the int at byte offset
+ * finc_workspace_bytes(C, k, n_layers)), goes on, and its image's result is
+ * invalid.
+ * finc_banded_plan: info[0] = workgroup threads, [1] = band rows R, [2] =
+ *   bands per image, [3] = LDS bytes; FINC_EUNSUPPORTED when no band fits a
+ *   workgroup (C > 16 or k = 1), FINC_EINVAL for a bad shape.
+ * finc_banded_workspace_bytes: the prepared weights of n_layers (1 or 4)
+ *   layers, then the flags; 0 for an unsupported shape.
+ * finc_inverse_banded: as finc_inverse (one layer, corner `corner`);
+ * finc_unit_inverse_banded: as finc_unit_inverse (four layers, one launch
+ *   each, the later ones in place on x).  workspace: device, at least
+ *   finc_banded_workspace_bytes(B, C, H, W, k, 1 or 4) bytes, 256-byte
+ *   aligned, overwritten.  x == y is allowed; other overlaps FINC_EINVAL.
+ *   Calls sharing one workspace must not overlap in time. */
+int finc_banded_plan(int C, int H, int W, int k, int *info);
+size_t finc_banded_workspace_bytes(int B, int C, int H, int W, int k, int n_layers);
+int finc_inverse_banded(const float *y, float *x, const float *K, int B, int C, int H,
+                        int W, int k, int corner, void *workspace, hipStream_t stream);
+int finc_unit_inverse_banded(const float *y, float *x, const float *K4, int B, int C,
+                             int H, int W, int k, void *workspace, hipStream_t stream);
+
 /* Diagnostic of Theorem 2's step count: the inverse of finc_inverse_prepared
  * (kind FINC_PLAN_LAYER, one layer with corner `corner`) or of
  * finc_split_inverse_prepared (kind FINC_PLAN_SPLIT, corner ignored), which

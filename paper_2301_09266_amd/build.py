@@ -29,7 +29,7 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function", "-Wno-unused-const-variable",
 ]
-INVERSE_GROUPS = 15   # kInverseGroups in finc.hip
+INVERSE_GROUPS = 18   # kInverseGroups in finc.hip
 
 
 def _jobs() -> int:

@@ -398,6 +398,11 @@ constexpr int kCritGather = 0, kCritRegs = 1, kOneLayer = 4;
 // columns to HBM, writes the input of the next kPhase diagonals (loaded a
 // phase earlier into registers) and issues the loads of the phase after.
 constexpr int kStream = 8;
+// (with kStream) the banded stream form: the workgroup is one band of rows
+// of an image, pipelined with the bands above and below through global
+// progress counts (instances of their own: the counts and the border rows
+// cost registers the plain stream form does not pay)
+constexpr int kBanded = 16;
 constexpr int kRing = 32, kPhase = 16;
 constexpr int kStreamRegs = 8;   // prefetched input values per thread
 
@@ -471,12 +476,18 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p, bool stream = false) 
     p.S = imax(1, imin(s_max, imax(p.FG, ceil_div(p.FG + p.SG, 2))));
     if (plan_groups(p) > kMaxGroups)
         return false;
-    p.NW = p.T * (1 + p.S);
+    const int nwork = p.T * (1 + p.S);   // critical and helper waves
+    p.NW = nwork;
     p.S4 = round_up4(p.S);
     p.offX = 0;
     if (stream) {
-        if (!p.regcrit || kPhase * H * C > kStreamRegs * p.NW * kWave)
+        // one phase's input is prefetched, kStreamRegs values a thread:
+        // idle waves join the workgroup for it when the working ones are
+        // too few
+        const int need = ceil_div(kPhase * H * C, kStreamRegs * kWave);
+        if (!p.regcrit || need > kMaxWaves)
             return false;
+        p.NW = imax(p.NW, need);
         p.offY = (H + p.P) * kRing * p.CP;
         p.offR = p.offY + H * kRing * p.CP;
     } else {
@@ -510,7 +521,7 @@ inline bool make_plan(int C, int H, int W, int K, Plan &p, bool stream = false) 
             role = 0;
             tile = w;
             ng = p.regcrit ? 2 : ceil_div(p.nq_crit, 4);
-        } else if (w < p.NW) {
+        } else if (w < nwork) {
             role = 1;
             tile = (w - p.T) / p.S;
             h = (w - p.T) - tile * p.S;
@@ -557,8 +568,19 @@ struct InvArgs {
     // wave w of workgroup b writes steps[b * waves + w] = the number of
     // diagonal steps (each ended by the step barrier) that wave ran
     int *steps;
+    // banded stream form (0 bands otherwise): an image's frame rows cut into
+    // bands of the plan's H rows, one workgroup each, img_H rows in all;
+    // bflags = [timeout flag, ticket, diagonals drained per (image, band)],
+    // zeroed before the launch
+    int nbands, img_H;
+    int *bflags;
 };
 static_assert(sizeof(InvArgs) <= 4096, "kernel arguments are limited to 4 KB");
+
+// Spins of a band's wait for the band above before it gives up, sets the
+// timeout flag and goes on (about a second; the wait is never that long
+// when the band above runs)
+constexpr int kBandSpin = 1 << 20;
 
 // What one wave does at a level.  role 0: critical wave of `tile`; 1: helper
 // h of `tile`; 2: idle (barriers only).
@@ -916,8 +938,27 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
     // (consecutive threads take consecutive columns of one row).
     float ypre[kStreamRegs];
     const int nph = kPhase * H * C;
-    const float *zin = lv.z + b * (size_t)C * HW;
-    float *zout = a.out + b * (size_t)C * HW;
+    // banded stream form: the workgroup's image and band come from a ticket
+    // taken at its start (through the trash block, unused until the steps),
+    // so a band only ever waits on a band that started before it
+    constexpr bool banded = kStr && (MODE & kBanded) != 0;
+    int bimg = (int)b, band = 0;
+    if constexpr (banded) {
+        int *tk = reinterpret_cast<int *>(sm + pl.offT);
+        if (threadIdx.x == 0)
+            tk[0] = __hip_atomic_fetch_add(a.bflags + 1, 1, __ATOMIC_RELAXED,
+                                           __HIP_MEMORY_SCOPE_AGENT);
+        __syncthreads();
+        const int t = tk[0];
+        __syncthreads();
+        bimg = t / a.nbands;
+        band = t - bimg * a.nbands;
+    }
+    const int imgH = banded ? a.img_H : H;   // rows of the whole image
+    const int i0 = band * H;                 // the band's first frame row
+    const int HWi = imgH * W;
+    const float *zin = lv.z + (size_t)bimg * C * HWi;
+    float *zout = a.out + (size_t)bimg * C * HWi;
     const int scorner = corner_at(0);
     const bool sfh = scorner == FINC_BL || scorner == FINC_BR;
     const bool sfw = scorner == FINC_TR || scorner == FINC_BR;
@@ -927,9 +968,9 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
         i = rc - c * H;
         j = d0 + (t & (kPhase - 1)) - i;
     };
-    // natural NCHW offset of frame pixel (i, j), channel c
+    // natural NCHW offset of frame pixel (i0 + i, j), channel c
     auto snat = [&](int c, int i, int j) __attribute__((always_inline)) {
-        return c * HW + (sfh ? H - 1 - i : i) * W + (sfw ? W - 1 - j : j);
+        return c * HWi + (sfh ? imgH - 1 - (i0 + i) : i0 + i) * W + (sfw ? W - 1 - j : j);
     };
     // loads of the input of diagonals d0 .. d0 + kPhase - 1 into registers
     auto sissue = [&](int d0) __attribute__((always_inline)) {
@@ -938,7 +979,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
             const int t = threadIdx.x + u * blockDim.x;
             int i, c, j;
             selem(t, d0, i, c, j);
-            const bool ok = t < nph && (unsigned)j < (unsigned)W;
+            const bool ok = t < nph && (unsigned)j < (unsigned)W && (!banded || i0 + i < imgH);
             ypre[u] = zin[ok ? snat(c, i, j) : 0];
         }
     };
@@ -958,10 +999,49 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
         for (int t = threadIdx.x; t < nph; t += blockDim.x) {
             int i, c, j;
             selem(t, d0, i, c, j);
-            if (d0 + (t & (kPhase - 1)) <= d1 && (unsigned)j < (unsigned)W)
+            if (d0 + (t & (kPhase - 1)) <= d1 && (unsigned)j < (unsigned)W &&
+                (!banded || i0 + i < imgH))
                 zout[snat(c, i, j)] =
                     sm[pl.offX + ((i + P) * kRing + (j & (kRing - 1))) * CP + c];
         }
+    };
+    // (banded) thread 0 waits until the band above has drained `need`
+    // diagonals (bounded: past kBandSpin tries the timeout flag is set and
+    // the band goes on) and acquires what it drained -- one cache
+    // invalidation for the workgroup, whose other waves wait at the barrier
+    auto bwait = [&](int need) __attribute__((always_inline)) {
+        if (threadIdx.x == 0) {
+            const int *f = a.bflags + 2 + bimg * a.nbands + band - 1;
+            for (int it = 0;
+                 __hip_atomic_load(f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < need; ++it) {
+                if (it >= kBandSpin) {
+                    __hip_atomic_store(a.bflags, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(4);
+            }
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        }
+        __syncthreads();
+    };
+    // (banded) frame rows i0 - P .. i0 - 1 -- the band above's last rows, as
+    // it drained them -- at columns c0 .. c1 into the solution ring's border
+    auto sborder = [&](int c0, int c1) __attribute__((always_inline)) {
+        const int ncol = c1 - c0 + 1, nb = P * ncol * C;
+        for (int t = threadIdx.x; t < nb; t += blockDim.x) {
+            const int jj = t % ncol, r2 = t / ncol, ii = r2 % P, c = r2 / P;
+            const int j = c0 + jj, i = ii - P;
+            sm[pl.offX + (ii * kRing + (j & (kRing - 1))) * CP + c] = zout[snat(c, i, j)];
+        }
+    };
+    // (banded) the count of diagonals this band has drained, published by a
+    // release store after the barrier (every wave's drain stores complete
+    // before it)
+    auto bpublish = [&](int ndiag) __attribute__((always_inline)) {
+        __syncthreads();
+        if (threadIdx.x == 0)
+            __hip_atomic_store(a.bflags + 2 + bimg * a.nbands + band, ndiag, __ATOMIC_RELEASE,
+                               __HIP_MEMORY_SCOPE_AGENT);
     };
     // end of diagonal step e: the barrier; in the stream form, at the end of
     // a phase, the exchange with HBM and one more barrier
@@ -977,6 +1057,16 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                 sdrain(e & ~(kPhase - 1), e);
                 if (pend)
                     sissue(e + 2 + kPhase);
+                if constexpr (banded) {
+                    bpublish(e + 1);
+                    // border columns of the next phase's diagonals: the band
+                    // above's pixel (H - 1, c) is on its diagonal c + H - 1
+                    if (band > 0 && pend && e + 2 < W) {
+                        const int c1 = imin(e + 1 + kPhase, W - 1);
+                        bwait(c1 + H);
+                        sborder(e + 2, c1);
+                    }
+                }
                 __syncthreads();
             }
         }
@@ -987,6 +1077,13 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
         decode();
         zero_floats(sm + pl.offX, pl.offT - pl.offX);   // rings, partial tiles, Z
         __syncthreads();
+        if constexpr (banded) {
+            if (band > 0) {   // border columns of diagonals 0 .. kPhase
+                const int c1 = imin(kPhase, W - 1);
+                bwait(c1 + H);
+                sborder(0, c1);
+            }
+        }
         sput(1);
         if (threadIdx.x < C)
             sm[pl.offY + threadIdx.x] = zin[snat(threadIdx.x, 0, 0)];
@@ -1206,7 +1303,10 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                 int ucol = pl.offX + ((uoi + P) * WP + P) * CP + fwo + 4 * kq + ju * dcol;
                 // (stream form: ring rows of the written row and of the row above)
                 const int wxs = pl.offX + (gic + P) * kRing * CP + nt * 16 + 4 * kq;
-                const int uxs = pl.offX + (imax(ui, 0) + P) * kRing * CP + 4 * kq;
+                // the first tile of a lower band: its row above is the band
+                // above's last row, in the ring's border (else zeros)
+                const bool upb = banded && band > 0 && mt == 0;
+                const int uxs = pl.offX + ((upb ? -1 : imax(ui, 0)) + P) * kRing * CP + 4 * kq;
                 const f32x4 *b1 = sbase(1, pad), *b2 = sbase(2, pad), *b3 = sbase(3, pad);
                 __syncthreads();
                 int e = 0;
@@ -1218,7 +1318,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                         const int ucur = kStr ? uxs + __mul24(ju & (kRing - 1), CP) : ucol;
                         const int wcur = kStr ? wxs + __mul24(j & (kRing - 1), CP) : wcol;
                         f32x4 up = zero;
-                        if (mt > 0)
+                        if (mt > 0 || upb)
                             up = *reinterpret_cast<const f32x4 *>(
                                 sm + ((li == 0 && 4 * kq < CP && (unsigned)ju < (unsigned)W) ? ucur
                                                                                         : zaddr));
@@ -1465,19 +1565,21 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
 
 // Inverse kernel instances, in groups of one workgroup size and one mode, by
 // quad groups per wave (1..kMaxGroups).  The host picks one by address.
-constexpr int kInverseGroups = 15;
-constexpr int kModesPerSize = 5;
-constexpr int kGroupThreads[kInverseGroups] = {256,  256,  256,  256,  256,  512,  512, 512,
-                                               512,  512,  1024, 1024, 1024, 1024, 1024};
+constexpr int kInverseGroups = 18;
+constexpr int kModesPerSize = 6;
+constexpr int kGroupThreads[kInverseGroups] = {256,  256,  256,  256,  256,  256,
+                                               512,  512,  512,  512,  512,  512,
+                                               1024, 1024, 1024, 1024, 1024, 1024};
 constexpr int kGroupModes[kModesPerSize] = {kCritGather,
                                             kCritRegs,
                                             kCritGather | kOneLayer,
                                             kCritRegs | kOneLayer,
-                                            kCritRegs | kOneLayer | kStream};
+                                            kCritRegs | kOneLayer | kStream,
+                                            kCritRegs | kOneLayer | kStream | kBanded};
 constexpr int kGroupMode[kInverseGroups] = {
-    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4],
-    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4],
-    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4]};
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4], kGroupModes[5],
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4], kGroupModes[5],
+    kGroupModes[0], kGroupModes[1], kGroupModes[2], kGroupModes[3], kGroupModes[4], kGroupModes[5]};
 
 template <int MAXT, int MODE>
 const void *inverse_instance_of(int ng) {
@@ -1496,7 +1598,8 @@ const void *inverse_instance_of(int ng) {
 }  // namespace
 
 #define FINC_GROUPS(X) \
-    X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14)
+    X(0) X(1) X(2) X(3) X(4) X(5) X(6) X(7) X(8) X(9) X(10) X(11) X(12) X(13) X(14) X(15) \
+        X(16) X(17)
 #define FINC_CAT2(a, b) a##b
 #define FINC_CAT(a, b) FINC_CAT2(a, b)
 
@@ -2069,6 +2172,89 @@ int launch_streamed(const InvArgs &a, const InvChoice &ch, int B, hipStream_t st
     return FINC_OK;
 }
 
+// ---- banded stream form: images whose level does not fit one workgroup --
+
+__global__ void zero_ints_kernel(int *p, int n) {
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x)
+        p[i] = 0;
+}
+
+// The band height of a single layer of C channels on H x W images: the
+// tallest multiple of 16 rows, at most 128 and at most the image's rows
+// rounded up, whose stream-form plan fits a workgroup (registers for one
+// phase's input, LDS); false if none does (C > 16 or k = 1).
+bool banded_choice(int C, int H, int W, int k, size_t lds_lim, InvChoice &c, int &R, int &nb) {
+    memset(&c, 0, sizeof(c));
+    for (R = imin(128, ceil_div(H, 16) * 16); R >= 16; R -= 16) {
+        if (!make_plan(C, R, W, k, c.sp, true))
+            continue;
+        c.lds = (size_t)c.sp.lds_floats * sizeof(float);
+        if (c.lds > lds_lim)
+            continue;
+        c.streamed = 1;
+        c.threads = c.sp.NW * kWave;
+        c.mode = kCritRegs | kOneLayer | kStream | kBanded;
+        c.ng = plan_groups(c.sp);
+        c.compact = c.sp.compact;
+        nb = ceil_div(H, R);
+        return true;
+    }
+    return false;
+}
+
+inline size_t banded_flag_ints(int B, int nb) { return 2 + (size_t)B * nb; }
+
+// n_layers layers (1: corner `corner`; 4: a unit, run BR, BL, TR, TL), each
+// one launch of B * nb workgroups after the flags are cleared; the layers
+// after the first work in place on x.
+int launch_banded(const float *y, float *x, const float *prep, int n_layers, int corner, int B,
+                  int C, int H, int W, int k, int *bflags, hipStream_t stream) {
+    size_t lim = kLdsBytes;
+    if (B > 0) {
+        const int lrc = lds_limit(&lim);
+        if (lrc != FINC_OK)
+            return lrc;
+    }
+    InvChoice ch;
+    int R = 0, nb = 0;
+    if (!banded_choice(C, H, W, k, lim, ch, R, nb))
+        return FINC_EUNSUPPORTED;
+    if (B == 0)
+        return FINC_OK;
+    const void *kern = inverse_instance(ch.threads, ch.mode, ch.ng);
+    if (!kern)
+        return FINC_EUNSUPPORTED;
+    if (hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)ch.lds) !=
+        hipSuccess)
+        (void)hipGetLastError();
+    const int nflags = (int)banded_flag_ints(B, nb);
+    for (int n = 0; n < n_layers; ++n) {
+        const int q = n_layers - 1 - n;
+        hipLaunchKernelGGL(zero_ints_kernel, dim3(imin(ceil_div(nflags, 256), 1024)), dim3(256), 0,
+                           stream, bflags, nflags);
+        int rc = launched();
+        if (rc != FINC_OK)
+            return rc;
+        InvArgs s;
+        memset(&s, 0, sizeof(s));
+        s.L = s.n_units = s.lpu = 1;
+        s.corner0 = n_layers == 1 ? corner : q;
+        s.out = x;
+        s.lv[0].z = n == 0 ? y : x;
+        s.lv[0].prep = prep + (size_t)(n_layers == 1 ? 0 : q) * ch.sp.lstride;
+        s.lv[0].pl = ch.sp;
+        s.nbands = nb;
+        s.img_H = H;
+        s.bflags = bflags;
+        void *args[] = {&s};
+        (void)hipLaunchKernel(kern, dim3(B * nb), dim3(ch.threads), args, ch.lds, stream);
+        rc = launched();
+        if (rc != FINC_OK)
+            return rc;
+    }
+    return FINC_OK;
+}
+
 int launch_inverse_chain(InvArgs &a, int B, hipStream_t stream) {
     size_t lim = kLdsBytes;
     if (B > 0) {
@@ -2628,6 +2814,67 @@ int finc_inverse_steps(int kind, const float *y, float *x, const void *prepared,
     a.steps = steps;
     const int rc = launch_inverse_chain(a, split ? 4 * B : B, stream);
     return rc == FINC_OK ? (int)count : rc;
+}
+
+int finc_banded_plan(int C, int H, int W, int k, int *info) {
+    if (!info || !valid_shape(1, C, H, W, k))
+        return FINC_EINVAL;
+    InvChoice ch;
+    int R = 0, nb = 0;
+    if (!banded_choice(C, H, W, k, kLdsBytes, ch, R, nb))
+        return FINC_EUNSUPPORTED;
+    info[0] = ch.threads;
+    info[1] = R;
+    info[2] = nb;
+    info[3] = (int)ch.lds;
+    return FINC_OK;
+}
+
+size_t finc_banded_workspace_bytes(int B, int C, int H, int W, int k, int n_layers) {
+    int info[4];
+    if ((n_layers != 1 && n_layers != 4) || B < 0 || finc_banded_plan(C, H, W, k, info) != FINC_OK ||
+        (long long)B * C * H * W >= (1ll << 31))
+        return 0;
+    const size_t prep = finc_workspace_bytes(C, k, n_layers);
+    return prep + ((banded_flag_ints(B, info[2]) * sizeof(int) + 255) & ~(size_t)255);
+}
+
+static int banded_call(const float *y, float *x, const float *K, int n_layers, int corner, int B,
+                       int C, int H, int W, int k, void *workspace, hipStream_t stream) {
+    if (!valid_shape(B, C, H, W, k) || !x || !y || !K || !workspace || !aligned256(workspace))
+        return FINC_EINVAL;
+    int info[4];
+    const int prc = finc_banded_plan(C, H, W, k, info);
+    if (prc != FINC_OK)
+        return prc;
+    const size_t wsb = finc_banded_workspace_bytes(B, C, H, W, k, n_layers);
+    const size_t bytes = (size_t)B * C * H * W * sizeof(float);
+    const size_t kb = (size_t)n_layers * C * C * k * k * sizeof(float);
+    if (!inverse_alias_ok(y, x, bytes) || overlap(workspace, wsb, x, bytes) ||
+        overlap(workspace, wsb, y, bytes) || overlap(workspace, wsb, K, kb))
+        return FINC_EINVAL;
+    int corners[4] = {FINC_TL, FINC_TR, FINC_BL, FINC_BR};
+    if (n_layers == 1)
+        corners[0] = corner;
+    const int rc = finc_prepare(K, n_layers, corners, C, k, workspace, stream);
+    if (rc != FINC_OK)
+        return rc;
+    int *flags = reinterpret_cast<int *>(static_cast<char *>(workspace) +
+                                         finc_workspace_bytes(C, k, n_layers));
+    return launch_banded(y, x, static_cast<const float *>(workspace), n_layers, corner, B, C, H, W,
+                         k, flags, stream);
+}
+
+int finc_inverse_banded(const float *y, float *x, const float *K, int B, int C, int H, int W,
+                        int k, int corner, void *workspace, hipStream_t stream) {
+    if (!valid_corner(corner))
+        return FINC_EINVAL;
+    return banded_call(y, x, K, 1, corner, B, C, H, W, k, workspace, stream);
+}
+
+int finc_unit_inverse_banded(const float *y, float *x, const float *K4, int B, int C, int H,
+                             int W, int k, void *workspace, hipStream_t stream) {
+    return banded_call(y, x, K4, 4, FINC_TL, B, C, H, W, k, workspace, stream);
 }
 
 int finc_split_inverse(const float *y, float *x, const float *Kq4, int B, int C, int H, int W,

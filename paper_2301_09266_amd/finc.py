@@ -30,6 +30,10 @@ SIGNATURES = {
     "finc_inverse_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i), _i]),
     "finc_forward_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i)]),
     "finc_inverse_steps": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp]),
+    "finc_banded_plan": (_i, [_i, _i, _i, _i, ctypes.POINTER(_i)]),
+    "finc_banded_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
+    "finc_inverse_banded": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
+    "finc_unit_inverse_banded": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_workspace_bytes": (_sz, [_i, _i, _i]),
     "finc_prepare": (_i, [_vp, _i, ctypes.POINTER(_i), _i, _i, _vp, _vp]),
     "finc_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp]),
@@ -311,6 +315,44 @@ def inverse_steps(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: int =
     if n < 0:
         _check(n, "finc_inverse_steps")
     return x, steps
+
+
+def banded_plan(C: int, H: int, W: int, k: int):
+    """dict(threads, rows, bands, lds) of the banded stream form
+    (finc_banded_plan), or the negative status."""
+    info = (ctypes.c_int * 4)()
+    rc = _require_lib().finc_banded_plan(C, H, W, k, info)
+    if rc < 0:
+        return rc
+    return dict(threads=info[0], rows=info[1], bands=info[2], lds=info[3])
+
+
+def _banded(fn, y, K, n_layers, corner, out, workspace):
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    k = K.shape[-1]
+    _dev(K, "K", (C, C, k, k) if n_layers == 1 else (4, C, C, k, k))
+    nbytes = int(L.finc_banded_workspace_bytes(B, C, H, W, k, n_layers))
+    if nbytes == 0:
+        raise FincError(EUNSUPPORTED if isinstance(banded_plan(C, H, W, k), int) else EINVAL, fn)
+    ws = _workspace(nbytes, y.device, workspace)
+    x = torch.empty_like(y) if out is None else _dev(out, "out", y.shape)
+    args = (_ptr(y), _ptr(x), _ptr(K), B, C, H, W, k) + ((corner,) if n_layers == 1 else ())
+    _check(getattr(L, fn)(*args, _ptr(ws), _stream()), fn)
+    return x, ws
+
+
+def inverse_banded(y, K, corner: int, out=None, workspace=None):
+    """(x, workspace) of finc_inverse_banded; the workspace's int at byte
+    offset workspace_bytes(C, k, 1) is the timeout flag."""
+    return _banded("finc_inverse_banded", y, K, 1, corner, out, workspace)
+
+
+def unit_inverse_banded(y, K4, out=None, workspace=None):
+    """(x, workspace) of finc_unit_inverse_banded (timeout flag at byte
+    offset workspace_bytes(C, k, 4))."""
+    return _banded("finc_unit_inverse_banded", y, K4, 4, TL, out, workspace)
 
 
 def backward(x: torch.Tensor, dy: torch.Tensor, K: torch.Tensor, corner: int,

@@ -184,6 +184,8 @@ WORKLOADS = {
 # batches of 1 .. 128 (the larger images exceed LDS and stream).
 SWEEP_SIZES = (16, 32, 64, 128)
 SWEEP_BATCHES = (1, 8, 32, 128)
+# sizes beyond one workgroup (the banded stream form)
+SWEEP_BANDED_SIZES = (256,)
 
 
 def sweep_case(n: int, B: int, C: int = 2, k: int = 3, seed: int = 0) -> dict:

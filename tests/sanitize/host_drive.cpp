@@ -60,6 +60,17 @@ static void plans() {
                 }
             }
     EXPECT(launches > 0);
+    for (int C = 0; C <= 18; ++C)
+        for (int k = 0; k <= FINC_MAX_K + 1; ++k)
+            for (const auto &hw : HW) {
+                int *bi = (int *)malloc(4 * sizeof(int));
+                const int r = finc_banded_plan(C, hw[0] * 2, hw[1], k, bi);
+                EXPECT(r == FINC_OK || r == FINC_EINVAL || r == FINC_EUNSUPPORTED);
+                if (r == FINC_OK)
+                    EXPECT(bi[1] % 16 == 0 && bi[1] <= 128 && bi[2] * bi[1] >= hw[0] * 2);
+                free(bi);
+                (void)finc_banded_workspace_bytes(5, C, hw[0] * 2, hw[1], k, 4);
+            }
     EXPECT(finc_inverse_plan(FINC_PLAN_LAYER, 1, 1, 12, 16, 16, 3, nullptr, 1) == FINC_EINVAL);
     EXPECT(finc_inverse_plan(7, 1, 1, 12, 16, 16, 3, nullptr, 1) == FINC_EINVAL);
 }

@@ -328,3 +328,28 @@ def test_inverse_steps_rejects():
                                   None) == finc.EINVAL
     assert lib.finc_inverse_steps(finc.PLAN_SPLIT, FAKE, FAKE2, P, B, 6, H, W, k, 0, S, 100,
                                   None) == finc.EINVAL
+
+
+def test_banded_rejects():
+    lib = finc.lib()
+    ws = ctypes.c_void_p(0x40000000)
+    info = (ctypes.c_int * 4)()
+    assert lib.finc_banded_plan(17, 256, 256, 3, info) == finc.EUNSUPPORTED   # C > 16
+    assert lib.finc_banded_plan(2, 256, 256, 1, info) == finc.EUNSUPPORTED    # k = 1
+    assert lib.finc_banded_plan(2, 256, 256, 3, None) == finc.EINVAL
+    assert lib.finc_banded_plan(2, 256, 256, 3, info) == finc.OK
+    assert info[1] == 128 and info[2] == 2 and info[0] % 64 == 0
+    assert lib.finc_banded_workspace_bytes(1, 17, 256, 256, 3, 1) == 0
+    assert lib.finc_banded_workspace_bytes(1, 2, 256, 256, 3, 2) == 0        # 1 or 4 layers
+    n1 = lib.finc_banded_workspace_bytes(3, 2, 256, 256, 3, 1)
+    assert n1 >= lib.finc_workspace_bytes(2, 3, 1) + 4 * (2 + 3 * 2)
+    args = (FAKE, FAKE2, FAKE3, 1, 2, 256, 256, 3)
+    assert lib.finc_inverse_banded(*args, 0, NULL, None) == finc.EINVAL              # no ws
+    assert lib.finc_inverse_banded(*args, 4, ws, None) == finc.EINVAL                # corner
+    assert lib.finc_inverse_banded(*args, 0, ctypes.c_void_p(0x40000010), None) == finc.EINVAL
+    assert lib.finc_inverse_banded(FAKE, ctypes.c_void_p(0x100000 + 64), FAKE3, 1, 2, 256, 256, 3,
+                                   0, ws, None) == finc.EINVAL                       # x over y
+    assert lib.finc_unit_inverse_banded(FAKE, FAKE2, FAKE3, 1, 17, 64, 64, 3, ws,
+                                        None) == finc.EUNSUPPORTED
+    assert lib.finc_unit_inverse_banded(FAKE, FAKE2, FAKE3, 1, 2, 64, 64, 3,
+                                        ctypes.c_void_p(0x1100000 - 256), None) == finc.EINVAL

@@ -423,12 +423,24 @@ def pin_squeeze_reshape(o):
 
 
 def pin_actnorm(o):
+    """Actnorm is the per-channel affine map: its dense Jacobian (the forward
+    on basis vectors, bias removed) is diagonal with s[c] on every entry of
+    channel c's plane (a channel index taken from the wrong axis or a shared
+    scale would not be), so log|det| = H W sum log|s| by slogdet; the
+    constant part is b; the inverse undoes it."""
     rng = np.random.default_rng(23)
     x = rng.normal(size=(2, 4, 3, 5))
-    s, b = np.exp(rng.normal(size=4)), rng.normal(size=4)
-    y = o.actnorm_forward(x, s, b)
-    close(y, x * s[None, :, None, None] + b[None, :, None, None], 1e-15, "actnorm forward")
-    close(o.actnorm_inverse(y, s, b), x, 1e-14, "actnorm inverse")
+    s = np.exp(rng.normal(size=4)) * np.array([1.0, -1.0, 1.0, -1.0])
+    b = rng.normal(size=4)
+    C, H, W = 4, 3, 5
+    zero = np.zeros((1, C, H, W))
+    J = dense_jacobian(lambda v: o.actnorm_forward(v, s, b) - o.actnorm_forward(
+        np.zeros_like(v), s, b), C, H, W)
+    close(J, np.diag(np.repeat(s, H * W)), 1e-15, "actnorm Jacobian")
+    close(np.linalg.slogdet(J)[1], H * W * np.log(np.abs(s)).sum(), 1e-12, "actnorm log|det|")
+    close(o.actnorm_forward(zero, s, b)[0], np.broadcast_to(b[:, None, None], (C, H, W)), 0.0,
+          "actnorm bias")
+    close(o.actnorm_inverse(o.actnorm_forward(x, s, b), s, b), x, 1e-14, "actnorm inverse")
 
 
 def _compose_stack_inverse(o, z, K, scale, bias, levels, units):
@@ -447,9 +459,41 @@ def _compose_stack_inverse(o, z, K, scale, bias, levels, units):
     return h
 
 
+def _torch_stack_forward(x, K, scale, bias, levels, units):
+    """The stack's forward direction written independently in torch (fp64):
+    per level, units of four masked conv2d blocks (corners TL, TR, BL, BR)
+    each followed by the affine actnorm; below the top, the second half of
+    the channels is the latent and the first half is squeezed by
+    reshape/permute."""
+    h = torch.tensor(x)
+    z = []
+    for l in range(levels):
+        for u in range(units):
+            for q in range(4):
+                h, _ = _torch_layer(h, torch.tensor(K[l][u][q]), q)
+            h = h * torch.tensor(scale[l][u])[None, :, None, None] + \
+                torch.tensor(bias[l][u])[None, :, None, None]
+        if l < levels - 1:
+            C = h.shape[1]
+            z.append(h[:, C // 2:].numpy())
+            h = h[:, :C // 2]
+            B, C2, H, W = h.shape
+            h = h.reshape(B, C2, H // 2, 2, W // 2, 2).permute(0, 1, 3, 5, 2, 4).reshape(
+                B, 4 * C2, H // 2, W // 2)
+    z.append(h.numpy())
+    return z
+
+
 def pin_stack(o):
-    """Stack inverse = composition of the pinned pieces, and it inverts the
-    stack forward (split keeps the first half, Sec. 4.4)."""
+    """Stack forward = an independent torch composition (conv2d blocks,
+    affine actnorm, slicing, reshape squeeze); stack inverse = composition of
+    the pinned pieces; and the inverse inverts the forward (Sec. 4.4)."""
+    case0 = synth.stack_case(B=2, C1=4, H1=8, W1=8, levels=3, units=2, k=3)
+    xin = case0["x"][:, :4, :8, :8]
+    zt = _torch_stack_forward(xin, case0["K"], case0["scale"], case0["bias"], 3, 2)
+    zo = o.stack_forward(xin, case0["K"], case0["scale"], case0["bias"], levels=3, units=2, k=3)
+    for l in range(3):
+        close(zo[l], zt[l], 1e-10, f"stack forward latent {l} vs torch")
     case = synth.stack_case(B=2, C1=4, H1=8, W1=8, levels=3, units=2, k=3)
     a = dict(levels=3, units=2, k=3)
     x = o.stack_inverse(case["z"], case["K"], case["scale"], case["bias"], C1=4, H1=8,

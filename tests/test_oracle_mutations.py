@@ -68,6 +68,14 @@ MUTANTS = [
     ("nll drops the normalising constant", "q += 0.5 * (v * v + log2pi);", "q += 0.5 * v * v;", 0),
     ("nll adds the log|det|", "nll[b] = q - logdet[b];", "nll[b] = q + logdet[b];", 0),
     ("bpd in nats", "bpd[b] = nll[b] / ((double)D * log(2.0));", "bpd[b] = nll[b] / (double)D;", 0),
+    ("stack forward keeps the latent half",
+     "memcpy(t + b * Ch * hw, h + b * C * hw, sizeof(double) * Ch * hw);",
+     "memcpy(t + b * Ch * hw, h + (b * C + Ch) * hw, sizeof(double) * Ch * hw);", 0),
+    ("stack forward passes the scale as the bias",
+     "orc_actnorm_forward(t, h, sl + (long)u * C, bl + (long)u * C, B, C, H, W);",
+     "orc_actnorm_forward(t, h, sl + (long)u * C, sl + (long)u * C, B, C, H, W);", 0),
+    ("actnorm forward reads the scale of the next channel", "y[o] = s[c] * x[o] + b[c];",
+     "y[o] = s[(c + 1) % C] * x[o] + b[c];", 0),
     ("backward weight gradient reads the mirrored tap",
      "x[n * img + ci * plane + (long)ii * W + jj];",
      "x[n * img + ci * plane + (long)(H - 1 - ii) * W + jj];", 0),

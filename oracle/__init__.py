@@ -51,6 +51,9 @@ def load(path: str = LIB):
         "orc_split_backward": [_dp, _dp, _dp, _dp, _dp, ctypes.c_double, L, I, I, I, I],
         "orc_actnorm_backward": [_dp, _dp, _dp, _dp, _dp, _dp, ctypes.c_double, L, I, I, I],
         "orc_gauss_nll": [ctypes.POINTER(_dp), ctypes.POINTER(L), I, L, _dp, _dp, _dp],
+        "orc_stack_logdet": [_dp, _dp, I, I, I, I, I, I, _dp],
+        "orc_stack_backward": [_dp, ctypes.POINTER(_dp), _dp, _dp, _dp, _dp, _dp, _dp, _dp,
+                               ctypes.c_double, L, I, I, I, I, I, I],
         "orc_unit_forward": [_dp, _dp, _dp, L, I, I, I, I],
         "orc_unit_inverse": [_dp, _dp, _dp, L, I, I, I, I],
         "orc_unit_logdet": [_dp, I, I, I, I, _dp],
@@ -267,6 +270,29 @@ class Oracle:
         _check(self.lib.orc_stack_forward(_p(x), zp, _p(Kf), _p(sf), _p(bf), B, levels,
                                           units, C1, H1, W1, k))
         return z
+
+    def stack_logdet(self, K, scale, levels: int, units: int, C1: int, H1: int, W1: int,
+                     k: int) -> float:
+        """log|det| of the stack's forward direction, one image."""
+        Kf, sf, _ = self._stack_params(K, scale, scale)
+        out = np.zeros(1)
+        _check(self.lib.orc_stack_logdet(_p(Kf), _p(sf), levels, units, C1, H1, W1, k, _p(out)))
+        return float(out[0])
+
+    def stack_backward(self, x, dz, K, scale, bias, levels: int, units: int, k: int,
+                       gld: float = 0.0):
+        """(dx, dK, dscale, dbias) of the stack's forward direction, flat
+        parameter layouts as K, scale, bias (see orc_stack_backward)."""
+        x = _c(x)
+        B, C1, H1, W1 = x.shape
+        Kf, sf, bf = self._stack_params(K, scale, bias)
+        dzs = [_c(a) for a in dz]
+        zp = (_dp * levels)(*[_p(a) for a in dzs])
+        dx, dK, ds, db = np.empty_like(x), np.empty_like(Kf), np.empty_like(sf), np.empty_like(bf)
+        _check(self.lib.orc_stack_backward(_p(x), zp, _p(Kf), _p(sf), _p(bf), _p(dx), _p(dK),
+                                           _p(ds), _p(db), float(gld), B, levels, units, C1, H1,
+                                           W1, k))
+        return dx, dK, ds, db
 
     def stack_inverse(self, z, K, scale, bias, levels: int, units: int, k: int,
                       C1: int, H1: int, W1: int) -> np.ndarray:

@@ -688,6 +688,136 @@ int orc_gauss_nll(const double *const *z, const long *n, int L, long B, const do
     return ORC_OK;
 }
 
+/* log|det| of the stack's forward direction, one image: every unit's (the
+ * sum of its blocks') plus every actnorm's H W sum_c log|s_c|, at the
+ * level's spatial size (the split and squeeze move values: no term). */
+int orc_stack_logdet(const double *K, const double *scale, int L, int U, int C1, int H1, int W1,
+                     int k, double *out)
+{
+    if (L < 1 || U < 0 || C1 < 1 || H1 < 1 || W1 < 1 || k < 1 || !K || !scale || !out)
+        return ORC_EINVAL;
+    double s = 0.0;
+    int rc = ORC_OK;
+    for (int l = 0; l < L; ++l) {
+        const int C = C1 << l, H = H1 >> l, W = W1 >> l;
+        const long ksz = (long)C * C * k * k;
+        const double *Kl = K + stack_koff(l, U, C1, k);
+        const double *sl = scale + stack_soff(l, U, C1);
+        for (int u = 0; u < U; ++u) {
+            double v;
+            const int r = orc_unit_logdet(Kl + (long)u * 4 * ksz, C, k, H, W, &v);
+            if (r == ORC_EINVAL)
+                return r;
+            if (r != ORC_OK)
+                rc = r;
+            s += v;
+            for (int c = 0; c < C; ++c)
+                s += (double)H * W * log(fabs(sl[(long)u * C + c]));
+        }
+    }
+    *out = s;
+    return rc;
+}
+
+/* Backward of the stack's forward direction (orc_stack_forward) for the
+ * gradients dz[l] of a loss with respect to its latents, plus gld times the
+ * stack's log|det| of one image (orc_stack_logdet; -B for the log|det| part
+ * of a batch's summed negative log-likelihood).
+ * Every unit's input and every actnorm's input are recomputed by the forward;
+ * then, level by level from the top: the level output's gradient is the
+ * unsqueezed gradient of the next level's input (its first half, which went
+ * on) beside dz[l] (its second half, the latent); the units run in reverse,
+ * each actnorm's backward before its unit's.  Outputs: dx (the input's
+ * gradient) and dK, dscale, dbias in the layouts of K, scale and bias; any
+ * may be NULL. */
+int orc_stack_backward(const double *x, const double *const *dz, const double *K,
+                       const double *scale, const double *bias, double *dx, double *dK,
+                       double *dscale, double *dbias, double gld, long B, int L, int U, int C1,
+                       int H1, int W1, int k)
+{
+    if (L < 1 || U < 0 || B < 0 || C1 < 1 || H1 < 1 || W1 < 1 || k < 1 || !x || !dz || !K ||
+        !scale || !bias)
+        return ORC_EINVAL;
+    if (((H1 | W1) & ((1 << (L - 1)) - 1)) || (L > 1 && (C1 & 1)))
+        return ORC_EINVAL;
+    const long n0 = B * (long)C1 * H1 * W1;
+    const size_t bytes = sizeof(double) * (n0 > 0 ? n0 : 1);
+    /* per level: the level's input, then per unit its input and its
+     * actnorm's input (2 U + 1 activations of the level's size) */
+    long total = 0;
+    for (int l = 0; l < L; ++l)
+        total += (2L * U + 1) * (n0 >> l);
+    double *acts = malloc(sizeof(double) * (total > 0 ? total : 1));
+    double *g = malloc(bytes), *gn = malloc(bytes), *gt = malloc(bytes);
+    int rc = (acts && g && gn && gt) ? ORC_OK : ORC_ENOMEM;
+    long off[8];
+    /* forward, keeping the activations */
+    long o = 0;
+    for (int l = 0; l < L && rc == ORC_OK; ++l) {
+        const int C = C1 << l, H = H1 >> l, W = W1 >> l;
+        const long n = B * (long)C * H * W, ksz = (long)C * C * k * k;
+        const double *Kl = K + stack_koff(l, U, C1, k);
+        const double *sl = scale + stack_soff(l, U, C1), *bl = bias + stack_soff(l, U, C1);
+        off[l] = o;
+        double *in = acts + o;
+        if (l == 0)
+            memcpy(in, x, sizeof(double) * n);
+        for (int u = 0; u < U && rc == ORC_OK; ++u) {
+            /* h_u (the unit's input), t_u = unit(h_u), h_{u+1} = actnorm(t_u) */
+            double *hu = in + (2L * u) * n, *tu = hu + n, *next = tu + n;
+            rc = orc_unit_forward(hu, tu, Kl + (long)u * 4 * ksz, B, C, H, W, k);
+            orc_actnorm_forward(tu, next, sl + (long)u * C, bl + (long)u * C, B, C, H, W);
+        }
+        o += (2L * U + 1) * n;
+        if (l < L - 1 && rc == ORC_OK) {
+            /* the level's output; its first half, squeezed, is the next input */
+            const double *hout = in + (2L * U) * n;
+            const int Ch = C / 2;
+            const long hw = (long)H * W;
+            for (long b = 0; b < B; ++b)
+                memcpy(gn + b * Ch * hw, hout + b * C * hw, sizeof(double) * Ch * hw);
+            orc_squeeze(gn, acts + o, B, Ch, H, W);
+        }
+    }
+    /* backward, from the top level down */
+    for (int l = L - 1; l >= 0 && rc == ORC_OK; --l) {
+        const int C = C1 << l, H = H1 >> l, W = W1 >> l;
+        const long n = B * (long)C * H * W, ksz = (long)C * C * k * k, hw = (long)H * W;
+        const double *Kl = K + stack_koff(l, U, C1, k);
+        const double *sl = scale + stack_soff(l, U, C1);
+        double *in = acts + off[l];
+        if (l == L - 1) {
+            memcpy(g, dz[l], sizeof(double) * n);
+        } else {
+            /* g holds the next level's input gradient (2C channels at H/2) */
+            const int Ch = C / 2;
+            orc_unsqueeze(g, gn, B, 2 * C, H / 2, W / 2);
+            for (long b = 0; b < B; ++b) {
+                memcpy(g + b * C * hw, gn + b * Ch * hw, sizeof(double) * Ch * hw);
+                memcpy(g + (b * C + Ch) * hw, dz[l] + b * Ch * hw, sizeof(double) * Ch * hw);
+            }
+        }
+        for (int u = U - 1; u >= 0 && rc == ORC_OK; --u) {
+            double *hu = in + (2L * u) * n, *tu = hu + n;
+            const long so = stack_soff(l, U, C1) + (long)u * C;
+            rc = orc_actnorm_backward(tu, g, sl + (long)u * C, gt, dscale ? dscale + so : NULL,
+                                      dbias ? dbias + so : NULL, gld, B, C, H, W);
+            if (rc == ORC_OK)
+                rc = orc_unit_backward(hu, gt, Kl + (long)u * 4 * ksz, g,
+                                       dK ? dK + stack_koff(l, U, C1, k) + (long)u * 4 * ksz
+                                          : NULL,
+                                       gld, B, C, H, W, k);
+        }
+    }
+    if (rc == ORC_OK && dx)
+        memcpy(dx, g, sizeof(double) * n0);
+    free(acts);
+    free(g);
+    free(gn);
+    free(gt);
+    return rc;
+}
+
 /* ==========================================================================
  * The full FInC Flow (Sec. 4.4 "Architecture", Fig. 2b and 2c).
  *

@@ -513,6 +513,52 @@ def pin_stack(o):
     close(zf[0], h[:, 2:], 1e-12, "split keeps the first half")
 
 
+def pin_stack_backward_autograd(o):
+    """Backward of the stack's forward direction = torch autograd (fp64) of
+    L = sum_l <z_l, dz_l> + gld log|det| (the stack's log|det| of one image:
+    every block's diagonal term and every actnorm's H W sum log|s|) through
+    the independent torch composition; the oracle's log|det| equals that
+    torch sum."""
+    rng = np.random.default_rng(47)
+    case = synth.stack_case(B=2, C1=4, H1=8, W1=8, levels=2, units=2, k=3)
+    x = case["x"][:, :4, :8, :8]
+    K, sc, bi = case["K"], case["scale"], case["bias"]
+    xt = torch.tensor(x, requires_grad=True)
+    Kt = [[torch.tensor(K[l][u], requires_grad=True) for u in range(2)] for l in range(2)]
+    st = [[torch.tensor(sc[l][u], requires_grad=True) for u in range(2)] for l in range(2)]
+    bt = [[torch.tensor(bi[l][u], requires_grad=True) for u in range(2)] for l in range(2)]
+    h, z, ld = xt, [], 0.0
+    for l in range(2):
+        for u in range(2):
+            for q in range(4):
+                h, l1 = _torch_layer(h, Kt[l][u][q], q)
+                ld = ld + l1
+            h = h * st[l][u][None, :, None, None] + bt[l][u][None, :, None, None]
+            ld = ld + h.shape[2] * h.shape[3] * torch.log(st[l][u].abs()).sum()
+        if l == 0:
+            C = h.shape[1]
+            z.append(h[:, C // 2:])
+            hh = h[:, :C // 2]
+            B, C2, H, W = hh.shape
+            h = hh.reshape(B, C2, H // 2, 2, W // 2, 2).permute(0, 1, 3, 5, 2, 4).reshape(
+                B, 4 * C2, H // 2, W // 2)
+    z.append(h)
+    dz = [rng.normal(size=t.shape) for t in z]
+    gld = -0.6
+    loss = sum((t * torch.tensor(d)).sum() for t, d in zip(z, dz)) + gld * ld
+    loss.backward()
+    close(o.stack_logdet(K, sc, levels=2, units=2, C1=4, H1=8, W1=8, k=3), float(ld.detach()),
+          1e-10, "stack log|det|")
+    dx, dK, ds, db = o.stack_backward(x, dz, K, sc, bi, levels=2, units=2, k=3, gld=gld)
+    close(dx, xt.grad.numpy(), 1e-10, "stack backward dx")
+    want_dK = np.concatenate([Kt[l][u].grad.numpy().ravel() for l in range(2) for u in range(2)])
+    want_ds = np.concatenate([st[l][u].grad.numpy() for l in range(2) for u in range(2)])
+    want_db = np.concatenate([bt[l][u].grad.numpy() for l in range(2) for u in range(2)])
+    close(dK, want_dK, 1e-10, "stack backward dK")
+    close(ds, want_ds, 1e-10, "stack backward dscale")
+    close(db, want_db, 1e-10, "stack backward dbias")
+
+
 def pin_backward_autograd(o):
     """Backward = torch autograd (fp64) of L = sum(y * dy) + gld * log|det|
     with y = conv2d of the corner-padded input with K * mask: dx = x.grad,
@@ -808,6 +854,7 @@ ALL_PINS = [
     pin_flip_equivalence, pin_wavefront_schedule, pin_unit_dense, pin_unit_round_trip,
     pin_split_dense, pin_split_round_trip, pin_squeeze_reshape, pin_actnorm, pin_stack,
     pin_backward_autograd, pin_backward_dense, pin_unit_backward_autograd,
-    pin_split_backward_autograd, pin_actnorm_backward_autograd, pin_gauss_nll, pin_conv1x1,
+    pin_split_backward_autograd, pin_actnorm_backward_autograd, pin_gauss_nll,
+    pin_stack_backward_autograd, pin_conv1x1,
     pin_coupling, pin_step, pin_flow,
 ]

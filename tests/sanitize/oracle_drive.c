@@ -34,6 +34,10 @@ int orc_stack_forward(const double *, double *const *, const double *, const dou
                       const double *, long, int, int, int, int, int, int);
 int orc_stack_inverse(const double *const *, double *, const double *, const double *,
                       const double *, long, int, int, int, int, int, int);
+int orc_stack_logdet(const double *, const double *, int, int, int, int, int, int, double *);
+int orc_stack_backward(const double *, const double *const *, const double *, const double *,
+                       const double *, double *, double *, double *, double *, double, long, int,
+                       int, int, int, int, int);
 int orc_gauss_nll(const double *const *, const long *, int, long, const double *, double *,
                   double *);
 int orc_conv1x1_forward(const double *, double *, const double *, long, int, int, int);
@@ -163,6 +167,11 @@ static void stack(long B, int L, int U, int C1, int H1, int W1, int k) {
     xr = arr(B * C1 * H1 * W1);
     CHECK(orc_stack_forward(x, z, K, sc, bi, B, L, U, C1, H1, W1, k));
     CHECK(orc_stack_inverse((const double *const *)z, xr, K, sc, bi, B, L, U, C1, H1, W1, k));
+    double ld, *dx = arr(B * C1 * H1 * W1), *dK = arr(nK), *ds = arr(nS), *db = arr(nS);
+    CHECK(orc_stack_logdet(K, sc, L, U, C1, H1, W1, k, &ld));
+    CHECK(orc_stack_backward(x, (const double *const *)z, K, sc, bi, dx, dK, ds, db, -1.0, B, L,
+                             U, C1, H1, W1, k));
+    free(dx); free(dK); free(ds); free(db);
     for (int l = 0; l < L; ++l)
         free(z[l]);
     free(K); free(sc); free(bi); free(x); free(xr);

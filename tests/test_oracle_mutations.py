@@ -76,6 +76,14 @@ MUTANTS = [
      "orc_actnorm_forward(t, h, sl + (long)u * C, sl + (long)u * C, B, C, H, W);", 0),
     ("actnorm forward reads the scale of the next channel", "y[o] = s[c] * x[o] + b[c];",
      "y[o] = s[(c + 1) % C] * x[o] + b[c];", 0),
+    ("stack logdet forgets the actnorms", "s += (double)H * W * log(fabs(sl[(long)u * C + c]));",
+     "s += 0.0;", 0),
+    ("stack backward puts the latent gradient first",
+     "memcpy(g + (b * C + Ch) * hw, dz[l] + b * Ch * hw, sizeof(double) * Ch * hw);",
+     "memcpy(g + b * C * hw, dz[l] + b * Ch * hw, sizeof(double) * Ch * hw);", 0),
+    ("stack backward feeds the unit's output to its actnorm's backward as input",
+     "rc = orc_actnorm_backward(tu, g, sl + (long)u * C, gt,",
+     "rc = orc_actnorm_backward(tu + n, g, sl + (long)u * C, gt,", 0),
     ("backward weight gradient reads the mirrored tap",
      "x[n * img + ci * plane + (long)ii * W + jj];",
      "x[n * img + ci * plane + (long)(H - 1 - ii) * W + jj];", 0),

@@ -358,6 +358,51 @@ def scaling_sweep(dev) -> dict:
             "rows": rows}
 
 
+def stack_training(dev) -> dict:
+    """One training step of the sampling stack's model (3 levels x 8 units
+    with actnorm, 12 x 32 x 32, batch 64): the forward to latents and
+    log|det|, the batch's negative log-likelihood, and the backward of the
+    summed NLL to every weight, scale and bias (the forward is run again
+    inside it); by the paper's protocol (11 runs, the first dropped)."""
+    import numpy as np
+    import torch
+
+    from paper_2301_09266_amd import finc, synth
+
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    spec = synth.WORKLOADS["stack_3x8_c12_32x32_b64_k3"]
+    B, C1, H1, W1, L, U, k = (spec[n] for n in ("B", "C1", "H1", "W1", "levels", "units", "k"))
+    c = synth.stack_case(B=B, C1=C1, H1=H1, W1=W1, levels=L, units=U, k=k)
+    x = d(c["x"][:, :C1, :H1, :W1])
+    Kf = d(np.concatenate([np.ravel(a) for a in c["K"]]))
+    sf = d(np.concatenate([np.ravel(a) for a in c["scale"]]))
+    bf = d(np.concatenate([np.ravel(a) for a in c["bias"]]))
+    ws = torch.empty(finc.lib().finc_stack_train_workspace_bytes(B, L, U, C1, H1, W1, k),
+                     dtype=torch.uint8, device=dev)
+    state = {}
+
+    def fwd():
+        state["z"], state["ld"] = finc.stack_forward(x, Kf, sf, bf, L, U, k, workspace=ws)
+
+    def nll():
+        state["nll"], state["bpd"] = finc.gauss_nll(state["z"], state["ld"])
+
+    def bwd():
+        finc.stack_backward(x, state["z"], Kf, sf, bf, L, U, k, gld=-float(B), workspace=ws)
+
+    fwd(), nll(), bwd()
+    torch.cuda.synchronize()
+    out = {"workload": "stack_3x8_c12_32x32_b64_k3", "B": B}
+    for name, fn in (("forward", fwd), ("nll", nll), ("backward", bwd)):
+        out[name] = protocol_runs(lambda: event_ms(fn))
+    step = sum(out[n]["mean_ms"] for n in ("forward", "nll", "backward"))
+    out["step_ms"] = step
+    out["images_per_s"] = B / (step * 1e-3)
+    out["note"] = ("untrained random weights (the latents grow to ~1e9 through 24 units): the "
+                   "NLL value is not a model quality figure")
+    return out
+
+
 def banded_layers(dev) -> list:
     """Single layers beyond one workgroup (banded stream form): 12 x 128 x 128
     and 16 x 256 x 64 at k = 3, batch 8, weights prepared inside the call."""
@@ -734,6 +779,7 @@ def main():
         out["per_config"] = per_config(dev)
         out["scaling_sweep"] = scaling_sweep(dev)
         out["banded_layers"] = banded_layers(dev)
+        out["stack_training"] = stack_training(dev)
         out["batch_scaling"] = batch_scaling(dev)
     if not args.no_configs:
         out["step_cost"] = step_cost(dev)

@@ -336,6 +336,37 @@ int finc_actnorm_backward(const float *x, const float *dy, const float *s, float
                           float *ds, float *db, double gld, int B, int C, int H, int W,
                           void *workspace, hipStream_t stream);
 
+/* Training direction of the multi-scale stack (the stack of
+ * finc_stack_inverse, its layout of K, scale and bias): the forward maps
+ * images to latents -- per level U x [unit, actnorm], then below the top the
+ * split (second half: the level's latent) and the squeeze of the first half
+ * (Sec. 4.4, Fig. 2c) -- and its backward gives the gradients of a loss L
+ * with respect to the input and every parameter, from the latents'
+ * gradients dz[l] = dL/dz[l], plus gld times the gradient of the stack's
+ * log|det| of one image (gld = -B for the log|det| part of a batch's summed
+ * negative log-likelihood, whose latent gradients are dz = z).
+ * finc_stack_forward: x device (B, C1, H1, W1); z host array of L device
+ *   pointers shaped as for finc_stack_inverse (written); logdet: NULL or
+ *   device doubles, B, each the stack's log|det| (every block's and every
+ *   actnorm's; the same for every image).
+ * finc_stack_backward: dz as z (read); dx (B, C1, H1, W1), dK, dscale, dbias
+ *   in the layouts of x, K, scale and bias (written; any may be NULL, and
+ *   the masked weights' gradients are 0).  The forward is run again inside
+ *   the call to recompute the activations.
+ * workspace: device, >= finc_stack_train_workspace_bytes(B, L, U, C1, H1, W1,
+ *   k) bytes, 256-byte aligned, overwritten.  Requirements as for
+ *   finc_stack_inverse, and the units' forward supported at every level
+ *   (finc_forward_plan).  Outputs overlapping any input, the workspace or
+ *   each other: FINC_EINVAL.  Deterministic (fixed summation orders). */
+size_t finc_stack_train_workspace_bytes(int B, int L, int U, int C1, int H1, int W1, int k);
+int finc_stack_forward(const float *x, float *const *z, double *logdet, const float *K,
+                       const float *scale, const float *bias, int B, int L, int U, int C1,
+                       int H1, int W1, int k, void *workspace, hipStream_t stream);
+int finc_stack_backward(const float *x, const float *const *dz, const float *K,
+                        const float *scale, const float *bias, float *dx, float *dK,
+                        float *dscale, float *dbias, double gld, int B, int L, int U, int C1,
+                        int H1, int W1, int k, void *workspace, hipStream_t stream);
+
 /* Negative log-likelihood of each image under a standard normal latent
  * (Sec. 3, the log-probability equation negated) and its bits per dimension
  * (Sec. 5, BPD equation):

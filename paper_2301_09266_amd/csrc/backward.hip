@@ -29,6 +29,7 @@
 namespace {
 
 inline size_t up256b(size_t n) { return (n + 255) & ~(size_t)255; }
+inline size_t imax_sz(size_t a, size_t b) { return a > b ? a : b; }
 inline bool overlapb(const void *a, size_t na, const void *b, size_t nb) {
     const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
     return x < y + nb && y < x + na;
@@ -439,6 +440,216 @@ __global__ __launch_bounds__(256) void gauss_nll_kernel(NllArgs a) {
     }
 }
 
+
+// ---- the multi-scale stack's training direction ----------------------------
+// (B C H W < 2^31 values: int indices)
+
+// y = s[c] x + b[c] (actnorm forward).
+__global__ __launch_bounds__(256) void affine_kernel(const float *x, float *y, const float *s,
+                                                     const float *b, int n, Div d_HW, Div d_C,
+                                                     int C) {
+    for (int e = blockIdx.x * 256 + threadIdx.x; e < n; e += gridDim.x * 256) {
+        const int pl = divi(e, d_HW), c = pl - divi(pl, d_C) * C;
+        y[e] = s[c] * x[e] + b[c];
+    }
+}
+
+// Split and squeeze of a level's output h (B, C, H, W): channels [C/2, C)
+// go to the latent z (B, C/2, H, W); channel c < C/2 at (2 i + dy, 2 j + dx)
+// goes to channel 4 c + 2 dy + dx of the next level's input (B, 2C, H/2, W/2).
+__global__ __launch_bounds__(256) void split_squeeze_kernel(const float *h, float *nxt, float *z,
+                                                            int n, int C, int H, int W, Div d_HW,
+                                                            Div d_C, Div d_W) {
+    const int HW = H * W, Ch = C / 2;
+    for (int e = blockIdx.x * 256 + threadIdx.x; e < n; e += gridDim.x * 256) {
+        const int pl = divi(e, d_HW), p = e - pl * HW;
+        const int b = divi(pl, d_C), c = pl - b * C;
+        if (c >= Ch) {
+            z[(b * Ch + c - Ch) * HW + p] = h[e];
+        } else {
+            const int i = divi(p, d_W), j = p - i * W;
+            const int co = 4 * c + 2 * (i & 1) + (j & 1);
+            nxt[((b * 2 * C + co) * (H / 2) + (i >> 1)) * (W / 2) + (j >> 1)] = h[e];
+        }
+    }
+}
+
+// Its adjoint: the gradient of a level's output, g (B, C, H, W), from the
+// gradient of the next level's input gn (B, 2C, H/2, W/2) -- unsqueezed,
+// first half -- and the latent's gradient dz (B, C/2, H, W), second half.
+__global__ __launch_bounds__(256) void unsqueeze_concat_kernel(const float *gn, const float *dz,
+                                                               float *g, int n, int C, int H,
+                                                               int W, Div d_HW, Div d_C,
+                                                               Div d_W) {
+    const int HW = H * W, Ch = C / 2;
+    for (int e = blockIdx.x * 256 + threadIdx.x; e < n; e += gridDim.x * 256) {
+        const int pl = divi(e, d_HW), p = e - pl * HW;
+        const int b = divi(pl, d_C), c = pl - b * C;
+        if (c >= Ch) {
+            g[e] = dz[(b * Ch + c - Ch) * HW + p];
+        } else {
+            const int i = divi(p, d_W), j = p - i * W;
+            const int co = 4 * c + 2 * (i & 1) + (j & 1);
+            g[e] = gn[((b * 2 * C + co) * (H / 2) + (i >> 1)) * (W / 2) + (j >> 1)];
+        }
+    }
+}
+
+// The stack's log|det| for one image -- every block's H W sum_c
+// log|K[c][c][self]| and every actnorm's H W sum_c log|s_c| -- in fp64, each
+// thread's terms in order and a fixed tree; written for every image.
+__global__ __launch_bounds__(256) void stack_logdet_kernel(const float *K, const float *scale,
+                                                           int L, int U, int C1, int H1, int W1,
+                                                           int k, double *logdet, int B) {
+    __shared__ double red[256];
+    const int tid = threadIdx.x;
+    double acc = 0.0;
+    long long koff = 0, soff = 0;
+    for (int l = 0; l < L; ++l) {
+        const int C = C1 << l;
+        const double hw = (double)(H1 >> l) * (double)(W1 >> l);
+        const long long ksz = (long long)C * C * k * k;
+        // per unit: 4 C diagonal entries, then C scales
+        for (int t = tid; t < U * 5 * C; t += 256) {
+            const int u = t / (5 * C), r = t - u * 5 * C;
+            if (r < 4 * C) {
+                const int q = r / C, c = r - q * C;
+                const int oh = (q == 0 || q == 1) ? k - 1 : 0, ow = (q == 0 || q == 2) ? k - 1 : 0;
+                const float d = K[koff + (4ll * u + q) * ksz + ((long long)(c * C + c) * k + oh) * k + ow];
+                acc += hw * log(fabs((double)d));
+            } else {
+                acc += hw * log(fabs((double)scale[soff + (long long)u * C + (r - 4 * C)]));
+            }
+        }
+        koff += 4ll * U * ksz;
+        soff += (long long)U * C;
+    }
+    red[tid] = acc;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+        if (tid < h)
+            red[tid] += red[tid + h];
+        __syncthreads();
+    }
+    for (int b = tid; b < B; b += 256)
+        logdet[b] = red[0];
+}
+
+int ew_blocks(long long n) { return (int)(n / 256 + 1 < 4096 ? n / 256 + 1 : 4096); }
+
+struct StackShape {
+    int B, L, U, C1, H1, W1, k;
+    long long n0;   // values of a level-0 activation
+    int C(int l) const { return C1 << l; }
+    int H(int l) const { return H1 >> l; }
+    int W(int l) const { return W1 >> l; }
+    long long n(int l) const { return n0 >> l; }   // (C doubles, H W quarters)
+    long long koff(int l) const {
+        long long o = 0;
+        for (int m = 0; m < l; ++m)
+            o += 4ll * U * C(m) * C(m) * k * k;
+        return o;
+    }
+    long long soff(int l) const {
+        long long o = 0;
+        for (int m = 0; m < l; ++m)
+            o += (long long)U * C(m);
+        return o;
+    }
+    long long kfloats() const { return koff(L); }
+    long long sfloats() const { return soff(L); }
+};
+
+bool stack_shape_ok(const StackShape &s) {
+    if (s.B < 0 || s.L < 1 || s.L > 8 || s.U < 0 || s.C1 < 1 || s.H1 < 1 || s.W1 < 1 || s.k < 1 ||
+        s.k > FINC_MAX_K)
+        return false;
+    if (s.L > 1 && ((s.C1 & 1) || ((s.H1 | s.W1) & ((1 << (s.L - 1)) - 1))))
+        return false;
+    return (s.C1 << (s.L - 1)) <= FINC_MAX_C && s.n0 < (1ll << 31);
+}
+
+// Workspace of the stack's training calls: per level its 2 U + 1 activations
+// (unit inputs, unit outputs, the level's output), three level-0 gradient
+// buffers, and the unit and actnorm backward workspaces of the largest level.
+struct StackWs {
+    size_t acts, grads, unit_ws, an_ws, total;
+};
+StackWs stack_ws(const StackShape &s) {
+    StackWs w;
+    long long na = 0;
+    for (int l = 0; l < s.L; ++l)
+        na += (2ll * s.U + 1) * s.n(l);
+    w.acts = up256b((size_t)na * sizeof(float));
+    w.grads = 3 * up256b((size_t)s.n0 * sizeof(float));
+    w.unit_ws = 0;
+    w.an_ws = 0;
+    for (int l = 0; l < s.L; ++l) {
+        w.unit_ws = imax_sz(w.unit_ws, finc_unit_backward_workspace_bytes(s.B, s.C(l), s.H(l), s.W(l), s.k));
+        w.an_ws = imax_sz(w.an_ws, finc_actnorm_backward_workspace_bytes(s.B, s.C(l), s.H(l), s.W(l)));
+    }
+    w.unit_ws = up256b(w.unit_ws);
+    w.an_ws = up256b(w.an_ws);
+    w.total = w.acts + w.grads + w.unit_ws + w.an_ws;
+    return w;
+}
+
+// The forward direction, keeping every level's activations in acts (level l
+// at acts + aoff[l]: h_0 = the level's input, t_0, h_1, t_1, ..., h_U = its
+// output; t_u = unit(h_u), h_{u+1} = actnorm(t_u)); level 0's h_0 is x
+// itself and the top level's h_U is written to its latent z[L-1] directly.
+inline const float *stack_h(const float *x, const float *acts, const long long *aoff,
+                            const StackShape &s, int l, int u) {
+    return (l == 0 && u == 0) ? x : acts + aoff[l] + 2ll * u * s.n(l);
+}
+
+int stack_forward_keep(const float *x, float *const *z, const float *K, const float *scale,
+                       const float *bias, const StackShape &s, float *acts, long long *aoff,
+                       hipStream_t st) {
+    long long o = 0;
+    for (int l = 0; l < s.L; ++l) {
+        const int C = s.C(l), H = s.H(l), W = s.W(l);
+        const long long n = s.n(l), ksz = (long long)C * C * s.k * s.k;
+        aoff[l] = o;
+        o += (2ll * s.U + 1) * n;
+        const bool top = l == s.L - 1;
+        for (int u = 0; u < s.U; ++u) {
+            const float *hu = stack_h(x, acts, aoff, s, l, u);
+            float *tu = acts + aoff[l] + (2ll * u + 1) * n;
+            float *nx = (top && u == s.U - 1) ? z[l] : tu + n;
+            int rc = finc_unit_forward(hu, tu, K + s.koff(l) + 4ll * u * ksz, nullptr, nullptr,
+                                       s.B, C, H, W, s.k, st);
+            if (rc != FINC_OK)
+                return rc;
+            if (s.B > 0) {
+                hipLaunchKernelGGL(affine_kernel, dim3(ew_blocks(n)), dim3(256), 0, st, tu, nx,
+                                   scale + s.soff(l) + (long long)u * C,
+                                   bias + s.soff(l) + (long long)u * C, (int)n, make_div(H * W),
+                                   make_div(C), C);
+                rc = conv_launched();
+                if (rc != FINC_OK)
+                    return rc;
+            }
+        }
+        if (s.B == 0)
+            continue;
+        const float *hout = stack_h(x, acts, aoff, s, l, s.U);
+        if (top) {
+            if (s.U == 0 && hipMemcpyAsync(z[l], hout, (size_t)n * sizeof(float),
+                                           hipMemcpyDeviceToDevice, st) != hipSuccess)
+                return FINC_EHIP;
+        } else {
+            hipLaunchKernelGGL(split_squeeze_kernel, dim3(ew_blocks(n)), dim3(256), 0, st, hout,
+                               acts + o, z[l], (int)n, C, H, W, make_div(H * W), make_div(C),
+                               make_div(W));
+            const int rc = conv_launched();
+            if (rc != FINC_OK)
+                return rc;
+        }
+    }
+    return FINC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -643,6 +854,163 @@ int finc_gauss_nll(const float *const *z, const long long *n, int L, int B, cons
         return FINC_OK;
     hipLaunchKernelGGL(gauss_nll_kernel, dim3(B), dim3(256), 0, stream, a);
     return conv_launched();
+}
+
+
+// ---- the multi-scale stack's training direction ------------------------------
+
+size_t finc_stack_train_workspace_bytes(int B, int L, int U, int C1, int H1, int W1, int k) {
+    StackShape s{B, L, U, C1, H1, W1, k, (long long)B * C1 * H1 * W1};
+    if (!stack_shape_ok(s))
+        return 0;
+    return stack_ws(s).total;
+}
+
+static bool stack_buffers_ok(const StackShape &s, const float *x, const float *const *z,
+                             const float *K, const float *scale, const float *bias,
+                             void *workspace, const void *const *outs, const size_t *outsz,
+                             int nouts) {
+    if ((s.B > 0 && !x) || !z || !K || !scale || !bias || !workspace ||
+        ((uintptr_t)workspace & 255u))
+        return false;
+    const size_t wsb = stack_ws(s).total;
+    const size_t xb = (size_t)s.n0 * sizeof(float);
+    const void *ins[4] = {x, K, scale, bias};
+    const size_t insz[4] = {xb, (size_t)s.kfloats() * sizeof(float),
+                            (size_t)s.sfloats() * sizeof(float),
+                            (size_t)s.sfloats() * sizeof(float)};
+    for (int l = 0; l < s.L; ++l)
+        if (s.B > 0 && !z[l])
+            return false;
+    for (int i = 0; i < 4; ++i)
+        if (overlapb(workspace, wsb, ins[i], insz[i]))
+            return false;
+    for (int o = 0; o < nouts; ++o) {
+        if (!outs[o])
+            continue;
+        if (overlapb(outs[o], outsz[o], workspace, wsb))
+            return false;
+        for (int i = 0; i < 4; ++i)
+            if (overlapb(outs[o], outsz[o], ins[i], insz[i]))
+                return false;
+        for (int o2 = o + 1; o2 < nouts; ++o2)
+            if (outs[o2] && overlapb(outs[o], outsz[o], outs[o2], outsz[o2]))
+                return false;
+    }
+    return true;
+}
+
+int finc_stack_forward(const float *x, float *const *z, double *logdet, const float *K,
+                       const float *scale, const float *bias, int B, int L, int U, int C1,
+                       int H1, int W1, int k, void *workspace, hipStream_t stream) {
+    StackShape s{B, L, U, C1, H1, W1, k, (long long)B * C1 * H1 * W1};
+    if (!stack_shape_ok(s) || !z)
+        return FINC_EINVAL;
+    const void *outs[10];
+    size_t outsz[10];
+    int no = 0;
+    for (int l = 0; l < L; ++l) {
+        outs[no] = z[l];
+        outsz[no++] = (size_t)(l == L - 1 ? s.n(l) : s.n(l) / 2) * sizeof(float);
+    }
+    outs[no] = logdet;
+    outsz[no++] = (size_t)B * sizeof(double);
+    if (!stack_buffers_ok(s, x, (const float *const *)z, K, scale, bias, workspace, outs, outsz,
+                          no))
+        return FINC_EINVAL;
+    long long aoff[8];
+    int rc = stack_forward_keep(x, z, K, scale, bias, s, (float *)workspace, aoff, stream);
+    if (rc != FINC_OK || !logdet || B == 0)
+        return rc;
+    hipLaunchKernelGGL(stack_logdet_kernel, dim3(1), dim3(256), 0, stream, K, scale, L, U, C1,
+                       H1, W1, k, logdet, B);
+    return conv_launched();
+}
+
+int finc_stack_backward(const float *x, const float *const *dz, const float *K,
+                        const float *scale, const float *bias, float *dx, float *dK,
+                        float *dscale, float *dbias, double gld, int B, int L, int U, int C1,
+                        int H1, int W1, int k, void *workspace, hipStream_t stream) {
+    StackShape s{B, L, U, C1, H1, W1, k, (long long)B * C1 * H1 * W1};
+    if (!stack_shape_ok(s) || !dz)
+        return FINC_EINVAL;
+    const void *outs[4] = {dx, dK, dscale, dbias};
+    const size_t outsz[4] = {(size_t)s.n0 * sizeof(float), (size_t)s.kfloats() * sizeof(float),
+                             (size_t)s.sfloats() * sizeof(float),
+                             (size_t)s.sfloats() * sizeof(float)};
+    if (!stack_buffers_ok(s, x, dz, K, scale, bias, workspace, outs, outsz, 4))
+        return FINC_EINVAL;
+    for (int l = 0; l < L; ++l) {   // the latents' gradients are inputs too
+        const size_t zb = (size_t)(l == L - 1 ? s.n(l) : s.n(l) / 2) * sizeof(float);
+        for (int o = 0; o < 4; ++o)
+            if (outs[o] && overlapb(outs[o], outsz[o], dz[l], zb))
+                return FINC_EINVAL;
+        if (overlapb(workspace, stack_ws(s).total, dz[l], zb))
+            return FINC_EINVAL;
+    }
+    const StackWs w = stack_ws(s);
+    char *base = (char *)workspace;
+    float *acts = (float *)base;
+    float *gbuf[3];
+    for (int i = 0; i < 3; ++i)
+        gbuf[i] = (float *)(base + w.acts + i * up256b((size_t)s.n0 * sizeof(float)));
+    void *unit_ws = base + w.acts + w.grads, *an_ws = base + w.acts + w.grads + w.unit_ws;
+    // the forward again, keeping its activations (the latents it writes go to
+    // a gradient buffer, unused until the forward is done)
+    float *zscratch[8];
+    for (int l = 0; l < L; ++l)
+        zscratch[l] = gbuf[2];
+    long long aoff[8];
+    int rc = stack_forward_keep(x, zscratch, K, scale, bias, s, acts, aoff, stream);
+    if (rc != FINC_OK)
+        return rc;
+    // gin: the gradient of the activation reached so far (the top latent's
+    // gradient first); results alternate between two buffers, the input's
+    // gradient goes to dx
+    float *buf[2] = {gbuf[0], gbuf[2]}, *gt = gbuf[1];
+    int cur = 0;
+    const float *gin = dz[L - 1];
+    for (int l = L - 1; l >= 0; --l) {
+        const int C = s.C(l), H = s.H(l), W = s.W(l);
+        const long long n = s.n(l), ksz = (long long)C * C * k * k;
+        if (l < L - 1 && B > 0) {   // gin: the next level's input gradient
+            float *o = buf[cur];
+            cur ^= 1;
+            hipLaunchKernelGGL(unsqueeze_concat_kernel, dim3(ew_blocks(n)), dim3(256), 0, stream,
+                               gin, dz[l], o, (int)n, C, H, W, make_div(H * W), make_div(C),
+                               make_div(W));
+            rc = conv_launched();
+            if (rc != FINC_OK)
+                return rc;
+            gin = o;
+        }
+        for (int u = U - 1; u >= 0; --u) {
+            const float *hu = stack_h(x, acts, aoff, s, l, u);
+            const float *tu = acts + aoff[l] + (2ll * u + 1) * n;
+            const long long so = s.soff(l) + (long long)u * C;
+            rc = finc_actnorm_backward(tu, gin, scale + so, gt, dscale ? dscale + so : nullptr,
+                                       dbias ? dbias + so : nullptr, gld, B, C, H, W, an_ws,
+                                       stream);
+            if (rc != FINC_OK)
+                return rc;
+            const bool last = l == 0 && u == 0;
+            float *o = last ? dx : buf[cur];
+            if (!last)
+                cur ^= 1;
+            rc = finc_unit_backward(hu, gt, K + s.koff(l) + 4ll * u * ksz, o,
+                                    dK ? dK + s.koff(l) + 4ll * u * ksz : nullptr, gld, B, C, H,
+                                    W, k, unit_ws, stream);
+            if (rc != FINC_OK)
+                return rc;
+            gin = o;
+        }
+    }
+    // (no unit at level 0: the input's gradient is the level's)
+    if (dx && U == 0 && B > 0 &&
+        hipMemcpyAsync(dx, gin, (size_t)s.n0 * sizeof(float), hipMemcpyDeviceToDevice, stream) !=
+            hipSuccess)
+        return FINC_EHIP;
+    return FINC_OK;
 }
 
 }  // extern "C"

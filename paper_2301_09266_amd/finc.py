@@ -55,6 +55,11 @@ SIGNATURES = {
                                    _i, _vp, _vp]),
     "finc_gauss_nll": (_i, [ctypes.POINTER(_vp), ctypes.POINTER(ctypes.c_longlong), _i, _i, _vp,
                             _vp, _vp, _vp]),
+    "finc_stack_train_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
+    "finc_stack_forward": (_i, [_vp, ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _i, _i, _i, _i,
+                                _i, _i, _i, _vp, _vp]),
+    "finc_stack_backward": (_i, [_vp, ctypes.POINTER(_vp), _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                 ctypes.c_double, _i, _i, _i, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_forward": (_i, [_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "finc_unit_logdet": (_i, [_vp, _i, _i, _i, _i, _vp, _vp]),
     "finc_unit_inverse": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp, _vp]),
@@ -433,6 +438,52 @@ def actnorm_backward(x, dy, s, gld: float = 0.0, workspace=None):
                                    float(gld), B, C, H, W, _ptr(ws), _stream()),
            "finc_actnorm_backward")
     return dx, ds, db
+
+
+def _stack_latents(B, L_levels, C1, H1, W1, device):
+    return [torch.empty((B, (C1 << l) if l == L_levels - 1 else (C1 << l) // 2, H1 >> l, W1 >> l),
+                        device=device) for l in range(L_levels)]
+
+
+def stack_forward(x, K, scale, bias, L_levels: int, U: int, k: int, workspace=None):
+    """(latents, logdet) of the stack's forward direction (finc_stack_forward);
+    K, scale, bias flat in the stack's layout."""
+    L = _require_lib()
+    _dev(x, "x")
+    B, C1, H1, W1 = x.shape
+    _stack_params(L_levels, U, C1, k, scale, bias, K)
+    z = _stack_latents(B, L_levels, C1, H1, W1, x.device)
+    zp = (ctypes.c_void_p * L_levels)(*[t.data_ptr() for t in z])
+    ld = torch.empty(B, dtype=torch.float64, device=x.device)
+    nbytes = int(L.finc_stack_train_workspace_bytes(B, L_levels, U, C1, H1, W1, k))
+    if nbytes == 0:
+        raise FincError(EINVAL, "finc_stack_forward")
+    ws = _workspace(nbytes, x.device, workspace)
+    _check(L.finc_stack_forward(_ptr(x), zp, _ptr(ld), _ptr(K), _ptr(scale), _ptr(bias), B,
+                                L_levels, U, C1, H1, W1, k, _ptr(ws), _stream()),
+           "finc_stack_forward")
+    return z, ld
+
+
+def stack_backward(x, dz, K, scale, bias, L_levels: int, U: int, k: int, gld: float = 0.0,
+                   want_dx: bool = True, workspace=None):
+    """(dx, dK, dscale, dbias) of the stack's forward direction for latent
+    gradients dz (finc_stack_backward); dx is None when not wanted."""
+    L = _require_lib()
+    _dev(x, "x")
+    B, C1, H1, W1 = x.shape
+    _stack_params(L_levels, U, C1, k, scale, bias, K)
+    zp = _stack_args(dz, L_levels, C1, H1, W1)
+    dx = torch.empty_like(x) if want_dx else None
+    dK, ds, db = torch.empty_like(K), torch.empty_like(scale), torch.empty_like(bias)
+    nbytes = int(L.finc_stack_train_workspace_bytes(B, L_levels, U, C1, H1, W1, k))
+    if nbytes == 0:
+        raise FincError(EINVAL, "finc_stack_backward")
+    ws = _workspace(nbytes, x.device, workspace)
+    _check(L.finc_stack_backward(_ptr(x), zp, _ptr(K), _ptr(scale), _ptr(bias), _ptr(dx),
+                                 _ptr(dK), _ptr(ds), _ptr(db), float(gld), B, L_levels, U, C1,
+                                 H1, W1, k, _ptr(ws), _stream()), "finc_stack_backward")
+    return dx, dK, ds, db
 
 
 def gauss_nll(zs, logdet):

@@ -353,3 +353,25 @@ def test_banded_rejects():
                                         None) == finc.EUNSUPPORTED
     assert lib.finc_unit_inverse_banded(FAKE, FAKE2, FAKE3, 1, 2, 64, 64, 3,
                                         ctypes.c_void_p(0x1100000 - 256), None) == finc.EINVAL
+
+
+def test_stack_train_rejects():
+    lib = finc.lib()
+    ws = ctypes.c_void_p(0x40000000)
+    z = (ctypes.c_void_p * 2)(0x2000000, 0x3000000)
+    K, S, Bb = ctypes.c_void_p(0x5000000), ctypes.c_void_p(0x6000000), ctypes.c_void_p(0x6100000)
+    args = (FAKE, z, NULL, K, S, Bb)
+    assert lib.finc_stack_train_workspace_bytes(2, 2, 2, 3, 16, 16, 3) == 0        # odd C1
+    assert lib.finc_stack_train_workspace_bytes(2, 2, 2, 4, 15, 16, 3) == 0        # odd H1
+    assert lib.finc_stack_train_workspace_bytes(2, 2, 2, 48, 16, 16, 3) == 0       # 96 > 64
+    assert lib.finc_stack_train_workspace_bytes(2, 2, 2, 4, 16, 16, 3) > 0
+    assert lib.finc_stack_forward(*args, 2, 2, 2, 4, 16, 16, 3, NULL, None) == finc.EINVAL
+    assert lib.finc_stack_forward(*args, 2, 2, 2, 4, 16, 16, 3, ctypes.c_void_p(0x40000010),
+                                  None) == finc.EINVAL
+    zbad = (ctypes.c_void_p * 2)(0x100000 + 64, 0x3000000)                        # z over x
+    assert lib.finc_stack_forward(FAKE, zbad, NULL, K, S, Bb, 2, 2, 2, 4, 16, 16, 3, ws,
+                                  None) == finc.EINVAL
+    assert lib.finc_stack_backward(FAKE, z, K, S, Bb, NULL, S, NULL, NULL, 0.0, 2, 2, 2, 4, 16,
+                                   16, 3, ws, None) == finc.EINVAL                 # dK over scale
+    assert lib.finc_stack_backward(FAKE, z, K, S, Bb, NULL, NULL, NULL, NULL, 0.0, 2, 2, 2, 4, 16,
+                                   16, 3, ctypes.c_void_p(0x2000000 - 256), None) == finc.EINVAL

@@ -159,3 +159,78 @@ def test_gauss_nll(orc, B):
     g_nll, g_bpd = nll.cpu().numpy(), bpd.cpu().numpy()
     assert np.max(np.abs(g_nll - want_nll) / np.abs(want_nll)) < 1e-12
     assert np.max(np.abs(g_bpd - want_bpd) / np.abs(want_bpd)) < 1e-12
+
+
+def _stack_flat(c):
+    return (np.concatenate([np.ravel(a) for a in c["K"]]),
+            np.concatenate([np.ravel(a) for a in c["scale"]]),
+            np.concatenate([np.ravel(a) for a in c["bias"]]))
+
+
+STACK_CASES = [
+    # (B, C1, H1, W1, levels, units, k)
+    (2, 4, 16, 16, 2, 2, 3), (3, 2, 8, 12, 3, 1, 2), (1, 6, 8, 8, 1, 3, 3),
+    (4, 12, 32, 32, 3, 8, 3),   # the sampling stack's shape (4 images)
+]
+
+
+@pytest.mark.parametrize("case", STACK_CASES, ids=lambda c: "x".join(map(str, c)))
+def test_stack_training_step(orc, case):
+    """One training step of the multi-scale stack: the forward's latents and
+    log|det| against the oracle; the batch's NLL; and the gradients of the
+    summed NLL (latent gradients z, gld = -B) of the input, the blocks'
+    weights, the actnorms' scales and biases against the oracle's backward of
+    the same latents.  Weight, scale and bias gradients sum over the batch
+    and, through the chain, over many paths: each is held to 1e-4 of
+    max(1, |oracle|, the largest |oracle| of its parameter block), the scale
+    of the rounding of sums that cancel (the terms' own sizes are not
+    available through the chain).  The 24-unit stack with random weights
+    grows its latents to |z| ~ 1e5 (level 1) and 1e9 (level 2), and fp32
+    rounding there is set by those magnitudes: as for its inverse, every
+    tensor is held to max |gpu - oracle| <= 1e-4 max(1, max |oracle|)."""
+    B, C1, H1, W1, L, U, k = case
+    print(f"stack training step {case}", flush=True)
+    c = synth.stack_case(B=B, C1=C1, H1=H1, W1=W1, levels=L, units=U, k=k)
+    x = c["x"][:, :C1, :H1, :W1]
+    # the parameters as the GPU sees them (fp32), for both sides
+    c = dict(c, K=[f64(a) for a in c["K"]], scale=[f64(a) for a in c["scale"]],
+             bias=[f64(a) for a in c["bias"]])
+    Kf, sf, bf = _stack_flat(c)
+    deep = L * U >= 8
+
+    def check(g, r, what, scale=None):
+        if deep:
+            err = float(np.max(np.abs(g - r)))
+            assert err <= 1e-4 * max(1.0, float(np.max(np.abs(r)))), (what, err)
+        else:
+            assert_close(g, r, what, scale=scale)
+
+    z, ld = finc.stack_forward(dev(x), dev(Kf), dev(sf), dev(bf), L, U, k)
+    want_z = orc.stack_forward(f64(x), c["K"], c["scale"], c["bias"], levels=L, units=U, k=k)
+    for l in range(L):
+        check(host(z[l]), want_z[l], f"stack forward latent {l} {case}")
+    want_ld = orc.stack_logdet(c["K"], c["scale"], levels=L, units=U, C1=C1, H1=H1, W1=W1, k=k)
+    assert np.allclose(ld.cpu().numpy(), want_ld, rtol=1e-9, atol=1e-9), (ld, want_ld)
+    nll, bpd = finc.gauss_nll(z, ld)
+    want_nll, _ = orc.gauss_nll([host(t) for t in z], np.full(B, want_ld))
+    assert np.max(np.abs(nll.cpu().numpy() - want_nll) / np.abs(want_nll)) < 1e-9
+    dx, dK, ds, db = finc.stack_backward(dev(x), z, dev(Kf), dev(sf), dev(bf), L, U, k,
+                                         gld=-float(B))
+    wx, wK, ws_, wb = orc.stack_backward(f64(x), [host(t) for t in z], c["K"], c["scale"],
+                                         c["bias"], levels=L, units=U, k=k, gld=-float(B))
+    check(host(dx), wx, f"stack backward dx {case}")
+    # per parameter block (a unit's weights, an actnorm's scale or bias): the
+    # block's largest magnitude sets the scale of its sums' rounding
+    blocks = []
+    o = 0
+    for l in range(L):
+        n = 4 * (C1 << l) ** 2 * k * k
+        for u in range(U):
+            blocks.append((o, o + n))
+            o += n
+    scale_K = np.concatenate([np.full(e - b0, np.abs(wK[b0:e]).max()) for b0, e in blocks])
+    check(host(dK), wK, f"stack backward dK {case}", scale=scale_K)
+    check(host(ds), ws_, f"stack backward dscale {case}", scale=np.abs(ws_).max())
+    check(host(db), wb, f"stack backward dbias {case}", scale=np.abs(wb).max())
+    again = finc.stack_backward(dev(x), z, dev(Kf), dev(sf), dev(bf), L, U, k, gld=-float(B))
+    assert all(torch.equal(a, b) for a, b in zip((dx, dK, ds, db), again))

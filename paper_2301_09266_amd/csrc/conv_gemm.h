@@ -82,6 +82,10 @@ struct ConvArgs {
     // output channel (co > ci here): the input gradient's weights of a
     // masked convolution with kernel M.
     int flip, fself;
+    // trows (R = 1 launches; 0 = off): Wt is a 3 x 3 kernel M (trows, K, 3, 3)
+    // read with the taps as rows, W[t trows + c][k] = M[c][k][t]: the GEMM
+    // whose nine row blocks, shifted and added, give M's convolution
+    int trows;
 };
 
 constexpr int kConvThreads = 256;
@@ -132,17 +136,24 @@ __device__ __forceinline__ void conv_tile(const ConvArgs &a, int bx, int by, int
             const int col = idx >> 4, kk = k0 + 4 * (idx & 15);
             const int co = co0 + col;
             const float *w = a.Wt + (long long)(co < a.Co ? co : 0) * a.K;
+            long long trow = 0;   // (trows) M's row c and tap t of row co
+            int ttap = 0;
+            if (a.trows) {
+                const int cc = co < a.Co ? co : 0;
+                ttap = cc / a.trows;
+                trow = (long long)(cc - ttap * a.trows) * a.K;
+            }
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 bool ok = co < a.Co && kk + e < a.K;
-                long long off = kk + e;
+                long long off = a.trows ? (trow + kk + e) * 9 + ttap : kk + e;
                 if (a.flip) {   // M[ci][co][R^2 - 1 - t], t = a R + c
                     const int ci = (int)((unsigned)(kk + e) / (R * R));
                     const int t = R * R - 1 - (kk + e - ci * R * R);
                     off = ((long long)ci * a.Co + co) * (R * R) + t;
                     ok = ok && !(t == a.fself && co > ci);
                 }
-                const float v = (a.flip ? a.Wt : w)[ok ? off : 0];
+                const float v = (a.flip || a.trows ? a.Wt : w)[ok ? off : 0];
                 ra[u][e] = ok ? v : 0.0f;
             }
         }
@@ -289,6 +300,33 @@ constexpr int kMaxParts = 8;
 // covers the chip: the number of parts depends on K only (not on the batch)
 // and the parts are added in order, so results stay deterministic and
 // independent of B.  partial: kMaxParts Co B H W floats, or null (no split).
+// The shifted sum of the nine row blocks of a tap-rows GEMM Z (B, 9 C, H, W):
+// y[b][c][i][j] = (bias[c] + sum over taps t = 3 a + d, in order, of
+// Z[b][t C + c][i + a - 1][j + d - 1], zero outside) * exp(3 ls[c]).
+__global__ __launch_bounds__(256) void shift_add_kernel(const float *Z, float *y, long long ys,
+                                                        const float *bias, const float *ls,
+                                                        int B, int C, int H, int W, Div d_HW,
+                                                        Div d_W, Div d_C) {
+    const int HW = H * W, n = B * C * HW;
+    for (int e = blockIdx.x * 256 + threadIdx.x; e < n; e += gridDim.x * 256) {
+        const int pl = divi(e, d_HW), p = e - pl * HW;
+        const int b = divi(pl, d_C), c = pl - b * C;
+        const int i = divi(p, d_W), j = p - i * W;
+        const float *zb = Z + (long long)b * 9 * C * HW;
+        float v = 0.0f;
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+            const int ii = i + t / 3 - 1, jj = j + t % 3 - 1;
+            if (ii >= 0 && ii < H && jj >= 0 && jj < W)
+                v += zb[(long long)(t * C + c) * HW + ii * W + jj];
+        }
+        v += bias ? bias[c] : 0.0f;
+        if (ls)
+            v *= expf(3.0f * ls[c]);
+        y[(long long)b * ys + (long long)c * HW + p] = v;
+    }
+}
+
 template <int R>
 int launch_conv_r(const float *x, long long xs, float *y, long long ys, const float *Wt,
                   const float *bias, const float *ls, int relu, int B, int Ci, int Co, int H, int W,

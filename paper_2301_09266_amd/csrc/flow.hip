@@ -319,6 +319,44 @@ int launch_conv(const float *x, long long xs, float *y, long long ys, const floa
                             partial);
 }
 
+// A 3 x 3 "same" convolution with few output channels (9 C >= 64) and a
+// long K: the nine taps' 1 x 1 products as one GEMM with 9 C rows and no
+// gather (Z = W_t x for every tap t, in Z (B, 9 C, H, W)), then their
+// shifted sum with the bias and exp(3 ls) scale.  Z: 9 B C H W floats.
+int launch_conv_taps(const float *x, long long xs, float *y, long long ys, const float *Wt,
+                     const float *bias, const float *ls, int B, int Ci, int C, int H, int W,
+                     hipStream_t st, float *Z) {
+    if (B == 0)
+        return FINC_OK;
+    ConvArgs a;
+    memset(&a, 0, sizeof(a));
+    a.x = x;
+    a.y = Z;
+    a.Wt = Wt;
+    a.B = B;
+    a.Ci = Ci;
+    a.Co = 9 * C;
+    a.H = H;
+    a.W = W;
+    a.K = Ci;
+    a.xs = xs;
+    a.ys = (long long)9 * C * H * W;
+    a.d_HW = make_div(H * W);
+    a.d_W = make_div(W);
+    a.trows = C;
+    const long long Q = (long long)B * H * W;
+    const dim3 grid(cdiv(Q, 64), cdiv(9 * C, 64));
+    hipLaunchKernelGGL((conv_kernel<1, 4, 4>), grid, dim3(kConvThreads), 0, st, a);
+    int rc = launched();
+    if (rc != FINC_OK)
+        return rc;
+    const long long n = (long long)B * C * H * W;
+    hipLaunchKernelGGL(shift_add_kernel, dim3((unsigned)(n / 256 + 1 < 8192 ? n / 256 + 1 : 8192)),
+                       dim3(256), 0, st, Z, y, ys, bias, ls, B, C, H, W, make_div(H * W),
+                       make_div(W), make_div(C));
+    return launched();
+}
+
 // Offsets (floats) of one Step's parameters.
 struct StepLayout {
     int C, q, Ch, k, hid;
@@ -401,14 +439,16 @@ int launch_squeeze(const float *in, float *out, int B, int C, int H, int W, long
 
 // Scratch of a Step at (B, C, H, W): u (B C HW), hh (B C HW), t1, t2
 // (B hid HW each), the partial sums of the coupling's last convolution
-// (kMaxParts B C HW), floats, each 256-byte aligned.
+// (kMaxParts B C HW) or its nine taps' products (9 B C HW), floats, each
+// 256-byte aligned.
 struct StepScratch {
     float *u, *hh, *t1, *t2, *part;
 };
 size_t step_scratch_bytes(int B, int C, int H, int W, int hid) {
     const size_t hw = (size_t)H * W;
+    const size_t parts = kMaxParts > 9 ? kMaxParts : 9;   // (K-split sums, or the taps' Z)
     return 2 * up256((size_t)B * C * hw * 4) + 2 * up256((size_t)B * hid * hw * 4) +
-           up256((size_t)kMaxParts * B * C * hw * 4);
+           up256(parts * B * C * hw * 4);
 }
 StepScratch carve(void *ws, int B, int C, int H, int W, int hid) {
     const size_t hw = (size_t)H * W;
@@ -435,10 +475,14 @@ int coupling_net(const float *v, long long vs, const float *sp, const StepLayout
     if (rc == FINC_OK)
         rc = launch_conv(s.t1, (long long)L.hid * hw, s.t2, (long long)L.hid * hw, sp + L.w2,
                          sp + L.b2, nullptr, 1, B, L.hid, L.hid, H, W, 1, st);
-    if (rc == FINC_OK)
-        rc = launch_conv(s.t2, (long long)L.hid * hw, s.hh, (long long)L.C * hw, sp + L.w3,
-                         sp + L.b3, sp + L.ls3, 0, B, L.hid, L.C, H, W, 3, st, s.part);
-    return rc;
+    if (rc != FINC_OK)
+        return rc;
+    if (9 * L.C >= 64 && L.hid >= 64)
+        return launch_conv_taps(s.t2, (long long)L.hid * hw, s.hh, (long long)L.C * hw,
+                                sp + L.w3, sp + L.b3, sp + L.ls3, B, L.hid, L.C, H, W, st,
+                                s.part);
+    return launch_conv(s.t2, (long long)L.hid * hw, s.hh, (long long)L.C * hw, sp + L.w3,
+                       sp + L.b3, sp + L.ls3, 0, B, L.hid, L.C, H, W, 3, st, s.part);
 }
 
 // Step forward in place on h (B, C, H, W; image stride C H W): unit, then

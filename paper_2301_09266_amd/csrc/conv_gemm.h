@@ -89,13 +89,22 @@ struct ConvArgs {
 };
 
 constexpr int kConvThreads = 256;
-constexpr int kKc = 64;     // k values staged at a time
-constexpr int kSK = 68;     // LDS row stride (floats)
+constexpr int kSK = 68;     // LDS row stride (floats) of 64-value k chunks
 
-// LDS floats of one block of the <WCO, NS> configuration.
+// k values staged at a time: 32 for the 64 c_out x 64 px tile (half the LDS
+// of 64, so twice the blocks a compute unit holds: 4-19% faster on the
+// flow's 1 x 1 GEMMs), 64 for the narrow tiles (a block's 16 weight rows
+// are staged by 256 threads a quad each).
+template <int WCO>
+constexpr int conv_kc() {
+    return WCO == 4 ? 32 : 64;
+}
+
+// LDS floats of one block of the <WCO, NS> configuration (rows of kc + 4
+// floats).
 template <int WCO, int NS>
 constexpr int conv_lds_floats() {
-    return (16 * WCO + 16 * NS * (4 / WCO)) * kSK;
+    return (16 * WCO + 16 * NS * (4 / WCO)) * (conv_kc<WCO>() + 4);
 }
 
 // One output tile (bx along pixels, by along c_out, bz the part of K) with
@@ -103,10 +112,12 @@ constexpr int conv_lds_floats() {
 template <int R, int WCO, int NS>
 __device__ __forceinline__ void conv_tile(const ConvArgs &a, int bx, int by, int bz, float *lds) {
     constexpr int BM = 16 * WCO, BN = 16 * NS * (4 / WCO);
+    constexpr int KC = conv_kc<WCO>(), SK = KC + 4, KQ = KC / 4;   // chunk, row stride, quads
     constexpr int TPP = kConvThreads / BN;   // threads per staged pixel
-    constexpr int QPT = 16 / TPP;            // k quads per thread (B)
-    constexpr int AQ = BM * 16 / kConvThreads;   // weight quads per thread
-    float *As = lds, *Bs = lds + BM * kSK;
+    constexpr int QPT = KQ / TPP;            // k quads per thread (B)
+    constexpr int AQ = BM * KQ / kConvThreads;   // weight quads per thread
+    static_assert(QPT >= 1 && AQ >= 1, "every thread stages whole quads");
+    float *As = lds, *Bs = lds + BM * SK;
     const int tid = threadIdx.x, lane = tid & 63, kq = lane >> 4, li = lane & 15;
     const int wave = tid >> 6, wco = wave % WCO, wpx = wave / WCO;
     const int co0 = by * BM;
@@ -133,7 +144,7 @@ __device__ __forceinline__ void conv_tile(const ConvArgs &a, int bx, int by, int
 #pragma unroll
         for (int u = 0; u < AQ; ++u) {
             const int idx = tid + u * kConvThreads;
-            const int col = idx >> 4, kk = k0 + 4 * (idx & 15);
+            const int col = idx / KQ, kk = k0 + 4 * (idx % KQ);
             const int co = co0 + col;
             const float *w = a.Wt + (long long)(co < a.Co ? co : 0) * a.K;
             long long trow = 0;   // (trows) M's row c and tap t of row co
@@ -177,12 +188,12 @@ __device__ __forceinline__ void conv_tile(const ConvArgs &a, int bx, int by, int
 #pragma unroll
         for (int u = 0; u < AQ; ++u) {
             const int idx = tid + u * kConvThreads;
-            *reinterpret_cast<float4 *>(&As[(idx >> 4) * kSK + 4 * (idx & 15)]) =
+            *reinterpret_cast<float4 *>(&As[(idx / KQ) * SK + 4 * (idx % KQ)]) =
                 make_float4(ra[u][0], ra[u][1], ra[u][2], ra[u][3]);
         }
 #pragma unroll
         for (int u = 0; u < QPT; ++u)
-            *reinterpret_cast<float4 *>(&Bs[spx * kSK + 4 * (sk0 + u * TPP)]) =
+            *reinterpret_cast<float4 *>(&Bs[spx * SK + 4 * (sk0 + u * TPP)]) =
                 make_float4(rb[u][0], rb[u][1], rb[u][2], rb[u][3]);
     };
 
@@ -190,23 +201,23 @@ __device__ __forceinline__ void conv_tile(const ConvArgs &a, int bx, int by, int
 #pragma unroll
     for (int s = 0; s < NS; ++s)
         acc[s] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-    const int nall = (a.K + kKc - 1) / kKc;
+    const int nall = (a.K + KC - 1) / KC;
     const int cbeg = a.partial ? bz * a.cps : 0;
     const int nchunk = a.partial ? min(a.cps, nall - cbeg) : nall;
-    load_chunk(cbeg * kKc);
+    load_chunk(cbeg * KC);
     store_chunk();
     __syncthreads();
-    const float *arow = &As[(wco * 16 + li) * kSK + 4 * kq];
-    const float *brow = &Bs[(wpx * 16 * NS + li) * kSK + 4 * kq];
+    const float *arow = &As[(wco * 16 + li) * SK + 4 * kq];
+    const float *brow = &Bs[(wpx * 16 * NS + li) * SK + 4 * kq];
     for (int c = 0; c < nchunk; ++c) {
         if (c + 1 < nchunk)
-            load_chunk((cbeg + c + 1) * kKc);   // in flight during the MFMAs
+            load_chunk((cbeg + c + 1) * KC);   // in flight during the MFMAs
 #pragma unroll
-        for (int blk = 0; blk < kKc / 16; ++blk) {
+        for (int blk = 0; blk < KC / 16; ++blk) {
             const float4 w4 = *reinterpret_cast<const float4 *>(arow + 16 * blk);
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-                const float4 b4 = *reinterpret_cast<const float4 *>(brow + 16 * s * kSK + 16 * blk);
+                const float4 b4 = *reinterpret_cast<const float4 *>(brow + 16 * s * SK + 16 * blk);
                 acc[s] = mfma4(w4.x, b4.x, acc[s]);
                 acc[s] = mfma4(w4.y, b4.y, acc[s]);
                 acc[s] = mfma4(w4.z, b4.z, acc[s]);
@@ -359,7 +370,7 @@ int launch_conv_r(const float *x, long long xs, float *y, long long ys, const fl
         hipLaunchKernelGGL((conv_kernel<R, 4, 4>), grid, dim3(kConvThreads), 0, st, a);
         return conv_launched();
     }
-    const int nchunk = cdiv(a.K, kKc);
+    const int nchunk = cdiv(a.K, conv_kc<1>());
     int parts = 1;
     if (partial)
         while (parts < kMaxParts && nchunk >= 16 * parts)

@@ -89,30 +89,33 @@ struct ConvArgs {
 };
 
 constexpr int kConvThreads = 256;
+constexpr long long kWideSmallGrid = 256;   // blocks: one per compute unit
 constexpr int kSK = 68;     // LDS row stride (floats) of 64-value k chunks
 
-// k values staged at a time: 32 for the 64 c_out x 64 px tile (half the LDS
-// of 64, so twice the blocks a compute unit holds: 4-19% faster on the
-// flow's 1 x 1 GEMMs), 64 for the narrow tiles (a block's 16 weight rows
-// are staged by 256 threads a quad each).
+// k values staged at a time (KC): by default 32 for the 64 c_out x 64 px
+// tile (half the LDS of 64, so twice the blocks a compute unit holds: 4-19%
+// faster on the flow's 1 x 1 GEMMs when the grid covers the chip), 64 for
+// the narrow tiles (a block's 16 weight rows are staged by 256 threads a
+// quad each).  Grids of fewer blocks than compute units take 64: there the
+// chunk loop's length, not occupancy, sets the time.
 template <int WCO>
 constexpr int conv_kc() {
     return WCO == 4 ? 32 : 64;
 }
 
-// LDS floats of one block of the <WCO, NS> configuration (rows of kc + 4
+// LDS floats of one block of the <WCO, NS, KC> configuration (rows of KC + 4
 // floats).
-template <int WCO, int NS>
+template <int WCO, int NS, int KC = conv_kc<WCO>()>
 constexpr int conv_lds_floats() {
-    return (16 * WCO + 16 * NS * (4 / WCO)) * (conv_kc<WCO>() + 4);
+    return (16 * WCO + 16 * NS * (4 / WCO)) * (KC + 4);
 }
 
 // One output tile (bx along pixels, by along c_out, bz the part of K) with
-// the block's LDS at lds (conv_lds_floats<WCO, NS>() floats, 16-byte aligned).
-template <int R, int WCO, int NS>
+// the block's LDS at lds (conv_lds_floats<WCO, NS, KC>() floats, 16-byte aligned).
+template <int R, int WCO, int NS, int KC = conv_kc<WCO>()>
 __device__ __forceinline__ void conv_tile(const ConvArgs &a, int bx, int by, int bz, float *lds) {
     constexpr int BM = 16 * WCO, BN = 16 * NS * (4 / WCO);
-    constexpr int KC = conv_kc<WCO>(), SK = KC + 4, KQ = KC / 4;   // chunk, row stride, quads
+    constexpr int SK = KC + 4, KQ = KC / 4;   // row stride, quads per chunk row
     constexpr int TPP = kConvThreads / BN;   // threads per staged pixel
     constexpr int QPT = KQ / TPP;            // k quads per thread (B)
     constexpr int AQ = BM * KQ / kConvThreads;   // weight quads per thread
@@ -273,10 +276,19 @@ __device__ __forceinline__ void conv_tile(const ConvArgs &a, int bx, int by, int
     }
 }
 
-template <int R, int WCO, int NS>
+template <int R, int WCO, int NS, int KC = conv_kc<WCO>()>
 __global__ __launch_bounds__(kConvThreads) void conv_kernel(ConvArgs a) {
-    __shared__ __attribute__((aligned(16))) float lds[conv_lds_floats<WCO, NS>()];
-    conv_tile<R, WCO, NS>(a, blockIdx.x, blockIdx.y, blockIdx.z, lds);
+    __shared__ __attribute__((aligned(16))) float lds[conv_lds_floats<WCO, NS, KC>()];
+    conv_tile<R, WCO, NS, KC>(a, blockIdx.x, blockIdx.y, blockIdx.z, lds);
+}
+
+// The 64 x 64 tile's launch, its chunk chosen by the grid's size.
+template <int R>
+void launch_wide(const ConvArgs &a, dim3 grid, hipStream_t st) {
+    if ((long long)grid.x * grid.y * grid.z < kWideSmallGrid)
+        hipLaunchKernelGGL((conv_kernel<R, 4, 4, 64>), grid, dim3(kConvThreads), 0, st, a);
+    else
+        hipLaunchKernelGGL((conv_kernel<R, 4, 4, 32>), grid, dim3(kConvThreads), 0, st, a);
 }
 
 // The parts of a K-split convolution added in order (part 0 first), then
@@ -367,7 +379,7 @@ int launch_conv_r(const float *x, long long xs, float *y, long long ys, const fl
     const long long Q = (long long)B * H * W;
     if (Co >= 64) {
         const dim3 grid(cdiv(Q, 64), cdiv(Co, 64));
-        hipLaunchKernelGGL((conv_kernel<R, 4, 4>), grid, dim3(kConvThreads), 0, st, a);
+        launch_wide<R>(a, grid, st);
         return conv_launched();
     }
     const int nchunk = cdiv(a.K, conv_kc<1>());

@@ -346,7 +346,7 @@ int launch_conv_taps(const float *x, long long xs, float *y, long long ys, const
     a.trows = C;
     const long long Q = (long long)B * H * W;
     const dim3 grid(cdiv(Q, 64), cdiv(9 * C, 64));
-    hipLaunchKernelGGL((conv_kernel<1, 4, 4>), grid, dim3(kConvThreads), 0, st, a);
+    launch_wide<1>(a, grid, st);
     int rc = launched();
     if (rc != FINC_OK)
         return rc;

@@ -23,6 +23,7 @@
 //    deterministic and independent of the batch size.
 
 #include <hip/hip_runtime.h>
+#include <cstddef>
 #include <mutex>
 #include <type_traits>
 
@@ -98,6 +99,23 @@ __host__ __device__ inline void tap_of(int t, int K, int &dp, int &dq) {
             dq = s - dp;
             return;
         }
+        n += cnt;
+    }
+}
+
+// tap_of for a tap number that differs across the lanes of a wave: the same
+// walk over the distances with a trip count that does not (K is uniform)
+// and selects in place of the early return, so the wave does not branch.
+__device__ inline void tap_of_lanes(int t, int K, int &dp, int &dq) {
+    dp = 0;
+    dq = 0;
+    int n = 0;
+    for (int s = 1; s <= 2 * (K - 1); ++s) {
+        const int lo = s - (K - 1) > 0 ? s - (K - 1) : 0, hi = s < K - 1 ? s : K - 1;
+        const int cnt = hi - lo + 1;
+        const bool here = t >= n && t < n + cnt;
+        dp = here ? lo + (t - n) : dp;
+        dq = here ? s - (lo + (t - n)) : dq;
         n += cnt;
     }
 }
@@ -385,6 +403,23 @@ __global__ __launch_bounds__(kWave) void logdet_kernel(const float *K, int n, in
 // ---------------------------------------------------------------------------
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// Threads of the workgroup: the 16-bit group size at byte 12 of the implicit
+// kernel arguments (code object v5), read with one scalar load.  Every launch
+// here is a whole number of workgroups, so no remainder case is needed; the
+// compiler's blockDim.x covers one with a 16-bit vector load, which would
+// wait behind every vector load issued before it (the image loads that go
+// out first thing).
+typedef __attribute__((address_space(4))) const unsigned *KernargU32;
+__device__ __forceinline__ int block_threads() {
+    const KernargU32 gs = (KernargU32)(
+        (__attribute__((address_space(4))) const char *)__builtin_amdgcn_implicitarg_ptr() + 12);
+    return (int)(*gs & 0xffffu);
+}
+
+// Word 3 of a raw buffer descriptor (gfx9 family: 32-bit data format); with
+// stride 0 a load past num_records bytes returns 0 and touches no memory.
+constexpr int kBufferWord3 = 0x00020000;
+
 constexpr int kMaxWaves = 16;
 constexpr size_t kLdsBytes = 160 * 1024;   // LDS of a gfx950 workgroup
 constexpr int kMaxGroups = 8;                       // quad groups (x4 quads) per wave
@@ -618,6 +653,17 @@ __device__ inline int quad_of(const Plan &pl, const Role &r, int g, int kq) {
 
 __device__ inline int corner_of(const InvArgs &a, int q) { return a.lpu == 1 ? a.corner0 : q; }
 
+// Row order of the register-fed critical path's tiles (one channel tile of
+// CP = 4 EQ channels, EQ = ncq): accumulator row 4 kq + e (lane group kq,
+// register e) holds channel EQ kq + e for e < EQ, and rows with e >= EQ are
+// empty.  The channels then fill registers 0 .. EQ-1 of every lane group,
+// so a tap's contraction over the previous diagonal's channels, fed from
+// those registers, takes EQ MFMAs instead of 4.  Returns the channel of row
+// m, or -1.
+__host__ __device__ inline int crit_row(int m, int eq) {
+    return (m & 3) < eq ? eq * (m >> 2) + (m & 3) : -1;
+}
+
 // The A operands (prepared weights) of this lane's quads for one layer: lane
 // (kq, li) holds, for group g and element e, the weight of input channel
 // 4 (u % ncq) + e of quad u = quad_of(g, kq) into output channel 16 nt + li --
@@ -626,40 +672,53 @@ __device__ inline int corner_of(const InvArgs &a, int q) { return a.lpu == 1 ? a
 // the zero block of the prepared layer).
 template <int NG>
 __device__ inline void load_weights(float (&w)[NG][4], const Plan &pl, const Role &r,
-                                    const float *__restrict__ prep) {
+                                    const float *__restrict__ prep, bool perm) {
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
-    const int co = r.nt * 16 + li;
-    const float4 *W4 = reinterpret_cast<const float4 *>(prep);
-    const float4 *zero = reinterpret_cast<const float4 *>(prep + prep_zero_offset(pl.C, pl.K)) + li;
+    // output channel of A row li: 16 nt + li, or (perm: the tile's critical
+    // wave is register-fed) the row order of crit_row
+    const int co = perm ? crit_row(li, pl.ncq) : r.nt * 16 + li;
+    // raw buffer loads over the prepared layer: slots that do not exist read
+    // past its end, which returns 0 (one 32-bit offset per load, no branch)
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(prep), (short)0, pl.lstride * 4, kBufferWord3);
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
         const int u = quad_of(pl, r, g, kq);
-        const bool valid = u >= 0 && co < pl.C;
-        const float4 v = *(valid ? W4 + (size_t)u * pl.CP + co : zero);
-        w[g][0] = v.x;
-        w[g][1] = v.y;
-        w[g][2] = v.z;
-        w[g][3] = v.w;
+        const bool valid = u >= 0 && co >= 0 && co < pl.C;
+        // (four 32-bit loads: this compiler lowers the 128-bit raw buffer
+        // load builtin to a 32-bit load)
+        const int off = valid ? (u * pl.CP + co) * 16 : pl.lstride * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            w[g][e] = __builtin_bit_cast(float,
+                                         __builtin_amdgcn_raw_buffer_load_b32(rs, off + 4 * e, 0, 0));
     }
 }
 
 // Weights of the register-fed critical path (one channel tile): group t is
-// tap t of the quad order ((0,1), then (1,0)); lane (kq, li) holds the
-// weight of input channel 4 kq + e into output channel li (A operand).
+// tap t of the quad order ((0,1), then (1,0)); lane (kq, li) holds, for
+// element e < EQ = ncq, the weight of input channel EQ kq + e into output
+// channel crit_row(li) (A operand; 0 where either does not exist).
 template <int NG>
 __device__ inline void load_crit_weights(float (&w)[NG][4], const Plan &pl,
                                          const float *__restrict__ prep) {
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
-    const float4 *W4 = reinterpret_cast<const float4 *>(prep);
-    const float4 *zero = reinterpret_cast<const float4 *>(prep + prep_zero_offset(pl.C, pl.K)) + li;
+    const int eq = pl.ncq, o = crit_row(li, eq);
+    // raw buffer loads over the prepared layer; weights that do not exist
+    // read past its end, which returns 0
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(prep), (short)0, pl.lstride * 4, kBufferWord3);
 #pragma unroll
     for (int t = 0; t < (NG < 2 ? NG : 2); ++t) {
-        const bool valid = kq < pl.ncq && li < pl.C;
-        const float4 v = *(valid ? W4 + (size_t)(t * pl.ncq + kq) * pl.CP + li : zero);
-        w[t][0] = v.x;
-        w[t][1] = v.y;
-        w[t][2] = v.z;
-        w[t][3] = v.w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int c = eq * kq + e;
+            const bool valid = o >= 0 && o < pl.C && e < eq && c < pl.C;
+            const int at = (((t * pl.ncq + (c >> 2)) * pl.CP + o) << 2) + (c & 3);
+            w[t][e] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(rs, valid ? 4 * at : pl.lstride * 4,
+                                                             0, 0));
+        }
     }
 }
 
@@ -667,7 +726,7 @@ __device__ inline void load_crit_weights(float (&w)[NG][4], const Plan &pl,
 __device__ inline void zero_floats(float *dst, int n) {   // n multiple of 4, dst 16B aligned
     float4 *d4 = reinterpret_cast<float4 *>(dst);
     const float4 z = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    for (int i = threadIdx.x; i < n / 4; i += blockDim.x)
+    for (int i = threadIdx.x; i < n / 4; i += block_threads())
         d4[i] = z;
 }
 
@@ -676,7 +735,7 @@ __device__ inline void copy_solution(float *sm, const Plan &pl) {
     const int n4 = pl.H * pl.W * pl.CP / 4, cp4 = pl.CP / 4;
     float4 *Y = reinterpret_cast<float4 *>(sm + pl.offY);
     const float4 *X = reinterpret_cast<const float4 *>(sm + pl.offX);
-    for (int idx = threadIdx.x; idx < n4; idx += blockDim.x) {
+    for (int idx = threadIdx.x; idx < n4; idx += block_threads()) {
         const int p = fdiv(idx, pl.d_cp4), c4 = idx - p * cp4;
         const int i = fdiv(p, pl.d_W), j = p - i * pl.W;
         Y[idx] = X[((i + pl.P) * pl.WP + j + pl.P) * cp4 + c4];
@@ -692,12 +751,43 @@ __device__ inline void copy_solution(float *sm, const Plan &pl) {
 // scalar loads, one LDS store).  All of a thread's loads are in flight before
 // the first store; `during` (work that does not touch Y) runs while the
 // first round of loads is in flight.
-template <typename F>
-__device__ inline void load_input(float *sm, const Plan &pl, const float *__restrict__ src,
-                                  bool vec4, F during) {
+// The first round of a thread's input loads (below), issued on their own:
+// single-layer inverses issue them right after the kernel's arguments arrive,
+// so that the set-up of the roles, weights and addresses runs under their
+// latency.  Always the one-pixel form (slot u: channels 4 cq .. +3 of pixel
+// p): each load lands in the register quad its 16-byte LDS store reads, so
+// nothing between the issue and the store waits for the loads.  Raw buffer
+// loads over the image's C H W floats: a 32-bit offset per load, and reads
+// past the image (padding channels, threads without a slot) return 0.
+struct InputRound {
+    float s[4][4];
+};
+__device__ __forceinline__ void input_issue(const Plan &pl, const float *__restrict__ src,
+                                            int tid, InputRound &q) {
+    const int HW = pl.H * pl.W;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(src), (short)0, pl.C * HW * 4, kBufferWord3);
+    const int nthr = block_threads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const int idx = tid + u * nthr;
+        const int cq = fdiv(idx, pl.d_HW), p = idx - cq * HW;
+        const int off = (4 * cq * HW + p) * 4;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            q.s[u][e] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(rs, off + e * HW * 4, 0, 0));
+    }
+}
+
+// PRE: the first round was issued by input_issue into q (the one-pixel form
+// then serves every round).
+template <bool PRE, typename F>
+__device__ __forceinline__ void load_input(float *sm, const Plan &pl,
+                                           const float *__restrict__ src, bool vec4, F during,
+                                           const InputRound &q) {
     const int HW = pl.H * pl.W, CP = pl.CP, C = pl.C, nq = CP / 4;
     float *Y = sm + pl.offY;
-    bool first = true;
     auto pad0 = [&](float4 w, int cq) {   // padding channels are zero
         if (4 * cq + 3 >= C) {
             w.x = 4 * cq < C ? w.x : 0.0f;
@@ -707,75 +797,97 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
         }
         return w;
     };
-    if (vec4) {
+    if (vec4 && !PRE) {
         const int total = nq * (HW / 4);   // (pixel group, quad), quad fastest
         const float4 *s4 = reinterpret_cast<const float4 *>(src);
         constexpr int U = 2;
-        for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
-            float e4[U][4][4];
+        // one round: the loads of slots u of base, `during` after the first,
+        // then the transposed LDS stores
+        auto round = [&](int base, auto first) {
+            float4 v[U][4];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = base + u * blockDim.x;
+                const int idx = base + u * block_threads();
                 const int pg = fdiv(idx, pl.d_cp4), cq = idx - pg * nq;
                 const bool in = idx < total;
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int c = 4 * cq + e;
-                    const float4 v = s4[in && c < C ? (size_t)c * (HW / 4) + pg : 0];
-                    e4[u][e][0] = v.x;
-                    e4[u][e][1] = v.y;
-                    e4[u][e][2] = v.z;
-                    e4[u][e][3] = v.w;
+                    v[u][e] = s4[in && c < C ? (size_t)c * (HW / 4) + pg : 0];
                 }
             }
-            if (first)
+            if constexpr (decltype(first)::value)
                 during();
-            first = false;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = base + u * blockDim.x;
+                const int idx = base + u * block_threads();
                 if (idx < total) {
                     const int pg = fdiv(idx, pl.d_cp4), cq = idx - pg * nq;
-#pragma unroll
-                    for (int i = 0; i < 4; ++i)
-                        *reinterpret_cast<float4 *>(Y + (size_t)(4 * pg + i) * CP + 4 * cq) =
-                            pad0(make_float4(e4[u][0][i], e4[u][1][i], e4[u][2][i], e4[u][3][i]),
-                                 cq);
+                    *reinterpret_cast<float4 *>(Y + (size_t)(4 * pg + 0) * CP + 4 * cq) =
+                        pad0(make_float4(v[u][0].x, v[u][1].x, v[u][2].x, v[u][3].x), cq);
+                    *reinterpret_cast<float4 *>(Y + (size_t)(4 * pg + 1) * CP + 4 * cq) =
+                        pad0(make_float4(v[u][0].y, v[u][1].y, v[u][2].y, v[u][3].y), cq);
+                    *reinterpret_cast<float4 *>(Y + (size_t)(4 * pg + 2) * CP + 4 * cq) =
+                        pad0(make_float4(v[u][0].z, v[u][1].z, v[u][2].z, v[u][3].z), cq);
+                    *reinterpret_cast<float4 *>(Y + (size_t)(4 * pg + 3) * CP + 4 * cq) =
+                        pad0(make_float4(v[u][0].w, v[u][1].w, v[u][2].w, v[u][3].w), cq);
                 }
             }
+        };
+        int base = threadIdx.x;
+        if (base < total) {
+            round(base, std::true_type{});
+            base += U * block_threads();
+        } else {
+            during();   // this thread had nothing to load
         }
+        for (; base < total; base += U * block_threads())
+            round(base, std::false_type{});
     } else {
         const int total = nq * HW;   // (quad, pixel), pixel fastest
         constexpr int U = 4;
-        for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
-            float e4[U][4];
+        // one round: slots u of base (loads, or the prefetched first round),
+        // `during` after the first, then the LDS stores
+        auto round = [&](int base, auto pre, auto first) {
+            float4 v[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = base + u * blockDim.x;
+                const int idx = base + u * block_threads();
                 const int cq = fdiv(idx, pl.d_HW), p = idx - cq * HW;
                 const bool in = idx < total;
+                if constexpr (decltype(pre)::value) {
+                    v[u] = make_float4(q.s[u][0], q.s[u][1], q.s[u][2], q.s[u][3]);
+                } else {
+                    float t[4];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int c = 4 * cq + e;
-                    e4[u][e] = src[in && c < C ? (size_t)c * HW + p : 0];
+                    for (int e = 0; e < 4; ++e) {
+                        const int c = 4 * cq + e;
+                        t[e] = src[in && c < C ? (size_t)c * HW + p : 0];
+                    }
+                    v[u] = make_float4(t[0], t[1], t[2], t[3]);
                 }
             }
-            if (first)
+            if constexpr (decltype(first)::value)
                 during();
-            first = false;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = base + u * blockDim.x;
+                const int idx = base + u * block_threads();
                 if (idx < total) {
                     const int cq = fdiv(idx, pl.d_HW), p = idx - cq * HW;
-                    *reinterpret_cast<float4 *>(Y + (size_t)p * CP + 4 * cq) =
-                        pad0(make_float4(e4[u][0], e4[u][1], e4[u][2], e4[u][3]), cq);
+                    *reinterpret_cast<float4 *>(Y + (size_t)p * CP + 4 * cq) = pad0(v[u], cq);
                 }
             }
+        };
+        int base = threadIdx.x;
+        if (PRE || base < total) {
+            round(base, std::integral_constant<bool, PRE>{}, std::true_type{});
+            base += U * block_threads();
+        } else {
+            during();   // this thread had nothing to load
         }
+        for (; base < total; base += U * block_threads())
+            round(base, std::false_type{}, std::false_type{});
     }
-    if (first)   // this thread had nothing to load
-        during();
 }
 
 // Input of level l: the chain's input at the top; below, concat(unsqueeze(h),
@@ -784,9 +896,10 @@ __device__ inline void load_input(float *sm, const Plan &pl, const float *__rest
 // the solution buffer (with its zero border) and the zero block are cleared.
 // `work` (register-only set-up) runs while the top level's input is on its
 // way.
-template <bool HIN, typename F>
-__device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm, size_t b,
-                            bool vec4, const float *hin, int hin_stride, F work) {
+template <bool HIN, bool PRE, typename F>
+__device__ __forceinline__ void level_input(const Level &lv, bool top, const Plan &up, float *sm,
+                                            size_t b, bool vec4, const float *hin,
+                                            int hin_stride, F work, const InputRound &q) {
     const Plan &pl = lv.pl;
     const int C = pl.C, CP = pl.CP, W = pl.W, HW = pl.H * pl.W;
     float *Y = sm + pl.offY;
@@ -805,11 +918,11 @@ __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm
         const float *hb = hin + b * (size_t)hin_stride;
         const float *lat = lv.z + b * (size_t)Ch * HW;
         constexpr int U = 8;
-        for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
+        for (int base = threadIdx.x; base < total; base += U * block_threads()) {
             float v[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = imin(base + u * blockDim.x, total - 1);
+                const int idx = imin(base + u * block_threads(), total - 1);
                 const int c = fdiv(idx, pl.d_HW), p = idx - c * HW;
                 const int i = fdiv(p, pl.d_W), j = p - i * W;
                 const float *src =
@@ -823,7 +936,7 @@ __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm
                 pin(v[u]);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = base + u * blockDim.x;
+                const int idx = base + u * block_threads();
                 if (idx < total) {
                     const int c = fdiv(idx, pl.d_HW), p = idx - c * HW;
                     Y[p * CP + c] = c < C ? v[u] : 0.0f;
@@ -833,15 +946,15 @@ __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm
     } else if (top) {
         // the solution buffer and the partial tiles are cleared while the
         // image is on its way
-        load_input(sm, pl, lv.z + b * (size_t)C * HW, vec4, [&] {
+        load_input<PRE>(sm, pl, lv.z + b * (size_t)C * HW, vec4, [&] {
             work();
             clear();
-        });
+        }, q);
     } else {
         work();
         const int Ch = C / 2;
         const float *lat = lv.z + b * (size_t)Ch * HW;
-        for (int idx = threadIdx.x; idx < CP * HW; idx += blockDim.x) {
+        for (int idx = threadIdx.x; idx < CP * HW; idx += block_threads()) {
             const int c = fdiv(idx, pl.d_HW), p = idx - c * HW;
             const int i = fdiv(p, pl.d_W), j = p - i * W;
             float v = 0.0f;
@@ -860,12 +973,15 @@ __device__ void level_input(const Level &lv, bool top, const Plan &up, float *sm
 }
 
 // All layers of one level for one wave (NG quad groups).  Weights of the
-// next layer are fetched into registers while the current one runs.
+// next layer are fetched into registers while the current one runs.  inq:
+// the input's first round of loads, issued by the kernel (single-layer
+// instances that hold the image in LDS; unused otherwise).
 template <int NG, int MAXT, int MODE>
 __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, const Level &lv,
                                                            bool top, const Plan &up,
                                                            const Plan &pl, const Role &r,
-                                                           float *sm, size_t b) {
+                                                           float *sm, size_t b,
+                                                           const InputRound &inq) {
     constexpr int G = NG > 0 ? NG : 1;
     // weights of the next layer prefetched into registers when they fit (with
     // 16 waves a lane has 128 registers)
@@ -906,7 +1022,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
         if (regc)
             load_crit_weights(dst, pl, prep_of(n));
         else
-            load_weights(dst, pl, r, prep_of(n));
+            load_weights(dst, pl, r, prep_of(n), CRIT == kCritRegs && pl.regcrit);
     };
     // first layer's weights in flight while the level's input is loaded
     if (nlayers > 0) {
@@ -916,20 +1032,21 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
             fetch(w, 0);
     }
     // corner-free geometry of each group's quad: dp | dq << 4 | cq << 8, or
-    // -1 where the quad does not exist (decoded while the input loads)
+    // -1 where the quad does not exist (decoded while the input is on its way)
     int geo[G];
     auto decode = [&] {
+        // lane l holds the back-offset of tap l (taps number at most 49); a
+        // group's lanes fetch their taps' from those lanes (one cross-lane
+        // read per group instead of one walk over the distances)
+        int dpl, dql;
+        tap_of_lanes(lane, pl.K, dpl, dql);
+        const int tapv = dpl | dql << 4;
 #pragma unroll
         for (int g = 0; g < NG; ++g) {
-            const int uq = quad_of(pl, r, g, kq);
-            if (uq < 0) {
-                geo[g] = -1;
-            } else {
-                const int t = fdiv(uq, pl.d_ncq), cq = uq - t * pl.ncq;
-                int dp, dq;
-                tap_of(t, pl.K, dp, dq);
-                geo[g] = dp | dq << 4 | cq << 8;
-            }
+            const int uq = quad_of(pl, r, g, kq), uc = uq < 0 ? 0 : uq;
+            const int t = fdiv(uc, pl.d_ncq), cq = uc - t * pl.ncq;
+            const int tv = __builtin_amdgcn_ds_bpermute(t << 2, tapv);
+            geo[g] = uq < 0 ? -1 : tv | cq << 8;
         }
     };
     // --- stream form: input and output move between HBM and the rings in
@@ -976,7 +1093,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
     auto sissue = [&](int d0) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < kStreamRegs; ++u) {
-            const int t = threadIdx.x + u * blockDim.x;
+            const int t = threadIdx.x + u * block_threads();
             int i, c, j;
             selem(t, d0, i, c, j);
             const bool ok = t < nph && (unsigned)j < (unsigned)W && (!banded || i0 + i < imgH);
@@ -987,7 +1104,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
     auto sput = [&](int d0) __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < kStreamRegs; ++u) {
-            const int t = threadIdx.x + u * blockDim.x;
+            const int t = threadIdx.x + u * block_threads();
             int i, c, j;
             selem(t, d0, i, c, j);
             if (t < nph && (unsigned)j < (unsigned)W)
@@ -996,7 +1113,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
     };
     // solved diagonals d0 .. d1 to HBM
     auto sdrain = [&](int d0, int d1) __attribute__((always_inline)) {
-        for (int t = threadIdx.x; t < nph; t += blockDim.x) {
+        for (int t = threadIdx.x; t < nph; t += block_threads()) {
             int i, c, j;
             selem(t, d0, i, c, j);
             if (d0 + (t & (kPhase - 1)) <= d1 && (unsigned)j < (unsigned)W &&
@@ -1028,7 +1145,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
     // it drained them -- at columns c0 .. c1 into the solution ring's border
     auto sborder = [&](int c0, int c1) __attribute__((always_inline)) {
         const int ncol = c1 - c0 + 1, nb = P * ncol * C;
-        for (int t = threadIdx.x; t < nb; t += blockDim.x) {
+        for (int t = threadIdx.x; t < nb; t += block_threads()) {
             const int jj = t % ncol, r2 = t / ncol, ii = r2 % P, c = r2 / P;
             const int j = c0 + jj, i = ii - P;
             sm[pl.offX + (ii * kRing + (j & (kRing - 1))) * CP + c] = zout[snat(c, i, j)];
@@ -1090,7 +1207,11 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
         sissue(1 + kPhase);
         __syncthreads();
     } else {
-        level_input<!kOne>(lv, top, up, sm, b, (a.vec & 1) != 0, a.hin, a.hin_stride, decode);
+        // (decode reads across lanes: every lane of the wave runs it here,
+        // outside the input loader's per-thread branches)
+        decode();
+        level_input<!kOne, kOne>(lv, top, up, sm, b, (a.vec & 1) != 0, a.hin, a.hin_stride,
+                                 [] {}, inq);
     }
     for (int n = 0; n < nlayers; ++n) {
         const int u = kOne ? 0 : a.n_units - 1 - n / a.lpu, q = kOne ? 0 : a.lpu - 1 - n % a.lpu;
@@ -1102,7 +1223,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
             float *Y = sm + pl.offY;
             const float *s = lv.scale + (size_t)u * C;
             const float *bi = lv.bias + (size_t)u * C;
-            for (int idx = threadIdx.x; idx < HW * C; idx += blockDim.x) {
+            for (int idx = threadIdx.x; idx < HW * C; idx += block_threads()) {
                 const int p = fdiv(idx, pl.d_C), c = idx - p * C;
                 Y[p * CP + c] = (Y[p * CP + c] - bi[c]) / s[c];
             }
@@ -1279,34 +1400,36 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
             else
                 run(std::false_type{});
         } else if (CRIT == kCritRegs && r.role == 0) {
-            // register-fed critical wave.  dprev: lane (kq, li) holds channels
-            // 4 kq .. +3 of row li's pixel of the previous diagonal (0 for rows
-            // not started).  Its MFMA chain needs nothing from LDS but, in a
-            // lower tile, lane li = 0's row above (the last row of the tile
-            // above); the partial tiles are read meanwhile and added last.
-            // The chain's first kPre MFMAs (own row) depend on nothing but
-            // dprev: they are issued before the barrier, while the write of
-            // the diagonal becomes visible.
-            auto crit = [&](auto pad) {
-                constexpr int kPre = 3;
+            // register-fed critical wave, its tile's rows in the order of
+            // crit_row (EQ = ncq channels per lane group).  dprev: lane (kq,
+            // li) holds channels EQ kq .. EQ kq + EQ-1 of row li's pixel of the
+            // previous diagonal (0 for rows not started).  Its MFMA chain needs
+            // nothing from LDS but, in a lower tile, lane li = 0's row above
+            // (the last row of the tile above); the partial tiles are read
+            // meanwhile and added last.  Each tap takes EQ MFMAs; the chain's
+            // first kPre MFMAs (own row) depend on nothing but dprev: they are
+            // issued before the barrier, while the write of the diagonal
+            // becomes visible.
+            auto crit = [&](auto pad, auto eqc) {
+                constexpr int EQ = decltype(eqc)::value;
+                constexpr int kPre = EQ < 4 ? EQ : 3;
                 f32x4 dprev = zero, pre = zero;
                 int j = e_lo - gi;   // frame column of row gi at the tile's first diagonal
                 // write address of frame column j (the affine form; used only while
-                // 0 <= j < W)
-                int wcol = wx0 + fwo + j * dcol;
+                // 0 <= j < W): channels EQ kq .. of the row's pixel
+                int wcol = bx0 + EQ * kq + fwo + j * dcol;
                 // lane li = 0 of a lower tile reads the tile above's last row
-                // (solved in the previous step; channel quads that exist); other
-                // lanes read zeros
+                // (solved in the previous step); other lanes read zeros
                 const int ui = mt * 16 - 1;
                 const int uoi = fh ? H - 1 - imax(ui, 0) : imax(ui, 0);
                 int ju = e_lo - 16 * mt;   // frame column of row 16 mt (and of the row above it)
-                int ucol = pl.offX + ((uoi + P) * WP + P) * CP + fwo + 4 * kq + ju * dcol;
+                int ucol = pl.offX + ((uoi + P) * WP + P) * CP + fwo + EQ * kq + ju * dcol;
                 // (stream form: ring rows of the written row and of the row above)
-                const int wxs = pl.offX + (gic + P) * kRing * CP + nt * 16 + 4 * kq;
+                const int wxs = pl.offX + (gic + P) * kRing * CP + EQ * kq;
                 // the first tile of a lower band: its row above is the band
                 // above's last row, in the ring's border (else zeros)
                 const bool upb = banded && band > 0 && mt == 0;
-                const int uxs = pl.offX + ((upb ? -1 : imax(ui, 0)) + P) * kRing * CP + 4 * kq;
+                const int uxs = pl.offX + ((upb ? -1 : imax(ui, 0)) + P) * kRing * CP + EQ * kq;
                 const f32x4 *b1 = sbase(1, pad), *b2 = sbase(2, pad), *b3 = sbase(3, pad);
                 __syncthreads();
                 int e = 0;
@@ -1317,14 +1440,17 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                         const int po = (e & 1) * (rstride / 4);
                         const int ucur = kStr ? uxs + __mul24(ju & (kRing - 1), CP) : ucol;
                         const int wcur = kStr ? wxs + __mul24(j & (kRing - 1), CP) : wcol;
-                        f32x4 up = zero;
-                        if (mt > 0 || upb)
-                            up = *reinterpret_cast<const f32x4 *>(
-                                sm + ((li == 0 && 4 * kq < CP && (unsigned)ju < (unsigned)W) ? ucur
-                                                                                        : zaddr));
+                        float up[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+                        if (mt > 0 || upb) {
+                            const float *ua =
+                                sm + ((li == 0 && (unsigned)ju < (unsigned)W) ? ucur : zaddr);
+#pragma unroll
+                            for (int e4 = 0; e4 < EQ; ++e4)
+                                up[e4] = ua[e4];
+                        }
                         // the first four partial tiles in flight during the MFMAs
                         const f32x4 q0 = R0[po], q1 = b1[po], q2 = b2[po], q3 = b3[po];
-                        const bool ok = wch && (unsigned)j < (unsigned)W;
+                        const bool ok = gi < H && (unsigned)j < (unsigned)W;
                         const int waddr = ok ? wcur : taddr;
                         __builtin_amdgcn_sched_barrier(0);
                         f32x4 p = pre;
@@ -1335,10 +1461,10 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                         // bit-casts a vector element lvalue as element 0.
                         if constexpr (G >= 2) {   // (instances with G < 2 never get regc)
 #pragma unroll
-                            for (int e4 = kPre; e4 < 4; ++e4)
+                            for (int e4 = kPre; e4 < EQ; ++e4)
                                 p = mfma4(w[0][e4], dprev[e4], p);
 #pragma unroll
-                            for (int e4 = 0; e4 < 4; ++e4) {
+                            for (int e4 = 0; e4 < EQ; ++e4) {
                                 const float de = dprev[e4], ue = up[e4];
                                 const float s1 = __int_as_float(__builtin_amdgcn_update_dpp(
                                     __float_as_int(ue), __float_as_int(de), 0x111, 0xf, 0xf, false));
@@ -1356,7 +1482,13 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                             rs += t0;
                         }
                         const f32x4 x = rs + p;
-                        *reinterpret_cast<f32x4 *>(sm + waddr) = x;
+                        if constexpr (EQ == 4) {
+                            *reinterpret_cast<f32x4 *>(sm + waddr) = x;
+                        } else {
+#pragma unroll
+                            for (int e4 = 0; e4 < EQ; ++e4)
+                                sm[waddr + e4] = x[e4];
+                        }
                         dprev = x;
                         __builtin_amdgcn_sched_barrier(0);
                         // next diagonal's own-row MFMAs, overlapping the write
@@ -1376,10 +1508,18 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                 for (; e < E; ++e)
                     step_end(e);
             };
+            auto crit_eq = [&](auto pad) {
+                switch (pl.ncq) {
+                    case 1: crit(pad, std::integral_constant<int, 1>{}); break;
+                    case 2: crit(pad, std::integral_constant<int, 2>{}); break;
+                    case 3: crit(pad, std::integral_constant<int, 3>{}); break;
+                    default: crit(pad, std::integral_constant<int, 4>{}); break;
+                }
+            };
             if (pl.compact)
-                crit(std::false_type{});
+                crit_eq(std::false_type{});
             else
-                crit(std::true_type{});
+                crit_eq(std::true_type{});
         } else if (CRIT == kCritGather && r.role == 0) {
             // critical wave that gathers its dp + dq = 1 taps from LDS (several
             // channel tiles: the previous diagonal's channels sit in several
@@ -1421,7 +1561,7 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
         }
     }
     if (a.steps && (threadIdx.x & 63) == 0)
-        a.steps[b * (blockDim.x >> 6) + (threadIdx.x >> 6)] = nsteps;
+        a.steps[b * (block_threads() >> 6) + (threadIdx.x >> 6)] = nsteps;
 }
 
 // A wave of a multi-level chain runs the level loop compiled for its own
@@ -1433,15 +1573,15 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
 template <int G, int NG, int MAXT, int MODE>
 __device__ __attribute__((always_inline)) void level_waves_for(int ng, const InvArgs &a, const Level &lv, bool top,
                                 const Plan &up, const Plan &pl, const Role &r, float *sm,
-                                size_t b) {
+                                size_t b, const InputRound &inq) {
     if constexpr (G < NG) {
         if (ng <= G) {
-            level_waves<G, MAXT, MODE>(a, lv, top, up, pl, r, sm, b);
+            level_waves<G, MAXT, MODE>(a, lv, top, up, pl, r, sm, b, inq);
             return;
         }
-        level_waves_for<G + 1, NG, MAXT, MODE>(ng, a, lv, top, up, pl, r, sm, b);
+        level_waves_for<G + 1, NG, MAXT, MODE>(ng, a, lv, top, up, pl, r, sm, b, inq);
     } else {
-        level_waves<NG, MAXT, MODE>(a, lv, top, up, pl, r, sm, b);
+        level_waves<NG, MAXT, MODE>(a, lv, top, up, pl, r, sm, b, inq);
     }
 }
 
@@ -1457,13 +1597,31 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
     const size_t b = blockIdx.x;
     Level lv = a.lv[0];
     Plan above = lv.pl;   // plan of the level run before (unused at the first)
-    {   // one round of scalar loads for everything the first level starts with
-        const int L = a.L, nu = a.n_units, lpu = a.lpu, c0 = a.corner0, sp = a.split,
-                  vc = a.vec;
-        asm volatile("" ::"s"(L), "s"(nu), "s"(lpu), "s"(c0), "s"(sp), "s"(vc), "s"(lv.z),
-                     "s"(lv.prep), "s"(lv.scale));
+    // one round of scalar loads for everything the first level starts with:
+    // one dword of every argument line up to the end of the first level, the
+    // wave's role word and the workgroup size (a line of the implicit
+    // arguments) -- later loads of these lines hit the scalar cache instead of
+    // each costing a round trip to memory.  tid comes out of the same barrier,
+    // so nothing that depends on it is scheduled (with a wait) before it.
+    int tid = threadIdx.x;
+    {
+        const int *ai = reinterpret_cast<const int *>(&a);
+        constexpr int kArgLines = (int)((offsetof(InvArgs, lv) + sizeof(Level) + 63) / 64);
+        static_assert(kArgLines <= 8, "first level's arguments span at most 8 lines");
+        auto line = [&](int l) { return ai[16 * (l < kArgLines ? l : kArgLines - 1)]; };
+        const int l0 = line(0), l1 = line(1), l2 = line(2), l3 = line(3), l4 = line(4),
+                  l5 = line(5), l6 = line(6), l7 = line(7), nthr = block_threads();
+        const int rw =
+            a.lv[0].pl.wave[__builtin_amdgcn_readfirstlane(threadIdx.x >> 6) & (kMaxWaves - 1)];
+        asm volatile("" : "+v"(tid) : "s"(l0), "s"(l1), "s"(l2), "s"(l3), "s"(l4), "s"(l5),
+                     "s"(l6), "s"(l7), "s"(nthr), "s"(rw));
     }
     constexpr bool kOne = (MODE & kOneLayer) != 0;
+    // a single layer held in LDS reads its input straight from z: the first
+    // round of those loads goes out now, ahead of the set-up
+    InputRound inq;
+    if constexpr (kOne && (MODE & kStream) == 0)
+        input_issue(lv.pl, lv.z + b * (size_t)lv.pl.C * lv.pl.H * lv.pl.W, tid, inq);
     for (int i = 0; i < (kOne ? 1 : a.L); ++i) {
         if (i > 0) {
             above = lv.pl;
@@ -1474,12 +1632,12 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
         float *Y = sm + pl.offY;
         if constexpr (!kOne && MAXT == 1024) {   // (chains whose levels differ most)
             const Role r = role_of(a, i);
-            level_waves_for<1, NG, MAXT, MODE>(r.ng, a, lv, i == 0, above, pl, r, sm, b);
+            level_waves_for<1, NG, MAXT, MODE>(r.ng, a, lv, i == 0, above, pl, r, sm, b, inq);
         } else {
-            level_waves<NG, MAXT, MODE>(a, lv, i == 0, above, pl, role_of(a, i), sm, b);
+            level_waves<NG, MAXT, MODE>(a, lv, i == 0, above, pl, role_of(a, i), sm, b, inq);
         }
         if (!kOne && a.n_units * a.lpu == 0) {   // no layers at this level: the input passes through
-            for (int idx = threadIdx.x; idx < HW * CP; idx += blockDim.x) {
+            for (int idx = threadIdx.x; idx < HW * CP; idx += block_threads()) {
                 const int p = fdiv(idx, pl.d_CP), c = idx - p * CP;
                 const int i = fdiv(p, pl.d_W), j = p - i * W;
                 sm[pl.offX + ((i + pl.P) * pl.WP + j + pl.P) * CP + c] = Y[idx];
@@ -1506,11 +1664,11 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
         const int tot = nq0 * (HW0 / 4);   // (pixel group, quad), quad fastest
         float4 *d4 = reinterpret_cast<float4 *>(dst);
         constexpr int U = 2;
-        for (int base = threadIdx.x; base < tot; base += U * blockDim.x) {
+        for (int base = threadIdx.x; base < tot; base += U * block_threads()) {
             float4 v[U][4];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = imin(base + u * blockDim.x, tot - 1);
+                const int idx = imin(base + u * block_threads(), tot - 1);
                 const int pg = fdiv(idx, p0.d_cp4), cq = idx - pg * nq0;
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
@@ -1518,7 +1676,7 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = base + u * blockDim.x;
+                const int idx = base + u * block_threads();
                 if (idx < tot) {
                     const int pg = fdiv(idx, p0.d_cp4), cq = idx - pg * nq0, c = 4 * cq;
                     float4 *d = d4 + (size_t)c * (HW0 / 4) + pg;
@@ -1536,17 +1694,17 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
     } else {
         constexpr int U = 4;
         const int tot = nq0 * HW0;   // (quad, pixel), pixel fastest
-        for (int base = threadIdx.x; base < tot; base += U * blockDim.x) {
+        for (int base = threadIdx.x; base < tot; base += U * block_threads()) {
             float4 v[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = imin(base + u * blockDim.x, tot - 1);
+                const int idx = imin(base + u * block_threads(), tot - 1);
                 const int cq = fdiv(idx, p0.d_HW), p = idx - cq * HW0;
                 v[u] = xat(p, cq);
             }
 #pragma unroll
             for (int u = 0; u < U; ++u) {
-                const int idx = base + u * blockDim.x;
+                const int idx = base + u * block_threads();
                 if (idx < tot) {
                     const int cq = fdiv(idx, p0.d_HW), p = idx - cq * HW0, c = 4 * cq;
                     float *d = dst + (size_t)c * HW0 + p;

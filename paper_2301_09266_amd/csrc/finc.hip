@@ -1833,10 +1833,34 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         return;
     }
     const int C = fp.C, CP = fp.CP, H = fp.H, W = fp.W, K = fp.K, P = fp.P, WP = fp.WP;
+    if (a.logdet && (int)blockIdx.x == npre) {
+        // log|det| on a block of its own (next after the preparation blocks,
+        // so it is dispatched early and no forward block carries its fp64
+        // logarithms): H W times the sum over the layers (or the four
+        // quarters) and channels of log|K[c,c,self]|, straight from K; lane
+        // l takes entries l, l + 64, ..., and the 64 lane sums meet in a
+        // fixed butterfly
+        if (threadIdx.x < 64) {
+            const int lane = threadIdx.x, nl = a.split ? 4 : fp.n;
+            double v = 0.0;
+            for (int m = lane; m < nl * C; m += 64) {
+                const int q = m / C, c = m - q * C;
+                int oh, ow;
+                self_tap(a.split ? q : (fp.n == 1 ? fp.corner0 : q), K, oh, ow);
+                const float d = a.K[(((size_t)q * C + c) * C + c) * K * K + oh * K + ow];
+                v += log(fabs((double)d));
+            }
+            for (int off = 32; off > 0; off >>= 1)
+                v += __shfl_xor(v, off);
+            if (lane == 0)
+                a.logdet[0] = (double)H * (double)W * v;
+        }
+        return;
+    }
     const int lane = threadIdx.x & 63, kq = lane >> 4, li = lane & 15;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int nwaves = blockDim.x >> 6;
-    const int bid = blockIdx.x - npre;
+    const int bid = blockIdx.x - npre - (a.logdet ? 1 : 0);
     const int b = bid / fp.nblk, blk = bid - b * fp.nblk;
     const int corner0 = a.split ? (b & 3) : fp.corner0;   // this block's (first) corner
     const float *Kb = a.K + (a.split ? (size_t)(b & 3) * fp.C * fp.C * fp.K * fp.K : 0);
@@ -1883,7 +1907,6 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
                     X[dst[u]] = inb[u] ? v[u] : 0.0f;
         }
     }
-    double ld_acc = 0.0;
     for (int q = 0; q < fp.n; ++q) {
         const int corner = fp.n == 1 ? corner0 : q;
         int oh, ow;
@@ -1946,36 +1969,6 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
             Dq[u] = u < fp.nq ? ((ka - oh) * WP + (kb - ow)) * CP + 4 * cq : kNoQuad;
         }
         __syncthreads();
-        // log|det| rides along: block 0's first wave sums log|K[c,c,self]| over
-        // the layers from the staged weights (self tap is quad t = oh K + ow)
-        if (a.logdet && bid == 0 && wave == 0 && a.split) {
-            // the four quarters' diagonals straight from K, in a fixed order
-            double v = 0.0;
-            for (int m = lane; m < 4 * C; m += 64) {
-                const int g = m / C, c = m - g * C;
-                int gh, gw;
-                self_tap(g, K, gh, gw);
-                const float d = a.K[(((size_t)g * C + c) * C + c) * K * K + gh * K + gw];
-                v += log(fabs((double)d));
-            }
-            for (int off = 32; off > 0; off >>= 1)
-                v += __shfl_xor(v, off);
-            if (lane == 0)
-                ld_acc += v;
-        } else if (a.logdet && bid == 0 && wave == 0) {
-            double v = 0.0;
-            for (int c = lane; c < C; c += 64) {
-                const int u = (oh * K + ow) * fp.ncq + (c >> 2);
-                const int g = u >> 2, l = (u & 3) * 16 + (c & 15);
-                const float4 wv = Wf[((c >> 4) * fp.NG + g) * 64 + l];
-                const float d = (c & 3) == 0 ? wv.x : (c & 3) == 1 ? wv.y : (c & 3) == 2 ? wv.z : wv.w;
-                v += log(fabs((double)d));
-            }
-            for (int off = 32; off > 0; off >>= 1)
-                v += __shfl_xor(v, off);
-            if (lane == 0)
-                ld_acc += v;
-        }
         const bool last = q == fp.n - 1;
         float *Yo = sm + fp.offO;
         // rows of this layer's output the block computes, rlo .. rhi - 1: its
@@ -2043,8 +2036,6 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
             __syncthreads();
         }
     }
-    if (a.logdet && bid == 0 && threadIdx.x == 0)
-        a.logdet[0] = (double)H * (double)W * ld_acc;
 }
 
 // ---------------------------------------------------------------------------
@@ -2502,7 +2493,8 @@ int launch_forward(const float *x, float *y, const float *K, double *logdet, flo
     if (hipFuncSetAttribute((const void *)forward_kernel,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
         (void)hipGetLastError();   // not needed on every runtime; the launch check decides
-    const unsigned blocks = (unsigned)(a.nfwd + (fuse ? nprep * a.ppl : 0));
+    // preparation blocks, then the log|det| block, then the forward blocks
+    const unsigned blocks = (unsigned)(a.nfwd + (fuse ? nprep * a.ppl : 0) + (logdet ? 1 : 0));
     hipLaunchKernelGGL(forward_kernel, dim3(blocks), dim3(kFwdThreads), lds, stream, a);
     rc = launched();
     if (rc != FINC_OK || !prepared || fuse)

@@ -1996,20 +1996,31 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
 #pragma unroll
             for (int v = 0; v < 4; ++v)
                 part[v] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+            // four groups at a time, without a branch: their offset reads,
+            // then their gathers and weight reads, then their MFMAs; groups
+            // past the last meet zero weights (their products add exact
+            // zeros) at a clamped in-bounds index
+            const float4 *S4 = reinterpret_cast<const float4 *>(sm);   // regions are 16-byte aligned
             for (int g0 = 0; g0 < fp.NG; g0 += 4) {
+                int d[4];
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    d[v] = Dq[4 * imin(g0 + v, fp.NG - 1) + kq];
+                float4 xv[4], wv[4];
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     const int g = g0 + v;
-                    if (g < fp.NG) {
-                        const int d = Dq[4 * g + kq];
-                        const float4 xv = *reinterpret_cast<const float4 *>(
-                            sm + (d != kNoQuad ? fp.offI + base + d : zaddr));
-                        const float4 wv = Wf[(nt * fp.NG + g) * 64 + lane];
-                        part[v] = mfma4(wv.x, xv.x, part[v]);
-                        part[v] = mfma4(wv.y, xv.y, part[v]);
-                        part[v] = mfma4(wv.z, xv.z, part[v]);
-                        part[v] = mfma4(wv.w, xv.w, part[v]);
-                    }
+                    const bool live = g < fp.NG;
+                    xv[v] = S4[(live && d[v] != kNoQuad ? fp.offI + base + d[v] : zaddr) >> 2];
+                    const float4 wl = Wf[(nt * fp.NG + imin(g, fp.NG - 1)) * 64 + lane];
+                    wv[v] = live ? wl : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                }
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    part[v] = mfma4(wv[v].x, xv[v].x, part[v]);
+                    part[v] = mfma4(wv[v].y, xv[v].y, part[v]);
+                    part[v] = mfma4(wv[v].z, xv[v].z, part[v]);
+                    part[v] = mfma4(wv[v].w, xv[v].w, part[v]);
                 }
             }
             const f32x4 acc = (part[0] + part[1]) + (part[2] + part[3]);

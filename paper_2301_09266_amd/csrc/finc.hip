@@ -1874,8 +1874,9 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     // zero-bordered input rows i0 - HB .. i0 + rb + HB - 1: every element of
     // the block is written once, with x where the taps of this launch read
     // the image and zero elsewhere (outside the image, padding channels, and
-    // for a single layer the halo side its corner never reads).  Loads are
-    // unconditional from clamped indices, eight in flight per thread.
+    // for a single layer the halo side its corner never reads).  Images
+    // past 2^31 bytes: one element an item, loads unconditional from clamped
+    // indices, eight in flight per thread.
     {
         int oh0, ow0;
         self_tap(corner0, K, oh0, ow0);
@@ -1883,28 +1884,70 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         const int lo = imax(0, i0 - up), hi = imin(H, i0 + rb + down);   // rows read
         const int nrow = rb + 2 * HB, plane = nrow * WP, total = CP * plane;
         const FastDiv dpl = blk == fp.nblk - 1 ? fp.d_plane_last : fp.d_plane;
-        constexpr int U = 8;
-        for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
-            float v[U];
-            bool inb[U];
-            int dst[U];
+        if ((long long)C * HW * 4 < (1LL << 31)) {
+            // (pixel, channel quad) items, pixel fastest: four raw buffer
+            // loads over the image's C H W floats each (32-bit offsets; reads
+            // past the image, padding channels included, return 0; a pixel
+            // outside the rows or columns read takes an offset past the
+            // end), then one 16-byte LDS store
+            const unsigned nrec = (unsigned)(C * HW * 4);
+            const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<float *>(xb), (short)0, (int)nrec, kBufferWord3);
+            const int nitem = plane * (CP / 4);
+            constexpr int U = 2;
+            for (int base = threadIdx.x; base < nitem; base += U * blockDim.x) {
+                float v[U][4];
+                int dst[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const int idx = base + u * blockDim.x;
-                const int c = fdiv(idx, dpl), rem = idx - c * plane;
-                const int pr = fdiv(rem, fp.d_WP), pc = rem - pr * WP;
-                const int i = i0 - HB + pr, j = pc - P;
-                inb[u] = idx < total && c < C && i >= lo && i < hi && j >= 0 && j < W;
-                v[u] = xb[inb[u] ? c * HW + (size_t)i * W + j : 0];
-                dst[u] = idx < total ? rem * CP + c : -1;
+                for (int u = 0; u < U; ++u) {
+                    const int idx = base + u * blockDim.x;
+                    const int q = fdiv(idx, dpl), px = idx - q * plane;
+                    const int pr = fdiv(px, fp.d_WP), pc = px - pr * WP;
+                    const int i = i0 - HB + pr, j = pc - P;
+                    const bool ok = idx < nitem && i >= lo && i < hi && j >= 0 && j < W;
+                    const unsigned off = ok ? (unsigned)(4 * q * HW + i * W + j) * 4u : nrec;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        v[u][e] = __builtin_bit_cast(
+                            float, __builtin_amdgcn_raw_buffer_load_b32(
+                                       rs, (int)(ok ? off + (unsigned)(e * HW * 4) : nrec), 0, 0));
+                    dst[u] = idx < nitem ? px * CP + 4 * q : -1;
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        pin(v[u][e]);
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (dst[u] >= 0)
+                        *reinterpret_cast<float4 *>(X + dst[u]) =
+                            make_float4(v[u][0], v[u][1], v[u][2], v[u][3]);
             }
+        } else {
+            constexpr int U = 8;
+            for (int base = threadIdx.x; base < total; base += U * blockDim.x) {
+                float v[U];
+                bool inb[U];
+                int dst[U];
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                pin(v[u]);
+                for (int u = 0; u < U; ++u) {
+                    const int idx = base + u * blockDim.x;
+                    const int c = fdiv(idx, dpl), rem = idx - c * plane;
+                    const int pr = fdiv(rem, fp.d_WP), pc = rem - pr * WP;
+                    const int i = i0 - HB + pr, j = pc - P;
+                    inb[u] = idx < total && c < C && i >= lo && i < hi && j >= 0 && j < W;
+                    v[u] = xb[inb[u] ? c * HW + (size_t)i * W + j : 0];
+                    dst[u] = idx < total ? rem * CP + c : -1;
+                }
 #pragma unroll
-            for (int u = 0; u < U; ++u)
-                if (dst[u] >= 0)
-                    X[dst[u]] = inb[u] ? v[u] : 0.0f;
+                for (int u = 0; u < U; ++u)
+                    pin(v[u]);
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    if (dst[u] >= 0)
+                        X[dst[u]] = inb[u] ? v[u] : 0.0f;
+            }
         }
     }
     for (int q = 0; q < fp.n; ++q) {

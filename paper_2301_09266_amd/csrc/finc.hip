@@ -176,12 +176,13 @@ constexpr int kPrepMax = 64;             // FINC_MAX_C rounded up to kPrepBlk
 
 __host__ __device__ inline int prep_cb(int C) { return (C + kPrepBlk - 1) / kPrepBlk * kPrepBlk; }
 
-// LDS (doubles) of prep_columns: L's strictly lower part (CB x CB), the
-// reciprocals of its diagonal (CB), and the rows beyond the first register
-// block of every thread's right-hand side.
+// LDS (doubles) of prep_columns: L's strictly lower part (CB x CB, kept in
+// fp32, the precision K holds it in), the reciprocals of its diagonal (CB),
+// and the rows beyond the first register block of every thread's
+// right-hand side.
 __host__ __device__ inline int prep_lds_doubles(int C, int nth) {
     const int cb = prep_cb(C);
-    return cb * cb + cb + (cb - kPrepBlk) * nth;
+    return cb * cb / 2 + cb + (cb - kPrepBlk) * nth;
 }
 
 // One block's share of one layer's preparation: output rows (columns of the
@@ -191,8 +192,10 @@ template <int NTH>
 __device__ void prep_columns(const float *__restrict__ K, float *out, int C, int k, int corner,
                              int col0, bool zero_tail, double *lds) {
     const int kk = k * k, CP = round_up4(C), CB = prep_cb(C), tid = threadIdx.x;
-    double *Lt = lds;                  // Lt[c CB + m] = L[m][c] for m > c, else 0
-    double *rinv = lds + CB * CB;      // 1 / L[c][c]; 1 beyond C
+    // Lt[c CB + m] = L[m][c] for m > c, else 0 (fp32: converting to fp64 is
+    // exact, and a column's multipliers are read 16 bytes at a time)
+    float *Lt = reinterpret_cast<float *>(lds);
+    double *rinv = lds + CB * CB / 2;  // 1 / L[c][c]; 1 beyond C
     double *zs = rinv + CB;            // zs[(m - 16) NTH + thread]: rows of later blocks
     int sh, sw;
     self_tap(corner, k, sh, sw);
@@ -222,7 +225,7 @@ __device__ void prep_columns(const float *__restrict__ K, float *out, int C, int
     auto put_l = [&](int idx, float v) {
         const int c = idx / CB, m = idx - c * CB;
         if (idx < nl)
-            Lt[c * CB + m] = (m > c && m < C) ? (double)v : 0.0;
+            Lt[c * CB + m] = (m > c && m < C) ? v : 0.0f;
     };
     auto l_at = [&](int idx) {
         const int c = idx / CB, m = idx - c * CB;
@@ -294,9 +297,21 @@ __device__ void prep_columns(const float *__restrict__ K, float *out, int C, int
 #pragma unroll
         for (int c = 0; c < kPrepBlk; ++c) {
             z[c] *= rinv[b0 + c];
+            // column c's multipliers of rows b0 .. b0 + 15 (16-byte aligned:
+            // CB and b0 are multiples of 16), read ahead of their use
+            const float4 *lc = reinterpret_cast<const float4 *>(Lt + (b0 + c) * CB + b0);
+            float lv[kPrepBlk];
+#pragma unroll
+            for (int q = c / 4; q < kPrepBlk / 4; ++q) {
+                const float4 v = lc[q];
+                lv[4 * q] = v.x;
+                lv[4 * q + 1] = v.y;
+                lv[4 * q + 2] = v.z;
+                lv[4 * q + 3] = v.w;
+            }
 #pragma unroll
             for (int m = c + 1; m < kPrepBlk; ++m)
-                z[m] -= Lt[(b0 + c) * CB + b0 + m] * z[c];
+                z[m] -= (double)lv[m] * z[c];
         }
         if (row_ok) {
 #pragma unroll
@@ -308,7 +323,7 @@ __device__ void prep_columns(const float *__restrict__ K, float *out, int C, int
             double acc = zs[(m - kPrepBlk) * NTH + tid];
 #pragma unroll
             for (int c = 0; c < kPrepBlk; ++c)
-                acc -= Lt[(b0 + c) * CB + m] * z[c];
+                acc -= (double)Lt[(b0 + c) * CB + m] * z[c];
             zs[(m - kPrepBlk) * NTH + tid] = acc;
         }
     }
@@ -1871,6 +1886,55 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     const size_t HW = (size_t)H * W;
     const float *xb = a.in + (size_t)b * C * HW;
     float *yb = a.out + (size_t)b * C * HW;
+    // weight fragments: Wf[(nt NG + g) 64 + lane].e = K[co][ci][tap] for
+    // co = 16 nt + li, quad u = 4 g + kq (tap u / ncq, ci = 4 (u % ncq) + e),
+    // the channel mask applied (self tap: ci <= co only).  A round is two
+    // fragments a thread: eight raw buffer loads over the layer's C^2 k^2
+    // floats at (co C + ci) k^2 + tap (entries that do not exist read past
+    // the end, which returns 0), all in flight before the stores.
+    const int nfrag = fp.NT * fp.NG * 64;
+    auto wload = [&](int q, int base, float(&v)[2][4]) {
+        const int K2 = K * K;
+        const unsigned nrec = (unsigned)(C * C * K2 * 4);
+        const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float *>(Kb + (size_t)q * C * C * K2), (short)0, (int)nrec, kBufferWord3);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int idx = base + h * blockDim.x;
+            const int f = idx >> 6, ln = idx & 63;
+            const int nt = fdiv(f, fp.d_NG), g = f - nt * fp.NG;
+            const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
+            const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
+            const bool ok = idx < nfrag && u < fp.nq && co < C;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int ci = 4 * cq + e;
+                const int off = ok && ci < C ? ((co * C + ci) * K2 + t) * 4 : (int)nrec;
+                v[h][e] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rk, off, 0, 0));
+            }
+        }
+    };
+    // the self tap (number selft) keeps ci <= co only
+    auto wstore = [&](float(&v)[2][4], int base, int selft) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int idx = base + h * blockDim.x;
+            const int f = idx >> 6, ln = idx & 63;
+            const int nt = fdiv(f, fp.d_NG), g = f - nt * fp.NG;
+            const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
+            const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (t == selft && 4 * cq + e > co)
+                    v[h][e] = 0.0f;
+            if (idx < nfrag)
+                Wf[idx] = make_float4(v[h][0], v[h][1], v[h][2], v[h][3]);
+        }
+    };
+    // the first layer's first round of weights goes out ahead of the input,
+    // so that one memory latency covers both
+    float wpre[2][4];
+    wload(0, threadIdx.x, wpre);
     // zero-bordered input rows i0 - HB .. i0 + rb + HB - 1: every element of
     // the block is written once, with x where the taps of this launch read
     // the image and zero elsewhere (outside the image, padding channels, and
@@ -1955,54 +2019,21 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         int oh, ow;
         self_tap(corner, K, oh, ow);
         const float *Kq = Kb + (size_t)q * C * C * K * K;
-        // weight fragments: Wf[(nt NG + g) 64 + lane].e = K[co][ci][tap] for
-        // co = 16 nt + li, quad u = 4 g + kq (tap u / ncq, ci = 4 (u % ncq) + e),
-        // the channel mask applied (self tap: ci <= co only)
-        // (unconditional loads from clamped indices, two fragments = eight
-        // loads in flight per thread, masked afterwards)
         const int nfrag = fp.NT * fp.NG * 64;
-        for (int base = threadIdx.x; base < nfrag; base += 2 * blockDim.x) {
+        int wb = threadIdx.x;
+        if (q == 0) {   // (the first round went out before the input)
+            wstore(wpre, wb, oh * K + ow);
+            wb += 2 * blockDim.x;
+        }
+        for (; wb < nfrag; wb += 2 * blockDim.x) {
             float v[2][4];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int idx = base + h * blockDim.x;
-                const int f = idx >> 6, ln = idx & 63;
-                const int nt = fdiv(f, fp.d_NG), g = f - nt * fp.NG;
-                const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
-                const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
-                const bool ok = idx < nfrag && u < fp.nq;
-                const int ka = ok ? fdiv(t, fp.d_K) : 0, kb = ok ? t - ka * K : 0;
-                const int co_c = co < C ? co : 0;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int ci = 4 * cq + e;
-                    v[h][e] = Kq[((size_t)(co_c * C + (ci < C ? ci : 0)) * K + ka) * K + kb];
-                }
-            }
+            wload(q, wb, v);
 #pragma unroll
             for (int h = 0; h < 2; ++h)
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     pin(v[h][e]);
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int idx = base + h * blockDim.x;
-                const int f = idx >> 6, ln = idx & 63;
-                const int nt = fdiv(f, fp.d_NG), g = f - nt * fp.NG;
-                const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
-                const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
-                const int ka = fdiv(t, fp.d_K), kb = t - ka * K;
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int ci = 4 * cq + e;
-                    const bool keep =
-                        u < fp.nq && co < C && ci < C && !(ka == oh && kb == ow && ci > co);
-                    if (!keep)
-                        v[h][e] = 0.0f;
-                }
-                if (idx < nfrag)
-                    Wf[idx] = make_float4(v[h][0], v[h][1], v[h][2], v[h][3]);
-            }
+            wstore(v, wb, oh * K + ow);
         }
         // gather offset of quad u relative to the output pixel's address (taps
         // reach up/left too: offsets are signed); padding quads get kNoQuad

@@ -1829,7 +1829,6 @@ struct FwdArgs {
 
 constexpr int kFwdThreads = 256;
 constexpr int kFwdMinBlocks = 256;   // a block per compute unit of the chip
-constexpr int kNoQuad = 1 << 30;   // quad offset marker: padding quad (zero weights)
 
 __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     extern __shared__ float sm[];
@@ -2018,7 +2017,6 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         const int corner = fp.n == 1 ? corner0 : q;
         int oh, ow;
         self_tap(corner, K, oh, ow);
-        const float *Kq = Kb + (size_t)q * C * C * K * K;
         const int nfrag = fp.NT * fp.NG * 64;
         int wb = threadIdx.x;
         if (q == 0) {   // (the first round went out before the input)
@@ -2036,11 +2034,12 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
             wstore(v, wb, oh * K + ow);
         }
         // gather offset of quad u relative to the output pixel's address (taps
-        // reach up/left too: offsets are signed); padding quads get kNoQuad
+        // reach up/left too: offsets are signed); padding quads, whose
+        // weights are zero, read the output pixel's own input (offset 0)
         for (int u = threadIdx.x; u < fp.NG * 4; u += blockDim.x) {
             const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
             const int ka = fdiv(t, fp.d_K), kb = t - ka * K;
-            Dq[u] = u < fp.nq ? ((ka - oh) * WP + (kb - ow)) * CP + 4 * cq : kNoQuad;
+            Dq[u] = u < fp.nq ? ((ka - oh) * WP + (kb - ow)) * CP + 4 * cq : 0;
         }
         __syncthreads();
         const bool last = q == fp.n - 1;
@@ -2063,31 +2062,26 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
             const int pc = valid ? p : 0;
             const int il = fdiv(pc, fp.d_W), j = pc - il * W;
             const int base = ((il + xrow) * WP + j + P) * CP;
-            const int zaddr = fp.offW;   // any valid address: its products meet zero weights
             // four accumulators over the quad groups (group g -> g mod 4), joined
             // pairwise: the rounding chain is a quarter as long as a single one
             f32x4 part[4];
 #pragma unroll
             for (int v = 0; v < 4; ++v)
                 part[v] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-            // four groups at a time, without a branch: their offset reads,
-            // then their gathers and weight reads, then their MFMAs; groups
-            // past the last meet zero weights (their products add exact
-            // zeros) at a clamped in-bounds index
+            // four groups at a time (NG is a multiple of four), without a
+            // branch: their offset reads, then their 16-byte gathers and
+            // weight reads, then their MFMAs
             const float4 *S4 = reinterpret_cast<const float4 *>(sm);   // regions are 16-byte aligned
             for (int g0 = 0; g0 < fp.NG; g0 += 4) {
                 int d[4];
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
-                    d[v] = Dq[4 * imin(g0 + v, fp.NG - 1) + kq];
+                    d[v] = Dq[4 * (g0 + v) + kq];
                 float4 xv[4], wv[4];
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
-                    const int g = g0 + v;
-                    const bool live = g < fp.NG;
-                    xv[v] = S4[(live && d[v] != kNoQuad ? fp.offI + base + d[v] : zaddr) >> 2];
-                    const float4 wl = Wf[(nt * fp.NG + imin(g, fp.NG - 1)) * 64 + lane];
-                    wv[v] = live ? wl : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+                    xv[v] = S4[(fp.offI + base + d[v]) >> 2];
+                    wv[v] = Wf[(nt * fp.NG + g0 + v) * 64 + lane];
                 }
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
@@ -2186,7 +2180,9 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B, boo
     p.NT = ceil_div(p.CP, 16);
     p.ncq = p.CP / 4;
     p.nq = K * K * p.ncq;
-    p.NG = ceil_div(p.nq, 4);
+    // quad groups, padded to a multiple of four (the MFMA loop takes four at
+    // a time; padding groups have zero weights and read the pixel itself)
+    p.NG = round_up4(ceil_div(p.nq, 4));
     p.n = n;
     p.corner0 = corner0;
     int rb_min;

@@ -84,6 +84,23 @@ __device__ inline void pin(T &x) {
     asm volatile("" : "+v"(x));
 }
 
+// Threads of the workgroup: the 16-bit group size at byte 12 of the implicit
+// kernel arguments (code object v5), read with one scalar load.  Every launch
+// here is a whole number of workgroups, so no remainder case is needed; the
+// compiler's blockDim.x covers one with a 16-bit vector load, which would
+// wait behind every vector load issued before it (the image loads that go
+// out first thing).
+typedef __attribute__((address_space(4))) const unsigned *KernargU32;
+__device__ __forceinline__ int block_threads() {
+    const KernargU32 gs = (KernargU32)(
+        (__attribute__((address_space(4))) const char *)__builtin_amdgcn_implicitarg_ptr() + 12);
+    return (int)(*gs & 0xffffu);
+}
+
+// Word 3 of a raw buffer descriptor (gfx9 family: 32-bit data format); with
+// stride 0 a load past num_records bytes returns 0 and touches no memory.
+constexpr int kBufferWord3 = 0x00020000;
+
 // Taps in the frame of a corner: back-offset (dp, dq) in [0, k-1]^2 of the
 // source pixel.  They are numbered by diagonal distance dp + dq = 1, 2, ...,
 // 2(k-1) (dp ascending within a distance), the self tap (0, 0) last.
@@ -205,41 +222,58 @@ __device__ void prep_columns(const float *__restrict__ K, float *out, int C, int
     const int ka = s / k, kb = s - ka * k;
     const bool is_self = (ka == sh && kb == sw);
     const bool real = row_ok && ci < C;   // padding rows stay zero
-    const int ci_c = real ? ci : 0, ka_c = row_ok ? ka : 0, kb_c = row_ok ? kb : 0;
-    auto Kself = [&](int m, int c) {   // clamped into K
-        return K[((size_t)((m < C ? m : 0) * C + (c < C ? c : 0)) * k + sh) * k + sw];
+    // K through a raw buffer (32-bit offsets): entries past its C^2 k^2
+    // floats read 0, so no index is clamped.  Entries of L with a channel of
+    // C or more are zeroed when stored; a right-hand side of a padding row is
+    // zero through rhs_val.
+    const int ckk = C * kk, ss = sh * k + sw;   // row stride of K's output channel; self tap
+    const unsigned nrec = (unsigned)(C * ckk * 4);
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float *>(K), (short)0, (int)nrec, kBufferWord3);
+    auto kat = [&](int off) {
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rk, off, 0, 0));
     };
-    // Staging: every load of a round is unconditional (clamped index) and
-    // pinned right after issue, so a round costs one memory latency; the
-    // first round holds the first 16 right-hand-side rows (kept in
-    // registers), 8 entries of L per thread and the diagonal (all of it for
-    // C <= 16).
+    auto Kself = [&](int m, int c) { return kat(((m * C + c) * kk + ss) * 4); };
+    // Staging: every load of a round is issued before the round's stores, so
+    // a round costs one memory latency; the first round holds the first 16
+    // right-hand-side rows (kept in registers), U entries of L per thread and
+    // the diagonal (all of it for C <= 16).
     constexpr int U = 8;
-    const int nl = CB * CB;
-    auto rhs = [&](int m) {
-        return K[((size_t)((m < C ? m : 0) * C + ci_c) * k + ka_c) * k + kb_c];
-    };
+    const int rbase = real ? (ci * kk + ka * k + kb) * 4 : (int)nrec;   // rhs(m) at rbase + m ckk 4
+    auto rhs = [&](int m) { return kat(rbase + m * ckk * 4); };
     auto rhs_val = [&](int m, float v) {
         return (m < C && real) ? (is_self ? (m == ci ? 1.0 : 0.0) : (double)v) : 0.0;
     };
-    auto put_l = [&](int idx, float v) {
-        const int c = idx / CB, m = idx - c * CB;
-        if (idx < nl)
-            Lt[c * CB + m] = (m > c && m < C) ? v : 0.0f;
+    // entry idx = c CB + m of L's staging (column c, row m), stepped by NTH
+    // from this thread's first one without a division per entry
+    const int dc = NTH / CB, dm = NTH - dc * CB;
+    int lc = tid / CB, lm = tid - lc * CB;
+    auto lstep = [&](int &c, int &m) {
+        c += dc;
+        m += dm;
+        if (m >= CB) {
+            m -= CB;
+            c += 1;
+        }
     };
-    auto l_at = [&](int idx) {
-        const int c = idx / CB, m = idx - c * CB;
-        return Kself(m, c);
+    auto put_l = [&](int c, int m, float v) {
+        if (c < CB)
+            Lt[c * CB + m] = (m > c && m < C) ? v : 0.0f;
     };
     double z[kPrepBlk];
     {
         float rv[kPrepBlk], lv[U];
+        int cs[U], ms[U];
 #pragma unroll
         for (int u = 0; u < kPrepBlk; ++u)
             rv[u] = rhs(u);
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            lv[u] = l_at(tid + u * NTH);
+        for (int u = 0; u < U; ++u) {
+            cs[u] = lc;
+            ms[u] = lm;
+            lv[u] = Kself(lm, lc);
+            lstep(lc, lm);
+        }
         float dv = Kself(tid, tid);
 #pragma unroll
         for (int u = 0; u < kPrepBlk; ++u)
@@ -253,21 +287,26 @@ __device__ void prep_columns(const float *__restrict__ K, float *out, int C, int
             z[u] = rhs_val(u, rv[u]);
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            put_l(tid + u * NTH, lv[u]);
+            put_l(cs[u], ms[u], lv[u]);
         if (tid < CB)
             rinv[tid] = tid < C ? 1.0 / (double)dv : 1.0;
     }
-    for (int base = tid + U * NTH; base < nl; base += U * NTH) {
+    while (lc < CB) {
         float v[U];
+        int cs[U], ms[U];
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            v[u] = l_at(base + u * NTH);
+        for (int u = 0; u < U; ++u) {
+            cs[u] = lc;
+            ms[u] = lm;
+            v[u] = Kself(lm, lc);
+            lstep(lc, lm);
+        }
 #pragma unroll
         for (int u = 0; u < U; ++u)
             pin(v[u]);
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            put_l(base + u * NTH, v[u]);
+            put_l(cs[u], ms[u], v[u]);
     }
     for (int base = kPrepBlk; base < CB; base += kPrepBlk) {
         float v[kPrepBlk];
@@ -418,22 +457,7 @@ __global__ __launch_bounds__(kWave) void logdet_kernel(const float *K, int n, in
 // ---------------------------------------------------------------------------
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-// Threads of the workgroup: the 16-bit group size at byte 12 of the implicit
-// kernel arguments (code object v5), read with one scalar load.  Every launch
-// here is a whole number of workgroups, so no remainder case is needed; the
-// compiler's blockDim.x covers one with a 16-bit vector load, which would
-// wait behind every vector load issued before it (the image loads that go
-// out first thing).
-typedef __attribute__((address_space(4))) const unsigned *KernargU32;
-__device__ __forceinline__ int block_threads() {
-    const KernargU32 gs = (KernargU32)(
-        (__attribute__((address_space(4))) const char *)__builtin_amdgcn_implicitarg_ptr() + 12);
-    return (int)(*gs & 0xffffu);
-}
 
-// Word 3 of a raw buffer descriptor (gfx9 family: 32-bit data format); with
-// stride 0 a load past num_records bytes returns 0 and touches no memory.
-constexpr int kBufferWord3 = 0x00020000;
 
 constexpr int kMaxWaves = 16;
 constexpr size_t kLdsBytes = 160 * 1024;   // LDS of a gfx950 workgroup

@@ -459,7 +459,7 @@ def event_ms(fn) -> float:
 def step_cost(dev) -> dict:
     """Where an inverse launch's time goes, from shipped kernels only.
     t_step: the inverse of the same batch and channels at two image widths
-    (e.g. H + W - 1 = 31 and 63 diagonal steps for 16 x 16 and 16 x 48), the
+    (e.g. H + W - 1 = 31 and 55 diagonal steps for 16 x 16 and 16 x 40), the
     time difference over the extra steps (it also carries those columns' share
     of the load and store); fixed: the 16 x 16 time less 31 t_step (launch,
     argument and weight loads, staging, the store).  t_barrier: a kernel
@@ -477,7 +477,7 @@ def step_cost(dev) -> dict:
     rows = []
     # (second widths: the widest that keeps the first's kernel instance and
     # partial-tile layout, per finc_inverse_plan)
-    for C, H, W1, W2, k in ((12, 16, 16, 48, 3), (12, 32, 32, 40, 3), (48, 8, 8, 32, 3),
+    for C, H, W1, W2, k in ((12, 16, 16, 40, 3), (12, 32, 32, 40, 3), (48, 8, 8, 32, 3),
                             (24, 16, 16, 32, 3)):
         inst = lambda W: [{key: v for key, v in p.items() if key != "lds"}
                           for p in finc.inverse_plan(finc.PLAN_LAYER, C, H, W, k)]

@@ -206,8 +206,8 @@ __host__ __device__ inline int prep_lds_doubles(int C, int nth) {
 // solves) col0 .. col0 + NTH - 1, row = (kernel position s, input channel
 // ci).  zero_tail: this block also writes the layer's zero block.
 template <int NTH>
-__device__ void prep_columns(const float *__restrict__ K, float *out, int C, int k, int corner,
-                             int col0, bool zero_tail, double *lds) {
+__device__ __forceinline__ void prep_columns(const float *__restrict__ K, float *out, int C, int k,
+                                             int corner, int col0, bool zero_tail, double *lds) {
     const int kk = k * k, CP = round_up4(C), CB = prep_cb(C), tid = threadIdx.x;
     // Lt[c CB + m] = L[m][c] for m > c, else 0 (fp32: converting to fp64 is
     // exact, and a column's multipliers are read 16 bytes at a time)
@@ -479,6 +479,9 @@ constexpr int kStream = 8;
 constexpr int kBanded = 16;
 constexpr int kRing = 32, kPhase = 16;
 constexpr int kStreamRegs = 8;   // prefetched input values per thread
+// a single layer in LDS stores its rows as they complete when a row has at
+// most kDrainRounds * 64 values (one value per lane and round)
+constexpr int kDrainRounds = 8;
 
 // Work split and LDS layout of one level (same for every layer of it).
 struct Plan {
@@ -637,6 +640,11 @@ struct InvArgs {
     // (2C, H/2, W/2) per image, hin_stride floats apart
     const float *hin;
     int hin_stride;
+    // drain (a single layer held in LDS): 1 + the index of an idle wave that
+    // stores each row of the solution as soon as its last pixel is solved, so
+    // that the store after the last diagonal is one row; 0: none (the whole
+    // image is stored after the last diagonal)
+    int drain;
     Level lv[kMaxLevels]; // in the order they run
     // steps (diagnostic, single-level calls only; null otherwise): lane 0 of
     // wave w of workgroup b writes steps[b * waves + w] = the number of
@@ -661,6 +669,8 @@ constexpr int kBandSpin = 1 << 20;
 struct Role {
     int role, tile, mt, nt, h, ng;   // tile = nt * MT + mt; ng: quad groups the wave owns
 };
+
+__device__ inline int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
 // This wave's role at level i (from the table the host filled in).
 __device__ inline Role role_of(const InvArgs &a, int i) {
@@ -1593,6 +1603,58 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
                 run(std::false_type{}, std::true_type{});
             else
                 run(std::false_type{}, std::false_type{});
+        } else if (kOne && !kStr && CRIT == kCritRegs && a.drain == wave_id() + 1) {
+            // the drain wave: frame row fi is solved with diagonal fi + W - 1;
+            // it goes out during the next step, the last one after the last
+            // barrier.  Lane t of round u takes element t + 64 u of a row as
+            // (channel, column); raw buffer stores over the image's output
+            // drop the offsets past it (lanes beyond C W).
+            const int nrounds = (C * W + kWave - 1) / kWave;   // <= kDrainRounds (host)
+            const bool fh = corner == FINC_BL || corner == FINC_BR;
+            const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
+                a.out + b * (size_t)a.out_stride, (short)0, C * HW * 4, kBufferWord3);
+            int lo[kDrainRounds], go[kDrainRounds];
+#pragma unroll
+            for (int u = 0; u < kDrainRounds; ++u) {
+                const int t = lane + kWave * u;
+                const int c = fdiv(t, pl.d_W), j = t - c * W;
+                const bool ok = t < C * W;
+                lo[u] = ok ? (j + P) * CP + c : 0;
+                go[u] = ok ? (c * HW + j) * 4 : C * HW * 4;
+            }
+            // one row: R rounds of an LDS read, then R stores, the row's
+            // offset in the stores' scalar offset
+            auto drain_row = [&](int fi, auto rc) {
+                constexpr int R = decltype(rc)::value;
+                const int nr = fh ? H - 1 - fi : fi;
+                const float *xr = sm + pl.offX + (nr + P) * WP * CP;
+                float v[R];
+#pragma unroll
+                for (int u = 0; u < R; ++u)
+                    v[u] = xr[lo[u]];
+#pragma unroll
+                for (int u = 0; u < R; ++u)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, v[u]), ro,
+                                                          go[u], nr * W * 4, 0);
+            };
+            auto drain_loop = [&](auto rc) {
+                __syncthreads();
+                for (int e = 0; e < E; ++e) {
+                    step_end(e);
+                    if (e >= W - 1)
+                        drain_row(e - (W - 1), rc);
+                }
+            };
+            switch (nrounds) {
+                case 1: drain_loop(std::integral_constant<int, 1>{}); break;
+                case 2: drain_loop(std::integral_constant<int, 2>{}); break;
+                case 3: drain_loop(std::integral_constant<int, 3>{}); break;
+                case 4: drain_loop(std::integral_constant<int, 4>{}); break;
+                case 5: drain_loop(std::integral_constant<int, 5>{}); break;
+                case 6: drain_loop(std::integral_constant<int, 6>{}); break;
+                case 7: drain_loop(std::integral_constant<int, 7>{}); break;
+                default: drain_loop(std::integral_constant<int, 8>{}); break;
+            }
         } else {
             __syncthreads();
             for (int e = 0; e < E; ++e)
@@ -1686,6 +1748,8 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
     }
     if constexpr ((MODE & kStream) != 0)
         return;   // (the solution went out phase by phase)
+    if (a.drain)
+        return;   // (the drain wave stored the rows as they were solved)
     const Plan &p0 = lv.pl;   // the last level run
     const int HW0 = p0.H * p0.W;
     float *dst = a.out + b * (size_t)a.out_stride;
@@ -1826,6 +1890,13 @@ namespace {
 struct FwdPlan {
     int C, CP, H, W, K, P, WP;
     int NT, ncq, nq, NG;         // channel tiles, quads per tile (all taps), quad groups
+                                 // (padded to a multiple of four)
+    int NGr;                     // quad groups with weights, ceil(nq / 4)
+    // padw 1: every quad group, padding ones included, has its fragments in
+    // LDS (zeros for padding groups; the loop reads them like any other);
+    // 0 (where those would not fit): padding groups read one shared zero
+    // fragment, chosen per group.  NGw: fragments of a channel tile in LDS.
+    int padw, NGw;
     int RB, nblk;                // rows per block, blocks per image
     int HB;                      // halo rows staged above and below a block
     int offI, offO, offW, offD;  // LDS floats: input rows (RB + 2P) x WP x CP, output
@@ -1833,8 +1904,8 @@ struct FwdPlan {
     int lds_floats;
     int n, corner0;              // layers (1, or 4 for a unit: TL, TR, BL, BR)
     // divisions of the index arithmetic: staged plane of a full and of the
-    // last row block, WP, NG, ncq, K, NT, W, CP / 4
-    FastDiv d_plane, d_plane_last, d_WP, d_NG, d_ncq, d_K, d_NT, d_W, d_cp4;
+    // last row block, WP, NGw, ncq, K, NT, W, CP / 4
+    FastDiv d_plane, d_plane_last, d_WP, d_NGw, d_ncq, d_K, d_NT, d_W, d_cp4;
 };
 
 struct FwdArgs {
@@ -1854,6 +1925,7 @@ struct FwdArgs {
 constexpr int kFwdThreads = 256;
 constexpr int kFwdMinBlocks = 256;   // a block per compute unit of the chip
 
+template <bool PADW>
 __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     extern __shared__ float sm[];
     const FwdPlan &fp = a.fp;
@@ -1909,13 +1981,13 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
     const size_t HW = (size_t)H * W;
     const float *xb = a.in + (size_t)b * C * HW;
     float *yb = a.out + (size_t)b * C * HW;
-    // weight fragments: Wf[(nt NG + g) 64 + lane].e = K[co][ci][tap] for
+    // weight fragments: Wf[(nt NGw + g) 64 + lane].e = K[co][ci][tap] for
     // co = 16 nt + li, quad u = 4 g + kq (tap u / ncq, ci = 4 (u % ncq) + e),
     // the channel mask applied (self tap: ci <= co only).  A round is two
     // fragments a thread: eight raw buffer loads over the layer's C^2 k^2
     // floats at (co C + ci) k^2 + tap (entries that do not exist read past
     // the end, which returns 0), all in flight before the stores.
-    const int nfrag = fp.NT * fp.NG * 64;
+    const int nfrag = fp.NT * fp.NGw * 64;
     auto wload = [&](int q, int base, float(&v)[2][4]) {
         const int K2 = K * K;
         const unsigned nrec = (unsigned)(C * C * K2 * 4);
@@ -1925,7 +1997,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         for (int h = 0; h < 2; ++h) {
             const int idx = base + h * blockDim.x;
             const int f = idx >> 6, ln = idx & 63;
-            const int nt = fdiv(f, fp.d_NG), g = f - nt * fp.NG;
+            const int nt = fdiv(f, fp.d_NGw), g = f - nt * fp.NGw;
             const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
             const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
             const bool ok = idx < nfrag && u < fp.nq && co < C;
@@ -1943,7 +2015,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         for (int h = 0; h < 2; ++h) {
             const int idx = base + h * blockDim.x;
             const int f = idx >> 6, ln = idx & 63;
-            const int nt = fdiv(f, fp.d_NG), g = f - nt * fp.NG;
+            const int nt = fdiv(f, fp.d_NGw), g = f - nt * fp.NGw;
             const int co = nt * 16 + (ln & 15), u = 4 * g + (ln >> 4);
             const int t = fdiv(u, fp.d_ncq), cq = u - t * fp.ncq;
 #pragma unroll
@@ -2041,11 +2113,13 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
         const int corner = fp.n == 1 ? corner0 : q;
         int oh, ow;
         self_tap(corner, K, oh, ow);
-        const int nfrag = fp.NT * fp.NG * 64;
+        const int nfrag = fp.NT * fp.NGw * 64;
         int wb = threadIdx.x;
         if (q == 0) {   // (the first round went out before the input)
             wstore(wpre, wb, oh * K + ow);
             wb += 2 * blockDim.x;
+            if (!PADW && threadIdx.x < 64)   // the padding groups' zero fragment
+                Wf[nfrag + threadIdx.x] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
         }
         for (; wb < nfrag; wb += 2 * blockDim.x) {
             float v[2][4];
@@ -2096,6 +2170,7 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
             // branch: their offset reads, then their 16-byte gathers and
             // weight reads, then their MFMAs
             const float4 *S4 = reinterpret_cast<const float4 *>(sm);   // regions are 16-byte aligned
+            const int zf = fp.NT * fp.NGw;   // (!PADW) the zero fragment
             for (int g0 = 0; g0 < fp.NG; g0 += 4) {
                 int d[4];
 #pragma unroll
@@ -2105,7 +2180,8 @@ __global__ __launch_bounds__(kFwdThreads) void forward_kernel(FwdArgs a) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     xv[v] = S4[(fp.offI + base + d[v]) >> 2];
-                    wv[v] = Wf[(nt * fp.NG + g0 + v) * 64 + lane];
+                    const int f = PADW || g0 + v < fp.NGr ? nt * fp.NGw + g0 + v : zf;
+                    wv[v] = Wf[f * 64 + lane];
                 }
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
@@ -2206,7 +2282,9 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B, boo
     p.nq = K * K * p.ncq;
     // quad groups, padded to a multiple of four (the MFMA loop takes four at
     // a time; padding groups have zero weights and read the pixel itself)
-    p.NG = round_up4(ceil_div(p.nq, 4));
+    p.NGr = ceil_div(p.nq, 4);
+    p.NG = round_up4(p.NGr);
+    p.padw = 1;
     p.n = n;
     p.corner0 = corner0;
     int rb_min;
@@ -2238,20 +2316,30 @@ FwdPlan make_fwd_plan(int C, int H, int W, int K, int n, int corner0, int B, boo
         p.offI = 0;
         p.offO = (p.RB + 2 * p.HB) * p.WP * p.CP;
         p.offW = p.offO + (n > 1 ? imin(H, p.RB + 3 * p.P) * W * p.CP : 0);
-        p.offD = p.offW + p.NT * p.NG * 256;
+        p.NGw = p.padw ? p.NG : p.NGr;
+        p.offD = p.offW + (p.NT * p.NGw + (p.padw ? 0 : 1)) * 256;   // (+ the zero fragment)
         p.lds_floats = p.offD + round_up4(4 * p.NG);
     };
-    layout();
-    while ((size_t)p.lds_floats * sizeof(float) > kLdsBytes && p.RB > rb_min &&
-           !(n > 1 && whole)) {
-        p.RB = imax(rb_min, p.RB / 2);
+    const int rb0 = p.RB;
+    auto fit = [&] {
+        p.RB = rb0;
         layout();
+        while ((size_t)p.lds_floats * sizeof(float) > kLdsBytes && p.RB > rb_min &&
+               !(n > 1 && whole)) {
+            p.RB = imax(rb_min, p.RB / 2);
+            layout();
+        }
+    };
+    fit();
+    if ((size_t)p.lds_floats * sizeof(float) > kLdsBytes && p.NG > p.NGr) {
+        p.padw = 0;   // the padding groups' fragments do not fit: one zero fragment
+        fit();
     }
     const int rb_last = H - (p.nblk - 1) * p.RB;
     p.d_plane = make_fastdiv((p.RB + 2 * p.HB) * p.WP);
     p.d_plane_last = make_fastdiv((rb_last + 2 * p.HB) * p.WP);
     p.d_WP = make_fastdiv(p.WP);
-    p.d_NG = make_fastdiv(p.NG);
+    p.d_NGw = make_fastdiv(p.NGw);
     p.d_ncq = make_fastdiv(p.ncq);
     p.d_K = make_fastdiv(K);
     p.d_NT = make_fastdiv(p.NT);
@@ -2388,6 +2476,24 @@ int choose_inverse(InvArgs &a, size_t lds_lim, InvChoice &c) {
     c.mode = mode;
     c.ng = ng;
     c.lds = lds;
+    // a single layer held in LDS with a register-fed critical path (one
+    // channel tile): one more (idle) wave stores the rows of the solution as
+    // they complete, on a SIMD that no critical wave uses (waves go to the
+    // four SIMDs in turn; waves skipped for that are idle too); not for rows
+    // of more than kDrainRounds values a lane.  (Chains of layers keep the
+    // store after the last diagonal: their extra wave would wait at every
+    // layer's barriers; the gathering critical forms keep their registers.)
+    a.drain = 0;
+    if ((mode & kOneLayer) != 0 && a.lv[0].pl.regcrit) {
+        const Plan &p = a.lv[0].pl;
+        int w = p.NW;
+        while (p.T < 4 && w % 4 < p.T)
+            ++w;
+        if (p.C * p.W <= kDrainRounds * kWave && w < kMaxWaves) {
+            a.drain = w + 1;
+            c.threads = (w + 1) * kWave;
+        }
+    }
     return FINC_OK;
 }
 
@@ -2595,12 +2701,15 @@ int launch_forward(const float *x, float *y, const float *K, double *logdet, flo
     int rc = check_lds(lds);
     if (rc != FINC_OK)
         return rc;
-    if (hipFuncSetAttribute((const void *)forward_kernel,
+    const void *fk = a.fp.padw ? reinterpret_cast<const void *>(forward_kernel<true>)
+                               : reinterpret_cast<const void *>(forward_kernel<false>);
+    if (hipFuncSetAttribute(fk,
                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess)
         (void)hipGetLastError();   // not needed on every runtime; the launch check decides
     // preparation blocks, then the log|det| block, then the forward blocks
     const unsigned blocks = (unsigned)(a.nfwd + (fuse ? nprep * a.ppl : 0) + (logdet ? 1 : 0));
-    hipLaunchKernelGGL(forward_kernel, dim3(blocks), dim3(kFwdThreads), lds, stream, a);
+    void *args[] = {&a};
+    (void)hipLaunchKernel(fk, dim3(blocks), dim3(kFwdThreads), args, lds, stream);
     rc = launched();
     if (rc != FINC_OK || !prepared || fuse)
         return rc;

@@ -113,7 +113,8 @@ def test_plan_rejects_bad_arguments():
     assert lib.finc_inverse_plan(2, 1, 1, 6, 16, 16, 3, info, 1) == finc.EINVAL
     assert lib.finc_inverse_plan(3, 3, 8, 12, 32, 32, 3, info, 2) == finc.EINVAL   # 3 launches
     assert lib.finc_inverse_plan(0, 1, 1, 12, 16, 16, 3, info, 1) == 1
-    assert info[0] == 256 and info[1] == 5 and info[2] == 2 and info[3] == 0
+    # four working waves, an idle one, and the wave that stores rows as they complete
+    assert info[0] == 384 and info[1] == 5 and info[2] == 2 and info[3] == 0
 
 
 def test_forward_plan():

@@ -59,6 +59,50 @@ def test_layer_forward_inverse(orc, shape, corner):
     assert torch.equal(y2, y)
 
 
+# Single layers whose rows are stored as they complete (one channel tile,
+# rows of at most 512 values) next to ones just past that bound, which store
+# the image after the last diagonal: every corner (the frame's rows run
+# bottom-up for the lower corners), one and several 16-row tiles, one row.
+DRAIN_SHAPES = [
+    # (B, C, H, W, k)
+    (2, 16, 16, 32, 3), (2, 16, 16, 33, 3), (1, 12, 20, 40, 3), (1, 12, 20, 43, 3),
+    (3, 12, 16, 16, 3), (1, 1, 1, 512, 3), (1, 1, 3, 513, 3), (2, 4, 9, 20, 7),
+]
+
+
+@pytest.mark.parametrize("corner", [0, 1, 2, 3])
+@pytest.mark.parametrize("shape", DRAIN_SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_layer_inverse_row_drain(orc, shape, corner):
+    B, C, H, W, k = shape
+    print(f"drain B={B} C={C} H={H} W={W} k={k} corner={corner}", flush=True)
+    rng = np.random.default_rng(hash(("drain", shape, corner)) % 2**32)
+    K = synth.masked_kernel(C, k, corner, 2000 + corner)
+    z = rng.normal(size=(B, C, H, W))
+    xz = finc.inverse(dev(z), dev(K), corner, out=poisoned(z.shape))
+    assert_close(host(xz), orc.inverse(f64(z), f64(K), corner), "inverse")
+    # in place: the whole image is in LDS before the first row goes out
+    zi = dev(z)
+    finc.inverse(zi, dev(K), corner, out=zi)
+    assert torch.equal(zi, xz)
+
+
+# Layers at the largest C the forward supports at k = 3, where the padding
+# quad groups' weight fragments do not fit in LDS beside the rows (those
+# groups read one shared zero fragment): every C from 57 at 8 x 8 and from 49
+# at 32 x 32 takes that form.
+@pytest.mark.parametrize("corner", [0, 3])
+@pytest.mark.parametrize("shape", [(2, 57, 8, 8, 3), (2, 60, 8, 8, 3), (1, 52, 32, 32, 3)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_forward_zero_fragment(orc, shape, corner):
+    B, C, H, W, k = shape
+    print(f"forward B={B} C={C} H={H} W={W} k={k} corner={corner}", flush=True)
+    rng = np.random.default_rng(hash(("zf", shape, corner)) % 2**32)
+    x = rng.normal(size=(B, C, H, W))
+    K = synth.garbage_in_mask(synth.masked_kernel(C, k, corner, 3000 + corner), corner)
+    y = finc.forward(dev(x), dev(K), corner, out=poisoned(x.shape))
+    assert_close(host(y), orc.forward(f64(x), f64(K), corner), "forward")
+
+
 def test_inverse_in_place(orc):
     c = synth.make("layer_c12_16x16_b64_k3", B=5)
     y = dev(orc.forward(c["x"], c["K"], 0))

@@ -477,7 +477,7 @@ def step_cost(dev) -> dict:
     rows = []
     # (second widths: the widest that keeps the first's kernel instance and
     # partial-tile layout, per finc_inverse_plan)
-    for C, H, W1, W2, k in ((12, 16, 16, 40, 3), (12, 32, 32, 40, 3), (48, 8, 8, 32, 3),
+    for C, H, W1, W2, k in ((12, 16, 16, 40, 3), (12, 32, 24, 40, 3), (48, 8, 8, 32, 3),
                             (24, 16, 16, 32, 3)):
         inst = lambda W: [{key: v for key, v in p.items() if key != "lds"}
                           for p in finc.inverse_plan(finc.PLAN_LAYER, C, H, W, k)]

@@ -507,6 +507,44 @@ def step_cost(dev) -> dict:
             "barrier_kernel_us": {"31": tb[0], "1031": tb[1]}}
 
 
+def inverse_timeline(dev, name: str = "layer_c12_16x16_b64_k3", reps: int = 20) -> dict:
+    """Where one inverse launch's time goes, from the shipped diagnostic
+    finc_inverse_timeline (the GPU's 100 MHz clock read by every wave when
+    its arguments arrived, its set-up was done, its last diagonal step was done
+    and its store was issued): per workgroup, set-up = the last wave's set-up
+    done less the first wave's arguments (weights, the image into LDS, roles
+    and addresses), loop = the last wave's
+    last step less that, store = the last store issued less the loop's end;
+    medians over the workgroups of `reps` launches, in microseconds, and the
+    spread of the workgroups' starts within a launch."""
+    import numpy as np
+    import torch
+
+    from paper_2301_09266_amd import finc, synth
+
+    c = synth.make(name)
+    d = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(dev)
+    y, K = d(c["x"]), d(c["K"])
+    prep = finc.prepare(K, [c["corner"]])
+    rows = []
+    for r in range(reps + 3):
+        _, st = finc.inverse_timeline(y, prep, c["k"], c["corner"])
+        if r < 3:
+            continue   # (warm-up)
+        t = st.cpu().numpy().astype(np.int64)
+        start, setup = t[:, :, 0].min(axis=1), t[:, :, 1].max(axis=1)
+        loop_end, store = t[:, :, 2].max(axis=1), t[:, :, 3].max(axis=1)
+        rows.append(np.stack([setup - start, loop_end - setup, store - loop_end,
+                              start - start.min()], axis=1))
+    a = np.concatenate(rows) * 0.01   # 100 MHz ticks -> microseconds
+    med = np.median(a, axis=0)
+    steps = c["H"] + c["W"] - 1
+    return {"workload": name, "launches": reps, "clock_mhz": 100,
+            "setup_us": float(med[0]), "loop_us": float(med[1]), "store_us": float(med[2]),
+            "loop_us_per_step": float(med[1] / steps),
+            "workgroup_start_spread_us": float(np.max(a[:, 3]))}
+
+
 def flow_sampling(dev, name: str = "flow_cifar10_L3_K28_b100") -> dict:
     """The whole FInC Flow at the paper's CIFAR-10 setting (Table 3: three
     levels of 28 Steps, 3 x 32 x 32, 512-wide coupling networks, n = 100
@@ -783,6 +821,7 @@ def main():
         out["batch_scaling"] = batch_scaling(dev)
     if not args.no_configs:
         out["step_cost"] = step_cost(dev)
+        out["inverse_timeline"] = inverse_timeline(dev)
     if not args.no_flow:
         out["flow_sampling"] = flow_sampling(dev)
     if args.cpu_seconds > 0:

@@ -143,6 +143,21 @@ int finc_inverse_steps(int kind, const float *y, float *x, const void *prepared,
                        int C, int H, int W, int k, int corner, int *steps, int max_steps,
                        hipStream_t stream);
 
+/* Diagnostic of where an inverse launch's time goes: the inverse of
+ * finc_inverse_steps (same kinds, shapes and checks), which also writes, for
+ * every wave w of workgroup b, stamps[(b * waves + w) * 4 + i] = the GPU's
+ * 100 MHz constant clock (10 ns a tick) when that wave i = 0 had its
+ * arguments, 1 had its set-up done (weights and the image in LDS; before its
+ * first step barrier), 2 had run its last diagonal step, 3 had issued its
+ * part of the solution's store (completion of the stores is not waited for).  stamps:
+ * device long longs, at least 4 per wave (max_stamps; FINC_EINVAL if fewer),
+ * not overlapping x, y or prepared.  Returns the number written, or an error
+ * as the inverse call would.  For tests and tools; the product calls read no
+ * clock. */
+int finc_inverse_timeline(int kind, const float *y, float *x, const void *prepared, int B,
+                          int C, int H, int W, int k, int corner, long long *stamps,
+                          int max_stamps, hipStream_t stream);
+
 /* The forward's work split (host arithmetic only): an image is cut into
  * blocks of rows, each staged in LDS with its halo rows and the layer's
  * weights; a unit keeps whole images, or bands of rows when the batch is

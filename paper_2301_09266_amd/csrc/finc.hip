@@ -625,6 +625,13 @@ struct Level {
 
 struct InvArgs {
     int L, n_units, lpu, corner0;
+    // stamps (diagnostic, single-level calls only; null otherwise): lane 0 of
+    // wave w of workgroup b writes stamps[(b * waves + w) * 4 + i], the
+    // 100 MHz constant clock at i = 0 the wave's arguments loaded (and its
+    // first image loads issued), 1 its set-up done (before the first step
+    // barrier), 2 its last step done, 3 its part of the store issued.  (In the
+    // first argument line, which the kernel's first round of loads brings.)
+    long long *stamps;
     // split: the channel-split unit, its batch seen as (4B, C/4, H, W): the
     // workgroup of image b' = 4 b + g inverts quarter g with corner g and the
     // g-th prepared layer (one level of one layer)
@@ -671,6 +678,20 @@ struct Role {
 };
 
 __device__ inline int wave_id() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
+
+// (diagnostic) stamp i of this wave of workgroup b, when asked for.  The
+// clock is read only then: its scalar read would hold up the next wait for
+// LDS operations.
+__device__ inline void stamp(long long *stamps, size_t b, int i) {
+    if (stamps) {
+        // (wave-uniform address arithmetic: nothing the compiler moves ahead
+        // of the test touches a vector register)
+        const long long t = __builtin_amdgcn_s_memrealtime();
+        const size_t slot = (b * (size_t)(block_threads() >> 6) + (size_t)wave_id()) * 4 + i;
+        if ((threadIdx.x & 63) == 0)
+            stamps[slot] = t;
+    }
+}
 
 // This wave's role at level i (from the table the host filled in).
 __device__ inline Role role_of(const InvArgs &a, int i) {
@@ -1414,6 +1435,8 @@ __device__ __attribute__((always_inline)) void level_waves(const InvArgs &a, con
             return s0;
         };
         const f32x4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (top && n == 0)
+            stamp(a.stamps, b, 1);
 
         if (r.role == 1) {
             // helper: during step e, the partial tile of diagonal e + 1 (every
@@ -1723,6 +1746,7 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
     InputRound inq;
     if constexpr (kOne && (MODE & kStream) == 0)
         input_issue(lv.pl, lv.z + b * (size_t)lv.pl.C * lv.pl.H * lv.pl.W, tid, inq);
+    stamp(a.stamps, b, 0);
     for (int i = 0; i < (kOne ? 1 : a.L); ++i) {
         if (i > 0) {
             above = lv.pl;
@@ -1746,10 +1770,13 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
             __syncthreads();
         }
     }
-    if constexpr ((MODE & kStream) != 0)
-        return;   // (the solution went out phase by phase)
-    if (a.drain)
-        return;   // (the drain wave stored the rows as they were solved)
+    stamp(a.stamps, b, 2);
+    if ((MODE & kStream) != 0 || a.drain) {
+        // (the solution went out phase by phase, or the drain wave stored
+        // the rows as they were solved)
+        stamp(a.stamps, b, 3);
+        return;
+    }
     const Plan &p0 = lv.pl;   // the last level run
     const int HW0 = p0.H * p0.W;
     float *dst = a.out + b * (size_t)a.out_stride;
@@ -1822,6 +1849,7 @@ __global__ __launch_bounds__(MAXT) void inverse_chain_kernel(InvArgs a) {
             }
         }
     }
+    stamp(a.stamps, b, 3);
 }
 
 // Inverse kernel instances, in groups of one workgroup size and one mode, by
@@ -2523,6 +2551,7 @@ int launch_streamed(const InvArgs &a, const InvChoice &ch, int B, hipStream_t st
         s.lv[0].prep = l0.prep + (size_t)(u * a.lpu + q) * p.lstride;
         s.lv[0].pl = p;
         s.steps = a.steps;   // (set for single layers only)
+        s.stamps = a.stamps;
         void *args[] = {&s};
         (void)hipLaunchKernel(k, dim3(B), dim3(threads), args, lds, stream);
         rc = launched();
@@ -3140,10 +3169,13 @@ int finc_split_inverse_prepared(const float *y, float *x, const void *prepared4,
     return launch_inverse_chain(a, 4 * B, stream);
 }
 
-int finc_inverse_steps(int kind, const float *y, float *x, const void *prepared, int B, int C,
-                       int H, int W, int k, int corner, int *steps, int max_steps,
-                       hipStream_t stream) {
-    if ((kind != FINC_PLAN_LAYER && kind != FINC_PLAN_SPLIT) || !steps || max_steps < 0 ||
+// The diagnostics' shared path: the prepared inverse of a layer or of a
+// channel-split unit with `per_wave` values of `elem` bytes written for every
+// wave of every workgroup into buf (steps: ints; stamps: long longs).
+static int inverse_diagnostic(int kind, const float *y, float *x, const void *prepared, int B,
+                              int C, int H, int W, int k, int corner, void *buf, size_t elem,
+                              int per_wave, int max_elems, hipStream_t stream) {
+    if ((kind != FINC_PLAN_LAYER && kind != FINC_PLAN_SPLIT) || !buf || max_elems < 0 ||
         !valid_corner(corner))
         return FINC_EINVAL;
     const bool split = kind == FINC_PLAN_SPLIT;
@@ -3158,13 +3190,12 @@ int finc_inverse_steps(int kind, const float *y, float *x, const void *prepared,
     const int n = finc_inverse_plan(kind, 1, 1, C, H, W, k, info, 1);
     if (n < 0)
         return n;
-    const long long count = (long long)(split ? 4 * B : B) * (info[0] / 64);
-    if (count > max_steps)
+    const long long count = (long long)(split ? 4 * B : B) * (info[0] / 64) * per_wave;
+    if (count > max_elems)
         return FINC_EINVAL;
+    const size_t bb = (size_t)count * elem;
     if (!inverse_alias_ok(y, x, bytes) || overlap(x, bytes, prepared, pb) ||
-        overlap(steps, (size_t)count * sizeof(int), x, bytes) ||
-        overlap(steps, (size_t)count * sizeof(int), y, bytes) ||
-        overlap(steps, (size_t)count * sizeof(int), prepared, pb))
+        overlap(buf, bb, x, bytes) || overlap(buf, bb, y, bytes) || overlap(buf, bb, prepared, pb))
         return FINC_EINVAL;
     InvArgs a;
     memset(&a, 0, sizeof(a));
@@ -3175,9 +3206,26 @@ int finc_inverse_steps(int kind, const float *y, float *x, const void *prepared,
     a.lpu = 1;
     a.corner0 = split ? FINC_TL : corner;
     a.split = split ? 1 : 0;
-    a.steps = steps;
+    if (elem == sizeof(int))
+        a.steps = static_cast<int *>(buf);
+    else
+        a.stamps = static_cast<long long *>(buf);
     const int rc = launch_inverse_chain(a, split ? 4 * B : B, stream);
     return rc == FINC_OK ? (int)count : rc;
+}
+
+int finc_inverse_steps(int kind, const float *y, float *x, const void *prepared, int B, int C,
+                       int H, int W, int k, int corner, int *steps, int max_steps,
+                       hipStream_t stream) {
+    return inverse_diagnostic(kind, y, x, prepared, B, C, H, W, k, corner, steps, sizeof(int), 1,
+                              max_steps, stream);
+}
+
+int finc_inverse_timeline(int kind, const float *y, float *x, const void *prepared, int B,
+                          int C, int H, int W, int k, int corner, long long *stamps,
+                          int max_stamps, hipStream_t stream) {
+    return inverse_diagnostic(kind, y, x, prepared, B, C, H, W, k, corner, stamps,
+                              sizeof(long long), 4, max_stamps, stream);
 }
 
 int finc_banded_plan(int C, int H, int W, int k, int *info) {

@@ -30,6 +30,7 @@ SIGNATURES = {
     "finc_inverse_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i), _i]),
     "finc_forward_plan": (_i, [_i, _i, _i, _i, _i, _i, _i, ctypes.POINTER(_i)]),
     "finc_inverse_steps": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp]),
+    "finc_inverse_timeline": (_i, [_i, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _i, _vp]),
     "finc_banded_plan": (_i, [_i, _i, _i, _i, ctypes.POINTER(_i)]),
     "finc_banded_workspace_bytes": (_sz, [_i, _i, _i, _i, _i, _i]),
     "finc_inverse_banded": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _vp, _vp]),
@@ -320,6 +321,33 @@ def inverse_steps(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: int =
     if n < 0:
         _check(n, "finc_inverse_steps")
     return x, steps
+
+
+def inverse_timeline(y: torch.Tensor, prepared: torch.Tensor, k: int, corner: int = TL,
+                     split: bool = False):
+    """(x, stamps): the inverse of a prepared layer (or, split=True, of a
+    prepared channel-split unit) and, for every wave of every workgroup, the
+    GPU's 100 MHz clock when its arguments arrived, its set-up was done, its
+    last step was done and its store was issued, as (workgroups, waves, 4)
+    int64 (see finc_inverse_timeline)."""
+    L = _require_lib()
+    _dev(y, "y")
+    B, C, H, W = y.shape
+    kind = PLAN_SPLIT if split else PLAN_LAYER
+    _bytes_buf(prepared, workspace_bytes(C // 4 if split else C, k, 4 if split else 1),
+               "prepared")
+    info = inverse_plan(kind, C, H, W, k)
+    if isinstance(info, int):
+        _check(info, "finc_inverse_timeline")
+    waves = info[0]["threads"] // 64
+    nwg = (4 * B if split else B)
+    stamps = torch.full((nwg, waves, 4), -1, dtype=torch.int64, device=y.device)
+    x = torch.empty_like(y)
+    n = L.finc_inverse_timeline(kind, _ptr(y), _ptr(x), _ptr(prepared), B, C, H, W, k, corner,
+                                _ptr(stamps), stamps.numel(), _stream())
+    if n < 0:
+        _check(n, "finc_inverse_timeline")
+    return x, stamps
 
 
 def banded_plan(C: int, H: int, W: int, k: int):

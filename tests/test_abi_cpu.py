@@ -330,6 +330,31 @@ def test_inverse_steps_rejects():
                                   None) == finc.EINVAL
 
 
+def test_inverse_timeline_rejects():
+    lib = finc.lib()
+    S = ctypes.c_void_p(0x2000000)
+    P = ctypes.c_void_p(0x40000000)
+    B, C, H, W, k = SHAPE
+    waves = finc.inverse_plan(finc.PLAN_LAYER, C, H, W, k)[0]["threads"] // 64
+    need = B * waves * 4
+    # unit kind, no buffer, one stamp short, stamps over y, misaligned
+    # prepared, bad corner, channels the split unit cannot take
+    assert lib.finc_inverse_timeline(finc.PLAN_UNIT, FAKE, FAKE2, P, B, C, H, W, k, 0, S, need,
+                                     None) == finc.EINVAL
+    assert lib.finc_inverse_timeline(finc.PLAN_LAYER, FAKE, FAKE2, P, B, C, H, W, k, 0, None,
+                                     need, None) == finc.EINVAL
+    assert lib.finc_inverse_timeline(finc.PLAN_LAYER, FAKE, FAKE2, P, B, C, H, W, k, 0, S,
+                                     need - 1, None) == finc.EINVAL
+    assert lib.finc_inverse_timeline(finc.PLAN_LAYER, FAKE, FAKE2, P, B, C, H, W, k, 0, FAKE,
+                                     need, None) == finc.EINVAL
+    assert lib.finc_inverse_timeline(finc.PLAN_LAYER, FAKE, FAKE2, ctypes.c_void_p(0x40000010),
+                                     B, C, H, W, k, 0, S, need, None) == finc.EINVAL
+    assert lib.finc_inverse_timeline(finc.PLAN_LAYER, FAKE, FAKE2, P, B, C, H, W, k, 4, S, need,
+                                     None) == finc.EINVAL
+    assert lib.finc_inverse_timeline(finc.PLAN_SPLIT, FAKE, FAKE2, P, B, 6, H, W, k, 0, S, need,
+                                     None) == finc.EINVAL
+
+
 def test_banded_rejects():
     lib = finc.lib()
     ws = ctypes.c_void_p(0x40000000)

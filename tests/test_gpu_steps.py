@@ -38,3 +38,28 @@ def test_step_count(case):
     ref = (finc.split_inverse_prepared(y, prep, k) if split
            else finc.inverse_prepared(y, prep, k, corner))
     assert torch.equal(x, ref)
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "-".join(map(str, c)))
+def test_timeline(case):
+    """finc_inverse_timeline: four stamps a wave, in order (start, set-up done,
+    last step done, store issued), and the inverse bit for bit that of the
+    call without stamps."""
+    kind, C, H, W, k = case
+    split = kind == "split"
+    corner = (C + H + W + k) % 4
+    print(f"timeline {case}", flush=True)
+    if split:
+        K = synth.split_kernels(C, k)
+        prep = finc.prepare(dev(K), [0, 1, 2, 3])
+    else:
+        K = synth.masked_kernel(C, k, corner, 1000 + C)
+        prep = finc.prepare(dev(K), [corner])
+    y = dev(np.random.default_rng(C + W).normal(size=(2, C, H, W)))
+    x, st = finc.inverse_timeline(y, prep, k, corner, split=split)
+    t = st.cpu().numpy()
+    assert (t > 0).all(), case
+    assert (np.diff(t, axis=2) >= 0).all(), case
+    ref = (finc.split_inverse_prepared(y, prep, k) if split
+           else finc.inverse_prepared(y, prep, k, corner))
+    assert torch.equal(x, ref)

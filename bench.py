@@ -270,6 +270,8 @@ def per_config(dev) -> list:
                "inverse_alg_bytes": alg, "inverse_hbm_gbs": gbs,
                "inverse_hbm_frac": gbs / HBM_PEAK_GBS,
                "us_per_diagonal_step": inv / steps if steps else None}
+        if kind == "layer":   # set-up, loop and store of one launch (finc_inverse_timeline)
+            row["inverse_timeline"] = inverse_timeline(dev, name, reps=5)
         row.update(oracle_row(c, kind, zd if kind == "stack" else y, out))
         rows.append(row)
     return rows

@@ -3,7 +3,7 @@ oracle: the banded stream form (finc_inverse_banded,
 finc_unit_inverse_banded) -- bands of rows in workgroups of their own,
 pipelined through drained-diagonal counts.  Shapes: 256 x 256 at C = 2 and
 128 x 128 at C = 12 (beyond one workgroup), ragged last bands, every corner,
-k = 2 .. 7, a unit.
+k = 2 .. 7, a unit, and a seeded sweep of random shapes.
 
 Bar: 1e-4 * max(1, |oracle|) elementwise against the oracle's raster-order
 inverse of the oracle's forward of x, and the round trip to x within 1e-4;
@@ -55,6 +55,32 @@ def test_banded_layer(orc, case):
     assert torch.equal(again, xr) and timeout_flag(ws2, C, k, 1) == 0
     one, _ = finc.inverse_banded(dev(y[-1:]), dev(K), corner)
     assert torch.equal(one[0], xr[-1])
+
+
+def draw_banded(seed):
+    """A seeded banded layer shape (B, C, H, W, k, corner) that the banded
+    form takes: C 1..16, k 2..7, H 17..159, W 2..47."""
+    rng = np.random.default_rng(seed)
+    while True:
+        C, k = int(rng.integers(1, 17)), int(rng.integers(2, 8))
+        H, W = int(rng.integers(17, 160)), int(rng.integers(2, 48))
+        corner, B = int(rng.integers(0, 4)), int(rng.integers(1, 3))
+        if C * H * W * C * k * k <= 6_000_000 and not isinstance(finc.banded_plan(C, H, W, k), int):
+            return B, C, H, W, k, corner
+
+
+@pytest.mark.parametrize("seed", range(24))
+def test_banded_layer_sweep(orc, seed):
+    """Random shapes cover band heights, thread counts and register budgets
+    that the listed cases miss."""
+    B, C, H, W, k, corner = case = draw_banded(500 + seed)
+    print(f"banded sweep {seed} {case} {finc.banded_plan(C, H, W, k)}", flush=True)
+    K = synth.garbage_in_mask(synth.masked_kernel(C, k, corner, 3000 + seed), corner)
+    x = np.random.default_rng(seed).normal(size=(B, C, H, W))
+    y = orc.forward(f64(x), f64(K), corner)
+    xr, ws = finc.inverse_banded(dev(y), dev(K), corner)
+    assert timeout_flag(ws, C, k, 1) == 0
+    assert_close(host(xr), orc.inverse(f64(y), f64(K), corner), f"banded sweep {case}")
 
 
 def test_banded_in_place(orc):
